@@ -1,0 +1,273 @@
+/*
+ * mtn.h -- C ABI of the windowed-KV frame-attention library (libmtn).
+ *
+ * The library serves the per-frame attention step of real-time interaction
+ * sessions as described by Metronome (arXiv 2607.02640): every session keeps
+ * its first S tokens pinned (the attention sinks) plus a sliding window of its
+ * last W tokens inside one shared, paged KV pool, and each frame appends a
+ * chunk of tokens (chunk prefill, causal inside the chunk and over the
+ * retained cache) followed by single-token decode steps.
+ *
+ *   - Retention and masking: §4.1 and App. A ("Window half", "Sink half").  A
+ *     query at absolute position t sees keys k <= t with k < S or k in the W
+ *     positions ending at t.
+ *   - Positions are absolute and never rebased (§4.1: the request keeps
+ *     growing logically while only the bound is retained).
+ *   - Frame structure: §2, "The task model" (prefill the chunk, then decode up
+ *     to tau tokens), batched over all due sessions (continuous batching).
+ *   - Pool: App. A pins ceil(S / block) blocks per session and counts them in
+ *     the admission cap; §3 shows that an exhausted pool stalls every session
+ *     silently.  Here exhaustion is a loud, atomic error code instead.
+ *
+ * Conventions for every call:
+ *   - Return value: MTN_OK (0) or a negative mtn_status.  On error nothing
+ *     changes (host state, device state, out-parameters) unless stated.
+ *   - Pointers documented as "device" are HIP device pointers owned by the
+ *     caller; "host" pointers are read during the call only.
+ *   - `stream` is a hipStream_t passed as void* (NULL = the null stream).  All
+ *     device work is asynchronous on it; device faults surface at the next
+ *     synchronisation.  All calls that belong to one plan must use the same
+ *     stream; a pool is driven from one host thread at a time.
+ *   - Layouts are row-major with the last index fastest.
+ *   - Element types: MTN_F32 is IEEE binary32, MTN_BF16 is bfloat16.  The KV
+ *     cache and q/k/v/out share one element type (kv_dtype == io_dtype).
+ *     Accumulation is fp32; bf16 results are rounded to nearest-even.
+ */
+#ifndef MTN_H
+#define MTN_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef int32_t mtn_status;
+
+#define MTN_OK                   0
+#define MTN_ERR_INVALID_ARG     (-1)  /* malformed argument or config          */
+#define MTN_ERR_BAD_SESSION     (-2)  /* session id not open / out of range    */
+#define MTN_ERR_CHUNK_TOO_LARGE (-3)  /* n_tok > max_chunk                     */
+#define MTN_ERR_NO_SESSION_SLOT (-4)  /* max_sessions sessions already open    */
+#define MTN_ERR_POOL_EXHAUSTED  (-5)  /* windowed: reservation at open fails;
+                                         unbounded: a plan needs more blocks   */
+#define MTN_ERR_SESSION_FULL    (-6)  /* unbounded: session would pass max_len */
+#define MTN_ERR_DEVICE          (-7)  /* a HIP call failed; see last_error     */
+#define MTN_ERR_BAD_STATE       (-8)  /* call out of order (plan open/missing,
+                                         layer not appended, ...)              */
+#define MTN_ERR_UNSUPPORTED     (-9)  /* shape/dtype with no compiled kernel   */
+
+enum { MTN_F32 = 0, MTN_BF16 = 1 };
+
+/* window value selecting the unbounded (vanilla) policy: no window, no
+ * eviction, sinks ignored, linear block table up to max_len tokens.          */
+#define MTN_WINDOW_UNBOUNDED (-1)
+
+/* flags */
+#define MTN_POOL_HOST_ONLY 1u /* no device work at all: planning, block tables
+                                 and counters only (kv_dev may be NULL); every
+                                 append/attend call returns MTN_ERR_BAD_STATE
+                                 and plans commit without per-layer appends    */
+
+typedef struct mtn_pool mtn_pool; /* opaque; owned by the library */
+
+typedef struct {
+    int32_t  n_layers;      /* >= 1                                            */
+    int32_t  n_q_heads;     /* Hq >= 1                                         */
+    int32_t  n_kv_heads;    /* Hkv >= 1, Hq % Hkv == 0; G = Hq / Hkv <= 8      */
+    int32_t  head_dim;      /* D: 64 or 128                                    */
+    int32_t  block_size;    /* tokens per KV block: must be 16                 */
+    int32_t  n_sink;        /* S >= 0 pinned tokens (ignored when unbounded)   */
+    int32_t  window;        /* W >= 1, or MTN_WINDOW_UNBOUNDED                 */
+    int32_t  max_chunk;     /* C_max >= 1: max tokens per session per plan     */
+    int32_t  max_sessions;  /* >= 1 concurrently open sessions                 */
+    int32_t  max_len;       /* unbounded only: per-session token cap (>= 1)    */
+    int64_t  n_blocks;      /* pool capacity in blocks (>= 1)                  */
+    int32_t  kv_dtype;      /* MTN_F32 | MTN_BF16                              */
+    int32_t  io_dtype;      /* must equal kv_dtype                             */
+    double   rope_theta;    /* RoPE base (> 1)                                 */
+    float    softmax_scale; /* 0 selects 1/sqrt(head_dim)                      */
+    uint32_t flags;         /* MTN_POOL_* flags                                */
+} mtn_pool_config;
+
+/*
+ * Pool memory.  The caller allocates the KV pool in device memory (e.g. a
+ * torch tensor) and keeps it alive until mtn_pool_destroy.  Layout, per layer
+ * l, physical block b, KV head h (16 tokens per block, element size e):
+ *
+ *   K tile   [16][D]  at ((l * n_blocks + b) * Hkv + h) * 2 * 16 * D * e
+ *   V^T tile [D][16]  immediately after the K tile
+ *
+ * K rows hold RoPE-rotated keys; the V tile is stored transposed (dimension-
+ * major) so that consecutive tokens of one dimension are adjacent.
+ */
+mtn_status mtn_pool_required_bytes(const mtn_pool_config *cfg, size_t *kv_bytes);
+
+/* Validates cfg, allocates the library's host state and its device metadata
+ * and workspace (hipMalloc on the current device), and takes kv_dev (device,
+ * caller-owned, >= required bytes, 256-byte aligned) as the pool.  The pool
+ * contents are not initialised.  *out receives the handle.                    */
+mtn_status mtn_pool_create(const mtn_pool_config *cfg, void *kv_dev, size_t kv_bytes,
+                           void *stream, mtn_pool **out);
+
+/* Frees the library's host and device state (not kv_dev).  Synchronises the
+ * device first.  NULL is accepted.                                            */
+void mtn_pool_destroy(mtn_pool *pool);
+
+/* Open a session: lowest free session id.  Windowed pools reserve the
+ * session's whole bounded footprint, ceil(S/16) sink blocks plus R/16 ring
+ * blocks with R = roundup(W + max_chunk - 1, 16), and fail with
+ * MTN_ERR_POOL_EXHAUSTED when the reservations would exceed n_blocks (App. A:
+ * the admission cap counts the pinned blocks).  Unbounded pools reserve
+ * nothing.  Blocks are assigned lazily, lowest free id first.                 */
+mtn_status mtn_session_open(mtn_pool *pool, int32_t *sid_out);
+
+/* Close a session: its blocks and reservation return to the pool, its id
+ * becomes free.  MTN_ERR_BAD_STATE while a plan is open.                      */
+mtn_status mtn_session_close(mtn_pool *pool, int32_t sid);
+
+/*
+ * Plans.  Positions advance once per token, not per layer, so per-layer calls
+ * act on one open plan:
+ *
+ *   mtn_plan_begin -> for every layer: mtn_frame_append_kv, then optionally an
+ *   attend call -> mtn_plan_commit
+ *
+ * mtn_plan_begin validates everything first (ids open and unique, 1 <= n_tok
+ * <= max_chunk, unbounded max_len and pool capacity), then assigns blocks for
+ * the n_tok[i] new positions L_i .. L_i + n_tok[i] - 1 of session sids[i] and
+ * uploads the plan (device metadata, RoPE angles) on `stream`.  Planned tokens
+ * are packed in plan order: sequence i owns rows off_i .. off_i + n_tok[i] - 1
+ * with off_i = n_tok[0] + ... + n_tok[i-1].
+ * Slot map: p < S goes to sink block p / 16, offset p % 16; p >= S goes to ring
+ * slot (p - S) mod R (unbounded: slot p), i.e. ring block slot / 16, offset
+ * slot % 16.  A ring slot is reused only by a position that is R >= W +
+ * max_chunk - 1 tokens later, so no key any planned query can see is
+ * overwritten (§4.1 per-query window under chunk prefill).
+ */
+mtn_status mtn_plan_begin(mtn_pool *pool, int32_t n_seq, const int32_t *sids /*host*/,
+                          const int32_t *n_tok /*host*/, void *stream);
+
+/* Advance every planned session by its n_tok.  MTN_ERR_BAD_STATE unless every
+ * layer was appended (host-only pools excepted).  Positions that leave the window are evicted logically
+ * (their slots become reusable); nothing is moved.                            */
+mtn_status mtn_plan_commit(mtn_pool *pool);
+
+/*
+ * Fused RoPE + append + evict for one layer of the open plan.
+ * k, v: device, [T][Hkv][D] in kv_dtype, T = total planned tokens, packed in
+ * plan order.  Each key row is rotated (rotate-half RoPE at its absolute
+ * position, angle computed in fp64) and written with its value into the
+ * token's slot of layer `layer`, overwriting whatever position left the window
+ * there (eviction is slot reuse).
+ */
+mtn_status mtn_frame_append_kv(mtn_pool *pool, int32_t layer, const void *k, const void *v,
+                               void *stream);
+
+/*
+ * Chunk-prefill attention for one layer of the open plan (after its append).
+ * q, out: device, [T][Hq][D], packed like k/v.  Each planned query row at
+ * position t is rotated at t and attends to sinks [0, min(S, t+1)) and window
+ * [max(S, t-W+1), t] of its own session (all earlier chunk tokens included).
+ * lse: device [T][Hq] fp32 natural-log sum-exp of the scaled scores, or NULL.
+ * bf16 pools run the MFMA kernel, fp32 pools the fp32 vector kernel.
+ */
+mtn_status mtn_attend_chunk_prefill(mtn_pool *pool, int32_t layer, const void *q, void *out,
+                                    float *lse, void *stream);
+
+/*
+ * GQA decode attention for one layer of the open plan, whose every sequence
+ * has n_tok == 1.  q, out: device, [n_seq][Hq][D]; lse: device [n_seq][Hq] or
+ * NULL.  The G query heads sharing a KV head read its sinks ∪ window once;
+ * n_split > 1 splits the keys into segments merged by log-sum-exp, sinks in
+ * segment 0 only (App. A segmented decode).  n_split = 0 picks a split from
+ * the batch size; 1 <= n_split <= 64 forces it.
+ */
+mtn_status mtn_attend_decode(mtn_pool *pool, int32_t layer, const void *q, void *out,
+                             float *lse, int32_t n_split, void *stream);
+
+/*
+ * One whole frame for a batch of sessions (§2 task model): plan the chunk,
+ * then for each layer append + chunk-prefill attend, commit; then for each
+ * decode round j (only sessions with n_decode[i] > j) plan one token, for each
+ * layer append + decode attend, commit.  Chunks of one token everywhere use the
+ * decode kernel.
+ */
+typedef struct {
+    int32_t        n_seq;
+    const int32_t *sids;       /* host [n_seq]                                */
+    const int32_t *chunk_len;  /* host [n_seq], 1 <= chunk_len <= max_chunk   */
+    const int32_t *n_decode;   /* host [n_seq], >= 0                          */
+    /* device [n_layers][sum(chunk_len)][H][D], rows packed in batch order    */
+    const void *q_chunk, *k_chunk, *v_chunk;
+    void       *out_chunk;     /* [n_layers][sum(chunk_len)][Hq][D]           */
+    float      *lse_chunk;     /* [n_layers][sum(chunk_len)][Hq] or NULL      */
+    /* device [max(n_decode)][n_layers][n_seq][H][D]; entry (j, l, i) is read
+     * (written) only when n_decode[i] > j                                    */
+    const void *q_dec, *k_dec, *v_dec;
+    void       *out_dec;       /* [max(n_decode)][n_layers][n_seq][Hq][D]     */
+    float      *lse_dec;       /* [max(n_decode)][n_layers][n_seq][Hq] or NULL */
+    int32_t     n_split;       /* decode split, 0 = automatic                 */
+} mtn_frame_batch;
+
+mtn_status mtn_frame_step(mtn_pool *pool, const mtn_frame_batch *batch, void *stream);
+
+/* ---- observability and test hooks ------------------------------------- */
+
+typedef struct {
+    int64_t capacity;       /* n_blocks                                        */
+    int64_t assigned;       /* blocks currently holding session data           */
+    int64_t reserved;       /* windowed: sum of open reservations; unbounded:
+                               equal to assigned                               */
+    int32_t open_sessions;
+    int32_t blocks_per_session; /* row length of the block table              */
+    int32_t ring_tokens;    /* R                                               */
+    int32_t sink_blocks;    /* ceil(S / 16) (0 when unbounded)                 */
+} mtn_pool_stats_t;
+
+mtn_status mtn_pool_stats(const mtn_pool *pool, mtn_pool_stats_t *out);
+
+/* Length (tokens appended so far, committed) and assigned block count. */
+mtn_status mtn_session_info(const mtn_pool *pool, int32_t sid, int64_t *len,
+                            int32_t *n_assigned);
+
+/* Copy the session's block-table row (-1 = unassigned) into host out[cap];
+ * *n_out receives the row length.  MTN_ERR_INVALID_ARG if cap is too small. */
+mtn_status mtn_session_block_table(const mtn_pool *pool, int32_t sid, int32_t *out,
+                                   int32_t cap, int32_t *n_out);
+
+/* For the open plan: host arrays of length >= T receive, per planned token,
+ * its absolute position, physical block and offset (any pointer may be NULL);
+ * evicted_lo/hi (length >= n_seq, may be NULL) receive each sequence's
+ * half-open range of positions that leave the window at commit.  *n_tok_out
+ * receives T.                                                                */
+mtn_status mtn_plan_info(const mtn_pool *pool, int64_t *pos, int32_t *block, int32_t *offset,
+                         int32_t cap, int64_t *evicted_lo, int64_t *evicted_hi,
+                         int32_t *n_tok_out);
+
+/* Debug: write NaN into every slot that no query may read: all unassigned
+ * blocks, sink-block slots at or past S, and ring slots of positions outside
+ * each open session's retained set.  Attention results must not change.       */
+mtn_status mtn_debug_poison_dead(mtn_pool *pool, void *stream);
+
+/* Per-kernel device timing.  When enabled, the library records HIP events
+ * around each launch it makes and accumulates per-kernel-class totals;
+ * mtn_pool_kernel_times synchronises those events and returns, for classes
+ * 0 append, 1 prefill, 2 decode, 3 merge, the launch count and the summed
+ * milliseconds (arrays of length >= 4), then resets the totals.               */
+mtn_status mtn_pool_set_timing(mtn_pool *pool, int32_t enable);
+mtn_status mtn_pool_kernel_times(mtn_pool *pool, int64_t *launches, double *ms);
+
+/* Plain device copy (dst = src, `bytes` a multiple of 16, both 16-byte
+ * aligned): the bandwidth reference for the HBM roofline and the scale of the
+ * profiler's byte counters.                                                   */
+mtn_status mtn_hbm_copy(const void *src, void *dst, size_t bytes, void *stream);
+
+const char *mtn_status_string(mtn_status s);
+const char *mtn_pool_last_error(const mtn_pool *pool);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* MTN_H */

@@ -1,0 +1,914 @@
+// Host side of libmtn: pool and session bookkeeping, the frame planner (block
+// table, ring-slot map, eviction ranges, exhaustion checks), plan upload and
+// kernel orchestration behind the C ABI declared in include/mtn.h.
+//
+// Method: Metronome (arXiv 2607.02640) §4.1 and App. A -- every session
+// retains its first S tokens (pinned sink blocks, counted in the admission
+// cap) and its last W tokens; §2 task model -- a frame prefills a chunk, then
+// decodes single tokens, for all due sessions in one batch.
+#include "mtn.h"
+#include "mtn_kernels.h"
+
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <cmath>
+#include <cstdio>
+#include <cstring>
+#include <string>
+#include <vector>
+
+using namespace mtn;
+
+namespace {
+
+constexpr int kStages = 4;  // pinned staging buffers in flight
+
+// Lowest-free-first block allocator over a bitmap (bit set = free).
+class BlockAllocator {
+  public:
+    void reset(int64_t n) {
+        n_ = n;
+        words_.assign((size_t)((n + 63) / 64), ~0ull);
+        if (n % 64) words_.back() = (1ull << (n % 64)) - 1;
+        hint_ = 0;
+        free_ = n;
+    }
+    int64_t n_free() const { return free_; }
+    int64_t take() {  // caller checks n_free() > 0
+        for (size_t w = hint_; w < words_.size(); ++w) {
+            if (words_[w]) {
+                int b = __builtin_ctzll(words_[w]);
+                words_[w] &= words_[w] - 1;
+                hint_ = w;
+                --free_;
+                return (int64_t)w * 64 + b;
+            }
+        }
+        return -1;
+    }
+    void give(int64_t b) {
+        words_[(size_t)(b / 64)] |= 1ull << (b % 64);
+        hint_ = std::min(hint_, (size_t)(b / 64));
+        ++free_;
+    }
+    bool is_free(int64_t b) const { return (words_[(size_t)(b / 64)] >> (b % 64)) & 1; }
+
+  private:
+    std::vector<uint64_t> words_;
+    size_t hint_ = 0;
+    int64_t n_ = 0, free_ = 0;
+};
+
+struct EventPair {
+    hipEvent_t a, b;
+};
+
+}  // namespace
+
+struct mtn_pool {
+    mtn_pool_config cfg;
+    bool host_only = false;
+    bool unbounded = false;
+    int S = 0, W = -1, R = 0, nsb = 0, row_len = 0, G = 1;
+    size_t elt = 4;
+    int64_t tile_bytes = 0, head_stride = 0, block_stride = 0, layer_stride = 0;
+    float scale = 1.f;
+    uint8_t *kv = nullptr;
+
+    // host state
+    std::vector<int32_t> table;   // [max_sessions][row_len]
+    std::vector<uint8_t> is_open;
+    std::vector<int64_t> len;
+    std::vector<int32_t> n_assigned;
+    BlockAllocator alloc;
+    int64_t assigned = 0, reserved = 0;
+    int32_t n_open = 0;
+
+    // open plan
+    bool plan_open = false;
+    void *plan_stream = nullptr;
+    int32_t n_seq = 0, T = 0, max_ntok = 0;
+    bool all_single = false;
+    std::vector<int32_t> seq_sid, seq_ntok, seq_first;
+    std::vector<int64_t> seq_pos0;
+    std::vector<int32_t> tok_sid, tok_pos, tok_row, tok_block, tok_off;
+    std::vector<int32_t> upd_idx, upd_val;
+    std::vector<uint8_t> layer_done;
+
+    // device
+    int32_t max_tok = 0;           // capacity of one plan in tokens
+    int32_t *d_table = nullptr;
+    int32_t *d_meta = nullptr;     // packed plan metadata
+    float2 *d_rope = nullptr;      // [max_tok][D/2]
+    double *d_inv_freq = nullptr;  // [D/2]
+    float *d_part = nullptr;       // decode split partials
+    size_t part_floats = 0;
+    int32_t *h_stage[kStages] = {};
+    hipEvent_t stage_ev[kStages] = {};
+    bool stage_used[kStages] = {};
+    int stage_i = 0;
+    PlanView view{};
+    int32_t *d_seq_first = nullptr, *d_seq_ntok = nullptr;
+
+    // timing
+    bool timing = false;
+    std::vector<EventPair> ev_open[4];
+    std::vector<hipEvent_t> ev_spare;
+    int64_t t_launch[4] = {};
+    double t_ms[4] = {};
+
+    std::string last_error;
+};
+
+namespace {
+
+mtn_status fail(mtn_pool *p, mtn_status s, const char *msg) {
+    if (p) p->last_error = msg;
+    return s;
+}
+
+mtn_status hip_fail(mtn_pool *p, hipError_t e, const char *where) {
+    if (p) {
+        p->last_error = std::string(where) + ": " + hipGetErrorString(e);
+    }
+    return MTN_ERR_DEVICE;
+}
+
+#define HIP_TRY(p, expr)                                            \
+    do {                                                            \
+        hipError_t e_ = (expr);                                     \
+        if (e_ != hipSuccess) return hip_fail((p), e_, #expr);      \
+    } while (0)
+
+int64_t ceil_div(int64_t a, int64_t b) { return (a + b - 1) / b; }
+
+mtn_status validate(const mtn_pool_config *c) {
+    if (!c) return MTN_ERR_INVALID_ARG;
+    if (c->n_layers < 1 || c->n_q_heads < 1 || c->n_kv_heads < 1) return MTN_ERR_INVALID_ARG;
+    if (c->n_q_heads % c->n_kv_heads) return MTN_ERR_INVALID_ARG;
+    if (c->n_q_heads / c->n_kv_heads > 8) return MTN_ERR_UNSUPPORTED;
+    if (c->head_dim != 64 && c->head_dim != 128) return MTN_ERR_UNSUPPORTED;
+    if (c->block_size != kBlock) return MTN_ERR_UNSUPPORTED;
+    if (c->max_chunk < 1 || c->max_sessions < 1 || c->n_blocks < 1) return MTN_ERR_INVALID_ARG;
+    if (c->window == MTN_WINDOW_UNBOUNDED) {
+        if (c->max_len < 1) return MTN_ERR_INVALID_ARG;
+    } else {
+        if (c->window < 1 || c->n_sink < 0) return MTN_ERR_INVALID_ARG;
+        if ((int64_t)c->window + c->max_chunk + c->n_sink > (int64_t)1 << 30)
+            return MTN_ERR_INVALID_ARG;
+    }
+    if (c->kv_dtype != MTN_F32 && c->kv_dtype != MTN_BF16) return MTN_ERR_INVALID_ARG;
+    if (c->io_dtype != c->kv_dtype) return MTN_ERR_UNSUPPORTED;
+    if (!(c->rope_theta > 1.0)) return MTN_ERR_INVALID_ARG;
+    if (c->softmax_scale < 0.f || !std::isfinite(c->softmax_scale)) return MTN_ERR_INVALID_ARG;
+    if ((int64_t)c->max_sessions * c->max_chunk > (int64_t)1 << 24) return MTN_ERR_INVALID_ARG;
+    if (c->flags & ~MTN_POOL_HOST_ONLY) return MTN_ERR_INVALID_ARG;
+    return MTN_OK;
+}
+
+// Logical (block index in the session row, offset) of absolute position p.
+inline void logical_slot(const mtn_pool *P, int64_t p, int32_t *lb, int32_t *off) {
+    if (p < P->S) {
+        *lb = (int32_t)(p / kBlock);
+        *off = (int32_t)(p % kBlock);
+        return;
+    }
+    int64_t sigma = P->unbounded ? p : (p - P->S) % P->R;
+    *lb = P->nsb + (int32_t)(sigma / kBlock);
+    *off = (int32_t)(sigma % kBlock);
+}
+
+// Number of not-yet-assigned logical blocks session `sid` touches when
+// growing from L to L + n tokens.
+int64_t new_blocks_needed(const mtn_pool *P, int32_t sid, int64_t L, int64_t n,
+                          std::vector<uint8_t> &seen) {
+    const int32_t *row = &P->table[(size_t)sid * P->row_len];
+    int64_t need = 0;
+    std::vector<int32_t> touched;
+    for (int64_t p = L; p < L + n; ++p) {
+        int32_t lb, off;
+        logical_slot(P, p, &lb, &off);
+        if (row[lb] < 0 && !seen[lb]) {
+            seen[lb] = 1;
+            touched.push_back(lb);
+            ++need;
+        }
+    }
+    for (int32_t lb : touched) seen[lb] = 0;
+    return need;
+}
+
+mtn_status timing_begin(mtn_pool *P, hipStream_t s, hipEvent_t *out) {
+    *out = nullptr;
+    if (!P->timing) return MTN_OK;
+    hipEvent_t e;
+    if (!P->ev_spare.empty()) {
+        e = P->ev_spare.back();
+        P->ev_spare.pop_back();
+    } else {
+        HIP_TRY(P, hipEventCreate(&e));
+    }
+    HIP_TRY(P, hipEventRecord(e, s));
+    *out = e;
+    return MTN_OK;
+}
+
+mtn_status timing_end(mtn_pool *P, int cls, hipEvent_t a, hipStream_t s) {
+    if (!P->timing || !a) return MTN_OK;
+    hipEvent_t e;
+    if (!P->ev_spare.empty()) {
+        e = P->ev_spare.back();
+        P->ev_spare.pop_back();
+    } else {
+        HIP_TRY(P, hipEventCreate(&e));
+    }
+    HIP_TRY(P, hipEventRecord(e, s));
+    P->ev_open[cls].push_back({a, e});
+    return MTN_OK;
+}
+
+// Internal plan begin.  rows == nullptr packs io rows in plan order.
+mtn_status plan_begin(mtn_pool *P, int32_t n_seq, const int32_t *sids, const int32_t *n_tok,
+                      const int32_t *rows, void *stream) {
+    if (P->plan_open) return fail(P, MTN_ERR_BAD_STATE, "a plan is already open");
+    if (n_seq < 1 || n_seq > P->cfg.max_sessions || !sids || !n_tok)
+        return fail(P, MTN_ERR_INVALID_ARG, "bad sequence count or null array");
+    // ---- validation: nothing changes before every check has passed
+    std::vector<uint8_t> seen((size_t)P->cfg.max_sessions, 0);
+    int64_t T = 0;
+    for (int32_t i = 0; i < n_seq; ++i) {
+        int32_t sid = sids[i];
+        if (sid < 0 || sid >= P->cfg.max_sessions || !P->is_open[sid])
+            return fail(P, MTN_ERR_BAD_SESSION, "session not open");
+        if (seen[sid]) return fail(P, MTN_ERR_INVALID_ARG, "duplicate session in plan");
+        seen[sid] = 1;
+        if (n_tok[i] < 1) return fail(P, MTN_ERR_INVALID_ARG, "n_tok < 1");
+        if (n_tok[i] > P->cfg.max_chunk)
+            return fail(P, MTN_ERR_CHUNK_TOO_LARGE, "n_tok > max_chunk");
+        if (P->unbounded && P->len[sid] + n_tok[i] > P->cfg.max_len)
+            return fail(P, MTN_ERR_SESSION_FULL, "session would pass max_len");
+        if (!P->unbounded && P->len[sid] + n_tok[i] > ((int64_t)1 << 31) - 1)
+            return fail(P, MTN_ERR_SESSION_FULL, "position overflow");
+        T += n_tok[i];
+    }
+    {
+        std::vector<uint8_t> lbseen((size_t)P->row_len, 0);
+        int64_t need = 0;
+        for (int32_t i = 0; i < n_seq; ++i)
+            need += new_blocks_needed(P, sids[i], P->len[sids[i]], n_tok[i], lbseen);
+        if (need > P->alloc.n_free()) return fail(P, MTN_ERR_POOL_EXHAUSTED, "pool exhausted");
+    }
+    int32_t *stage = nullptr;
+    if (!P->host_only) {
+        // wait until the staging buffer we are about to overwrite was consumed
+        int si = P->stage_i;
+        if (P->stage_used[si]) HIP_TRY(P, hipEventSynchronize(P->stage_ev[si]));
+        stage = P->h_stage[si];
+    }
+    // ---- assignment (lowest free first, plan order)
+    P->n_seq = n_seq;
+    P->T = (int32_t)T;
+    P->seq_sid.assign(sids, sids + n_seq);
+    P->seq_ntok.assign(n_tok, n_tok + n_seq);
+    P->seq_first.resize(n_seq);
+    P->seq_pos0.resize(n_seq);
+    P->tok_sid.resize(T);
+    P->tok_pos.resize(T);
+    P->tok_row.resize(T);
+    P->tok_block.resize(T);
+    P->tok_off.resize(T);
+    P->upd_idx.clear();
+    P->upd_val.clear();
+    P->max_ntok = 0;
+    int32_t t = 0;
+    for (int32_t i = 0; i < n_seq; ++i) {
+        int32_t sid = sids[i];
+        int32_t *row = &P->table[(size_t)sid * P->row_len];
+        P->seq_first[i] = t;
+        P->seq_pos0[i] = P->len[sid];
+        P->max_ntok = std::max(P->max_ntok, n_tok[i]);
+        for (int32_t j = 0; j < n_tok[i]; ++j, ++t) {
+            int64_t pos = P->len[sid] + j;
+            int32_t lb, off;
+            logical_slot(P, pos, &lb, &off);
+            if (row[lb] < 0) {
+                int64_t b = P->alloc.take();
+                row[lb] = (int32_t)b;
+                P->n_assigned[sid]++;
+                P->assigned++;
+                P->upd_idx.push_back(sid * P->row_len + lb);
+                P->upd_val.push_back((int32_t)b);
+            }
+            P->tok_sid[t] = sid;
+            P->tok_pos[t] = (int32_t)pos;
+            P->tok_row[t] = rows ? rows[i] : t;
+            P->tok_block[t] = row[lb];
+            P->tok_off[t] = off;
+        }
+    }
+    if (P->unbounded) P->reserved = P->assigned;
+    P->all_single = (P->max_ntok == 1);
+    P->layer_done.assign((size_t)P->cfg.n_layers, 0);
+    P->plan_open = true;
+    P->plan_stream = stream;
+    if (P->host_only) return MTN_OK;
+
+    // ---- upload: one packed blob, then the apply kernel (table + RoPE)
+    const int32_t U = (int32_t)P->upd_idx.size();
+    int32_t *h = stage;
+    size_t o = 0;
+    auto put = [&](const int32_t *src, int32_t n) {
+        std::memcpy(h + o, src, sizeof(int32_t) * (size_t)n);
+        o += (size_t)n;
+    };
+    put(P->tok_sid.data(), T);
+    put(P->tok_pos.data(), T);
+    put(P->tok_row.data(), T);
+    put(P->tok_block.data(), T);
+    put(P->tok_off.data(), T);
+    put(P->seq_first.data(), n_seq);
+    put(P->seq_ntok.data(), n_seq);
+    put(P->upd_idx.data(), U);
+    put(P->upd_val.data(), U);
+    hipStream_t s = (hipStream_t)stream;
+    int32_t *d = P->d_meta;
+    HIP_TRY(P, hipMemcpyAsync(d, h, o * sizeof(int32_t), hipMemcpyHostToDevice, s));
+    HIP_TRY(P, hipEventRecord(P->stage_ev[P->stage_i], s));
+    P->stage_used[P->stage_i] = true;
+    P->stage_i = (P->stage_i + 1) % kStages;
+    P->view.tok_sid = d;
+    P->view.tok_pos = d + T;
+    P->view.tok_row = d + 2 * T;
+    P->view.tok_block = d + 3 * T;
+    P->view.tok_off = d + 4 * T;
+    P->d_seq_first = d + 5 * T;
+    P->d_seq_ntok = d + 5 * T + n_seq;
+    P->view.rope = P->d_rope;
+    P->view.n_tok = (int32_t)T;
+    const int32_t *d_upd_idx = d + 5 * T + 2 * n_seq;
+    HIP_TRY(P, launch_plan_apply(d_upd_idx, d_upd_idx + U, U, P->d_table, P->view.tok_pos,
+                                 (int32_t)T, P->d_inv_freq, P->cfg.head_dim / 2, P->d_rope, s));
+    return MTN_OK;
+}
+
+mtn_status plan_commit(mtn_pool *P) {
+    if (!P->plan_open) return fail(P, MTN_ERR_BAD_STATE, "no open plan");
+    if (!P->host_only)
+        for (auto d : P->layer_done)
+            if (!d) return fail(P, MTN_ERR_BAD_STATE, "commit before every layer was appended");
+    for (int32_t i = 0; i < P->n_seq; ++i) P->len[P->seq_sid[i]] += P->seq_ntok[i];
+    P->plan_open = false;
+    return MTN_OK;
+}
+
+PoolGeom geom(const mtn_pool *P) {
+    PoolGeom g;
+    g.kv = P->kv;
+    g.layer_stride = P->layer_stride;
+    g.block_stride = P->block_stride;
+    g.head_stride = P->head_stride;
+    g.tile_bytes = P->tile_bytes;
+    g.table = P->d_table;
+    g.row_len = P->row_len;
+    g.n_sink = P->S;
+    g.window = P->W;
+    g.ring = P->R;
+    g.n_sink_blocks = P->nsb;
+    g.hq = P->cfg.n_q_heads;
+    g.hkv = P->cfg.n_kv_heads;
+    g.d = P->cfg.head_dim;
+    return g;
+}
+
+mtn_status check_call(mtn_pool *P, int32_t layer, void *stream) {
+    if (!P) return MTN_ERR_INVALID_ARG;
+    if (P->host_only) return fail(P, MTN_ERR_BAD_STATE, "host-only pool has no device path");
+    if (!P->plan_open) return fail(P, MTN_ERR_BAD_STATE, "no open plan");
+    if (stream != P->plan_stream) return fail(P, MTN_ERR_INVALID_ARG, "stream differs from plan's");
+    if (layer < 0 || layer >= P->cfg.n_layers) return fail(P, MTN_ERR_INVALID_ARG, "bad layer");
+    return MTN_OK;
+}
+
+mtn_status append_impl(mtn_pool *P, int32_t layer, const void *k, const void *v, void *stream) {
+    hipStream_t s = (hipStream_t)stream;
+    hipEvent_t e0;
+    mtn_status st = timing_begin(P, s, &e0);
+    if (st) return st;
+    HIP_TRY(P, launch_append(P->cfg.kv_dtype, geom(P), P->view, layer, k, v, s));
+    st = timing_end(P, 0, e0, s);
+    if (st) return st;
+    P->layer_done[layer] = 1;
+    return MTN_OK;
+}
+
+AttnArgs attn_args(mtn_pool *P, int32_t layer, const void *q, void *out, float *lse,
+                   int32_t n_split) {
+    AttnArgs a;
+    a.g = geom(P);
+    a.p = P->view;
+    a.layer = layer;
+    a.q = q;
+    a.out = out;
+    a.lse = lse;
+    a.part = P->d_part;
+    a.n_split = n_split;
+    a.scale_log2 = P->scale * 1.4426950408889634f;
+    return a;
+}
+
+// Decode split heuristic: enough wave-level work units to fill the chip
+// several times over, without splitting short windows into tiny segments.
+int32_t auto_split(const mtn_pool *P, int32_t n_items) {
+    int64_t units = (int64_t)n_items * P->cfg.n_kv_heads;
+    int64_t max_keys = P->unbounded ? P->cfg.max_len : (int64_t)P->S + P->W;
+    int64_t blocks = ceil_div(max_keys, kBlock) + 1;
+    int64_t target = 4096;  // waves: 256 CUs x 16
+    int64_t sp = ceil_div(target, std::max<int64_t>(units, 1));
+    sp = std::min<int64_t>(sp, std::max<int64_t>(1, blocks / 8));
+    sp = std::max<int64_t>(1, std::min<int64_t>(sp, kMaxSplit));
+    return (int32_t)sp;
+}
+
+mtn_status decode_impl(mtn_pool *P, int32_t layer, const void *q, void *out, float *lse,
+                       int32_t n_split, void *stream) {
+    hipStream_t s = (hipStream_t)stream;
+    if (n_split == 0) n_split = auto_split(P, P->T);
+    int64_t need = (int64_t)P->T * P->cfg.n_q_heads * n_split * (P->cfg.head_dim + 2);
+    if (n_split > 1 && (size_t)need > P->part_floats) {
+        // fall back to the largest split the workspace holds
+        n_split = (int32_t)std::max<int64_t>(
+            1, (int64_t)P->part_floats /
+                   ((int64_t)P->T * P->cfg.n_q_heads * (P->cfg.head_dim + 2)));
+        n_split = std::min(n_split, kMaxSplit);
+    }
+    AttnArgs a = attn_args(P, layer, q, out, lse, n_split);
+    hipEvent_t e0;
+    mtn_status st = timing_begin(P, s, &e0);
+    if (st) return st;
+    HIP_TRY(P, launch_attn_valu(P->cfg.kv_dtype, a, s));
+    st = timing_end(P, 2, e0, s);
+    if (st) return st;
+    if (n_split > 1) {
+        st = timing_begin(P, s, &e0);
+        if (st) return st;
+        HIP_TRY(P, launch_merge(P->cfg.kv_dtype, a, s));
+        st = timing_end(P, 3, e0, s);
+        if (st) return st;
+    }
+    return MTN_OK;
+}
+
+mtn_status prefill_impl(mtn_pool *P, int32_t layer, const void *q, void *out, float *lse,
+                        void *stream) {
+    hipStream_t s = (hipStream_t)stream;
+    if (P->all_single) return decode_impl(P, layer, q, out, lse, 0, stream);
+    AttnArgs a = attn_args(P, layer, q, out, lse, 1);
+    hipEvent_t e0;
+    mtn_status st = timing_begin(P, s, &e0);
+    if (st) return st;
+    if (prefill_mfma_supported(P->cfg.kv_dtype, P->cfg.head_dim, P->G)) {
+        HIP_TRY(P, launch_prefill_mfma(a, P->max_ntok * P->G, P->d_seq_first, P->d_seq_ntok,
+                                       P->n_seq, s));
+    } else {
+        HIP_TRY(P, launch_attn_valu(P->cfg.kv_dtype, a, s));
+    }
+    return timing_end(P, 1, e0, s);
+}
+
+}  // namespace
+
+extern "C" {
+
+const char *mtn_status_string(mtn_status s) {
+    switch (s) {
+        case MTN_OK: return "ok";
+        case MTN_ERR_INVALID_ARG: return "invalid argument";
+        case MTN_ERR_BAD_SESSION: return "bad session id";
+        case MTN_ERR_CHUNK_TOO_LARGE: return "chunk larger than max_chunk";
+        case MTN_ERR_NO_SESSION_SLOT: return "no free session slot";
+        case MTN_ERR_POOL_EXHAUSTED: return "KV pool exhausted";
+        case MTN_ERR_SESSION_FULL: return "session at max_len";
+        case MTN_ERR_DEVICE: return "device error";
+        case MTN_ERR_BAD_STATE: return "call out of order";
+        case MTN_ERR_UNSUPPORTED: return "unsupported shape or dtype";
+        default: return "unknown status";
+    }
+}
+
+const char *mtn_pool_last_error(const mtn_pool *pool) {
+    return pool ? pool->last_error.c_str() : "";
+}
+
+mtn_status mtn_pool_required_bytes(const mtn_pool_config *cfg, size_t *kv_bytes) {
+    mtn_status st = validate(cfg);
+    if (st) return st;
+    if (!kv_bytes) return MTN_ERR_INVALID_ARG;
+    size_t e = cfg->kv_dtype == MTN_BF16 ? 2 : 4;
+    size_t per_block = (size_t)cfg->n_kv_heads * 2 * kBlock * cfg->head_dim * e;
+    *kv_bytes = per_block * (size_t)cfg->n_blocks * (size_t)cfg->n_layers;
+    return MTN_OK;
+}
+
+mtn_status mtn_pool_create(const mtn_pool_config *cfg, void *kv_dev, size_t kv_bytes,
+                           void *stream, mtn_pool **out) {
+    if (!out) return MTN_ERR_INVALID_ARG;
+    size_t need;
+    mtn_status st = mtn_pool_required_bytes(cfg, &need);
+    if (st) return st;
+    bool host_only = cfg->flags & MTN_POOL_HOST_ONLY;
+    if (!host_only) {
+        if (!kv_dev || kv_bytes < need || ((uintptr_t)kv_dev & 255)) return MTN_ERR_INVALID_ARG;
+        if (!attn_valu_supported(cfg->kv_dtype, cfg->head_dim, cfg->n_q_heads / cfg->n_kv_heads))
+            return MTN_ERR_UNSUPPORTED;
+    }
+    mtn_pool *P = new mtn_pool();
+    P->cfg = *cfg;
+    P->host_only = host_only;
+    P->unbounded = cfg->window == MTN_WINDOW_UNBOUNDED;
+    P->G = cfg->n_q_heads / cfg->n_kv_heads;
+    P->elt = cfg->kv_dtype == MTN_BF16 ? 2 : 4;
+    if (P->unbounded) {
+        P->S = 0;
+        P->W = -1;
+        P->nsb = 0;
+        P->R = (int32_t)(ceil_div(cfg->max_len, kBlock) * kBlock);
+    } else {
+        P->S = cfg->n_sink;
+        P->W = cfg->window;
+        P->nsb = (int32_t)ceil_div(cfg->n_sink, kBlock);
+        P->R = (int32_t)(ceil_div((int64_t)cfg->window + cfg->max_chunk - 1, kBlock) * kBlock);
+    }
+    P->row_len = P->nsb + P->R / kBlock;
+    P->tile_bytes = (int64_t)kBlock * cfg->head_dim * (int64_t)P->elt;
+    P->head_stride = 2 * P->tile_bytes;
+    P->block_stride = P->head_stride * cfg->n_kv_heads;
+    P->layer_stride = P->block_stride * cfg->n_blocks;
+    P->scale = cfg->softmax_scale > 0.f ? cfg->softmax_scale
+                                        : (float)(1.0 / std::sqrt((double)cfg->head_dim));
+    P->kv = (uint8_t *)kv_dev;
+    P->table.assign((size_t)cfg->max_sessions * P->row_len, -1);
+    P->is_open.assign((size_t)cfg->max_sessions, 0);
+    P->len.assign((size_t)cfg->max_sessions, 0);
+    P->n_assigned.assign((size_t)cfg->max_sessions, 0);
+    P->alloc.reset(cfg->n_blocks);
+    P->max_tok = cfg->max_sessions * cfg->max_chunk;
+    if (!host_only) {
+        auto bail = [&](hipError_t e, const char *w) {
+            mtn_pool_destroy(P);
+            (void)e;
+            (void)w;
+            return MTN_ERR_DEVICE;
+        };
+        hipError_t e;
+        size_t tbl = sizeof(int32_t) * P->table.size();
+        if ((e = hipMalloc(&P->d_table, tbl)) != hipSuccess) return bail(e, "table");
+        if ((e = hipMemcpyAsync(P->d_table, P->table.data(), tbl, hipMemcpyHostToDevice,
+                                (hipStream_t)stream)) != hipSuccess)
+            return bail(e, "table upload");
+        size_t meta = sizeof(int32_t) * ((size_t)P->max_tok * 7 + 2 * (size_t)cfg->max_sessions + 64);
+        if ((e = hipMalloc(&P->d_meta, meta)) != hipSuccess) return bail(e, "meta");
+        for (int i = 0; i < kStages; ++i) {
+            if ((e = hipHostMalloc(&P->h_stage[i], meta, hipHostMallocDefault)) != hipSuccess)
+                return bail(e, "stage");
+            if ((e = hipEventCreateWithFlags(&P->stage_ev[i], hipEventDisableTiming)) != hipSuccess)
+                return bail(e, "event");
+        }
+        size_t half = (size_t)cfg->head_dim / 2;
+        if ((e = hipMalloc(&P->d_rope, sizeof(float2) * half * (size_t)P->max_tok)) != hipSuccess)
+            return bail(e, "rope");
+        std::vector<double> inv(half);
+        for (size_t i = 0; i < half; ++i)
+            inv[i] = std::pow(cfg->rope_theta, -2.0 * (double)i / (double)cfg->head_dim);
+        if ((e = hipMalloc(&P->d_inv_freq, sizeof(double) * half)) != hipSuccess)
+            return bail(e, "inv_freq");
+        if ((e = hipMemcpy(P->d_inv_freq, inv.data(), sizeof(double) * half,
+                           hipMemcpyHostToDevice)) != hipSuccess)
+            return bail(e, "inv_freq upload");
+        P->part_floats = (size_t)cfg->max_sessions * cfg->n_q_heads * 32 * (cfg->head_dim + 2);
+        if ((e = hipMalloc(&P->d_part, sizeof(float) * P->part_floats)) != hipSuccess)
+            return bail(e, "partials");
+        if ((e = hipStreamSynchronize((hipStream_t)stream)) != hipSuccess)
+            return bail(e, "sync");
+    }
+    *out = P;
+    return MTN_OK;
+}
+
+void mtn_pool_destroy(mtn_pool *P) {
+    if (!P) return;
+    if (!P->host_only) {
+        (void)hipDeviceSynchronize();
+        (void)hipFree(P->d_table);
+        (void)hipFree(P->d_meta);
+        (void)hipFree(P->d_rope);
+        (void)hipFree(P->d_inv_freq);
+        (void)hipFree(P->d_part);
+        for (int i = 0; i < kStages; ++i) {
+            if (P->h_stage[i]) (void)hipHostFree(P->h_stage[i]);
+            if (P->stage_ev[i]) (void)hipEventDestroy(P->stage_ev[i]);
+        }
+        for (auto &v : P->ev_open)
+            for (auto &pr : v) {
+                (void)hipEventDestroy(pr.a);
+                (void)hipEventDestroy(pr.b);
+            }
+        for (auto e : P->ev_spare) (void)hipEventDestroy(e);
+    }
+    delete P;
+}
+
+mtn_status mtn_session_open(mtn_pool *P, int32_t *sid_out) {
+    if (!P || !sid_out) return MTN_ERR_INVALID_ARG;
+    int32_t sid = -1;
+    for (int32_t i = 0; i < P->cfg.max_sessions; ++i)
+        if (!P->is_open[i]) {
+            sid = i;
+            break;
+        }
+    if (sid < 0) return fail(P, MTN_ERR_NO_SESSION_SLOT, "no free session slot");
+    if (!P->unbounded) {
+        if (P->reserved + P->row_len > P->cfg.n_blocks)
+            return fail(P, MTN_ERR_POOL_EXHAUSTED, "reservation exceeds pool capacity");
+        P->reserved += P->row_len;
+    }
+    P->is_open[sid] = 1;
+    P->len[sid] = 0;
+    P->n_assigned[sid] = 0;
+    P->n_open++;
+    *sid_out = sid;
+    return MTN_OK;
+}
+
+mtn_status mtn_session_close(mtn_pool *P, int32_t sid) {
+    if (!P) return MTN_ERR_INVALID_ARG;
+    if (P->plan_open) return fail(P, MTN_ERR_BAD_STATE, "plan open");
+    if (sid < 0 || sid >= P->cfg.max_sessions || !P->is_open[sid])
+        return fail(P, MTN_ERR_BAD_SESSION, "session not open");
+    int32_t *row = &P->table[(size_t)sid * P->row_len];
+    for (int32_t j = 0; j < P->row_len; ++j) {
+        if (row[j] >= 0) {
+            P->alloc.give(row[j]);
+            P->assigned--;
+            row[j] = -1;
+        }
+    }
+    if (!P->unbounded) P->reserved -= P->row_len;
+    else P->reserved = P->assigned;
+    P->is_open[sid] = 0;
+    P->len[sid] = 0;
+    P->n_assigned[sid] = 0;
+    P->n_open--;
+    // The device copy of the row is left as is: kernels still in flight may
+    // read it, and a reopened session only ever reads logical blocks that its
+    // own plans assigned (and uploaded, in stream order) again.
+    return MTN_OK;
+}
+
+mtn_status mtn_plan_begin(mtn_pool *P, int32_t n_seq, const int32_t *sids, const int32_t *n_tok,
+                          void *stream) {
+    if (!P) return MTN_ERR_INVALID_ARG;
+    return plan_begin(P, n_seq, sids, n_tok, nullptr, stream);
+}
+
+mtn_status mtn_plan_commit(mtn_pool *P) {
+    if (!P) return MTN_ERR_INVALID_ARG;
+    return plan_commit(P);
+}
+
+mtn_status mtn_frame_append_kv(mtn_pool *P, int32_t layer, const void *k, const void *v,
+                               void *stream) {
+    mtn_status st = check_call(P, layer, stream);
+    if (st) return st;
+    if (!k || !v) return fail(P, MTN_ERR_INVALID_ARG, "null k or v");
+    return append_impl(P, layer, k, v, stream);
+}
+
+mtn_status mtn_attend_chunk_prefill(mtn_pool *P, int32_t layer, const void *q, void *out,
+                                    float *lse, void *stream) {
+    mtn_status st = check_call(P, layer, stream);
+    if (st) return st;
+    if (!q || !out) return fail(P, MTN_ERR_INVALID_ARG, "null q or out");
+    if (!P->layer_done[layer]) return fail(P, MTN_ERR_BAD_STATE, "layer not appended");
+    return prefill_impl(P, layer, q, out, lse, stream);
+}
+
+mtn_status mtn_attend_decode(mtn_pool *P, int32_t layer, const void *q, void *out, float *lse,
+                             int32_t n_split, void *stream) {
+    mtn_status st = check_call(P, layer, stream);
+    if (st) return st;
+    if (!q || !out) return fail(P, MTN_ERR_INVALID_ARG, "null q or out");
+    if (!P->all_single) return fail(P, MTN_ERR_BAD_STATE, "decode needs n_tok == 1 everywhere");
+    if (n_split < 0 || n_split > kMaxSplit) return fail(P, MTN_ERR_INVALID_ARG, "bad n_split");
+    if (!P->layer_done[layer]) return fail(P, MTN_ERR_BAD_STATE, "layer not appended");
+    return decode_impl(P, layer, q, out, lse, n_split, stream);
+}
+
+mtn_status mtn_frame_step(mtn_pool *P, const mtn_frame_batch *b, void *stream) {
+    if (!P || !b) return MTN_ERR_INVALID_ARG;
+    if (P->host_only) return fail(P, MTN_ERR_BAD_STATE, "host-only pool has no device path");
+    if (P->plan_open) return fail(P, MTN_ERR_BAD_STATE, "a plan is already open");
+    const int32_t n = b->n_seq;
+    if (n < 1 || n > P->cfg.max_sessions || !b->sids || !b->chunk_len || !b->n_decode)
+        return fail(P, MTN_ERR_INVALID_ARG, "bad batch");
+    if (!b->q_chunk || !b->k_chunk || !b->v_chunk || !b->out_chunk)
+        return fail(P, MTN_ERR_INVALID_ARG, "null chunk buffer");
+    if (b->n_split < 0 || b->n_split > kMaxSplit) return fail(P, MTN_ERR_INVALID_ARG, "bad n_split");
+    int32_t max_dec = 0;
+    int64_t Tc = 0;
+    std::vector<uint8_t> seen((size_t)P->cfg.max_sessions, 0);
+    for (int32_t i = 0; i < n; ++i) {
+        int32_t sid = b->sids[i];
+        if (sid < 0 || sid >= P->cfg.max_sessions || !P->is_open[sid])
+            return fail(P, MTN_ERR_BAD_SESSION, "session not open");
+        if (seen[sid]) return fail(P, MTN_ERR_INVALID_ARG, "duplicate session in batch");
+        seen[sid] = 1;
+        if (b->chunk_len[i] < 1) return fail(P, MTN_ERR_INVALID_ARG, "chunk_len < 1");
+        if (b->chunk_len[i] > P->cfg.max_chunk)
+            return fail(P, MTN_ERR_CHUNK_TOO_LARGE, "chunk_len > max_chunk");
+        if (b->n_decode[i] < 0) return fail(P, MTN_ERR_INVALID_ARG, "n_decode < 0");
+        if (P->unbounded && P->len[sid] + b->chunk_len[i] + b->n_decode[i] > P->cfg.max_len)
+            return fail(P, MTN_ERR_SESSION_FULL, "frame would pass max_len");
+        max_dec = std::max(max_dec, b->n_decode[i]);
+        Tc += b->chunk_len[i];
+    }
+    if (max_dec > 0 && (!b->q_dec || !b->k_dec || !b->v_dec || !b->out_dec))
+        return fail(P, MTN_ERR_INVALID_ARG, "null decode buffer");
+    {   // whole-frame capacity check before any launch
+        std::vector<uint8_t> lbseen((size_t)P->row_len, 0);
+        int64_t need = 0;
+        for (int32_t i = 0; i < n; ++i)
+            need += new_blocks_needed(P, b->sids[i], P->len[b->sids[i]],
+                                      (int64_t)b->chunk_len[i] + b->n_decode[i], lbseen);
+        if (need > P->alloc.n_free()) return fail(P, MTN_ERR_POOL_EXHAUSTED, "pool exhausted");
+    }
+    const int32_t L = P->cfg.n_layers, Hq = P->cfg.n_q_heads, Hkv = P->cfg.n_kv_heads;
+    const size_t e = P->elt, D = (size_t)P->cfg.head_dim;
+    auto off = [&](const void *base, size_t elems) {
+        return (const void *)((const uint8_t *)base + elems * e);
+    };
+    mtn_status st = plan_begin(P, n, b->sids, b->chunk_len, nullptr, stream);
+    if (st) return st;
+    for (int32_t l = 0; l < L; ++l) {
+        size_t rq = (size_t)l * Tc * Hq * D, rk = (size_t)l * Tc * Hkv * D;
+        st = append_impl(P, l, off(b->k_chunk, rk), off(b->v_chunk, rk), stream);
+        if (st) return st;
+        float *lse = b->lse_chunk ? b->lse_chunk + (size_t)l * Tc * Hq : nullptr;
+        if (P->all_single)
+            st = decode_impl(P, l, off(b->q_chunk, rq), (void *)off(b->out_chunk, rq), lse,
+                             b->n_split, stream);
+        else
+            st = prefill_impl(P, l, off(b->q_chunk, rq), (void *)off(b->out_chunk, rq), lse,
+                              stream);
+        if (st) return st;
+    }
+    st = plan_commit(P);
+    if (st) return st;
+    std::vector<int32_t> sids, ones, rows;
+    for (int32_t j = 0; j < max_dec; ++j) {
+        sids.clear();
+        rows.clear();
+        for (int32_t i = 0; i < n; ++i)
+            if (b->n_decode[i] > j) {
+                sids.push_back(b->sids[i]);
+                rows.push_back(i);
+            }
+        ones.assign(sids.size(), 1);
+        st = plan_begin(P, (int32_t)sids.size(), sids.data(), ones.data(), rows.data(), stream);
+        if (st) return st;
+        for (int32_t l = 0; l < L; ++l) {
+            size_t base = ((size_t)j * L + l) * n;
+            st = append_impl(P, l, off(b->k_dec, base * Hkv * D), off(b->v_dec, base * Hkv * D),
+                             stream);
+            if (st) return st;
+            float *lse = b->lse_dec ? b->lse_dec + base * Hq : nullptr;
+            st = decode_impl(P, l, off(b->q_dec, base * Hq * D),
+                             (void *)off(b->out_dec, base * Hq * D), lse, b->n_split, stream);
+            if (st) return st;
+        }
+        st = plan_commit(P);
+        if (st) return st;
+    }
+    return MTN_OK;
+}
+
+mtn_status mtn_pool_stats(const mtn_pool *P, mtn_pool_stats_t *out) {
+    if (!P || !out) return MTN_ERR_INVALID_ARG;
+    out->capacity = P->cfg.n_blocks;
+    out->assigned = P->assigned;
+    out->reserved = P->unbounded ? P->assigned : P->reserved;
+    out->open_sessions = P->n_open;
+    out->blocks_per_session = P->row_len;
+    out->ring_tokens = P->R;
+    out->sink_blocks = P->nsb;
+    return MTN_OK;
+}
+
+mtn_status mtn_session_info(const mtn_pool *P, int32_t sid, int64_t *len, int32_t *n_assigned) {
+    if (!P) return MTN_ERR_INVALID_ARG;
+    if (sid < 0 || sid >= P->cfg.max_sessions || !P->is_open[sid]) return MTN_ERR_BAD_SESSION;
+    if (len) *len = P->len[sid];
+    if (n_assigned) *n_assigned = P->n_assigned[sid];
+    return MTN_OK;
+}
+
+mtn_status mtn_session_block_table(const mtn_pool *P, int32_t sid, int32_t *out, int32_t cap,
+                                   int32_t *n_out) {
+    if (!P || !out) return MTN_ERR_INVALID_ARG;
+    if (sid < 0 || sid >= P->cfg.max_sessions || !P->is_open[sid]) return MTN_ERR_BAD_SESSION;
+    if (cap < P->row_len) return MTN_ERR_INVALID_ARG;
+    std::memcpy(out, &P->table[(size_t)sid * P->row_len], sizeof(int32_t) * P->row_len);
+    if (n_out) *n_out = P->row_len;
+    return MTN_OK;
+}
+
+mtn_status mtn_plan_info(const mtn_pool *P, int64_t *pos, int32_t *block, int32_t *offset,
+                         int32_t cap, int64_t *ev_lo, int64_t *ev_hi, int32_t *n_tok_out) {
+    if (!P) return MTN_ERR_INVALID_ARG;
+    if (!P->plan_open) return MTN_ERR_BAD_STATE;
+    if ((pos || block || offset) && cap < P->T) return MTN_ERR_INVALID_ARG;
+    if ((ev_lo || ev_hi) && cap < P->n_seq) return MTN_ERR_INVALID_ARG;
+    for (int32_t t = 0; t < P->T; ++t) {
+        if (pos) pos[t] = P->tok_pos[t];
+        if (block) block[t] = P->tok_block[t];
+        if (offset) offset[t] = P->tok_off[t];
+    }
+    for (int32_t i = 0; i < P->n_seq; ++i) {
+        int64_t lo = 0, hi = 0;
+        if (!P->unbounded) {
+            int64_t L0 = P->seq_pos0[i];
+            lo = std::max<int64_t>(P->S, L0 - P->W);
+            hi = std::max<int64_t>(lo, L0 + P->seq_ntok[i] - P->W);
+        }
+        if (ev_lo) ev_lo[i] = lo;
+        if (ev_hi) ev_hi[i] = hi;
+    }
+    if (n_tok_out) *n_tok_out = P->T;
+    return MTN_OK;
+}
+
+mtn_status mtn_debug_poison_dead(mtn_pool *P, void *stream) {
+    if (!P) return MTN_ERR_INVALID_ARG;
+    if (P->host_only) return fail(P, MTN_ERR_BAD_STATE, "host-only pool has no device path");
+    if (P->plan_open) return fail(P, MTN_ERR_BAD_STATE, "plan open");
+    // live[b] bit o set <=> slot o of block b holds a retained position
+    std::vector<uint16_t> live((size_t)P->cfg.n_blocks, 0);
+    for (int32_t sid = 0; sid < P->cfg.max_sessions; ++sid) {
+        if (!P->is_open[sid]) continue;
+        const int32_t *row = &P->table[(size_t)sid * P->row_len];
+        int64_t L = P->len[sid];
+        int64_t lo = P->unbounded ? 0 : std::max<int64_t>(P->S, L - P->W);
+        auto mark = [&](int64_t p) {
+            int32_t lb, off;
+            logical_slot(P, p, &lb, &off);
+            if (row[lb] >= 0) live[(size_t)row[lb]] |= (uint16_t)(1u << off);
+        };
+        for (int64_t p = 0; p < std::min<int64_t>(P->S, L); ++p) mark(p);
+        for (int64_t p = lo; p < L; ++p) mark(p);
+    }
+    hipStream_t s = (hipStream_t)stream;
+    uint16_t *d_live = nullptr;
+    HIP_TRY(P, hipMalloc(&d_live, sizeof(uint16_t) * live.size()));
+    HIP_TRY(P, hipMemcpy(d_live, live.data(), sizeof(uint16_t) * live.size(),
+                         hipMemcpyHostToDevice));
+    HIP_TRY(P, launch_poison(P->cfg.kv_dtype, geom(P), P->cfg.n_layers, P->cfg.n_blocks, d_live, s));
+    HIP_TRY(P, hipStreamSynchronize(s));
+    HIP_TRY(P, hipFree(d_live));
+    return MTN_OK;
+}
+
+mtn_status mtn_pool_set_timing(mtn_pool *P, int32_t enable) {
+    if (!P) return MTN_ERR_INVALID_ARG;
+    P->timing = enable != 0;
+    return MTN_OK;
+}
+
+mtn_status mtn_pool_kernel_times(mtn_pool *P, int64_t *launches, double *ms) {
+    if (!P || !launches || !ms) return MTN_ERR_INVALID_ARG;
+    for (int c = 0; c < 4; ++c) {
+        for (auto &pr : P->ev_open[c]) {
+            HIP_TRY(P, hipEventSynchronize(pr.b));
+            float t = 0.f;
+            HIP_TRY(P, hipEventElapsedTime(&t, pr.a, pr.b));
+            P->t_ms[c] += t;
+            P->t_launch[c]++;
+            P->ev_spare.push_back(pr.a);
+            P->ev_spare.push_back(pr.b);
+        }
+        P->ev_open[c].clear();
+        launches[c] = P->t_launch[c];
+        ms[c] = P->t_ms[c];
+        P->t_launch[c] = 0;
+        P->t_ms[c] = 0.0;
+    }
+    return MTN_OK;
+}
+
+mtn_status mtn_hbm_copy(const void *src, void *dst, size_t bytes, void *stream) {
+    if (!src || !dst || (bytes % 16) || ((uintptr_t)src % 16) || ((uintptr_t)dst % 16))
+        return MTN_ERR_INVALID_ARG;
+    hipError_t e = launch_copy(src, dst, bytes, (hipStream_t)stream);
+    return e == hipSuccess ? MTN_OK : MTN_ERR_DEVICE;
+}
+
+}  // extern "C"

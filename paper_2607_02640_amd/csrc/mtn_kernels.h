@@ -1,0 +1,79 @@
+// Internal launch interface between the host library (mtn_host.cpp) and the
+// gfx950 kernels (mtn_kernels.hip).  Not part of the public C ABI.
+#pragma once
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace mtn {
+
+// Geometry of the paged pool as the kernels see it.  Byte strides; the pool
+// layout is [layer][block][kv_head]{K tile [16][D], V^T tile [D][16]}.
+struct PoolGeom {
+    const uint8_t *kv;       // pool base (device)
+    int64_t layer_stride;    // bytes per layer
+    int64_t block_stride;    // bytes per (layer, block)
+    int64_t head_stride;     // bytes per (layer, block, kv head) = 2 tiles
+    int64_t tile_bytes;      // bytes of one K (or V^T) tile
+    const int32_t *table;    // [max_sessions][row_len] physical block ids
+    int32_t row_len;
+    int32_t n_sink;          // S (0 when unbounded)
+    int32_t window;          // W, or -1 when unbounded
+    int32_t ring;            // R tokens (unbounded: row_len * 16)
+    int32_t n_sink_blocks;   // ceil(S / 16)
+    int32_t hq, hkv, d;
+};
+
+// One planned token: which session, absolute position, io row, slot.
+struct PlanView {
+    const int32_t *tok_sid;
+    const int32_t *tok_pos;
+    const int32_t *tok_row;
+    const int32_t *tok_block;
+    const int32_t *tok_off;
+    const float2  *rope;     // [T][D/2] (cos, sin) of pos * theta^(-2i/D)
+    int32_t n_tok;
+};
+
+struct AttnArgs {
+    PoolGeom g;
+    PlanView p;
+    int32_t layer;
+    const void *q;           // [rows][Hq][D], row = tok_row[t]
+    void *out;               // [rows][Hq][D]
+    float *lse;              // [rows][Hq] or null
+    float *part;             // split partials (acc [unit][G][D] then ml [unit][G][2])
+    int32_t n_split;
+    float scale_log2;        // softmax scale * log2(e)
+};
+
+// dtype codes match the public MTN_F32 / MTN_BF16
+hipError_t launch_plan_apply(const int32_t *upd_idx, const int32_t *upd_val, int32_t n_upd,
+                             int32_t *table, const int32_t *tok_pos, int32_t n_tok,
+                             const double *inv_freq, int32_t half_d, float2 *rope,
+                             hipStream_t s);
+
+hipError_t launch_append(int dtype, const PoolGeom &g, const PlanView &p, int32_t layer,
+                         const void *k, const void *v, hipStream_t s);
+
+// Vector (VALU) attention over items = planned tokens: decode, and the fp32
+// chunk prefill.  Returns hipErrorInvalidValue for shapes with no instance.
+hipError_t launch_attn_valu(int dtype, const AttnArgs &a, hipStream_t s);
+hipError_t launch_merge(int dtype, const AttnArgs &a, hipStream_t s);
+
+// MFMA chunk-prefill attention (bf16, D = 128).
+hipError_t launch_prefill_mfma(const AttnArgs &a, int32_t max_rows_per_seq,
+                               const int32_t *seq_first_tok, const int32_t *seq_ntok,
+                               int32_t n_seq, hipStream_t s);
+
+hipError_t launch_poison(int dtype, const PoolGeom &g, int32_t n_layers, int64_t n_blocks,
+                         const uint16_t *live_mask, hipStream_t s);
+
+hipError_t launch_copy(const void *src, void *dst, size_t bytes, hipStream_t s);
+
+bool attn_valu_supported(int dtype, int d, int g);
+bool prefill_mfma_supported(int dtype, int d, int g);
+
+constexpr int kBlock = 16;      // tokens per KV block
+constexpr int kMaxSplit = 64;   // decode split cap
+
+}  // namespace mtn

@@ -1,0 +1,624 @@
+// gfx950 (CDNA4) kernels of libmtn: plan upload/apply (block-table updates
+// and fp64 RoPE angles), fused RoPE + append + evict, vector GQA attention
+// over sinks ∪ window (decode, and the fp32 chunk prefill) with a split-K
+// log-sum-exp merge, the debug poison kernel and the HBM copy probe.
+//
+// Method: Metronome (arXiv 2607.02640) §4.1 / App. A -- a query at absolute
+// position t attends to keys k <= t with k < S or k in the W positions ending
+// at t; sinks are visited first, segments of a split decode are merged once.
+#include "mtn_kernels.h"
+
+#include <hip/hip_runtime.h>
+#include <math.h>
+#include <stdint.h>
+
+#include <algorithm>
+
+namespace mtn {
+namespace {
+
+typedef __attribute__((ext_vector_type(2))) __bf16 bf16x2_t;
+
+// ---------------------------------------------------------------------------
+// element helpers
+// ---------------------------------------------------------------------------
+struct bf16_t {
+    uint16_t bits;
+};
+
+__device__ __forceinline__ float to_f32(float x) { return x; }
+__device__ __forceinline__ float to_f32(bf16_t x) {
+    return __uint_as_float((uint32_t)x.bits << 16);
+}
+template <typename T>
+__device__ __forceinline__ T from_f32(float x);
+template <>
+__device__ __forceinline__ float from_f32<float>(float x) {
+    return x;
+}
+template <>
+__device__ __forceinline__ bf16_t from_f32<bf16_t>(float x) {
+    __bf16 b = (__bf16)x;  // round to nearest even (hardware cvt on gfx950)
+    return bf16_t{__builtin_bit_cast(uint16_t, b)};
+}
+__device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
+    bf16x2_t v = {(__bf16)lo, (__bf16)hi};
+    return __builtin_bit_cast(uint32_t, v);
+}
+__device__ __forceinline__ float dot2_bf16(uint32_t a, uint32_t b, float c) {
+    return __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2_t, a),
+                                           __builtin_bit_cast(bf16x2_t, b), c, false);
+}
+
+// DPP helpers (row = 16 lanes, quad = 4 lanes)
+template <int CTRL>
+__device__ __forceinline__ float dpp(float x) {
+    return __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(
+                                         0, __builtin_bit_cast(int, x), CTRL, 0xf, 0xf, false));
+}
+constexpr int kQuadXor1 = 0xB1;  // quad_perm [1,0,3,2]
+constexpr int kQuadXor2 = 0x4E;  // quad_perm [2,3,0,1]
+constexpr int kRowRor4 = 0x124;  // row_ror:4
+constexpr int kRowRor8 = 0x128;  // row_ror:8
+
+__device__ __forceinline__ float shfl_xor_f(float x, int m) {
+    return __shfl_xor(x, m, 64);
+}
+
+// max / sum over the 16 lanes that share (lane & 3) -- i.e. over the 16 keys
+// of a block for one quarter index
+__device__ __forceinline__ float keys_max(float x) {
+    x = fmaxf(x, dpp<kRowRor4>(x));
+    x = fmaxf(x, dpp<kRowRor8>(x));
+    x = fmaxf(x, shfl_xor_f(x, 16));
+    x = fmaxf(x, shfl_xor_f(x, 32));
+    return x;
+}
+__device__ __forceinline__ float keys_sum(float x) {
+    x += dpp<kRowRor4>(x);
+    x += dpp<kRowRor8>(x);
+    x += shfl_xor_f(x, 16);
+    x += shfl_xor_f(x, 32);
+    return x;
+}
+
+__device__ __forceinline__ void wave_sync() {
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+}
+
+// ---------------------------------------------------------------------------
+// visible-range geometry of one query (sinks first, then the ring run)
+// ---------------------------------------------------------------------------
+struct VisRange {
+    int sink_tokens;  // min(S, t+1)
+    int n_sb;         // sink blocks read
+    int first;        // ring slot of the first window position
+    int ring_n;       // window positions (0 = none)
+    int n_rb;         // ring blocks read (a block may appear twice on a wrap)
+};
+
+__device__ __forceinline__ VisRange vis_range(const PoolGeom &g, int t) {
+    VisRange r;
+    r.sink_tokens = min(g.n_sink, t + 1);
+    r.n_sb = (r.sink_tokens + kBlock - 1) / kBlock;
+    int a = g.window < 0 ? 0 : max(g.n_sink, t - g.window + 1);
+    if (a <= t) {
+        r.ring_n = t - a + 1;
+        r.first = g.window < 0 ? a : (a - g.n_sink) % g.ring;
+        r.n_rb = ((r.first % kBlock) + r.ring_n + kBlock - 1) / kBlock;
+    } else {
+        r.ring_n = 0;
+        r.first = 0;
+        r.n_rb = 0;
+    }
+    return r;
+}
+
+// logical block and valid slot range [lo, hi) of virtual block v
+__device__ __forceinline__ void vblock(const PoolGeom &g, const VisRange &r, int v, int *lb,
+                                       int *lo, int *hi) {
+    if (v < r.n_sb) {
+        *lb = v;
+        *lo = 0;
+        *hi = min(kBlock, r.sink_tokens - v * kBlock);
+        return;
+    }
+    int u = v - r.n_sb;
+    int ring_blocks = g.ring / kBlock;
+    *lb = g.n_sink_blocks + (r.first / kBlock + u) % ring_blocks;
+    *lo = (u == 0) ? r.first % kBlock : 0;
+    *hi = (u == r.n_rb - 1) ? ((r.first % kBlock) + r.ring_n - 1) % kBlock + 1 : kBlock;
+}
+
+// ---------------------------------------------------------------------------
+// plan apply: block-table updates + RoPE (cos, sin) table in fp64
+// ---------------------------------------------------------------------------
+__global__ void k_plan_apply(const int32_t *__restrict__ upd_idx,
+                             const int32_t *__restrict__ upd_val, int32_t n_upd,
+                             int32_t *__restrict__ table, const int32_t *__restrict__ tok_pos,
+                             int32_t n_tok, const double *__restrict__ inv_freq, int32_t half_d,
+                             float2 *__restrict__ rope) {
+    int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (i < n_upd) table[upd_idx[i]] = upd_val[i];
+    int64_t total = (int64_t)n_tok * half_d;
+    for (int64_t j = i; j < total; j += (int64_t)gridDim.x * blockDim.x) {
+        int32_t t = (int32_t)(j / half_d), f = (int32_t)(j % half_d);
+        double a = (double)tok_pos[t] * inv_freq[f];
+        double sn, cs;
+        sincos(a, &sn, &cs);
+        rope[j] = make_float2((float)cs, (float)sn);
+    }
+}
+
+// ---------------------------------------------------------------------------
+// fused RoPE + append + evict: one thread per (token, kv head, rotation pair)
+// ---------------------------------------------------------------------------
+template <typename T>
+__global__ void k_append(PoolGeom g, PlanView p, int32_t layer, const T *__restrict__ k,
+                         const T *__restrict__ v) {
+    const int half = g.d / 2;
+    int64_t idx = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    int64_t total = (int64_t)p.n_tok * g.hkv * half;
+    if (idx >= total) return;
+    int i = (int)(idx % half);
+    int64_t th = idx / half;
+    int h = (int)(th % g.hkv);
+    int t = (int)(th / g.hkv);
+    int64_t row = p.tok_row[t];
+    const T *kr = k + (row * g.hkv + h) * g.d;
+    const T *vr = v + (row * g.hkv + h) * g.d;
+    float2 cs = p.rope[(int64_t)t * half + i];
+    float x0 = to_f32(kr[i]), x1 = to_f32(kr[i + half]);
+    float y0 = fmaf(x0, cs.x, -x1 * cs.y);
+    float y1 = fmaf(x1, cs.x, x0 * cs.y);
+    uint8_t *tile = (uint8_t *)g.kv + (int64_t)layer * g.layer_stride +
+                    (int64_t)p.tok_block[t] * g.block_stride + (int64_t)h * g.head_stride;
+    T *K = (T *)tile;
+    T *VT = (T *)(tile + g.tile_bytes);
+    int off = p.tok_off[t];
+    K[off * g.d + i] = from_f32<T>(y0);
+    K[off * g.d + i + half] = from_f32<T>(y1);
+    VT[i * kBlock + off] = vr[i];
+    VT[(i + half) * kBlock + off] = vr[i + half];
+}
+
+// ---------------------------------------------------------------------------
+// vector attention: one wavefront per (query token, kv head, split segment)
+// ---------------------------------------------------------------------------
+template <typename T, int D>
+struct Lay {
+    static constexpr int E = (int)sizeof(T);
+    static constexpr int NB = D * E / 4;       // bytes per lane of a K (or V^T) tile
+    static constexpr int NV4 = NB / 16;        // uint4 loads per lane per tile
+    static constexpr int QD = D / 4;           // K dims per lane (one quarter row)
+    static constexpr int VD = D / 64;          // V^T rows (dims) per lane
+    static constexpr int VW = kBlock * E / 4;  // dwords per V^T row
+    static_assert(NB % 16 == 0, "tile slice must be whole uint4s");
+};
+
+template <typename T, int D, int G>
+struct QRegs;
+template <int D, int G>
+struct QRegs<bf16_t, D, G> {
+    uint32_t v[G][D / 8];  // bf16 pairs of the lane's quarter, pre-scaled
+};
+template <int D, int G>
+struct QRegs<float, D, G> {
+    float v[G][D / 4];
+};
+
+template <typename T, int D>
+struct Tile {
+    uint4 k[Lay<T, D>::NV4];
+    uint4 v[Lay<T, D>::NV4];
+};
+
+constexpr int kWaves = 4;  // independent waves per workgroup
+
+template <typename T, int D, int G>
+__global__ __launch_bounds__(64 * kWaves) void k_attn_valu(AttnArgs a) {
+    using L = Lay<T, D>;
+    constexpr int NH = (G + 3) / 4;  // heads owned per lane in the softmax
+    __shared__ float sPf[kWaves][2][G][kBlock];
+    __shared__ float sA[kWaves][2][G];
+    __shared__ float sM[kWaves][G], sL[kWaves][G];
+
+    const int lane = threadIdx.x & 63;
+    const int wv = threadIdx.x >> 6;
+    const int64_t unit = (int64_t)blockIdx.x * kWaves + wv;
+    const PoolGeom &g = a.g;
+    const int64_t n_units = (int64_t)a.p.n_tok * g.hkv * a.n_split;
+    if (unit >= n_units) return;
+    const int split = (int)(unit % a.n_split);
+    const int kvh = (int)((unit / a.n_split) % g.hkv);
+    const int t = (int)(unit / ((int64_t)a.n_split * g.hkv));
+    const int sid = a.p.tok_sid[t];
+    const int pos = a.p.tok_pos[t];
+    const int64_t row = a.p.tok_row[t];
+    const int key = lane >> 2, qtr = lane & 3;
+
+    // ---- q prologue: rotate at pos, fold the softmax scale (log2 domain)
+    QRegs<T, D, G> q;
+    {
+        const T *qb = (const T *)a.q + (row * g.hq + (int64_t)kvh * G) * D;
+        const float2 *rp = a.p.rope + (int64_t)t * (D / 2) + (qtr & 1) * L::QD;
+        const int d0 = qtr * L::QD;
+        const int dp = (qtr ^ 2) * L::QD;
+        const float sgn = (qtr < 2) ? -1.f : 1.f;
+#pragma unroll
+        for (int h = 0; h < G; ++h) {
+            const T *qh = qb + (int64_t)h * D;
+#pragma unroll
+            for (int i = 0; i < L::QD; i += 2) {
+                float2 c0 = rp[i], c1 = rp[i + 1];
+                float x0 = to_f32(qh[d0 + i]), x1 = to_f32(qh[d0 + i + 1]);
+                float y0 = to_f32(qh[dp + i]), y1 = to_f32(qh[dp + i + 1]);
+                float r0 = fmaf(x0, c0.x, sgn * y0 * c0.y) * a.scale_log2;
+                float r1 = fmaf(x1, c1.x, sgn * y1 * c1.y) * a.scale_log2;
+                if constexpr (sizeof(T) == 2) {
+                    q.v[h][i / 2] = pack_bf16x2(r0, r1);
+                } else {
+                    q.v[h][i] = r0;
+                    q.v[h][i + 1] = r1;
+                }
+            }
+        }
+    }
+
+    // ---- work range
+    const VisRange vr = vis_range(g, pos);
+    const int nv = vr.n_sb + vr.n_rb;
+    const int v0 = (int)((int64_t)split * nv / a.n_split);
+    const int v1 = (int)((int64_t)(split + 1) * nv / a.n_split);
+    const uint8_t *layer_base = g.kv + (int64_t)a.layer * g.layer_stride + (int64_t)kvh * g.head_stride;
+    const int32_t *trow = g.table + (int64_t)sid * g.row_len;
+
+    float m[NH], lsum[NH];
+#pragma unroll
+    for (int j = 0; j < NH; ++j) {
+        m[j] = -INFINITY;
+        lsum[j] = 0.f;
+    }
+    float acc[G][L::VD];
+#pragma unroll
+    for (int h = 0; h < G; ++h)
+#pragma unroll
+        for (int r = 0; r < L::VD; ++r) acc[h][r] = 0.f;
+
+    auto load = [&](int v, Tile<T, D> &tl) {
+        int lb, lo, hi;
+        vblock(g, vr, v, &lb, &lo, &hi);
+        int phys = trow[lb];
+        phys = phys < 0 ? 0 : phys;
+        const uint8_t *tile = layer_base + (int64_t)phys * g.block_stride;
+        const uint4 *kp = (const uint4 *)(tile + lane * L::NB);
+        const uint4 *vp = (const uint4 *)(tile + g.tile_bytes + lane * L::NB);
+#pragma unroll
+        for (int i = 0; i < L::NV4; ++i) tl.k[i] = kp[i];
+#pragma unroll
+        for (int i = 0; i < L::NV4; ++i) tl.v[i] = vp[i];
+    };
+
+    int buf = 0;
+    auto process = [&](int v, Tile<T, D> &tl) {
+        int lb, lo, hi;
+        vblock(g, vr, v, &lb, &lo, &hi);
+        if (trow[lb] < 0) hi = lo;  // unassigned block: nothing visible
+        // QK: partial dot over this lane's quarter, then the quad all-reduce
+        float sc[G];
+        const uint32_t *kw = (const uint32_t *)tl.k;
+#pragma unroll
+        for (int h = 0; h < G; ++h) {
+            float s = 0.f;
+            if constexpr (sizeof(T) == 2) {
+#pragma unroll
+                for (int i = 0; i < D / 8; ++i) s = dot2_bf16(q.v[h][i], kw[i], s);
+            } else {
+#pragma unroll
+                for (int i = 0; i < D / 4; ++i) s = fmaf(q.v[h][i], __uint_as_float(kw[i]), s);
+            }
+            s += dpp<kQuadXor1>(s);
+            s += dpp<kQuadXor2>(s);
+            sc[h] = s;
+        }
+        const bool valid = key >= lo && key < hi;
+        // online softmax for the heads this lane owns (h = qtr + 4j)
+#pragma unroll
+        for (int j = 0; j < NH; ++j) {
+            const int h = qtr + 4 * j;
+            const int hs = (h < G) ? h : (h % G);
+            float s = sc[0];
+#pragma unroll
+            for (int c = 1; c < G; ++c) s = (hs == c) ? sc[c] : s;
+            s = valid ? s : -INFINITY;
+            float mx = keys_max(s);
+            float m_new = fmaxf(m[j], mx);
+            float mn = (m_new == -INFINITY) ? 0.f : m_new;
+            float alpha = __builtin_amdgcn_exp2f(m[j] - mn);
+            float p = __builtin_amdgcn_exp2f(s - mn);
+            lsum[j] = lsum[j] * alpha + p;
+            m[j] = m_new;
+            if (h < G) {
+                sPf[wv][buf][h][key] = p;
+                if (key == 0) sA[wv][buf][h] = alpha;
+            }
+        }
+        wave_sync();
+        // PV: lane owns V dims lane*VD .. +VD for all G heads
+        const uint32_t *vw = (const uint32_t *)tl.v;
+        uint32_t vv[L::VD][L::VW];
+#pragma unroll
+        for (int r = 0; r < L::VD; ++r)
+#pragma unroll
+            for (int c = 0; c < L::VW; ++c) vv[r][c] = vw[r * L::VW + c];
+        if (lo > 0 || hi < kBlock) {  // zero values of invisible slots (may be NaN)
+#pragma unroll
+            for (int c = 0; c < L::VW; ++c) {
+                uint32_t mask;
+                if constexpr (sizeof(T) == 2) {
+                    int k0 = 2 * c, k1 = 2 * c + 1;
+                    mask = ((k0 >= lo && k0 < hi) ? 0x0000FFFFu : 0u) |
+                           ((k1 >= lo && k1 < hi) ? 0xFFFF0000u : 0u);
+                } else {
+                    mask = (c >= lo && c < hi) ? 0xFFFFFFFFu : 0u;
+                }
+#pragma unroll
+                for (int r = 0; r < L::VD; ++r) vv[r][c] &= mask;
+            }
+        }
+#pragma unroll
+        for (int h = 0; h < G; ++h) {
+            const float al = sA[wv][buf][h];
+            const float *ph = sPf[wv][buf][h];
+#pragma unroll
+            for (int r = 0; r < L::VD; ++r) acc[h][r] *= al;
+            if constexpr (sizeof(T) == 2) {
+                uint32_t pp[kBlock / 2];
+#pragma unroll
+                for (int c = 0; c < kBlock / 2; ++c) pp[c] = pack_bf16x2(ph[2 * c], ph[2 * c + 1]);
+#pragma unroll
+                for (int r = 0; r < L::VD; ++r)
+#pragma unroll
+                    for (int c = 0; c < kBlock / 2; ++c) acc[h][r] = dot2_bf16(pp[c], vv[r][c], acc[h][r]);
+            } else {
+#pragma unroll
+                for (int r = 0; r < L::VD; ++r)
+#pragma unroll
+                    for (int c = 0; c < kBlock; ++c)
+                        acc[h][r] = fmaf(ph[c], __uint_as_float(vv[r][c]), acc[h][r]);
+            }
+        }
+        buf ^= 1;
+    };
+
+    if (v0 < v1) {
+        Tile<T, D> A, B;
+        load(v0, A);
+        for (int v = v0; v < v1; v += 2) {
+            if (v + 1 < v1) load(v + 1, B);
+            process(v, A);
+            if (v + 1 >= v1) break;
+            if (v + 2 < v1) load(v + 2, A);
+            process(v + 1, B);
+        }
+    }
+
+    // ---- finish: reduce the per-lane partial sums, publish (m, l) per head
+#pragma unroll
+    for (int j = 0; j < NH; ++j) {
+        const int h = qtr + 4 * j;
+        float lt = keys_sum(lsum[j]);
+        if (h < G && key == 0) {
+            sM[wv][h] = m[j];
+            sL[wv][h] = lt;
+        }
+    }
+    wave_sync();
+    const int hq0 = kvh * G;
+    if (a.n_split == 1) {
+        T *ob = (T *)a.out + (row * g.hq + hq0) * D;
+#pragma unroll
+        for (int h = 0; h < G; ++h) {
+            const float inv = 1.f / sL[wv][h];
+#pragma unroll
+            for (int r = 0; r < L::VD; ++r) ob[(int64_t)h * D + lane * L::VD + r] = from_f32<T>(acc[h][r] * inv);
+        }
+        if (a.lse && lane < G)
+            a.lse[row * g.hq + hq0 + lane] =
+                (sM[wv][lane] + __builtin_amdgcn_logf(sL[wv][lane])) * 0.6931471805599453f;
+    } else {
+        const int64_t ns = a.n_split;
+        float *pacc = a.part;
+        float *pml = a.part + (int64_t)a.p.n_tok * g.hq * ns * D;
+#pragma unroll
+        for (int h = 0; h < G; ++h) {
+            int64_t base = (((int64_t)t * g.hq + hq0 + h) * ns + split);
+#pragma unroll
+            for (int r = 0; r < L::VD; ++r) pacc[base * D + lane * L::VD + r] = acc[h][r];
+        }
+        if (lane < G) {
+            int64_t base = (((int64_t)t * g.hq + hq0 + lane) * ns + split);
+            pml[base * 2] = sM[wv][lane];
+            pml[base * 2 + 1] = sL[wv][lane];
+        }
+    }
+}
+
+// merge split partials: one wave per (token, q head)
+template <typename T, int D>
+__global__ __launch_bounds__(64) void k_merge(AttnArgs a) {
+    const int64_t th = blockIdx.x;  // t * Hq + hq
+    const int lane = threadIdx.x;
+    const int64_t ns = a.n_split;
+    const float *pacc = a.part;
+    const float *pml = a.part + (int64_t)a.p.n_tok * a.g.hq * ns * D;
+    float M = -INFINITY;
+    for (int s = 0; s < ns; ++s) M = fmaxf(M, pml[(th * ns + s) * 2]);
+    constexpr int VD = D / 64;
+    float acc[VD];
+#pragma unroll
+    for (int r = 0; r < VD; ++r) acc[r] = 0.f;
+    float Lsum = 0.f;
+    for (int s = 0; s < ns; ++s) {
+        float ms = pml[(th * ns + s) * 2], ls = pml[(th * ns + s) * 2 + 1];
+        float w = (ms == -INFINITY) ? 0.f : __builtin_amdgcn_exp2f(ms - M);
+        Lsum += ls * w;
+#pragma unroll
+        for (int r = 0; r < VD; ++r) acc[r] += w * pacc[(th * ns + s) * D + lane * VD + r];
+    }
+    const int t = (int)(th / a.g.hq), hq = (int)(th % a.g.hq);
+    const int64_t row = a.p.tok_row[t];
+    T *ob = (T *)a.out + (row * a.g.hq + hq) * D;
+    const float inv = 1.f / Lsum;
+#pragma unroll
+    for (int r = 0; r < VD; ++r) ob[lane * VD + r] = from_f32<T>(acc[r] * inv);
+    if (a.lse && lane == 0)
+        a.lse[row * a.g.hq + hq] = (M + __builtin_amdgcn_logf(Lsum)) * 0.6931471805599453f;
+}
+
+// ---------------------------------------------------------------------------
+// debug poison: NaN into every slot whose live bit is clear
+// ---------------------------------------------------------------------------
+template <typename T>
+__global__ void k_poison(PoolGeom g, int32_t n_layers, int64_t n_blocks,
+                         const uint16_t *__restrict__ live) {
+    const int64_t n_items = (int64_t)n_layers * n_blocks * g.hkv;
+    T nan_v;
+    if constexpr (sizeof(T) == 2) nan_v = __builtin_bit_cast(T, (uint16_t)0x7FC0);
+    else nan_v = __builtin_bit_cast(T, 0x7FC00000u);
+    for (int64_t it = blockIdx.x; it < n_items; it += gridDim.x) {
+        int h = (int)(it % g.hkv);
+        int64_t b = (it / g.hkv) % n_blocks;
+        int l = (int)(it / ((int64_t)g.hkv * n_blocks));
+        uint16_t lm = live[b];
+        if (lm == 0xFFFF) continue;
+        uint8_t *tile = (uint8_t *)g.kv + (int64_t)l * g.layer_stride + b * g.block_stride +
+                        (int64_t)h * g.head_stride;
+        T *K = (T *)tile;
+        T *VT = (T *)(tile + g.tile_bytes);
+        for (int e = threadIdx.x; e < kBlock * g.d; e += blockDim.x) {
+            int off = e / g.d, d = e % g.d;
+            if (!((lm >> off) & 1)) {
+                K[e] = nan_v;
+                VT[d * kBlock + off] = nan_v;
+            }
+        }
+    }
+}
+
+__global__ void k_copy(const uint4 *__restrict__ src, uint4 *__restrict__ dst, int64_t n) {
+    for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n;
+         i += (int64_t)gridDim.x * blockDim.x)
+        dst[i] = src[i];
+}
+
+template <typename T, int D, int G>
+hipError_t launch_valu_t(const AttnArgs &a, hipStream_t s) {
+    int64_t units = (int64_t)a.p.n_tok * a.g.hkv * a.n_split;
+    if (units == 0) return hipSuccess;
+    int64_t grid = (units + kWaves - 1) / kWaves;
+    hipLaunchKernelGGL((k_attn_valu<T, D, G>), dim3((unsigned)grid), dim3(64 * kWaves), 0, s, a);
+    return hipGetLastError();
+}
+
+template <typename T, int D>
+hipError_t launch_valu_d(const AttnArgs &a, int G, hipStream_t s) {
+    switch (G) {
+        case 1: return launch_valu_t<T, D, 1>(a, s);
+        case 2: return launch_valu_t<T, D, 2>(a, s);
+        case 4: return launch_valu_t<T, D, 4>(a, s);
+        case 8: return launch_valu_t<T, D, 8>(a, s);
+        default: return hipErrorInvalidValue;
+    }
+}
+
+}  // namespace
+
+bool attn_valu_supported(int dtype, int d, int g) {
+    if (g != 1 && g != 2 && g != 4 && g != 8) return false;
+    if (d != 64 && d != 128) return false;
+    if (dtype == 0 && d == 128 && g == 8) return false;  // register budget
+    return dtype == 0 || dtype == 1;
+}
+
+bool prefill_mfma_supported(int, int, int) { return false; }
+
+hipError_t launch_plan_apply(const int32_t *upd_idx, const int32_t *upd_val, int32_t n_upd,
+                             int32_t *table, const int32_t *tok_pos, int32_t n_tok,
+                             const double *inv_freq, int32_t half_d, float2 *rope,
+                             hipStream_t s) {
+    int64_t total = std::max<int64_t>((int64_t)n_tok * half_d, n_upd);
+    if (total == 0) return hipSuccess;
+    int64_t grid = std::min<int64_t>((total + 255) / 256, 4096);
+    hipLaunchKernelGGL(k_plan_apply, dim3((unsigned)grid), dim3(256), 0, s, upd_idx, upd_val, n_upd,
+                       table, tok_pos, n_tok, inv_freq, half_d, rope);
+    return hipGetLastError();
+}
+
+hipError_t launch_append(int dtype, const PoolGeom &g, const PlanView &p, int32_t layer,
+                         const void *k, const void *v, hipStream_t s) {
+    int64_t total = (int64_t)p.n_tok * g.hkv * (g.d / 2);
+    if (total == 0) return hipSuccess;
+    unsigned grid = (unsigned)((total + 255) / 256);
+    if (dtype == 1)
+        hipLaunchKernelGGL(k_append<bf16_t>, dim3(grid), dim3(256), 0, s, g, p, layer,
+                           (const bf16_t *)k, (const bf16_t *)v);
+    else
+        hipLaunchKernelGGL(k_append<float>, dim3(grid), dim3(256), 0, s, g, p, layer,
+                           (const float *)k, (const float *)v);
+    return hipGetLastError();
+}
+
+hipError_t launch_attn_valu(int dtype, const AttnArgs &a, hipStream_t s) {
+    const int G = a.g.hq / a.g.hkv;
+    if (!attn_valu_supported(dtype, a.g.d, G)) return hipErrorInvalidValue;
+    if (dtype == 1) {
+        return a.g.d == 128 ? launch_valu_d<bf16_t, 128>(a, G, s) : launch_valu_d<bf16_t, 64>(a, G, s);
+    }
+    return a.g.d == 128 ? launch_valu_d<float, 128>(a, G, s) : launch_valu_d<float, 64>(a, G, s);
+}
+
+hipError_t launch_merge(int dtype, const AttnArgs &a, hipStream_t s) {
+    int64_t n = (int64_t)a.p.n_tok * a.g.hq;
+    if (n == 0) return hipSuccess;
+    if (dtype == 1) {
+        if (a.g.d == 128)
+            hipLaunchKernelGGL((k_merge<bf16_t, 128>), dim3((unsigned)n), dim3(64), 0, s, a);
+        else
+            hipLaunchKernelGGL((k_merge<bf16_t, 64>), dim3((unsigned)n), dim3(64), 0, s, a);
+    } else {
+        if (a.g.d == 128)
+            hipLaunchKernelGGL((k_merge<float, 128>), dim3((unsigned)n), dim3(64), 0, s, a);
+        else
+            hipLaunchKernelGGL((k_merge<float, 64>), dim3((unsigned)n), dim3(64), 0, s, a);
+    }
+    return hipGetLastError();
+}
+
+hipError_t launch_prefill_mfma(const AttnArgs &, int32_t, const int32_t *, const int32_t *, int32_t,
+                               hipStream_t) {
+    return hipErrorInvalidValue;
+}
+
+hipError_t launch_poison(int dtype, const PoolGeom &g, int32_t n_layers, int64_t n_blocks,
+                         const uint16_t *live, hipStream_t s) {
+    unsigned grid = 8192;
+    if (dtype == 1)
+        hipLaunchKernelGGL(k_poison<bf16_t>, dim3(grid), dim3(256), 0, s, g, n_layers, n_blocks, live);
+    else
+        hipLaunchKernelGGL(k_poison<float>, dim3(grid), dim3(256), 0, s, g, n_layers, n_blocks, live);
+    return hipGetLastError();
+}
+
+hipError_t launch_copy(const void *src, void *dst, size_t bytes, hipStream_t s) {
+    int64_t n = (int64_t)(bytes / 16);
+    if (n == 0) return hipSuccess;
+    int64_t grid = std::min<int64_t>((n + 255) / 256, 256 * 16);
+    hipLaunchKernelGGL(k_copy, dim3((unsigned)grid), dim3(256), 0, s, (const uint4 *)src,
+                       (uint4 *)dst, n);
+    return hipGetLastError();
+}
+
+}  // namespace mtn

@@ -1,0 +1,163 @@
+"""Helpers for the GPU parity tests: drive sessions through the C ABI and the
+float64 oracle on identical seeded inputs and compare."""
+import math
+import sys
+
+import numpy as np
+import torch
+
+import paper_2607_02640_amd as mtn
+from oracle import windowed_attention as wa
+from workload import session_rng, draw_qkv
+
+TDT = {"f32": torch.float32, "bf16": torch.bfloat16}
+TOL = {"f32": 1e-5, "bf16": 2e-2}
+
+
+def say(*a):
+    print(*a, flush=True)
+    sys.stdout.flush()
+
+
+def quantize(x: np.ndarray, dtype: str) -> torch.Tensor:
+    """float32 numpy -> torch tensor of the pool dtype (host)."""
+    return torch.from_numpy(np.ascontiguousarray(x)).to(TDT[dtype])
+
+
+def f64(t: torch.Tensor) -> np.ndarray:
+    return t.detach().to("cpu", torch.float64).numpy()
+
+
+def make_pool(*, n_layers, hq, hkv, d, S, W, cmax, max_sessions, n_blocks, dtype, theta=1e4,
+              max_len=0):
+    kw = dict(n_layers=n_layers, n_q_heads=hq, n_kv_heads=hkv, head_dim=d, n_sink=S, window=W,
+              max_chunk=cmax, max_sessions=max_sessions, n_blocks=n_blocks, dtype=dtype,
+              max_len=max_len, rope_theta=theta)
+    nbytes = mtn.Pool.required(**kw)
+    kv = torch.empty(nbytes, dtype=torch.uint8, device="cuda")
+    pool = mtn.Pool(**kw, kv=kv)
+    return pool
+
+
+class Harness:
+    """N sessions driven frame by frame through mtn_frame_step (or the
+    per-layer calls) and, in lockstep, through float64 oracle sessions."""
+
+    def __init__(self, pool, *, n_sessions, n_layers, hq, hkv, d, S, W, dtype, theta=1e4,
+                 seed=0, literal=False):
+        self.pool = pool
+        self.L, self.hq, self.hkv, self.d = n_layers, hq, hkv, d
+        self.dtype = dtype
+        self.sids = [pool.session_open() for _ in range(n_sessions)]
+        self.orc = [wa.OracleSession(hq, hkv, d, S, W, theta=theta, n_layers=n_layers)
+                    for _ in range(n_sessions)]
+        self.rng = [session_rng(1000 + seed, i) for i in range(n_sessions)]
+        self.max_err = 0.0
+        self.max_lse_err = 0.0
+
+    def _draw(self, i, n_tok):
+        q, k, v = draw_qkv(self.rng[i], self.L, n_tok, self.hq, self.hkv, self.d)
+        return quantize(q, self.dtype), quantize(k, self.dtype), quantize(v, self.dtype)
+
+    def _oracle_step(self, i, q, k, v):
+        """q/k/v: host tensors [L, n, H, D]; returns (out [L,n,Hq,D], lse [L,n,Hq])."""
+        o = self.orc[i]
+        o.begin(q.shape[1])
+        outs, lses = [], []
+        for l in range(self.L):
+            r = o.layer_step(l, f64(q[l]), f64(k[l]), f64(v[l]))
+            outs.append(r[0])
+            lses.append(r[1])
+        o.commit()
+        return np.stack(outs), np.stack(lses)
+
+    def _cmp(self, got, ref, got_lse, ref_lse, what):
+        err = float(np.max(np.abs(f64(got) - ref))) if ref.size else 0.0
+        lerr = float(np.max(np.abs(f64(got_lse) - ref_lse))) if ref.size else 0.0
+        self.max_err = max(self.max_err, err)
+        self.max_lse_err = max(self.max_lse_err, lerr)
+        tol = TOL[self.dtype]
+        assert np.all(np.isfinite(f64(got))), f"{what}: non-finite output"
+        assert err <= tol, f"{what}: max abs err {err:.3e} > {tol}"
+        assert lerr <= max(tol, 1e-4), f"{what}: lse err {lerr:.3e}"
+
+    def frame(self, chunk_len, n_dec, n_split=0, check=True, use_frame_step=True):
+        n = len(self.sids)
+        draws_c = [self._draw(i, chunk_len[i]) for i in range(n)]
+        tc = sum(chunk_len)
+        cat = lambda j: torch.cat([dc[j] for dc in draws_c], dim=1).contiguous()
+        qc, kc, vc = (cat(j).cuda() for j in range(3))
+        oc = torch.empty_like(qc)
+        lc = torch.empty((self.L, tc, self.hq), dtype=torch.float32, device="cuda")
+        md = max(n_dec) if n_dec else 0
+        dec_draws = [[self._draw(i, 1) if n_dec[i] > j else None for i in range(n)]
+                     for j in range(md)]
+        if md:
+            def dstack(j_comp):
+                out = torch.zeros((md, self.L, n, self.hq if j_comp == 0 else self.hkv, self.d),
+                                  dtype=TDT[self.dtype])
+                for j in range(md):
+                    for i in range(n):
+                        if dec_draws[j][i] is not None:
+                            out[j, :, i] = dec_draws[j][i][j_comp][:, 0]
+                return out.cuda()
+            qd, kd, vd = dstack(0), dstack(1), dstack(2)
+            od = torch.zeros_like(qd)
+            ld = torch.zeros((md, self.L, n, self.hq), dtype=torch.float32, device="cuda")
+        else:
+            qd = kd = vd = od = ld = None
+        if use_frame_step:
+            self.pool.frame_step(self.sids, chunk_len, n_dec, qc, kc, vc, oc, qd, kd, vd, od,
+                                 lse_chunk=lc, lse_dec=ld, n_split=n_split)
+        else:
+            self._per_layer(chunk_len, n_dec, qc, kc, vc, oc, lc, qd, kd, vd, od, ld, n_split)
+        torch.cuda.synchronize()
+        if not check:
+            for i in range(n):
+                self._oracle_step(i, *draws_c[i])
+                for j in range(md):
+                    if dec_draws[j][i] is not None:
+                        self._oracle_step(i, *dec_draws[j][i])
+            return
+        off = 0
+        oc_h, lc_h = oc.cpu(), lc.cpu()
+        od_h = od.cpu() if md else None
+        ld_h = ld.cpu() if md else None
+        for i in range(n):
+            ref, rl = self._oracle_step(i, *draws_c[i])
+            c = chunk_len[i]
+            self._cmp(oc_h[:, off:off + c], ref, lc_h[:, off:off + c], rl, f"chunk s{i}")
+            off += c
+        for j in range(md):
+            for i in range(n):
+                if dec_draws[j][i] is None:
+                    continue
+                ref, rl = self._oracle_step(i, *dec_draws[j][i])
+                self._cmp(od_h[j, :, i:i + 1], ref, ld_h[j, :, i:i + 1], rl, f"decode{j} s{i}")
+
+    def _per_layer(self, chunk_len, n_dec, qc, kc, vc, oc, lc, qd, kd, vd, od, ld, n_split):
+        p = self.pool
+        p.plan_begin(self.sids, chunk_len)
+        for l in range(self.L):
+            p.frame_append_kv(l, kc[l], vc[l])
+            if max(chunk_len) == 1:
+                p.attend_decode(l, qc[l], oc[l], lc[l], n_split=n_split)
+            else:
+                p.attend_chunk_prefill(l, qc[l], oc[l], lc[l])
+        p.plan_commit()
+        md = max(n_dec) if n_dec else 0
+        for j in range(md):
+            idx = [i for i in range(len(self.sids)) if n_dec[i] > j]
+            p.plan_begin([self.sids[i] for i in idx], [1] * len(idx))
+            ii = torch.tensor(idx, device="cuda")
+            for l in range(self.L):
+                q = qd[j, l].index_select(0, ii).contiguous()
+                k = kd[j, l].index_select(0, ii).contiguous()
+                v = vd[j, l].index_select(0, ii).contiguous()
+                o = torch.empty_like(q)
+                lse = torch.empty((len(idx), self.hq), dtype=torch.float32, device="cuda")
+                p.frame_append_kv(l, k, v)
+                p.attend_decode(l, q, o, lse, n_split=n_split)
+                od[j, l].index_copy_(0, ii, o)
+                ld[j, l].index_copy_(0, ii, lse)
+            p.plan_commit()

@@ -1,0 +1,152 @@
+"""CPU tests of the C ABI: the library loads, exports every declared symbol,
+and its host planner (block tables, ring-slot map, evicted ranges, pool
+counters, error codes) matches the independent index model bit-exactly.
+No GPU: pools are created with MTN_POOL_HOST_ONLY."""
+import os
+import random
+import re
+
+import pytest
+
+import paper_2607_02640_amd as mtn
+from oracle import index_model as im
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+def test_library_exports_every_declared_symbol():
+    lib = mtn.load()
+    with open(os.path.join(ROOT, "include", "mtn.h")) as f:
+        hdr = f.read()
+    declared = set(re.findall(r"\b(mtn_[a-z_]+)\s*\(", hdr))
+    assert declared == set(mtn.EXPORTS), declared ^ set(mtn.EXPORTS)
+    for name in declared:
+        assert hasattr(lib, name), name
+
+
+def _pair(n_blocks, S, W, cmax, max_sessions, max_len=None):
+    pool = mtn.Pool(n_layers=2, n_q_heads=4, n_kv_heads=2, head_dim=64, n_sink=S, window=W,
+                    max_chunk=cmax, max_sessions=max_sessions, n_blocks=n_blocks, dtype="f32",
+                    max_len=max_len or 0, host_only=True)
+    model = im.IndexModel(n_blocks, 16, S, W, cmax, max_sessions, max_len=max_len)
+    return pool, model
+
+
+def _code(fn, *a):
+    try:
+        r = fn(*a)
+        return 0, r
+    except mtn.MtnError as e:
+        return e.code, None
+    except im.IndexError_ as e:
+        return e.code, None
+
+
+def _compare(pool, model):
+    st = pool.stats()
+    assert st["assigned"] == model.assigned()
+    assert st["reserved"] == model.reserved_blocks()
+    assert st["blocks_per_session"] == model.row_len
+    assert st["ring_tokens"] == model.ring
+    assert st["sink_blocks"] == model.n_sink_blocks
+    for sid, s in model.sessions.items():
+        assert pool.block_table(sid) == model.block_table(sid)
+        ln, na = pool.session_info(sid)
+        assert ln == s.length
+        assert na == sum(1 for b in s.row if b >= 0)
+
+
+@pytest.mark.parametrize("policy", ["windowed", "unbounded"])
+@pytest.mark.parametrize("seed", range(6))
+def test_host_planner_matches_index_model(policy, seed):
+    rnd = random.Random(seed)
+    S = rnd.choice([0, 1, 4, 16, 20])
+    W = None if policy == "unbounded" else rnd.choice([1, 5, 16, 33, 64])
+    cmax = rnd.choice([1, 3, 8, 25])
+    max_sessions = rnd.choice([2, 5])
+    n_blocks = rnd.choice([8, 20, 60])
+    max_len = rnd.choice([40, 100]) if W is None else None
+    pool, model = _pair(n_blocks, S, W, cmax, max_sessions, max_len)
+    for _ in range(250):
+        op = rnd.random()
+        if op < 0.12:
+            a, ra = _code(pool.session_open)
+            b, rb = _code(model.open)
+            assert a == b and ra == rb
+        elif op < 0.2 and model.sessions:
+            sid = rnd.choice(list(model.sessions) + [max_sessions + 1])
+            a, _ = _code(pool.session_close, sid)
+            b, _ = _code(model.close, sid)
+            assert a == b
+        elif model.sessions:
+            k = rnd.randint(1, len(model.sessions))
+            sids = rnd.sample(sorted(model.sessions), k)
+            if rnd.random() < 0.05:
+                sids.append(sids[0])   # duplicate -> invalid
+            n_tok = [rnd.randint(0 if rnd.random() < 0.03 else 1,
+                                 cmax + (1 if rnd.random() < 0.05 else 0)) for _ in sids]
+            a, _ = _code(pool.plan_begin, sids, n_tok)
+            b, _ = _code(model.plan_begin, sids, n_tok)
+            assert a == b, (a, b, sids, n_tok)
+            if a == 0:
+                pos, blk, off, lo, hi = pool.plan_info(len(sids))
+                assert pos == [t.pos for t in model.plan_tokens]
+                assert blk == [t.block for t in model.plan_tokens]
+                assert off == [t.offset for t in model.plan_tokens]
+                assert list(zip(lo, hi)) == model.plan_evicted
+                # a second plan cannot open over this one
+                c, _ = _code(pool.plan_begin, sids[:1], [1])
+                assert c == mtn.MTN_ERR_BAD_STATE
+                if rnd.random() < 0.1:   # closing during a plan is refused
+                    c, _ = _code(pool.session_close, sids[0])
+                    assert c == mtn.MTN_ERR_BAD_STATE
+                pool.plan_commit()
+                model.plan_commit()
+        _compare(pool, model)
+
+
+def test_device_calls_refused_on_host_only_pool():
+    pool, _ = _pair(10, 4, 16, 4, 2)
+    sid = pool.session_open()
+    pool.plan_begin([sid], [2])
+    lib = pool.lib
+    assert lib.mtn_frame_append_kv(pool.h, 0, None, None, None) == mtn.MTN_ERR_BAD_STATE
+    assert lib.mtn_attend_decode(pool.h, 0, None, None, None, 0, None) == mtn.MTN_ERR_BAD_STATE
+    pool.plan_commit()
+    assert pool.session_info(sid) == (2, 1)
+
+
+def test_config_validation():
+    bad = dict(n_layers=1, n_q_heads=8, n_kv_heads=3, head_dim=64, n_sink=4, window=16,
+               max_chunk=4, max_sessions=2, n_blocks=10, dtype="f32", host_only=True)
+    with pytest.raises(mtn.MtnError) as e:
+        mtn.Pool(**bad)
+    assert e.value.code == mtn.MTN_ERR_INVALID_ARG
+    with pytest.raises(mtn.MtnError) as e:
+        mtn.Pool(**{**bad, "n_kv_heads": 2, "head_dim": 96})
+    assert e.value.code == mtn.MTN_ERR_UNSUPPORTED
+    with pytest.raises(mtn.MtnError) as e:
+        mtn.Pool(**{**bad, "n_kv_heads": 2, "block_size": 32})
+    assert e.value.code == mtn.MTN_ERR_UNSUPPORTED
+    with pytest.raises(mtn.MtnError) as e:
+        mtn.Pool(**{**bad, "n_kv_heads": 2, "window": 0})
+    assert e.value.code == mtn.MTN_ERR_INVALID_ARG
+
+
+def test_required_bytes_layout():
+    # [layer][block][kv_head]{K [16][D], V^T [D][16]}
+    n = mtn.Pool.required(n_layers=48, n_q_heads=32, n_kv_heads=4, head_dim=128, n_sink=4,
+                          window=4096, max_chunk=25, max_sessions=128, n_blocks=33152,
+                          dtype="bf16")
+    assert n == 48 * 33152 * 4 * 2 * 16 * 128 * 2
+
+
+def test_windowed_admission_counts_pinned_blocks():
+    # 3 blocks per session (1 sink + 2 ring); pool of 7 admits two sessions
+    pool, model = _pair(7, 4, 32, 1, 4)
+    assert pool.session_open() == 0 and pool.session_open() == 1
+    with pytest.raises(mtn.MtnError) as e:
+        pool.session_open()
+    assert e.value.code == mtn.MTN_ERR_POOL_EXHAUSTED
+    pool.session_close(0)
+    assert pool.session_open() == 0

@@ -1,0 +1,118 @@
+"""GPU parity: the HIP path through the C ABI against the float64 oracle on
+identical seeded inputs.  Tolerances: max-abs 1e-5 for fp32 pools, 2e-2 for
+bf16 pools (bf16 in, fp32 accumulate, bf16 out)."""
+import random
+
+import numpy as np
+import pytest
+import torch
+
+from tests._gpu_util import Harness, make_pool, say
+
+pytestmark = pytest.mark.gpu
+
+
+def _tiny(dtype="f32", d=64, hq=8, hkv=2, S=4, W=128, cmax=8, n=4, L=1, blocks=80):
+    pool = make_pool(n_layers=L, hq=hq, hkv=hkv, d=d, S=S, W=W, cmax=cmax, max_sessions=n,
+                     n_blocks=blocks, dtype=dtype)
+    h = Harness(pool, n_sessions=n, n_layers=L, hq=hq, hkv=hkv, d=d, S=S, W=W, dtype=dtype)
+    return pool, h
+
+
+def test_tiny_config_every_output_40_frames():
+    """4 sessions, GQA 8/2, D = 64, fp32, S = 4, W = 128, 8-token chunks and 4
+    decodes for 40 frames: the window wraps several times."""
+    say("tiny f32 40 frames")
+    pool, h = _tiny()
+    for f in range(40):
+        h.frame([8] * 4, [4] * 4)
+    say(f"max err {h.max_err:.2e} lse {h.max_lse_err:.2e}")
+    assert pool.session_info(h.sids[0])[0] == 480
+
+
+def test_per_layer_calls_match_oracle_ragged():
+    say("per-layer ragged f32")
+    pool, h = _tiny(S=3, W=37, cmax=11, n=5, L=2)
+    rnd = random.Random(1)
+    for f in range(30):
+        h.frame([rnd.randint(1, 11) for _ in range(5)], [rnd.randint(0, 5) for _ in range(5)],
+                use_frame_step=False)
+
+
+@pytest.mark.parametrize("g", [1, 2, 4, 8])
+def test_bf16_d128_gqa_groups(g):
+    say(f"bf16 d128 G={g}")
+    hkv = 2
+    pool, h = _tiny(dtype="bf16", d=128, hq=hkv * g, hkv=hkv, S=4, W=70, cmax=25, n=3, L=2,
+                    blocks=3 * 10)
+    rnd = random.Random(g)
+    for f in range(12):
+        h.frame([rnd.randint(1, 25) for _ in range(3)], [rnd.randint(0, 6) for _ in range(3)])
+    say(f"max err {h.max_err:.2e}")
+
+
+@pytest.mark.parametrize("dtype,d", [("f32", 128), ("bf16", 64)])
+def test_other_head_dims(dtype, d):
+    say(f"{dtype} d{d}")
+    pool, h = _tiny(dtype=dtype, d=d, hq=8, hkv=4, S=5, W=40, cmax=9, n=3)
+    rnd = random.Random(7)
+    for f in range(15):
+        h.frame([rnd.randint(1, 9) for _ in range(3)], [rnd.randint(0, 4) for _ in range(3)])
+
+
+@pytest.mark.parametrize("n_split", [1, 2, 3, 7, 64])
+def test_decode_split_counts(n_split):
+    say(f"split {n_split}")
+    pool, h = _tiny(S=4, W=90, cmax=8, n=3)
+    for f in range(14):
+        h.frame([8] * 3, [3] * 3, n_split=n_split)
+
+
+def test_no_sinks_and_unit_window():
+    say("S=0 W=1")
+    pool, h = _tiny(S=0, W=1, cmax=4, n=2)
+    for f in range(10):
+        h.frame([4, 1], [2, 3])
+
+
+def test_sinks_larger_than_a_block():
+    say("S=20")
+    pool, h = _tiny(S=20, W=24, cmax=6, n=2)
+    for f in range(12):
+        h.frame([6, 3], [2, 1])
+
+
+def test_unbounded_policy():
+    say("unbounded")
+    pool = make_pool(n_layers=1, hq=8, hkv=2, d=64, S=0, W=None, cmax=8, max_sessions=3,
+                     n_blocks=3 * 20, dtype="f32", max_len=300)
+    h = Harness(pool, n_sessions=3, n_layers=1, hq=8, hkv=2, d=64, S=0, W=None, dtype="f32")
+    for f in range(20):
+        h.frame([8, 5, 1], [4, 2, 0])
+
+
+def test_poisoned_dead_slots_are_never_read():
+    """NaN in every unassigned block, every sink-block slot past S and every
+    ring slot outside the retained set: the next frames stay finite and match."""
+    say("poison")
+    pool, h = _tiny(S=4, W=50, cmax=8, n=3, blocks=60)
+    rnd = random.Random(3)
+    for f in range(12):
+        h.frame([rnd.randint(1, 8) for _ in range(3)], [rnd.randint(0, 4) for _ in range(3)])
+        pool.poison_dead()
+    say(f"max err {h.max_err:.2e}")
+
+
+def test_session_churn_reuses_blocks():
+    say("churn")
+    pool, h = _tiny(S=4, W=40, cmax=8, n=3, blocks=3 * 8)
+    for f in range(8):
+        h.frame([8, 2, 5], [2, 2, 2])
+    # close session 1 and reopen it fresh (new oracle state, new inputs)
+    from oracle import windowed_attention as wa
+    pool.session_close(h.sids[1])
+    assert pool.session_open() == h.sids[1]
+    h.orc[1] = wa.OracleSession(8, 2, 64, 4, 40, theta=1e4, n_layers=1)
+    pool.poison_dead()
+    for f in range(8):
+        h.frame([8, 2, 5], [2, 2, 2])
