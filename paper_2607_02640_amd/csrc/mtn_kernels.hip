@@ -508,10 +508,319 @@ __global__ void k_poison(PoolGeom g, int32_t n_layers, int64_t n_blocks,
     }
 }
 
+// plain streaming copy, four 16-byte loads in flight per thread
 __global__ void k_copy(const uint4 *__restrict__ src, uint4 *__restrict__ dst, int64_t n) {
-    for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n;
-         i += (int64_t)gridDim.x * blockDim.x)
-        dst[i] = src[i];
+    const int64_t stride = (int64_t)gridDim.x * blockDim.x;
+    int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    for (; i + 3 * stride < n; i += 4 * stride) {
+        uint4 a = __builtin_nontemporal_load(src + i);
+        uint4 b = __builtin_nontemporal_load(src + i + stride);
+        uint4 c = __builtin_nontemporal_load(src + i + 2 * stride);
+        uint4 d = __builtin_nontemporal_load(src + i + 3 * stride);
+        __builtin_nontemporal_store(a, dst + i);
+        __builtin_nontemporal_store(b, dst + i + stride);
+        __builtin_nontemporal_store(c, dst + i + 2 * stride);
+        __builtin_nontemporal_store(d, dst + i + 3 * stride);
+    }
+    for (; i < n; i += stride) dst[i] = src[i];
+}
+
+// ---------------------------------------------------------------------------
+// MFMA chunk prefill (bf16, D = 128): one workgroup per (sequence, kv head)
+// ---------------------------------------------------------------------------
+// Rows of the chunk are (token j, group head g) -> r = j * G + g, in tiles of
+// 16.  Keys stream in stages of 32 (two 16-token blocks) through LDS.
+//   S^T[key][row] = K[key][:] . Qrot[row][:]      (A = K, B = Q^T)
+//   O^T[d][row]  += V^T[d][key] . P^T[key][row]   (A = V^T, B = P^T)
+// With the 16x16x32 MFMA output layout, lane l holds column (row) l % 16 of
+// both S^T and O^T, so the softmax state and the accumulators of a row live
+// in the same lane.  The B operand of the PV product is the lane's own eight
+// probabilities: keys 4g..4g+3 of the first block and 4g..4g+3 of the second
+// (g = l / 16) take the k slots 8g..8g+7, and the V^T operand uses the same
+// key order.
+typedef __attribute__((ext_vector_type(8))) __bf16 bf16x8_t;
+typedef __attribute__((ext_vector_type(4))) float f32x4_t;
+
+constexpr int kPfWaves = 8;   // waves per workgroup
+constexpr int kPfTpw = 2;     // 16-row query tiles per wave per pass
+constexpr int kPfRowsPerPass = kPfWaves * kPfTpw * 16;
+
+struct PfArgs {
+    AttnArgs a;
+    const int32_t *seq_first;  // first planned token of each sequence
+    const int32_t *seq_ntok;
+};
+
+__device__ __forceinline__ f32x4_t mfma16x16x32(const uint4 &a, const uint4 &b, f32x4_t c) {
+    return __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8_t, a),
+                                                    __builtin_bit_cast(bf16x8_t, b), c, 0, 0, 0);
+}
+
+// LDS addressing (bytes) inside one stage buffer: K of block b, then V^T.
+__device__ __forceinline__ int lds_k(int b, int key, int chunk16) {
+    return b * 4096 + key * 256 + ((chunk16 ^ (key & 7)) << 4);
+}
+__device__ __forceinline__ int lds_v(int b, int d, int chunk8) {
+    return 8192 + b * 4096 + d * 32 + ((chunk8 ^ ((d >> 2) & 3)) << 3);
+}
+
+template <int G>
+__global__ __launch_bounds__(64 * kPfWaves) void k_prefill_mfma(PfArgs pa) {
+    constexpr int D = 128;
+    __shared__ __attribute__((aligned(16))) uint8_t smem[2][16384];
+    const AttnArgs &a = pa.a;
+    const PoolGeom &g = a.g;
+    const int seq = blockIdx.x / g.hkv;
+    const int kvh = blockIdx.x % g.hkv;
+    const int tid = threadIdx.x;
+    const int lane = tid & 63, wv = tid >> 6;
+    const int ln16 = lane & 15, lg = lane >> 4;
+    const int tok0 = pa.seq_first[seq];
+    const int ntok = pa.seq_ntok[seq];
+    const int sid = a.p.tok_sid[tok0];
+    const int pos0 = a.p.tok_pos[tok0];
+    const int pos_last = pos0 + ntok - 1;
+    const int n_rows = ntok * G;
+    const int32_t *trow = g.table + (int64_t)sid * g.row_len;
+    const uint8_t *layer_base = g.kv + (int64_t)a.layer * g.layer_stride + (int64_t)kvh * g.head_stride;
+
+    // union of the visible sets of the chunk's queries: sinks, then the ring
+    // run [A, pos_last] with A = max(S, pos0 - W + 1)
+    const int sink_tokens = min(g.n_sink, pos_last + 1);
+    const int n_sb = (sink_tokens + kBlock - 1) / kBlock;
+    const int A = g.window < 0 ? 0 : max(g.n_sink, pos0 - g.window + 1);
+    const int ring_n = pos_last - A + 1;  // >= 1: the chunk itself is in the run
+    const int first = g.window < 0 ? A : (A - g.n_sink) % g.ring;
+    const int n_rb = ((first % kBlock) + ring_n + kBlock - 1) / kBlock;
+    const int nvb = n_sb + n_rb;
+    const int n_stages = (nvb + 1) / 2;
+    const int ring_blocks = g.ring / kBlock;
+
+    // virtual block -> (phys, lo, hi, position of slot 0)
+    auto vinfo = [&](int v, int *phys, int *lo, int *hi, int *p0) {
+        if (v >= nvb) {
+            *phys = -1; *lo = 0; *hi = 0; *p0 = 0;
+            return;
+        }
+        int lb;
+        if (v < n_sb) {
+            lb = v;
+            *lo = 0;
+            *hi = min(kBlock, sink_tokens - v * kBlock);
+            *p0 = v * kBlock;
+        } else {
+            int u = v - n_sb;
+            lb = g.n_sink_blocks + (first / kBlock + u) % ring_blocks;
+            *lo = (u == 0) ? first % kBlock : 0;
+            *hi = (u == n_rb - 1) ? ((first % kBlock) + ring_n - 1) % kBlock + 1 : kBlock;
+            *p0 = A + u * kBlock - first % kBlock;
+        }
+        *phys = trow[lb];
+        if (*phys < 0) *hi = *lo;
+    };
+
+    // staging: thread t moves 16 B of K and 16 B of V^T per stage
+    const int sb = tid >> 8;          // block of the stage this thread stages
+    const int q16 = tid & 255;        // 16-byte chunk inside the 4 KiB tile
+    uint4 rk, rv;
+    auto stage_load = [&](int st) {
+        int phys, lo, hi, p0;
+        vinfo(2 * st + sb, &phys, &lo, &hi, &p0);
+        if (phys < 0 || lo >= hi) {
+            rk = make_uint4(0, 0, 0, 0);
+            rv = make_uint4(0, 0, 0, 0);
+            return;
+        }
+        const uint8_t *tile = layer_base + (int64_t)phys * g.block_stride;
+        rk = *(const uint4 *)(tile + q16 * 16);
+        rv = *(const uint4 *)(tile + g.tile_bytes + q16 * 16);
+        if (lo > 0 || hi < kBlock) {  // zero values of slots outside the union
+            int k0 = (q16 & 1) * 8;
+            uint32_t w[4] = {rv.x, rv.y, rv.z, rv.w};
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+                int ka = k0 + 2 * e, kb = ka + 1;
+                uint32_t m = ((ka >= lo && ka < hi) ? 0x0000FFFFu : 0u) |
+                             ((kb >= lo && kb < hi) ? 0xFFFF0000u : 0u);
+                w[e] &= m;
+            }
+            rv = make_uint4(w[0], w[1], w[2], w[3]);
+        }
+    };
+    auto stage_store = [&](int buf) {
+        uint8_t *sm = smem[buf];
+        int key = q16 >> 4, c16 = q16 & 15;
+        *(uint4 *)(sm + lds_k(sb, key, c16)) = rk;
+        int d = q16 >> 1, c8 = (q16 & 1) * 2;
+        *(uint2 *)(sm + lds_v(sb, d, c8)) = make_uint2(rv.x, rv.y);
+        *(uint2 *)(sm + lds_v(sb, d, c8 + 1)) = make_uint2(rv.z, rv.w);
+    };
+
+    const int hq0 = kvh * G;
+    for (int pass_row0 = 0; pass_row0 < n_rows; pass_row0 += kPfRowsPerPass) {
+        // ---- per-wave query tiles: rows r = pass_row0 + (wv + 8 i) * 16 + ln16
+        uint4 qf[kPfTpw][4];
+        f32x4_t acc[kPfTpw][8];
+        float m_i[kPfTpw], l_i[kPfTpw];
+        int trow_tok[kPfTpw];
+        bool live[kPfTpw];
+#pragma unroll
+        for (int i = 0; i < kPfTpw; ++i) {
+            const int tile0 = pass_row0 + (wv + kPfWaves * i) * 16;
+            live[i] = tile0 < n_rows;
+            const int r = tile0 + ln16;
+            const bool rv_ = r < n_rows;
+            const int j = rv_ ? r / G : 0;
+            const int gh = rv_ ? r % G : 0;
+            trow_tok[i] = j;
+            m_i[i] = -INFINITY;
+            l_i[i] = 0.f;
+#pragma unroll
+            for (int dt = 0; dt < 8; ++dt) acc[i][dt] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+            const int t = tok0 + j;
+            const int64_t row = a.p.tok_row[t];
+            const bf16_t *qh = (const bf16_t *)a.q + (row * g.hq + hq0 + gh) * D;
+            const float2 *rp = a.p.rope + (int64_t)t * (D / 2);
+#pragma unroll
+            for (int s = 0; s < 4; ++s) {
+                // dims s*32 + 8*lg + e, e < 8; RoPE partner is d +- 64
+                uint32_t w[4];
+#pragma unroll
+                for (int e = 0; e < 8; e += 2) {
+                    float r2[2];
+#pragma unroll
+                    for (int u = 0; u < 2; ++u) {
+                        const int d = s * 32 + 8 * lg + e + u;
+                        const int f = d & 63;
+                        float2 cs = rp[f];
+                        float x = to_f32(qh[d]);
+                        float y = to_f32(qh[d ^ 64]);
+                        float sg = d < 64 ? -1.f : 1.f;
+                        r2[u] = rv_ ? fmaf(x, cs.x, sg * y * cs.y) * a.scale_log2 : 0.f;
+                    }
+                    w[e / 2] = pack_bf16x2(r2[0], r2[1]);
+                }
+                qf[i][s] = make_uint4(w[0], w[1], w[2], w[3]);
+            }
+        }
+
+        if (n_stages > 0) {
+            stage_load(0);
+            stage_store(0);
+        }
+        __syncthreads();
+        for (int st = 0; st < n_stages; ++st) {
+            const int buf = st & 1;
+            if (st + 1 < n_stages) stage_load(st + 1);
+            const uint8_t *sm = smem[buf];
+            // key metadata of the two blocks of this stage (uniform)
+            int ph0, lo0, hi0, p00, ph1, lo1, hi1, p01;
+            vinfo(2 * st, &ph0, &lo0, &hi0, &p00);
+            vinfo(2 * st + 1, &ph1, &lo1, &hi1, &p01);
+            const bool sink0 = (2 * st) < n_sb, sink1 = (2 * st + 1) < n_sb;
+            // QK: K fragments are read once per stage and shared by the tiles
+            f32x4_t s0[kPfTpw], s1[kPfTpw];
+#pragma unroll
+            for (int i = 0; i < kPfTpw; ++i) {
+                s0[i] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+                s1[i] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+            }
+#pragma unroll
+            for (int s = 0; s < 4; ++s) {
+                uint4 k0 = *(const uint4 *)(sm + lds_k(0, ln16, s * 4 + lg));
+                uint4 k1 = *(const uint4 *)(sm + lds_k(1, ln16, s * 4 + lg));
+#pragma unroll
+                for (int i = 0; i < kPfTpw; ++i) {
+                    if (!live[i]) continue;
+                    s0[i] = mfma16x16x32(k0, qf[i][s], s0[i]);
+                    s1[i] = mfma16x16x32(k1, qf[i][s], s1[i]);
+                }
+            }
+            // online softmax per row (lane holds row ln16, keys 4*lg + r)
+            uint4 pb[kPfTpw];
+#pragma unroll
+            for (int i = 0; i < kPfTpw; ++i) {
+                if (!live[i]) {
+                    pb[i] = make_uint4(0, 0, 0, 0);
+                    continue;
+                }
+                const int tq = pos0 + trow_tok[i];
+                float sc[8];
+#pragma unroll
+                for (int r = 0; r < 4; ++r) {
+                    const int o = 4 * lg + r;
+                    const int pA = p00 + o, pB = p01 + o;
+                    bool vA = o >= lo0 && o < hi0 && pA <= tq &&
+                              (sink0 || g.window < 0 || pA > tq - g.window);
+                    bool vB = o >= lo1 && o < hi1 && pB <= tq &&
+                              (sink1 || g.window < 0 || pB > tq - g.window);
+                    sc[r] = vA ? s0[i][r] : -INFINITY;
+                    sc[4 + r] = vB ? s1[i][r] : -INFINITY;
+                }
+                float mx = sc[0];
+#pragma unroll
+                for (int r = 1; r < 8; ++r) mx = fmaxf(mx, sc[r]);
+                mx = fmaxf(mx, shfl_xor_f(mx, 16));
+                mx = fmaxf(mx, shfl_xor_f(mx, 32));
+                const float m_new = fmaxf(m_i[i], mx);
+                const float mn = (m_new == -INFINITY) ? 0.f : m_new;
+                const float alpha = __builtin_amdgcn_exp2f(m_i[i] - mn);
+                m_i[i] = m_new;
+                float ps = 0.f;
+#pragma unroll
+                for (int r = 0; r < 8; ++r) {
+                    sc[r] = __builtin_amdgcn_exp2f(sc[r] - mn);
+                    ps += sc[r];
+                }
+                l_i[i] = l_i[i] * alpha + ps;
+                pb[i] = make_uint4(pack_bf16x2(sc[0], sc[1]), pack_bf16x2(sc[2], sc[3]),
+                                   pack_bf16x2(sc[4], sc[5]), pack_bf16x2(sc[6], sc[7]));
+#pragma unroll
+                for (int dt = 0; dt < 8; ++dt) acc[i][dt] *= alpha;
+            }
+            // PV: V^T fragments read once per stage, shared by the tiles
+#pragma unroll
+            for (int dt = 0; dt < 8; ++dt) {
+                const int d = dt * 16 + ln16;
+                uint2 va = *(const uint2 *)(sm + lds_v(0, d, lg));
+                uint2 vb = *(const uint2 *)(sm + lds_v(1, d, lg));
+                uint4 vf = make_uint4(va.x, va.y, vb.x, vb.y);
+#pragma unroll
+                for (int i = 0; i < kPfTpw; ++i) {
+                    if (!live[i]) continue;
+                    acc[i][dt] = mfma16x16x32(vf, pb[i], acc[i][dt]);
+                }
+            }
+            if (st + 1 < n_stages) stage_store(buf ^ 1);
+            __syncthreads();
+        }
+
+        // ---- epilogue: normalise and write rows of this pass
+#pragma unroll
+        for (int i = 0; i < kPfTpw; ++i) {
+            if (!live[i]) continue;
+            float lt = l_i[i];
+            lt += shfl_xor_f(lt, 16);
+            lt += shfl_xor_f(lt, 32);
+            const int r = pass_row0 + (wv + kPfWaves * i) * 16 + ln16;
+            if (r >= n_rows) continue;
+            const int j = r / G, gh = r % G;
+            const int t = tok0 + j;
+            const int64_t row = a.p.tok_row[t];
+            bf16_t *ob = (bf16_t *)a.out + (row * g.hq + hq0 + gh) * D;
+            const float inv = 1.f / lt;
+#pragma unroll
+            for (int dt = 0; dt < 8; ++dt) {
+                const int d0 = dt * 16 + 4 * lg;
+                uint2 w = make_uint2(pack_bf16x2(acc[i][dt][0] * inv, acc[i][dt][1] * inv),
+                                     pack_bf16x2(acc[i][dt][2] * inv, acc[i][dt][3] * inv));
+                *(uint2 *)(ob + d0) = w;
+            }
+            if (a.lse && lg == 0)
+                a.lse[row * g.hq + hq0 + gh] =
+                    (m_i[i] + __builtin_amdgcn_logf(lt)) * 0.6931471805599453f;
+        }
+    }
 }
 
 template <typename T, int D, int G>
@@ -543,7 +852,9 @@ bool attn_valu_supported(int dtype, int d, int g) {
     return dtype == 0 || dtype == 1;
 }
 
-bool prefill_mfma_supported(int, int, int) { return false; }
+bool prefill_mfma_supported(int dtype, int d, int g) {
+    return dtype == 1 && d == 128 && (g == 1 || g == 2 || g == 4 || g == 8);
+}
 
 hipError_t launch_plan_apply(const int32_t *upd_idx, const int32_t *upd_val, int32_t n_upd,
                              int32_t *table, const int32_t *tok_pos, int32_t n_tok,
@@ -597,9 +908,19 @@ hipError_t launch_merge(int dtype, const AttnArgs &a, hipStream_t s) {
     return hipGetLastError();
 }
 
-hipError_t launch_prefill_mfma(const AttnArgs &, int32_t, const int32_t *, const int32_t *, int32_t,
-                               hipStream_t) {
-    return hipErrorInvalidValue;
+hipError_t launch_prefill_mfma(const AttnArgs &a, int32_t, const int32_t *seq_first,
+                               const int32_t *seq_ntok, int32_t n_seq, hipStream_t s) {
+    const int G = a.g.hq / a.g.hkv;
+    if (!prefill_mfma_supported(1, a.g.d, G) || n_seq <= 0) return hipErrorInvalidValue;
+    PfArgs pa{a, seq_first, seq_ntok};
+    dim3 grid((unsigned)(n_seq * a.g.hkv)), block(64 * kPfWaves);
+    switch (G) {
+        case 1: hipLaunchKernelGGL(k_prefill_mfma<1>, grid, block, 0, s, pa); break;
+        case 2: hipLaunchKernelGGL(k_prefill_mfma<2>, grid, block, 0, s, pa); break;
+        case 4: hipLaunchKernelGGL(k_prefill_mfma<4>, grid, block, 0, s, pa); break;
+        default: hipLaunchKernelGGL(k_prefill_mfma<8>, grid, block, 0, s, pa); break;
+    }
+    return hipGetLastError();
 }
 
 hipError_t launch_poison(int dtype, const PoolGeom &g, int32_t n_layers, int64_t n_blocks,

@@ -51,6 +51,22 @@ def test_bf16_d128_gqa_groups(g):
     say(f"max err {h.max_err:.2e}")
 
 
+def test_bf16_chunk_longer_than_window():
+    """C > W: chunk tokens leave the window inside their own chunk."""
+    say("bf16 C > W")
+    pool, h = _tiny(dtype="bf16", d=128, hq=16, hkv=2, S=3, W=8, cmax=25, n=3, L=1, blocks=12)
+    for f in range(8):
+        h.frame([25, 9, 1], [2, 0, 3])
+
+
+def test_bf16_multi_pass_rows():
+    """C * G > 256 query rows per (sequence, kv head): several row passes."""
+    say("bf16 multi-pass rows")
+    pool, h = _tiny(dtype="bf16", d=128, hq=16, hkv=2, S=4, W=100, cmax=40, n=2, L=1, blocks=20)
+    for f in range(5):
+        h.frame([40, 33], [1, 2])
+
+
 @pytest.mark.parametrize("dtype,d", [("f32", 128), ("bf16", 64)])
 def test_other_head_dims(dtype, d):
     say(f"{dtype} d{d}")
