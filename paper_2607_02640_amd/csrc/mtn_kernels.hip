@@ -13,6 +13,7 @@
 #include <stdint.h>
 
 #include <algorithm>
+#include <type_traits>
 
 namespace mtn {
 namespace {
@@ -209,35 +210,94 @@ struct QRegs<float, D, G> {
     float v[G][D / 4];
 };
 
-template <typename T, int D>
-struct Tile {
-    uint4 k[Lay<T, D>::NV4];
-    uint4 v[Lay<T, D>::NV4];
-};
+constexpr int kWaves = 4;     // independent waves per workgroup
+constexpr int kRingBytes = 32768;  // per-wave LDS ring for K/V^T blocks
 
-constexpr int kWaves = 4;  // independent waves per workgroup
+// Asynchronous 16-byte-per-lane copy global -> LDS (gfx950 LDS DMA).  Lane i
+// of the wave writes LDS bytes [lds + 16 i, lds + 16 i + 16).  Issued from
+// inline assembly so that the compiler does not guard later LDS reads with a
+// full vmcnt(0); completion is awaited explicitly with vm_wait<N>().
+__device__ __forceinline__ void dma16(const void *gptr, uint32_t lds) {
+    asm volatile(
+        "s_mov_b32 m0, %1\n\t"
+        "global_load_lds_dwordx4 %0, off"
+        :
+        : "v"(gptr), "s"(__builtin_amdgcn_readfirstlane(lds))
+        : "memory", "m0");
+}
+template <int N>
+__device__ __forceinline__ void vm_wait() {
+    asm volatile("s_waitcnt vmcnt(%0)" : : "n"(N) : "memory");
+}
+__device__ __forceinline__ uint32_t lds_addr(const void *p) {
+    return (uint32_t)(uintptr_t)(const __attribute__((address_space(3))) void *)p;
+}
+// Read-only metadata (block table) fetched through the scalar unit: the
+// table is never written while a kernel runs, so the constant address space
+// is exact, and its loads are tracked apart from the vector-memory counter.
+__device__ __forceinline__ int32_t scalar_ld(const int32_t *p, int idx) {
+    return ((const __attribute__((address_space(4))) int32_t *)p)[idx];
+}
+
+// 16-byte chunk permutation of a block buffer (an involution that keeps each
+// aligned group of four chunks together): a lane's 64-byte slice lands
+// rotated so that eight consecutive lanes read eight distinct LDS bank groups.
+__device__ __forceinline__ int swz(int x) { return x ^ ((x >> 3) & 3); }
 
 template <typename T, int D, int G>
 __global__ __launch_bounds__(64 * kWaves) void k_attn_valu(AttnArgs a) {
     using L = Lay<T, D>;
-    constexpr int NH = (G + 3) / 4;  // heads owned per lane in the softmax
-    __shared__ float sPf[kWaves][2][G][kBlock];
+    constexpr int NH = (G + 3) / 4;                 // heads owned per lane in the softmax
+    constexpr int BLK = 2 * kBlock * D * L::E;      // K + V^T bytes of one block (one head)
+    constexpr int NBUF = kRingBytes / BLK < 4 ? kRingBytes / BLK : 4;
+    constexpr int NCH = BLK / 16;                   // 16-byte chunks per block
+    constexpr int NI = NCH / 64;                    // DMA instructions per block
+    static_assert(NBUF >= 2, "ring too small");
+    using PT = typename std::conditional<sizeof(T) == 2, uint16_t, float>::type;
+    __shared__ __attribute__((aligned(16))) uint8_t ring[kWaves][NBUF][BLK];
+    __shared__ __attribute__((aligned(16))) PT sP[kWaves][2][G][kBlock];
     __shared__ float sA[kWaves][2][G];
     __shared__ float sM[kWaves][G], sL[kWaves][G];
 
     const int lane = threadIdx.x & 63;
-    const int wv = threadIdx.x >> 6;
+    // wave-uniform indices live in scalar registers: the block-table and plan
+    // reads below become scalar loads, which do not share the vector-memory
+    // counter the LDS ring is synchronised with
+    const int wv = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
     const int64_t unit = (int64_t)blockIdx.x * kWaves + wv;
     const PoolGeom &g = a.g;
     const int64_t n_units = (int64_t)a.p.n_tok * g.hkv * a.n_split;
     if (unit >= n_units) return;
-    const int split = (int)(unit % a.n_split);
-    const int kvh = (int)((unit / a.n_split) % g.hkv);
-    const int t = (int)(unit / ((int64_t)a.n_split * g.hkv));
-    const int sid = a.p.tok_sid[t];
-    const int pos = a.p.tok_pos[t];
-    const int64_t row = a.p.tok_row[t];
+    const int split = __builtin_amdgcn_readfirstlane((int)(unit % a.n_split));
+    const int kvh = __builtin_amdgcn_readfirstlane((int)((unit / a.n_split) % g.hkv));
+    const int t = __builtin_amdgcn_readfirstlane((int)(unit / ((int64_t)a.n_split * g.hkv)));
+    const int sid = __builtin_amdgcn_readfirstlane(a.p.tok_sid[t]);
+    const int pos = __builtin_amdgcn_readfirstlane(a.p.tok_pos[t]);
+    const int64_t row = __builtin_amdgcn_readfirstlane(a.p.tok_row[t]);
     const int key = lane >> 2, qtr = lane & 3;
+
+    // ---- work range and the first prefetches (issued before the q prologue)
+    const VisRange vr = vis_range(g, pos);
+    const int nv = vr.n_sb + vr.n_rb;
+    const int v0 = __builtin_amdgcn_readfirstlane((int)((int64_t)split * nv / a.n_split));
+    const int v1 = __builtin_amdgcn_readfirstlane((int)((int64_t)(split + 1) * nv / a.n_split));
+    const int nblk = v1 - v0;
+    const uint8_t *head_base = g.kv + (int64_t)a.layer * g.layer_stride + (int64_t)kvh * g.head_stride;
+    const int32_t *trow = g.table + (int64_t)sid * g.row_len;
+    const uint32_t ring0 = lds_addr(&ring[wv][0][0]);
+
+    auto issue = [&](int i) {  // block i of this wave's range -> ring slot i % NBUF
+        int lb, lo, hi;
+        vblock(g, vr, v0 + i, &lb, &lo, &hi);
+        int phys = scalar_ld(trow, __builtin_amdgcn_readfirstlane(lb));
+        phys = phys < 0 ? 0 : phys;
+        const uint8_t *src = head_base + (int64_t)phys * g.block_stride;
+        const uint32_t dst = ring0 + (uint32_t)((i % NBUF) * BLK);
+#pragma unroll
+        for (int j = 0; j < NI; ++j) dma16(src + swz(j * 64 + lane) * 16, dst + j * 1024);
+    };
+    const int pre = nblk < NBUF - 1 ? nblk : NBUF - 1;
+    for (int i = 0; i < pre; ++i) issue(i);
 
     // ---- q prologue: rotate at pos, fold the softmax scale (log2 domain)
     QRegs<T, D, G> q;
@@ -267,14 +327,6 @@ __global__ __launch_bounds__(64 * kWaves) void k_attn_valu(AttnArgs a) {
         }
     }
 
-    // ---- work range
-    const VisRange vr = vis_range(g, pos);
-    const int nv = vr.n_sb + vr.n_rb;
-    const int v0 = (int)((int64_t)split * nv / a.n_split);
-    const int v1 = (int)((int64_t)(split + 1) * nv / a.n_split);
-    const uint8_t *layer_base = g.kv + (int64_t)a.layer * g.layer_stride + (int64_t)kvh * g.head_stride;
-    const int32_t *trow = g.table + (int64_t)sid * g.row_len;
-
     float m[NH], lsum[NH];
 #pragma unroll
     for (int j = 0; j < NH; ++j) {
@@ -287,44 +339,43 @@ __global__ __launch_bounds__(64 * kWaves) void k_attn_valu(AttnArgs a) {
 #pragma unroll
         for (int r = 0; r < L::VD; ++r) acc[h][r] = 0.f;
 
-    auto load = [&](int v, Tile<T, D> &tl) {
+    for (int i = 0; i < nblk; ++i) {
+        if (i + NBUF - 1 < nblk) issue(i + NBUF - 1);
+        // wait for block i: the blocks issued after it may stay in flight
+        const int after = min(NBUF - 1, nblk - 1 - i);
+        if (after >= 3) vm_wait<3 * NI>();
+        else if (after == 2) vm_wait<2 * NI>();
+        else if (after == 1) vm_wait<NI>();
+        else vm_wait<0>();
+        const uint8_t *blk = &ring[wv][i % NBUF][0];
+        const int buf = i & 1;
         int lb, lo, hi;
-        vblock(g, vr, v, &lb, &lo, &hi);
-        int phys = trow[lb];
-        phys = phys < 0 ? 0 : phys;
-        const uint8_t *tile = layer_base + (int64_t)phys * g.block_stride;
-        const uint4 *kp = (const uint4 *)(tile + lane * L::NB);
-        const uint4 *vp = (const uint4 *)(tile + g.tile_bytes + lane * L::NB);
-#pragma unroll
-        for (int i = 0; i < L::NV4; ++i) tl.k[i] = kp[i];
-#pragma unroll
-        for (int i = 0; i < L::NV4; ++i) tl.v[i] = vp[i];
-    };
+        vblock(g, vr, v0 + i, &lb, &lo, &hi);
+        if (scalar_ld(trow, __builtin_amdgcn_readfirstlane(lb)) < 0) hi = lo;  // unassigned: nothing visible
 
-    int buf = 0;
-    auto process = [&](int v, Tile<T, D> &tl) {
-        int lb, lo, hi;
-        vblock(g, vr, v, &lb, &lo, &hi);
-        if (trow[lb] < 0) hi = lo;  // unassigned block: nothing visible
-        // QK: partial dot over this lane's quarter, then the quad all-reduce
+        // QK: this lane's quarter of key `key`, then the quad all-reduce
+        uint32_t kw[L::NV4 * 4];
+#pragma unroll
+        for (int c = 0; c < L::NV4; ++c) {
+            uint4 x = *(const uint4 *)(blk + swz(L::NV4 * lane + c) * 16);
+            kw[4 * c] = x.x; kw[4 * c + 1] = x.y; kw[4 * c + 2] = x.z; kw[4 * c + 3] = x.w;
+        }
         float sc[G];
-        const uint32_t *kw = (const uint32_t *)tl.k;
 #pragma unroll
         for (int h = 0; h < G; ++h) {
             float s = 0.f;
             if constexpr (sizeof(T) == 2) {
 #pragma unroll
-                for (int i = 0; i < D / 8; ++i) s = dot2_bf16(q.v[h][i], kw[i], s);
+                for (int c = 0; c < D / 8; ++c) s = dot2_bf16(q.v[h][c], kw[c], s);
             } else {
 #pragma unroll
-                for (int i = 0; i < D / 4; ++i) s = fmaf(q.v[h][i], __uint_as_float(kw[i]), s);
+                for (int c = 0; c < D / 4; ++c) s = fmaf(q.v[h][c], __uint_as_float(kw[c]), s);
             }
             s += dpp<kQuadXor1>(s);
             s += dpp<kQuadXor2>(s);
             sc[h] = s;
         }
         const bool valid = key >= lo && key < hi;
-        // online softmax for the heads this lane owns (h = qtr + 4j)
 #pragma unroll
         for (int j = 0; j < NH; ++j) {
             const int h = qtr + 4 * j;
@@ -333,26 +384,31 @@ __global__ __launch_bounds__(64 * kWaves) void k_attn_valu(AttnArgs a) {
 #pragma unroll
             for (int c = 1; c < G; ++c) s = (hs == c) ? sc[c] : s;
             s = valid ? s : -INFINITY;
-            float mx = keys_max(s);
-            float m_new = fmaxf(m[j], mx);
-            float mn = (m_new == -INFINITY) ? 0.f : m_new;
-            float alpha = __builtin_amdgcn_exp2f(m[j] - mn);
-            float p = __builtin_amdgcn_exp2f(s - mn);
+            const float mx = keys_max(s);
+            const float m_new = fmaxf(m[j], mx);
+            const float mn = (m_new == -INFINITY) ? 0.f : m_new;
+            const float alpha = __builtin_amdgcn_exp2f(m[j] - mn);
+            const float p = __builtin_amdgcn_exp2f(s - mn);
             lsum[j] = lsum[j] * alpha + p;
             m[j] = m_new;
             if (h < G) {
-                sPf[wv][buf][h][key] = p;
+                if constexpr (sizeof(T) == 2) {
+                    sP[wv][buf][h][key] = __builtin_bit_cast(uint16_t, (__bf16)p);
+                } else {
+                    sP[wv][buf][h][key] = p;
+                }
                 if (key == 0) sA[wv][buf][h] = alpha;
             }
         }
         wave_sync();
         // PV: lane owns V dims lane*VD .. +VD for all G heads
-        const uint32_t *vw = (const uint32_t *)tl.v;
         uint32_t vv[L::VD][L::VW];
 #pragma unroll
-        for (int r = 0; r < L::VD; ++r)
-#pragma unroll
-            for (int c = 0; c < L::VW; ++c) vv[r][c] = vw[r * L::VW + c];
+        for (int c = 0; c < L::NV4; ++c) {
+            uint4 x = *(const uint4 *)(blk + swz(NCH / 2 + L::NV4 * lane + c) * 16);
+            uint32_t *f = &vv[0][0];
+            f[4 * c] = x.x; f[4 * c + 1] = x.y; f[4 * c + 2] = x.z; f[4 * c + 3] = x.w;
+        }
         if (lo > 0 || hi < kBlock) {  // zero values of invisible slots (may be NaN)
 #pragma unroll
             for (int c = 0; c < L::VW; ++c) {
@@ -371,37 +427,24 @@ __global__ __launch_bounds__(64 * kWaves) void k_attn_valu(AttnArgs a) {
 #pragma unroll
         for (int h = 0; h < G; ++h) {
             const float al = sA[wv][buf][h];
-            const float *ph = sPf[wv][buf][h];
 #pragma unroll
             for (int r = 0; r < L::VD; ++r) acc[h][r] *= al;
             if constexpr (sizeof(T) == 2) {
-                uint32_t pp[kBlock / 2];
-#pragma unroll
-                for (int c = 0; c < kBlock / 2; ++c) pp[c] = pack_bf16x2(ph[2 * c], ph[2 * c + 1]);
+                const uint4 *pp4 = (const uint4 *)&sP[wv][buf][h][0];
+                uint4 pa = pp4[0], pb = pp4[1];
+                uint32_t pp[8] = {pa.x, pa.y, pa.z, pa.w, pb.x, pb.y, pb.z, pb.w};
 #pragma unroll
                 for (int r = 0; r < L::VD; ++r)
 #pragma unroll
                     for (int c = 0; c < kBlock / 2; ++c) acc[h][r] = dot2_bf16(pp[c], vv[r][c], acc[h][r]);
             } else {
+                const float *ph = &sP[wv][buf][h][0];
 #pragma unroll
                 for (int r = 0; r < L::VD; ++r)
 #pragma unroll
                     for (int c = 0; c < kBlock; ++c)
                         acc[h][r] = fmaf(ph[c], __uint_as_float(vv[r][c]), acc[h][r]);
             }
-        }
-        buf ^= 1;
-    };
-
-    if (v0 < v1) {
-        Tile<T, D> A, B;
-        load(v0, A);
-        for (int v = v0; v < v1; v += 2) {
-            if (v + 1 < v1) load(v + 1, B);
-            process(v, A);
-            if (v + 1 >= v1) break;
-            if (v + 2 < v1) load(v + 2, A);
-            process(v + 1, B);
         }
     }
 
@@ -509,14 +552,15 @@ __global__ void k_poison(PoolGeom g, int32_t n_layers, int64_t n_blocks,
 }
 
 // plain streaming copy, four 16-byte loads in flight per thread
-__global__ void k_copy(const uint4 *__restrict__ src, uint4 *__restrict__ dst, int64_t n) {
+typedef __attribute__((ext_vector_type(4))) uint32_t u32x4_t;
+__global__ void k_copy(const u32x4_t *__restrict__ src, u32x4_t *__restrict__ dst, int64_t n) {
     const int64_t stride = (int64_t)gridDim.x * blockDim.x;
     int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
     for (; i + 3 * stride < n; i += 4 * stride) {
-        uint4 a = __builtin_nontemporal_load(src + i);
-        uint4 b = __builtin_nontemporal_load(src + i + stride);
-        uint4 c = __builtin_nontemporal_load(src + i + 2 * stride);
-        uint4 d = __builtin_nontemporal_load(src + i + 3 * stride);
+        u32x4_t a = __builtin_nontemporal_load(src + i);
+        u32x4_t b = __builtin_nontemporal_load(src + i + stride);
+        u32x4_t c = __builtin_nontemporal_load(src + i + 2 * stride);
+        u32x4_t d = __builtin_nontemporal_load(src + i + 3 * stride);
         __builtin_nontemporal_store(a, dst + i);
         __builtin_nontemporal_store(b, dst + i + stride);
         __builtin_nontemporal_store(c, dst + i + 2 * stride);
@@ -937,8 +981,8 @@ hipError_t launch_copy(const void *src, void *dst, size_t bytes, hipStream_t s) 
     int64_t n = (int64_t)(bytes / 16);
     if (n == 0) return hipSuccess;
     int64_t grid = std::min<int64_t>((n + 255) / 256, 256 * 16);
-    hipLaunchKernelGGL(k_copy, dim3((unsigned)grid), dim3(256), 0, s, (const uint4 *)src,
-                       (uint4 *)dst, n);
+    hipLaunchKernelGGL(k_copy, dim3((unsigned)grid), dim3(256), 0, s, (const u32x4_t *)src,
+                       (u32x4_t *)dst, n);
     return hipGetLastError();
 }
 
