@@ -12,7 +12,8 @@ import os
 from typing import Optional, Sequence
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
-LIB_PATH = os.path.join(_HERE, "libmtn.so")
+# MTN_LIB selects another build of the same library (e.g. a tuning variant)
+LIB_PATH = os.environ.get("MTN_LIB") or os.path.join(_HERE, "libmtn.so")
 
 MTN_OK = 0
 MTN_ERR_INVALID_ARG = -1

@@ -39,19 +39,22 @@ def _run(cmd, verbose):
         print(rest)
 
 
-def build(verbose: bool = False) -> str:
-    """Compile every source for gfx950 and link libmtn.so next to this file."""
+def build(verbose: bool = False, out: str = LIB, defines=()) -> str:
+    """Compile every source for gfx950 and link libmtn.so next to this file
+    (or at ``out``, with extra ``-D`` ``defines`` for tuning variants)."""
     objs = []
-    bdir = os.path.join(ROOT, "_build")
+    tag = "_".join(d.replace("=", "") for d in defines)
+    bdir = os.path.join(ROOT, "_build", tag) if tag else os.path.join(ROOT, "_build")
     os.makedirs(bdir, exist_ok=True)
     for src in SOURCES:
         obj = os.path.join(bdir, src + ".o")
-        _run([HIPCC, *COMMON, "-c", os.path.join(CSRC, src), "-o", obj], verbose)
+        _run([HIPCC, *COMMON, *[f"-D{d}" for d in defines], "-c", os.path.join(CSRC, src),
+              "-o", obj], verbose)
         objs.append(obj)
-    tmp = LIB + ".tmp"
+    tmp = out + ".tmp"
     _run([HIPCC, f"--offload-arch={ARCH}", "-shared", "-fPIC", *objs, "-o", tmp], verbose)
-    os.replace(tmp, LIB)
-    return LIB
+    os.replace(tmp, out)
+    return out
 
 
 if __name__ == "__main__":

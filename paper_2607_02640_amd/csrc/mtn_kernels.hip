@@ -66,21 +66,46 @@ __device__ __forceinline__ float shfl_xor_f(float x, int m) {
     return __shfl_xor(x, m, 64);
 }
 
+// Exchange between rows (16-lane groups) with the gfx950 permlane swaps: the
+// two results hold x of row pairs (0,1),(2,3) resp. of the two half-waves,
+// so combining them reduces across the pair.  Pure VALU, no LDS round trip.
+// The second operand is an opaque copy of x: given one value for both
+// operands the compiler folds the two results into one.
+__device__ __forceinline__ unsigned opaque_copy(unsigned x) {
+    unsigned y;
+    asm volatile("v_mov_b32 %0, %1" : "=v"(y) : "v"(x));
+    return y;
+}
+template <bool SUM, bool HALF>
+__device__ __forceinline__ float rows_pair(float x) {
+    const unsigned u = __builtin_bit_cast(unsigned, x);
+    unsigned a, b;
+    if constexpr (HALF) {
+        auto r = __builtin_amdgcn_permlane32_swap(u, opaque_copy(u), false, false);
+        a = r[0];
+        b = r[1];
+    } else {
+        auto r = __builtin_amdgcn_permlane16_swap(u, opaque_copy(u), false, false);
+        a = r[0];
+        b = r[1];
+    }
+    const float fa = __builtin_bit_cast(float, a), fb = __builtin_bit_cast(float, b);
+    return SUM ? fa + fb : fmaxf(fa, fb);
+}
+
 // max / sum over the 16 lanes that share (lane & 3) -- i.e. over the 16 keys
 // of a block for one quarter index
 __device__ __forceinline__ float keys_max(float x) {
     x = fmaxf(x, dpp<kRowRor4>(x));
     x = fmaxf(x, dpp<kRowRor8>(x));
-    x = fmaxf(x, shfl_xor_f(x, 16));
-    x = fmaxf(x, shfl_xor_f(x, 32));
-    return x;
+    x = rows_pair<false, false>(x);
+    return rows_pair<false, true>(x);
 }
 __device__ __forceinline__ float keys_sum(float x) {
     x += dpp<kRowRor4>(x);
     x += dpp<kRowRor8>(x);
-    x += shfl_xor_f(x, 16);
-    x += shfl_xor_f(x, 32);
-    return x;
+    x = rows_pair<true, false>(x);
+    return rows_pair<true, true>(x);
 }
 
 __device__ __forceinline__ void wave_sync() {
@@ -132,6 +157,40 @@ __device__ __forceinline__ void vblock(const PoolGeom &g, const VisRange &r, int
     *lo = (u == 0) ? r.first % kBlock : 0;
     *hi = (u == r.n_rb - 1) ? ((r.first % kBlock) + r.ring_n - 1) % kBlock + 1 : kBlock;
 }
+
+// Walks the virtual blocks v0, v0 + 1, ... of one query without integer
+// division inside the loop (one modulo at construction).
+struct BlockIter {
+    int v, n_sb, sink_tokens, n_rb, first_off, last_hi, rb, ring_blocks, nsb, rb_start;
+    __device__ __forceinline__ BlockIter(const PoolGeom &g, const VisRange &r, int v0) {
+        v = v0;
+        n_sb = r.n_sb;
+        sink_tokens = r.sink_tokens;
+        n_rb = r.n_rb;
+        first_off = r.first % kBlock;
+        last_hi = r.ring_n > 0 ? (first_off + r.ring_n - 1) % kBlock + 1 : 0;
+        ring_blocks = g.ring / kBlock;
+        nsb = g.n_sink_blocks;
+        rb_start = r.first / kBlock;
+        rb = v0 > n_sb ? (rb_start + (v0 - n_sb)) % ring_blocks : rb_start;
+    }
+    __device__ __forceinline__ void get(int *lb, int *lo, int *hi) const {
+        if (v < n_sb) {
+            *lb = v;
+            *lo = 0;
+            *hi = min(kBlock, sink_tokens - v * kBlock);
+        } else {
+            const int u = v - n_sb;
+            *lb = nsb + rb;
+            *lo = (u == 0) ? first_off : 0;
+            *hi = (u == n_rb - 1) ? last_hi : kBlock;
+        }
+    }
+    __device__ __forceinline__ void next() {
+        if (v >= n_sb) rb = (rb + 1 == ring_blocks) ? 0 : rb + 1;
+        ++v;
+    }
+};
 
 // ---------------------------------------------------------------------------
 // plan apply: block-table updates + RoPE (cos, sin) table in fp64
@@ -211,7 +270,10 @@ struct QRegs<float, D, G> {
 };
 
 constexpr int kWaves = 4;     // independent waves per workgroup
-constexpr int kRingBytes = 32768;  // per-wave LDS ring for K/V^T blocks
+#ifndef MTN_DECODE_RING_KB
+#define MTN_DECODE_RING_KB 32
+#endif
+constexpr int kRingBytes = MTN_DECODE_RING_KB * 1024;  // per-wave LDS ring of K/V^T blocks
 
 // Asynchronous 16-byte-per-lane copy global -> LDS (gfx950 LDS DMA).  Lane i
 // of the wave writes LDS bytes [lds + 16 i, lds + 16 i + 16).  Issued from
@@ -249,7 +311,7 @@ __global__ __launch_bounds__(64 * kWaves) void k_attn_valu(AttnArgs a) {
     using L = Lay<T, D>;
     constexpr int NH = (G + 3) / 4;                 // heads owned per lane in the softmax
     constexpr int BLK = 2 * kBlock * D * L::E;      // K + V^T bytes of one block (one head)
-    constexpr int NBUF = kRingBytes / BLK < 4 ? kRingBytes / BLK : 4;
+    constexpr int NBUF = kRingBytes / BLK < 2 ? 2 : (kRingBytes / BLK < 4 ? kRingBytes / BLK : 4);
     constexpr int NCH = BLK / 16;                   // 16-byte chunks per block
     constexpr int NI = NCH / 64;                    // DMA instructions per block
     static_assert(NBUF >= 2, "ring too small");
@@ -286,9 +348,11 @@ __global__ __launch_bounds__(64 * kWaves) void k_attn_valu(AttnArgs a) {
     const int32_t *trow = g.table + (int64_t)sid * g.row_len;
     const uint32_t ring0 = lds_addr(&ring[wv][0][0]);
 
-    auto issue = [&](int i) {  // block i of this wave's range -> ring slot i % NBUF
+    BlockIter it_issue(g, vr, v0), it_proc(g, vr, v0);
+    auto issue = [&](int i) {  // next block of this wave's range -> ring slot i % NBUF
         int lb, lo, hi;
-        vblock(g, vr, v0 + i, &lb, &lo, &hi);
+        it_issue.get(&lb, &lo, &hi);
+        it_issue.next();
         int phys = scalar_ld(trow, __builtin_amdgcn_readfirstlane(lb));
         phys = phys < 0 ? 0 : phys;
         const uint8_t *src = head_base + (int64_t)phys * g.block_stride;
@@ -302,26 +366,47 @@ __global__ __launch_bounds__(64 * kWaves) void k_attn_valu(AttnArgs a) {
     // ---- q prologue: rotate at pos, fold the softmax scale (log2 domain)
     QRegs<T, D, G> q;
     {
+        // each lane reads its quarter and the RoPE partner quarter of every
+        // head as whole 16-byte vectors
         const T *qb = (const T *)a.q + (row * g.hq + (int64_t)kvh * G) * D;
         const float2 *rp = a.p.rope + (int64_t)t * (D / 2) + (qtr & 1) * L::QD;
         const int d0 = qtr * L::QD;
         const int dp = (qtr ^ 2) * L::QD;
         const float sgn = (qtr < 2) ? -1.f : 1.f;
+        constexpr int EPV = 16 / L::E;        // elements per 16-byte vector
+        constexpr int NVQ = L::QD / EPV;      // vectors per quarter
 #pragma unroll
         for (int h = 0; h < G; ++h) {
-            const T *qh = qb + (int64_t)h * D;
+            const uint4 *qa = (const uint4 *)(qb + (int64_t)h * D + d0);
+            const uint4 *qp = (const uint4 *)(qb + (int64_t)h * D + dp);
 #pragma unroll
-            for (int i = 0; i < L::QD; i += 2) {
-                float2 c0 = rp[i], c1 = rp[i + 1];
-                float x0 = to_f32(qh[d0 + i]), x1 = to_f32(qh[d0 + i + 1]);
-                float y0 = to_f32(qh[dp + i]), y1 = to_f32(qh[dp + i + 1]);
-                float r0 = fmaf(x0, c0.x, sgn * y0 * c0.y) * a.scale_log2;
-                float r1 = fmaf(x1, c1.x, sgn * y1 * c1.y) * a.scale_log2;
-                if constexpr (sizeof(T) == 2) {
-                    q.v[h][i / 2] = pack_bf16x2(r0, r1);
-                } else {
-                    q.v[h][i] = r0;
-                    q.v[h][i + 1] = r1;
+            for (int vq = 0; vq < NVQ; ++vq) {
+                uint4 xa = qa[vq], xp = qp[vq];
+                const uint32_t wa[4] = {xa.x, xa.y, xa.z, xa.w};
+                const uint32_t wp[4] = {xp.x, xp.y, xp.z, xp.w};
+                float xs[EPV], ys[EPV];
+#pragma unroll
+                for (int e = 0; e < EPV; ++e) {
+                    if constexpr (sizeof(T) == 2) {
+                        xs[e] = __uint_as_float((e & 1) ? (wa[e / 2] & 0xFFFF0000u) : (wa[e / 2] << 16));
+                        ys[e] = __uint_as_float((e & 1) ? (wp[e / 2] & 0xFFFF0000u) : (wp[e / 2] << 16));
+                    } else {
+                        xs[e] = __uint_as_float(wa[e]);
+                        ys[e] = __uint_as_float(wp[e]);
+                    }
+                }
+#pragma unroll
+                for (int e = 0; e < EPV; e += 2) {
+                    const int i = vq * EPV + e;
+                    float2 c0 = rp[i], c1 = rp[i + 1];
+                    float r0 = fmaf(xs[e], c0.x, sgn * ys[e] * c0.y) * a.scale_log2;
+                    float r1 = fmaf(xs[e + 1], c1.x, sgn * ys[e + 1] * c1.y) * a.scale_log2;
+                    if constexpr (sizeof(T) == 2) {
+                        q.v[h][i / 2] = pack_bf16x2(r0, r1);
+                    } else {
+                        q.v[h][i] = r0;
+                        q.v[h][i + 1] = r1;
+                    }
                 }
             }
         }
@@ -350,7 +435,8 @@ __global__ __launch_bounds__(64 * kWaves) void k_attn_valu(AttnArgs a) {
         const uint8_t *blk = &ring[wv][i % NBUF][0];
         const int buf = i & 1;
         int lb, lo, hi;
-        vblock(g, vr, v0 + i, &lb, &lo, &hi);
+        it_proc.get(&lb, &lo, &hi);
+        it_proc.next();
         if (scalar_ld(trow, __builtin_amdgcn_readfirstlane(lb)) < 0) hi = lo;  // unassigned: nothing visible
 
         // QK: this lane's quarter of key `key`, then the quad all-reduce
