@@ -61,6 +61,7 @@ constexpr int kQuadXor1 = 0xB1;  // quad_perm [1,0,3,2]
 constexpr int kQuadXor2 = 0x4E;  // quad_perm [2,3,0,1]
 constexpr int kRowRor4 = 0x124;  // row_ror:4
 constexpr int kRowRor8 = 0x128;  // row_ror:8
+constexpr int kRowShr4 = 0x114;  // row_shr:4 (lane i takes lane i - 4 of its row)
 
 __device__ __forceinline__ float shfl_xor_f(float x, int m) {
     return __shfl_xor(x, m, 64);
@@ -269,11 +270,10 @@ struct QRegs<float, D, G> {
     float v[G][D / 4];
 };
 
-constexpr int kWaves = 4;     // independent waves per workgroup
 #ifndef MTN_DECODE_RING_KB
 #define MTN_DECODE_RING_KB 32
 #endif
-constexpr int kRingBytes = MTN_DECODE_RING_KB * 1024;  // per-wave LDS ring of K/V^T blocks
+constexpr int kRingBytes = MTN_DECODE_RING_KB * 1024;  // LDS ring of K/V^T blocks per unit
 
 // Asynchronous 16-byte-per-lane copy global -> LDS (gfx950 LDS DMA).  Lane i
 // of the wave writes LDS bytes [lds + 16 i, lds + 16 i + 16).  Issued from
@@ -306,30 +306,35 @@ __device__ __forceinline__ int32_t scalar_ld(const int32_t *p, int idx) {
 // rotated so that eight consecutive lanes read eight distinct LDS bank groups.
 __device__ __forceinline__ int swz(int x) { return x ^ ((x >> 3) & 3); }
 
-template <typename T, int D, int G>
-__global__ __launch_bounds__(64 * kWaves) void k_attn_valu(AttnArgs a) {
+// One work unit = (query token, kv head, split segment), served by one
+// workgroup of WPU waves.  The waves share a ring of K/V^T blocks in LDS
+// (each issues 1/WPU of every block's DMA) and split the G query heads of the
+// group: wave w owns heads w*HW .. w*HW + HW - 1, HW = G / WPU <= 4, so every
+// lane owns at most one head in the online softmax.  One barrier per block
+// publishes the landed block and frees the buffer consumed before it.
+template <typename T, int D, int G, int WPU>
+__global__ __launch_bounds__(64 * WPU) void k_attn_valu(AttnArgs a) {
     using L = Lay<T, D>;
-    constexpr int NH = (G + 3) / 4;                 // heads owned per lane in the softmax
+    constexpr int HW = G / WPU;                     // heads per wave
+    static_assert(HW * WPU == G && HW <= 4, "head split");
     constexpr int BLK = 2 * kBlock * D * L::E;      // K + V^T bytes of one block (one head)
     constexpr int NBUF = kRingBytes / BLK < 2 ? 2 : (kRingBytes / BLK < 4 ? kRingBytes / BLK : 4);
     constexpr int NCH = BLK / 16;                   // 16-byte chunks per block
     constexpr int NI = NCH / 64;                    // DMA instructions per block
-    static_assert(NBUF >= 2, "ring too small");
-    using PT = typename std::conditional<sizeof(T) == 2, uint16_t, float>::type;
-    __shared__ __attribute__((aligned(16))) uint8_t ring[kWaves][NBUF][BLK];
-    __shared__ __attribute__((aligned(16))) PT sP[kWaves][2][G][kBlock];
-    __shared__ float sA[kWaves][2][G];
-    __shared__ float sM[kWaves][G], sL[kWaves][G];
+    constexpr int NIW = NI / WPU;                   // ... issued by each wave
+    static_assert(NIW * WPU == NI && NIW >= 1, "DMA split");
+    __shared__ __attribute__((aligned(16))) uint8_t ring[NBUF][BLK];
+    __shared__ __attribute__((aligned(16))) float sP[WPU][sizeof(T) == 2 ? 1 : 2][HW][kBlock];
+    __shared__ float sA[WPU][2][HW];
+    __shared__ float sM[WPU][HW], sL[WPU][HW];
 
     const int lane = threadIdx.x & 63;
     // wave-uniform indices live in scalar registers: the block-table and plan
     // reads below become scalar loads, which do not share the vector-memory
     // counter the LDS ring is synchronised with
     const int wv = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
-    const int64_t unit = (int64_t)blockIdx.x * kWaves + wv;
+    const int64_t unit = blockIdx.x;
     const PoolGeom &g = a.g;
-    const int64_t n_units = (int64_t)a.p.n_tok * g.hkv * a.n_split;
-    if (unit >= n_units) return;
     const int split = __builtin_amdgcn_readfirstlane((int)(unit % a.n_split));
     const int kvh = __builtin_amdgcn_readfirstlane((int)((unit / a.n_split) % g.hkv));
     const int t = __builtin_amdgcn_readfirstlane((int)(unit / ((int64_t)a.n_split * g.hkv)));
@@ -337,6 +342,7 @@ __global__ __launch_bounds__(64 * kWaves) void k_attn_valu(AttnArgs a) {
     const int pos = __builtin_amdgcn_readfirstlane(a.p.tok_pos[t]);
     const int64_t row = __builtin_amdgcn_readfirstlane(a.p.tok_row[t]);
     const int key = lane >> 2, qtr = lane & 3;
+    const int h0 = wv * HW;  // first head of this wave inside the group
 
     // ---- work range and the first prefetches (issued before the q prologue)
     const VisRange vr = vis_range(g, pos);
@@ -346,10 +352,10 @@ __global__ __launch_bounds__(64 * kWaves) void k_attn_valu(AttnArgs a) {
     const int nblk = v1 - v0;
     const uint8_t *head_base = g.kv + (int64_t)a.layer * g.layer_stride + (int64_t)kvh * g.head_stride;
     const int32_t *trow = g.table + (int64_t)sid * g.row_len;
-    const uint32_t ring0 = lds_addr(&ring[wv][0][0]);
+    const uint32_t ring0 = lds_addr(&ring[0][0]);
 
     BlockIter it_issue(g, vr, v0), it_proc(g, vr, v0);
-    auto issue = [&](int i) {  // next block of this wave's range -> ring slot i % NBUF
+    auto issue = [&](int i) {  // next block of the range -> ring slot i % NBUF (this wave's share)
         int lb, lo, hi;
         it_issue.get(&lb, &lo, &hi);
         it_issue.next();
@@ -358,17 +364,20 @@ __global__ __launch_bounds__(64 * kWaves) void k_attn_valu(AttnArgs a) {
         const uint8_t *src = head_base + (int64_t)phys * g.block_stride;
         const uint32_t dst = ring0 + (uint32_t)((i % NBUF) * BLK);
 #pragma unroll
-        for (int j = 0; j < NI; ++j) dma16(src + swz(j * 64 + lane) * 16, dst + j * 1024);
+        for (int jj = 0; jj < NIW; ++jj) {
+            const int j = wv * NIW + jj;
+            dma16(src + swz(j * 64 + lane) * 16, dst + j * 1024);
+        }
     };
     const int pre = nblk < NBUF - 1 ? nblk : NBUF - 1;
     for (int i = 0; i < pre; ++i) issue(i);
 
     // ---- q prologue: rotate at pos, fold the softmax scale (log2 domain)
-    QRegs<T, D, G> q;
+    QRegs<T, D, HW> q;
     {
         // each lane reads its quarter and the RoPE partner quarter of every
         // head as whole 16-byte vectors
-        const T *qb = (const T *)a.q + (row * g.hq + (int64_t)kvh * G) * D;
+        const T *qb = (const T *)a.q + (row * g.hq + (int64_t)kvh * G + h0) * D;
         const float2 *rp = a.p.rope + (int64_t)t * (D / 2) + (qtr & 1) * L::QD;
         const int d0 = qtr * L::QD;
         const int dp = (qtr ^ 2) * L::QD;
@@ -376,7 +385,7 @@ __global__ __launch_bounds__(64 * kWaves) void k_attn_valu(AttnArgs a) {
         constexpr int EPV = 16 / L::E;        // elements per 16-byte vector
         constexpr int NVQ = L::QD / EPV;      // vectors per quarter
 #pragma unroll
-        for (int h = 0; h < G; ++h) {
+        for (int h = 0; h < HW; ++h) {
             const uint4 *qa = (const uint4 *)(qb + (int64_t)h * D + d0);
             const uint4 *qp = (const uint4 *)(qb + (int64_t)h * D + dp);
 #pragma unroll
@@ -412,27 +421,26 @@ __global__ __launch_bounds__(64 * kWaves) void k_attn_valu(AttnArgs a) {
         }
     }
 
-    float m[NH], lsum[NH];
+    // the head this lane owns in the softmax (lanes with qtr >= HW duplicate)
+    const int hown = qtr < HW ? qtr : qtr % HW;
+    float m = -INFINITY, lsum = 0.f;
+    float acc[HW][L::VD];
 #pragma unroll
-    for (int j = 0; j < NH; ++j) {
-        m[j] = -INFINITY;
-        lsum[j] = 0.f;
-    }
-    float acc[G][L::VD];
-#pragma unroll
-    for (int h = 0; h < G; ++h)
+    for (int h = 0; h < HW; ++h)
 #pragma unroll
         for (int r = 0; r < L::VD; ++r) acc[h][r] = 0.f;
 
     for (int i = 0; i < nblk; ++i) {
-        if (i + NBUF - 1 < nblk) issue(i + NBUF - 1);
-        // wait for block i: the blocks issued after it may stay in flight
-        const int after = min(NBUF - 1, nblk - 1 - i);
-        if (after >= 3) vm_wait<3 * NI>();
-        else if (after == 2) vm_wait<2 * NI>();
-        else if (after == 1) vm_wait<NI>();
+        // this wave's share of block i has landed once at most the shares of
+        // the blocks issued after it are outstanding; the barrier then covers
+        // the other waves' shares and frees the buffer of block i - 1
+        const int after = min(NBUF - 2, nblk - 1 - i);
+        if (after >= 2) vm_wait<2 * NIW>();
+        else if (after == 1) vm_wait<NIW>();
         else vm_wait<0>();
-        const uint8_t *blk = &ring[wv][i % NBUF][0];
+        if constexpr (WPU > 1) __syncthreads();
+        if (i + NBUF - 1 < nblk) issue(i + NBUF - 1);
+        const uint8_t *blk = &ring[i % NBUF][0];
         const int buf = i & 1;
         int lb, lo, hi;
         it_proc.get(&lb, &lo, &hi);
@@ -446,48 +454,7 @@ __global__ __launch_bounds__(64 * kWaves) void k_attn_valu(AttnArgs a) {
             uint4 x = *(const uint4 *)(blk + swz(L::NV4 * lane + c) * 16);
             kw[4 * c] = x.x; kw[4 * c + 1] = x.y; kw[4 * c + 2] = x.z; kw[4 * c + 3] = x.w;
         }
-        float sc[G];
-#pragma unroll
-        for (int h = 0; h < G; ++h) {
-            float s = 0.f;
-            if constexpr (sizeof(T) == 2) {
-#pragma unroll
-                for (int c = 0; c < D / 8; ++c) s = dot2_bf16(q.v[h][c], kw[c], s);
-            } else {
-#pragma unroll
-                for (int c = 0; c < D / 4; ++c) s = fmaf(q.v[h][c], __uint_as_float(kw[c]), s);
-            }
-            s += dpp<kQuadXor1>(s);
-            s += dpp<kQuadXor2>(s);
-            sc[h] = s;
-        }
-        const bool valid = key >= lo && key < hi;
-#pragma unroll
-        for (int j = 0; j < NH; ++j) {
-            const int h = qtr + 4 * j;
-            const int hs = (h < G) ? h : (h % G);
-            float s = sc[0];
-#pragma unroll
-            for (int c = 1; c < G; ++c) s = (hs == c) ? sc[c] : s;
-            s = valid ? s : -INFINITY;
-            const float mx = keys_max(s);
-            const float m_new = fmaxf(m[j], mx);
-            const float mn = (m_new == -INFINITY) ? 0.f : m_new;
-            const float alpha = __builtin_amdgcn_exp2f(m[j] - mn);
-            const float p = __builtin_amdgcn_exp2f(s - mn);
-            lsum[j] = lsum[j] * alpha + p;
-            m[j] = m_new;
-            if (h < G) {
-                if constexpr (sizeof(T) == 2) {
-                    sP[wv][buf][h][key] = __builtin_bit_cast(uint16_t, (__bf16)p);
-                } else {
-                    sP[wv][buf][h][key] = p;
-                }
-                if (key == 0) sA[wv][buf][h] = alpha;
-            }
-        }
-        wave_sync();
-        // PV: lane owns V dims lane*VD .. +VD for all G heads
+        // V^T slice read early: independent of the softmax
         uint32_t vv[L::VD][L::VW];
 #pragma unroll
         for (int c = 0; c < L::NV4; ++c) {
@@ -495,6 +462,38 @@ __global__ __launch_bounds__(64 * kWaves) void k_attn_valu(AttnArgs a) {
             uint32_t *f = &vv[0][0];
             f[4 * c] = x.x; f[4 * c + 1] = x.y; f[4 * c + 2] = x.z; f[4 * c + 3] = x.w;
         }
+        // heads innermost: HW independent accumulation chains interleave
+        float sc[HW];
+#pragma unroll
+        for (int h = 0; h < HW; ++h) sc[h] = 0.f;
+        if constexpr (sizeof(T) == 2) {
+#pragma unroll
+            for (int c = 0; c < D / 8; ++c)
+#pragma unroll
+                for (int h = 0; h < HW; ++h) sc[h] = dot2_bf16(q.v[h][c], kw[c], sc[h]);
+        } else {
+#pragma unroll
+            for (int c = 0; c < D / 4; ++c)
+#pragma unroll
+                for (int h = 0; h < HW; ++h) sc[h] = fmaf(q.v[h][c], __uint_as_float(kw[c]), sc[h]);
+        }
+#pragma unroll
+        for (int h = 0; h < HW; ++h) sc[h] += dpp<kQuadXor1>(sc[h]);
+#pragma unroll
+        for (int h = 0; h < HW; ++h) sc[h] += dpp<kQuadXor2>(sc[h]);
+        // online softmax of the owned head
+        const bool valid = key >= lo && key < hi;
+        float s = sc[0];
+#pragma unroll
+        for (int c = 1; c < HW; ++c) s = (hown == c) ? sc[c] : s;
+        s = valid ? s : -INFINITY;
+        const float mx = keys_max(s);
+        const float m_new = fmaxf(m, mx);
+        const float mn = (m_new == -INFINITY) ? 0.f : m_new;
+        const float alpha = __builtin_amdgcn_exp2f(m - mn);
+        const float p = __builtin_amdgcn_exp2f(s - mn);
+        lsum = lsum * alpha + p;
+        m = m_new;
         if (lo > 0 || hi < kBlock) {  // zero values of invisible slots (may be NaN)
 #pragma unroll
             for (int c = 0; c < L::VW; ++c) {
@@ -510,51 +509,74 @@ __global__ __launch_bounds__(64 * kWaves) void k_attn_valu(AttnArgs a) {
                 for (int r = 0; r < L::VD; ++r) vv[r][c] &= mask;
             }
         }
+        if constexpr (sizeof(T) == 2) {
+            // P and alpha reach the PV lanes through scalar registers: the lane
+            // of key 2c+1 packs (p[2c], p[2c+1]) (DPP row shift by one key),
+            // readlane broadcasts it, and dot2 takes it as a scalar operand
+            const float p_prev = dpp<kRowShr4>(p);
+            const uint32_t packed = pack_bf16x2(p_prev, p);
+            uint32_t pp[HW][kBlock / 2];
+            float al[HW];
 #pragma unroll
-        for (int h = 0; h < G; ++h) {
-            const float al = sA[wv][buf][h];
+            for (int h = 0; h < HW; ++h) {
+                al[h] = __builtin_bit_cast(float,
+                                           __builtin_amdgcn_readlane(__builtin_bit_cast(int, alpha), h));
 #pragma unroll
-            for (int r = 0; r < L::VD; ++r) acc[h][r] *= al;
-            if constexpr (sizeof(T) == 2) {
-                const uint4 *pp4 = (const uint4 *)&sP[wv][buf][h][0];
-                uint4 pa = pp4[0], pb = pp4[1];
-                uint32_t pp[8] = {pa.x, pa.y, pa.z, pa.w, pb.x, pb.y, pb.z, pb.w};
-#pragma unroll
-                for (int r = 0; r < L::VD; ++r)
-#pragma unroll
-                    for (int c = 0; c < kBlock / 2; ++c) acc[h][r] = dot2_bf16(pp[c], vv[r][c], acc[h][r]);
-            } else {
-                const float *ph = &sP[wv][buf][h][0];
-#pragma unroll
-                for (int r = 0; r < L::VD; ++r)
-#pragma unroll
-                    for (int c = 0; c < kBlock; ++c)
-                        acc[h][r] = fmaf(ph[c], __uint_as_float(vv[r][c]), acc[h][r]);
+                for (int c = 0; c < kBlock / 2; ++c)
+                    pp[h][c] = (uint32_t)__builtin_amdgcn_readlane((int)packed, 8 * c + 4 + h);
             }
+#pragma unroll
+            for (int h = 0; h < HW; ++h)
+#pragma unroll
+                for (int r = 0; r < L::VD; ++r) acc[h][r] *= al[h];
+#pragma unroll
+            for (int c = 0; c < kBlock / 2; ++c)
+#pragma unroll
+                for (int h = 0; h < HW; ++h)
+#pragma unroll
+                    for (int r = 0; r < L::VD; ++r) acc[h][r] = dot2_bf16(pp[h][c], vv[r][c], acc[h][r]);
+        } else {
+            if (qtr < HW) {
+                sP[wv][buf][qtr][key] = p;
+                if (key == 0) sA[wv][buf][qtr] = alpha;
+            }
+            wave_sync();
+#pragma unroll
+            for (int h = 0; h < HW; ++h) {
+                const float al = sA[wv][buf][h];
+#pragma unroll
+                for (int r = 0; r < L::VD; ++r) acc[h][r] *= al;
+            }
+#pragma unroll
+            for (int c = 0; c < kBlock; ++c)
+#pragma unroll
+                for (int h = 0; h < HW; ++h) {
+                    const float pc = sP[wv][buf][h][c];
+#pragma unroll
+                    for (int r = 0; r < L::VD; ++r) acc[h][r] = fmaf(pc, __uint_as_float(vv[r][c]), acc[h][r]);
+                }
         }
     }
 
     // ---- finish: reduce the per-lane partial sums, publish (m, l) per head
-#pragma unroll
-    for (int j = 0; j < NH; ++j) {
-        const int h = qtr + 4 * j;
-        float lt = keys_sum(lsum[j]);
-        if (h < G && key == 0) {
-            sM[wv][h] = m[j];
-            sL[wv][h] = lt;
+    {
+        const float lt = keys_sum(lsum);
+        if (qtr < HW && key == 0) {
+            sM[wv][qtr] = m;
+            sL[wv][qtr] = lt;
         }
     }
     wave_sync();
-    const int hq0 = kvh * G;
+    const int hq0 = kvh * G + h0;
     if (a.n_split == 1) {
         T *ob = (T *)a.out + (row * g.hq + hq0) * D;
 #pragma unroll
-        for (int h = 0; h < G; ++h) {
+        for (int h = 0; h < HW; ++h) {
             const float inv = 1.f / sL[wv][h];
 #pragma unroll
             for (int r = 0; r < L::VD; ++r) ob[(int64_t)h * D + lane * L::VD + r] = from_f32<T>(acc[h][r] * inv);
         }
-        if (a.lse && lane < G)
+        if (a.lse && lane < HW)
             a.lse[row * g.hq + hq0 + lane] =
                 (sM[wv][lane] + __builtin_amdgcn_logf(sL[wv][lane])) * 0.6931471805599453f;
     } else {
@@ -562,12 +584,12 @@ __global__ __launch_bounds__(64 * kWaves) void k_attn_valu(AttnArgs a) {
         float *pacc = a.part;
         float *pml = a.part + (int64_t)a.p.n_tok * g.hq * ns * D;
 #pragma unroll
-        for (int h = 0; h < G; ++h) {
+        for (int h = 0; h < HW; ++h) {
             int64_t base = (((int64_t)t * g.hq + hq0 + h) * ns + split);
 #pragma unroll
             for (int r = 0; r < L::VD; ++r) pacc[base * D + lane * L::VD + r] = acc[h][r];
         }
-        if (lane < G) {
+        if (lane < HW) {
             int64_t base = (((int64_t)t * g.hq + hq0 + lane) * ns + split);
             pml[base * 2] = sM[wv][lane];
             pml[base * 2 + 1] = sL[wv][lane];
@@ -955,10 +977,10 @@ __global__ __launch_bounds__(64 * kPfWaves) void k_prefill_mfma(PfArgs pa) {
 
 template <typename T, int D, int G>
 hipError_t launch_valu_t(const AttnArgs &a, hipStream_t s) {
+    constexpr int WPU = G >= 4 ? G / 4 : 1;
     int64_t units = (int64_t)a.p.n_tok * a.g.hkv * a.n_split;
     if (units == 0) return hipSuccess;
-    int64_t grid = (units + kWaves - 1) / kWaves;
-    hipLaunchKernelGGL((k_attn_valu<T, D, G>), dim3((unsigned)grid), dim3(64 * kWaves), 0, s, a);
+    hipLaunchKernelGGL((k_attn_valu<T, D, G, WPU>), dim3((unsigned)units), dim3(64 * WPU), 0, s, a);
     return hipGetLastError();
 }
 
@@ -978,7 +1000,6 @@ hipError_t launch_valu_d(const AttnArgs &a, int G, hipStream_t s) {
 bool attn_valu_supported(int dtype, int d, int g) {
     if (g != 1 && g != 2 && g != 4 && g != 8) return false;
     if (d != 64 && d != 128) return false;
-    if (dtype == 0 && d == 128 && g == 8) return false;  // register budget
     return dtype == 0 || dtype == 1;
 }
 
