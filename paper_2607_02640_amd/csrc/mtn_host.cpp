@@ -110,6 +110,7 @@ struct mtn_pool {
     int stage_i = 0;
     PlanView view{};
     int32_t *d_seq_first = nullptr, *d_seq_ntok = nullptr;
+    int32_t resident_units = 0;    // decode work units resident on the whole GPU
 
     // timing
     bool timing = false;
@@ -417,17 +418,21 @@ AttnArgs attn_args(mtn_pool *P, int32_t layer, const void *q, void *out, float *
     return a;
 }
 
-// Decode split heuristic: enough wave-level work units to fill the chip
-// several times over, without splitting short windows into tiny segments.
+// Decode split heuristic.  A unit (query, kv head, segment) streams its keys
+// through an LDS ring whose pipeline fills at the start and drains at the
+// end, so units should be long, and a partly filled last round of units
+// leaves CUs idle.  So: if the unsplit units already fill the resident slots,
+// keep them whole; otherwise split just enough to fill one round, keeping at
+// least 16 blocks per segment.
 int32_t auto_split(const mtn_pool *P, int32_t n_items) {
     int64_t units = (int64_t)n_items * P->cfg.n_kv_heads;
     int64_t max_keys = P->unbounded ? P->cfg.max_len : (int64_t)P->S + P->W;
     int64_t blocks = ceil_div(max_keys, kBlock) + 1;
-    int64_t target = 4096;  // waves: 256 CUs x 16
-    int64_t sp = ceil_div(target, std::max<int64_t>(units, 1));
-    sp = std::min<int64_t>(sp, std::max<int64_t>(1, blocks / 8));
-    sp = std::max<int64_t>(1, std::min<int64_t>(sp, kMaxSplit));
-    return (int32_t)sp;
+    int64_t resident = std::max<int32_t>(P->resident_units, 1);
+    if (units >= resident) return 1;
+    int64_t sp = resident / std::max<int64_t>(units, 1);
+    sp = std::min<int64_t>(sp, std::max<int64_t>(1, blocks / 16));
+    return (int32_t)std::max<int64_t>(1, std::min<int64_t>(sp, kMaxSplit));
 }
 
 mtn_status decode_impl(mtn_pool *P, int32_t layer, const void *q, void *out, float *lse,
@@ -588,6 +593,13 @@ mtn_status mtn_pool_create(const mtn_pool_config *cfg, void *kv_dev, size_t kv_b
         P->part_floats = (size_t)cfg->max_sessions * cfg->n_q_heads * 32 * (cfg->head_dim + 2);
         if ((e = hipMalloc(&P->d_part, sizeof(float) * P->part_floats)) != hipSuccess)
             return bail(e, "partials");
+        int dev = 0, n_cu = 0;
+        if ((e = hipGetDevice(&dev)) != hipSuccess) return bail(e, "device");
+        if ((e = hipDeviceGetAttribute(&n_cu, hipDeviceAttributeMultiprocessorCount, dev)) !=
+            hipSuccess)
+            return bail(e, "cu count");
+        P->resident_units =
+            n_cu * attn_valu_resident_per_cu(cfg->kv_dtype, cfg->head_dim, P->G);
         if ((e = hipStreamSynchronize((hipStream_t)stream)) != hipSuccess)
             return bail(e, "sync");
     }

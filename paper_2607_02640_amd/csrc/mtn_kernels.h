@@ -71,6 +71,8 @@ hipError_t launch_poison(int dtype, const PoolGeom &g, int32_t n_layers, int64_t
 hipError_t launch_copy(const void *src, void *dst, size_t bytes, hipStream_t s);
 
 bool attn_valu_supported(int dtype, int d, int g);
+// workgroups of the vector attention kernel resident per CU (occupancy query)
+int attn_valu_resident_per_cu(int dtype, int d, int g);
 bool prefill_mfma_supported(int dtype, int d, int g);
 
 constexpr int kBlock = 16;      // tokens per KV block

@@ -271,7 +271,7 @@ struct QRegs<float, D, G> {
 };
 
 #ifndef MTN_DECODE_RING_KB
-#define MTN_DECODE_RING_KB 32
+#define MTN_DECODE_RING_KB 64
 #endif
 constexpr int kRingBytes = MTN_DECODE_RING_KB * 1024;  // LDS ring of K/V^T blocks per unit
 
@@ -290,6 +290,17 @@ __device__ __forceinline__ void dma16(const void *gptr, uint32_t lds) {
 template <int N>
 __device__ __forceinline__ void vm_wait() {
     asm volatile("s_waitcnt vmcnt(%0)" : : "n"(N) : "memory");
+}
+// wait until at most `after` blocks of NIW DMA instructions are outstanding
+template <int NIW, int MAXA>
+__device__ __forceinline__ void vm_wait_blocks(int after) {
+    if constexpr (MAXA >= 6) { if (after >= 6) { vm_wait<6 * NIW>(); return; } }
+    if constexpr (MAXA >= 5) { if (after == 5) { vm_wait<5 * NIW>(); return; } }
+    if constexpr (MAXA >= 4) { if (after == 4) { vm_wait<4 * NIW>(); return; } }
+    if constexpr (MAXA >= 3) { if (after == 3) { vm_wait<3 * NIW>(); return; } }
+    if constexpr (MAXA >= 2) { if (after == 2) { vm_wait<2 * NIW>(); return; } }
+    if constexpr (MAXA >= 1) { if (after == 1) { vm_wait<NIW>(); return; } }
+    vm_wait<0>();
 }
 __device__ __forceinline__ uint32_t lds_addr(const void *p) {
     return (uint32_t)(uintptr_t)(const __attribute__((address_space(3))) void *)p;
@@ -318,7 +329,7 @@ __global__ __launch_bounds__(64 * WPU) void k_attn_valu(AttnArgs a) {
     constexpr int HW = G / WPU;                     // heads per wave
     static_assert(HW * WPU == G && HW <= 4, "head split");
     constexpr int BLK = 2 * kBlock * D * L::E;      // K + V^T bytes of one block (one head)
-    constexpr int NBUF = kRingBytes / BLK < 2 ? 2 : (kRingBytes / BLK < 4 ? kRingBytes / BLK : 4);
+    constexpr int NBUF = kRingBytes / BLK < 2 ? 2 : (kRingBytes / BLK < 8 ? kRingBytes / BLK : 8);
     constexpr int NCH = BLK / 16;                   // 16-byte chunks per block
     constexpr int NI = NCH / 64;                    // DMA instructions per block
     constexpr int NIW = NI / WPU;                   // ... issued by each wave
@@ -435,9 +446,7 @@ __global__ __launch_bounds__(64 * WPU) void k_attn_valu(AttnArgs a) {
         // the blocks issued after it are outstanding; the barrier then covers
         // the other waves' shares and frees the buffer of block i - 1
         const int after = min(NBUF - 2, nblk - 1 - i);
-        if (after >= 2) vm_wait<2 * NIW>();
-        else if (after == 1) vm_wait<NIW>();
-        else vm_wait<0>();
+        vm_wait_blocks<NIW, NBUF - 2>(after);
         if constexpr (WPU > 1) __syncthreads();
         if (i + NBUF - 1 < nblk) issue(i + NBUF - 1);
         const uint8_t *blk = &ring[i % NBUF][0];
@@ -975,9 +984,13 @@ __global__ __launch_bounds__(64 * kPfWaves) void k_prefill_mfma(PfArgs pa) {
     }
 }
 
+#ifndef MTN_DECODE_HEADS_PER_WAVE
+#define MTN_DECODE_HEADS_PER_WAVE 4
+#endif
 template <typename T, int D, int G>
 hipError_t launch_valu_t(const AttnArgs &a, hipStream_t s) {
-    constexpr int WPU = G >= 4 ? G / 4 : 1;
+    constexpr int HPW = MTN_DECODE_HEADS_PER_WAVE;
+    constexpr int WPU = G >= HPW ? G / HPW : 1;
     int64_t units = (int64_t)a.p.n_tok * a.g.hkv * a.n_split;
     if (units == 0) return hipSuccess;
     hipLaunchKernelGGL((k_attn_valu<T, D, G, WPU>), dim3((unsigned)units), dim3(64 * WPU), 0, s, a);
@@ -995,7 +1008,33 @@ hipError_t launch_valu_d(const AttnArgs &a, int G, hipStream_t s) {
     }
 }
 
+template <typename T, int D, int G>
+int resident_t() {
+    constexpr int HPW = MTN_DECODE_HEADS_PER_WAVE;
+    constexpr int WPU = G >= HPW ? G / HPW : 1;
+    int n = 0;
+    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, k_attn_valu<T, D, G, WPU>, 64 * WPU, 0) !=
+        hipSuccess)
+        return 1;
+    return n > 0 ? n : 1;
+}
+template <typename T, int D>
+int resident_d(int G) {
+    switch (G) {
+        case 1: return resident_t<T, D, 1>();
+        case 2: return resident_t<T, D, 2>();
+        case 4: return resident_t<T, D, 4>();
+        default: return resident_t<T, D, 8>();
+    }
+}
+
 }  // namespace
+
+int attn_valu_resident_per_cu(int dtype, int d, int g) {
+    if (!attn_valu_supported(dtype, d, g)) return 1;
+    if (dtype == 1) return d == 128 ? resident_d<bf16_t, 128>(g) : resident_d<bf16_t, 64>(g);
+    return d == 128 ? resident_d<float, 128>(g) : resident_d<float, 64>(g);
+}
 
 bool attn_valu_supported(int dtype, int d, int g) {
     if (g != 1 && g != 2 && g != 4 && g != 8) return false;
