@@ -51,13 +51,14 @@ class Workload:
 # Tiny single-layer parity check: 4 sessions, GQA 8/2, D = 64, fp32, S = 4,
 # W = 128, 8-token chunks then 4 decodes, 40 frames (the window wraps).
 TINY = Workload("tiny-gqa8x2-d64-f32", 4, 1, 8, 2, 64, "f32", 4, 128,
-                (8, 8), (4, 4), 40, 0.08, 1.0, workload_id=1)
+                (8, 8), (4, 4), 40, 0.08, 1.0, rope_theta=1.0e4, workload_id=1)
 
 # Moshi-like temporal transformer: 32 layers, MHA 32/32, D = 128, bf16,
 # 64 sessions, 80 ms frames of 1 appended token + 1 decode, S = 4, W = 2048,
 # 3750 frames (5 min); activations scaled by 1/sqrt(D).
 MOSHI = Workload("moshi-like-l32-h32-d128-bf16", 64, 32, 32, 32, 128, "bf16", 4, 2048,
-                 (1, 1), (1, 1), 3750, 0.08, 1.0 / np.sqrt(128.0), workload_id=2)
+                 (1, 1), (1, 1), 3750, 0.08, 1.0 / np.sqrt(128.0), rope_theta=1.0e4,
+                 workload_id=2)
 
 # Qwen3-Omni-30B-A3B-shaped attention: 48 layers, GQA 32/4, D = 128, bf16,
 # 128 sessions, 1.5 s frames of a 25-token chunk + 16 decodes, S = 4,
