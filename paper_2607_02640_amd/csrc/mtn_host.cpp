@@ -103,6 +103,7 @@ struct mtn_pool {
     float2 *d_rope = nullptr;      // [max_tok][D/2]
     double *d_inv_freq = nullptr;  // [D/2]
     float *d_part = nullptr;       // decode split partials
+    uint8_t *d_zero = nullptr;     // 8 KiB of zeros (DMA source of absent blocks)
     size_t part_floats = 0;
     int32_t *h_stage[kStages] = {};
     hipEvent_t stage_ev[kStages] = {};
@@ -473,8 +474,7 @@ mtn_status prefill_impl(mtn_pool *P, int32_t layer, const void *q, void *out, fl
     mtn_status st = timing_begin(P, s, &e0);
     if (st) return st;
     if (prefill_mfma_supported(P->cfg.kv_dtype, P->cfg.head_dim, P->G)) {
-        HIP_TRY(P, launch_prefill_mfma(a, P->max_ntok * P->G, P->d_seq_first, P->d_seq_ntok,
-                                       P->n_seq, s));
+        HIP_TRY(P, launch_prefill_mfma(a, P->d_seq_first, P->d_seq_ntok, P->n_seq, P->d_zero, s));
     } else {
         HIP_TRY(P, launch_attn_valu(P->cfg.kv_dtype, a, s));
     }
@@ -590,6 +590,9 @@ mtn_status mtn_pool_create(const mtn_pool_config *cfg, void *kv_dev, size_t kv_b
         if ((e = hipMemcpy(P->d_inv_freq, inv.data(), sizeof(double) * half,
                            hipMemcpyHostToDevice)) != hipSuccess)
             return bail(e, "inv_freq upload");
+        if ((e = hipMalloc(&P->d_zero, 8192)) != hipSuccess) return bail(e, "zero page");
+        if ((e = hipMemsetAsync(P->d_zero, 0, 8192, (hipStream_t)stream)) != hipSuccess)
+            return bail(e, "zero page clear");
         P->part_floats = (size_t)cfg->max_sessions * cfg->n_q_heads * 32 * (cfg->head_dim + 2);
         if ((e = hipMalloc(&P->d_part, sizeof(float) * P->part_floats)) != hipSuccess)
             return bail(e, "partials");
@@ -616,6 +619,7 @@ void mtn_pool_destroy(mtn_pool *P) {
         (void)hipFree(P->d_rope);
         (void)hipFree(P->d_inv_freq);
         (void)hipFree(P->d_part);
+        (void)hipFree(P->d_zero);
         for (int i = 0; i < kStages; ++i) {
             if (P->h_stage[i]) (void)hipHostFree(P->h_stage[i]);
             if (P->stage_ev[i]) (void)hipEventDestroy(P->stage_ev[i]);

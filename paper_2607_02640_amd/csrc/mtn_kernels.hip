@@ -705,11 +705,14 @@ typedef __attribute__((ext_vector_type(4))) float f32x4_t;
 constexpr int kPfWaves = 8;   // waves per workgroup
 constexpr int kPfTpw = 2;     // 16-row query tiles per wave per pass
 constexpr int kPfRowsPerPass = kPfWaves * kPfTpw * 16;
+constexpr int kPfStages = 8;  // LDS ring depth in stages of two blocks (16 KiB each)
+constexpr int kPfStageBytes = 16384;
 
 struct PfArgs {
     AttnArgs a;
     const int32_t *seq_first;  // first planned token of each sequence
     const int32_t *seq_ntok;
+    const uint8_t *zero_page;  // 8 KiB of zeros: the DMA source of absent blocks
 };
 
 __device__ __forceinline__ f32x4_t mfma16x16x32(const uint4 &a, const uint4 &b, f32x4_t c) {
@@ -717,33 +720,101 @@ __device__ __forceinline__ f32x4_t mfma16x16x32(const uint4 &a, const uint4 &b, 
                                                     __builtin_bit_cast(bf16x8_t, b), c, 0, 0, 0);
 }
 
-// LDS addressing (bytes) inside one stage buffer: K of block b, then V^T.
+// LDS addressing (bytes) inside one stage: K tiles of blocks 0, 1 (16-byte
+// chunks swizzled by key), then V^T tiles (16-byte chunks swizzled by d).
 __device__ __forceinline__ int lds_k(int b, int key, int chunk16) {
     return b * 4096 + key * 256 + ((chunk16 ^ (key & 7)) << 4);
 }
-__device__ __forceinline__ int lds_v(int b, int d, int chunk8) {
-    return 8192 + b * 4096 + d * 32 + ((chunk8 ^ ((d >> 2) & 3)) << 3);
+__device__ __forceinline__ int lds_v16(int b, int d, int chunk16) {
+    return 8192 + b * 4096 + d * 32 + ((chunk16 ^ ((d >> 2) & 1)) << 4);
 }
+// 8 bytes V^T[d][keys 4g .. 4g+3] of block b
+__device__ __forceinline__ int lds_v8(int b, int d, int g) {
+    return lds_v16(b, d, g >> 1) + ((g & 1) << 3);
+}
+// Global byte offset (inside the block's 8 KiB K + V^T pair) of the 16-byte
+// chunk that lands at stage byte offset `off` (block b = which of the two).
+__device__ __forceinline__ int stage_src(int off, int *b) {
+    if (off < 8192) {
+        *b = off >> 12;
+        const int r = off & 4095, key = r >> 8, pos = (r >> 4) & 15;
+        return key * 256 + ((pos ^ (key & 7)) << 4);
+    }
+    const int o2 = off - 8192;
+    *b = o2 >> 12;
+    const int r = o2 & 4095, d = r >> 5, pos = (r >> 4) & 1;
+    return 4096 + d * 32 + ((pos ^ ((d >> 2) & 1)) << 4);
+}
+
+// Walks the union's virtual blocks 0, 1, ... of a chunk (sinks, then the
+// ring run) without division: logical block, valid slots [lo, hi), the
+// absolute position of slot 0 and whether the block holds sinks.
+struct PfIter {
+    int v, nvb, n_sb, sink_tokens, n_rb, first_off, last_hi, rb, ring_blocks, nsb, ring_p0;
+    __device__ __forceinline__ void init(const PoolGeom &g, int n_sb_, int sink_tokens_, int n_rb_,
+                                         int first, int ring_n, int A) {
+        v = 0;
+        n_sb = n_sb_;
+        sink_tokens = sink_tokens_;
+        n_rb = n_rb_;
+        nvb = n_sb + n_rb;
+        first_off = first % kBlock;
+        last_hi = (first_off + ring_n - 1) % kBlock + 1;
+        ring_blocks = g.ring / kBlock;
+        nsb = g.n_sink_blocks;
+        rb = first / kBlock;
+        ring_p0 = A - first_off;
+    }
+    // returns false for a block past the end of the union
+    __device__ __forceinline__ bool get(int *lb, int *lo, int *hi, int *p0, bool *sink) const {
+        if (v >= nvb) return false;
+        if (v < n_sb) {
+            *lb = v;
+            *lo = 0;
+            *hi = min(kBlock, sink_tokens - v * kBlock);
+            *p0 = v * kBlock;
+            *sink = true;
+        } else {
+            const int u = v - n_sb;
+            *lb = nsb + rb;
+            *lo = (u == 0) ? first_off : 0;
+            *hi = (u == n_rb - 1) ? last_hi : kBlock;
+            *p0 = ring_p0;
+            *sink = false;
+        }
+        return true;
+    }
+    __device__ __forceinline__ void next() {
+        if (v >= n_sb) {
+            rb = (rb + 1 == ring_blocks) ? 0 : rb + 1;
+            ring_p0 += kBlock;
+        }
+        ++v;
+    }
+};
 
 template <int G>
 __global__ __launch_bounds__(64 * kPfWaves) void k_prefill_mfma(PfArgs pa) {
     constexpr int D = 128;
-    __shared__ __attribute__((aligned(16))) uint8_t smem[2][16384];
+    constexpr int NIW = kPfStageBytes / 1024 / kPfWaves;  // DMA instructions per wave per stage
+    __shared__ __attribute__((aligned(16))) uint8_t ring[kPfStages][kPfStageBytes];
     const AttnArgs &a = pa.a;
     const PoolGeom &g = a.g;
     const int seq = blockIdx.x / g.hkv;
     const int kvh = blockIdx.x % g.hkv;
     const int tid = threadIdx.x;
-    const int lane = tid & 63, wv = tid >> 6;
+    const int lane = tid & 63;
+    const int wv = __builtin_amdgcn_readfirstlane(tid >> 6);
     const int ln16 = lane & 15, lg = lane >> 4;
-    const int tok0 = pa.seq_first[seq];
-    const int ntok = pa.seq_ntok[seq];
-    const int sid = a.p.tok_sid[tok0];
-    const int pos0 = a.p.tok_pos[tok0];
+    const int tok0 = __builtin_amdgcn_readfirstlane(pa.seq_first[seq]);
+    const int ntok = __builtin_amdgcn_readfirstlane(pa.seq_ntok[seq]);
+    const int sid = __builtin_amdgcn_readfirstlane(a.p.tok_sid[tok0]);
+    const int pos0 = __builtin_amdgcn_readfirstlane(a.p.tok_pos[tok0]);
     const int pos_last = pos0 + ntok - 1;
     const int n_rows = ntok * G;
     const int32_t *trow = g.table + (int64_t)sid * g.row_len;
     const uint8_t *layer_base = g.kv + (int64_t)a.layer * g.layer_stride + (int64_t)kvh * g.head_stride;
+    const uint32_t ring0 = lds_addr(&ring[0][0]);
 
     // union of the visible sets of the chunk's queries: sinks, then the ring
     // run [A, pos_last] with A = max(S, pos0 - W + 1)
@@ -755,66 +826,43 @@ __global__ __launch_bounds__(64 * kPfWaves) void k_prefill_mfma(PfArgs pa) {
     const int n_rb = ((first % kBlock) + ring_n + kBlock - 1) / kBlock;
     const int nvb = n_sb + n_rb;
     const int n_stages = (nvb + 1) / 2;
-    const int ring_blocks = g.ring / kBlock;
 
-    // virtual block -> (phys, lo, hi, position of slot 0)
-    auto vinfo = [&](int v, int *phys, int *lo, int *hi, int *p0) {
-        if (v >= nvb) {
-            *phys = -1; *lo = 0; *hi = 0; *p0 = 0;
-            return;
-        }
-        int lb;
-        if (v < n_sb) {
-            lb = v;
-            *lo = 0;
-            *hi = min(kBlock, sink_tokens - v * kBlock);
-            *p0 = v * kBlock;
-        } else {
-            int u = v - n_sb;
-            lb = g.n_sink_blocks + (first / kBlock + u) % ring_blocks;
-            *lo = (u == 0) ? first % kBlock : 0;
-            *hi = (u == n_rb - 1) ? ((first % kBlock) + ring_n - 1) % kBlock + 1 : kBlock;
-            *p0 = A + u * kBlock - first % kBlock;
-        }
-        *phys = trow[lb];
-        if (*phys < 0) *hi = *lo;
-    };
-
-    // staging: thread t moves 16 B of K and 16 B of V^T per stage
-    const int sb = tid >> 8;          // block of the stage this thread stages
-    const int q16 = tid & 255;        // 16-byte chunk inside the 4 KiB tile
-    uint4 rk, rv;
-    auto stage_load = [&](int st) {
+    // block metadata of the stage being issued / processed
+    struct BlockMeta {
         int phys, lo, hi, p0;
-        vinfo(2 * st + sb, &phys, &lo, &hi, &p0);
-        if (phys < 0 || lo >= hi) {
-            rk = make_uint4(0, 0, 0, 0);
-            rv = make_uint4(0, 0, 0, 0);
-            return;
-        }
-        const uint8_t *tile = layer_base + (int64_t)phys * g.block_stride;
-        rk = *(const uint4 *)(tile + q16 * 16);
-        rv = *(const uint4 *)(tile + g.tile_bytes + q16 * 16);
-        if (lo > 0 || hi < kBlock) {  // zero values of slots outside the union
-            int k0 = (q16 & 1) * 8;
-            uint32_t w[4] = {rv.x, rv.y, rv.z, rv.w};
-#pragma unroll
-            for (int e = 0; e < 4; ++e) {
-                int ka = k0 + 2 * e, kb = ka + 1;
-                uint32_t m = ((ka >= lo && ka < hi) ? 0x0000FFFFu : 0u) |
-                             ((kb >= lo && kb < hi) ? 0xFFFF0000u : 0u);
-                w[e] &= m;
-            }
-            rv = make_uint4(w[0], w[1], w[2], w[3]);
-        }
+        bool sink;
     };
-    auto stage_store = [&](int buf) {
-        uint8_t *sm = smem[buf];
-        int key = q16 >> 4, c16 = q16 & 15;
-        *(uint4 *)(sm + lds_k(sb, key, c16)) = rk;
-        int d = q16 >> 1, c8 = (q16 & 1) * 2;
-        *(uint2 *)(sm + lds_v(sb, d, c8)) = make_uint2(rv.x, rv.y);
-        *(uint2 *)(sm + lds_v(sb, d, c8 + 1)) = make_uint2(rv.z, rv.w);
+    auto meta = [&](PfIter &it, BlockMeta &m) {
+        int lb;
+        if (it.get(&lb, &m.lo, &m.hi, &m.p0, &m.sink)) {
+            m.phys = scalar_ld(trow, __builtin_amdgcn_readfirstlane(lb));
+            if (m.phys < 0) m.hi = m.lo;
+        } else {
+            m.phys = -1;
+            m.lo = m.hi = m.p0 = 0;
+            m.sink = false;
+        }
+        it.next();
+    };
+    PfIter it_issue, it_proc;
+
+    // DMA of the next stage into ring slot st % kPfStages; each wave moves NIW KiB
+    auto issue_stage = [&](int st) {
+        BlockMeta m0, m1;
+        meta(it_issue, m0);
+        meta(it_issue, m1);
+        const uint8_t *b0 = (m0.phys < 0 || m0.lo >= m0.hi) ? pa.zero_page
+                                                            : layer_base + (int64_t)m0.phys * g.block_stride;
+        const uint8_t *b1 = (m1.phys < 0 || m1.lo >= m1.hi) ? pa.zero_page
+                                                            : layer_base + (int64_t)m1.phys * g.block_stride;
+        const uint32_t dst = ring0 + (uint32_t)((st % kPfStages) * kPfStageBytes);
+#pragma unroll
+        for (int jj = 0; jj < NIW; ++jj) {
+            const int j = wv * NIW + jj;
+            int b;
+            const int src = stage_src(j * 1024 + lane * 16, &b);
+            dma16((b ? b1 : b0) + src, dst + j * 1024);
+        }
     };
 
     const int hq0 = kvh * G;
@@ -865,21 +913,45 @@ __global__ __launch_bounds__(64 * kPfWaves) void k_prefill_mfma(PfArgs pa) {
             }
         }
 
-        if (n_stages > 0) {
-            stage_load(0);
-            stage_store(0);
-        }
-        __syncthreads();
+        it_issue.init(g, n_sb, sink_tokens, n_rb, first, ring_n, A);
+        it_proc.init(g, n_sb, sink_tokens, n_rb, first, ring_n, A);
+        const int pre = n_stages < kPfStages - 1 ? n_stages : kPfStages - 1;
+        for (int st = 0; st < pre; ++st) issue_stage(st);
         for (int st = 0; st < n_stages; ++st) {
-            const int buf = st & 1;
-            if (st + 1 < n_stages) stage_load(st + 1);
-            const uint8_t *sm = smem[buf];
+            // this wave's share of stage st landed; the barrier covers the other
+            // waves' shares and frees the slot consumed at st - 1
+            const int after = min(kPfStages - 2, n_stages - 1 - st);
+            vm_wait_blocks<NIW, kPfStages - 2>(after);
+            __syncthreads();
+            if (st + kPfStages - 1 < n_stages) issue_stage(st + kPfStages - 1);
+            uint8_t *sm = &ring[st % kPfStages][0];
             // key metadata of the two blocks of this stage (uniform)
-            int ph0, lo0, hi0, p00, ph1, lo1, hi1, p01;
-            vinfo(2 * st, &ph0, &lo0, &hi0, &p00);
-            vinfo(2 * st + 1, &ph1, &lo1, &hi1, &p01);
-            const bool sink0 = (2 * st) < n_sb, sink1 = (2 * st + 1) < n_sb;
+            BlockMeta m0, m1;
+            meta(it_proc, m0);
+            meta(it_proc, m1);
+            const bool part0 = m0.phys >= 0 && m0.lo < m0.hi && (m0.lo > 0 || m0.hi < kBlock);
+            const bool part1 = m1.phys >= 0 && m1.lo < m1.hi && (m1.lo > 0 || m1.hi < kBlock);
+            if (part0 || part1) {
+                // values of slots outside the union may be NaN: zero them in LDS
+                const int b = tid >> 8;            // 512 threads: 256 per block
+                const int d = (tid & 255) >> 1, half = tid & 1;
+                const int lo = b ? m1.lo : m0.lo, hi = b ? m1.hi : m0.hi;
+                if (b ? part1 : part0) {
+                    uint4 *pv = (uint4 *)(sm + lds_v16(b, d, half));
+                    uint4 x = *pv;
+                    uint32_t w[4] = {x.x, x.y, x.z, x.w};
+#pragma unroll
+                    for (int e = 0; e < 4; ++e) {
+                        const int ka = half * 8 + 2 * e, kb = ka + 1;
+                        w[e] &= ((ka >= lo && ka < hi) ? 0x0000FFFFu : 0u) |
+                                ((kb >= lo && kb < hi) ? 0xFFFF0000u : 0u);
+                    }
+                    *pv = make_uint4(w[0], w[1], w[2], w[3]);
+                }
+                __syncthreads();
+            }
             // QK: K fragments are read once per stage and shared by the tiles
+            // (tiles past the last row compute on zero queries and are dropped)
             f32x4_t s0[kPfTpw], s1[kPfTpw];
 #pragma unroll
             for (int i = 0; i < kPfTpw; ++i) {
@@ -892,37 +964,34 @@ __global__ __launch_bounds__(64 * kPfWaves) void k_prefill_mfma(PfArgs pa) {
                 uint4 k1 = *(const uint4 *)(sm + lds_k(1, ln16, s * 4 + lg));
 #pragma unroll
                 for (int i = 0; i < kPfTpw; ++i) {
-                    if (!live[i]) continue;
                     s0[i] = mfma16x16x32(k0, qf[i][s], s0[i]);
                     s1[i] = mfma16x16x32(k1, qf[i][s], s1[i]);
                 }
             }
-            // online softmax per row (lane holds row ln16, keys 4*lg + r)
+            // online softmax per row (lane holds row ln16, keys 4*lg + r).  The
+            // visible slots of a block for query position tq are one range:
+            // [max(lo, tq - W + 1 - p0), min(hi, tq + 1 - p0)), sinks exempt
+            // from the window bound.
             uint4 pb[kPfTpw];
 #pragma unroll
             for (int i = 0; i < kPfTpw; ++i) {
-                if (!live[i]) {
-                    pb[i] = make_uint4(0, 0, 0, 0);
-                    continue;
-                }
                 const int tq = pos0 + trow_tok[i];
+                const int wl = g.window < 0 ? -(1 << 30) : tq - g.window + 1;
+                const int ol0 = m0.sink ? m0.lo : max(m0.lo, wl - m0.p0);
+                const int oh0 = min(m0.hi, tq + 1 - m0.p0);
+                const int ol1 = m1.sink ? m1.lo : max(m1.lo, wl - m1.p0);
+                const int oh1 = min(m1.hi, tq + 1 - m1.p0);
                 float sc[8];
 #pragma unroll
                 for (int r = 0; r < 4; ++r) {
                     const int o = 4 * lg + r;
-                    const int pA = p00 + o, pB = p01 + o;
-                    bool vA = o >= lo0 && o < hi0 && pA <= tq &&
-                              (sink0 || g.window < 0 || pA > tq - g.window);
-                    bool vB = o >= lo1 && o < hi1 && pB <= tq &&
-                              (sink1 || g.window < 0 || pB > tq - g.window);
-                    sc[r] = vA ? s0[i][r] : -INFINITY;
-                    sc[4 + r] = vB ? s1[i][r] : -INFINITY;
+                    sc[r] = (o >= ol0 && o < oh0) ? s0[i][r] : -INFINITY;
+                    sc[4 + r] = (o >= ol1 && o < oh1) ? s1[i][r] : -INFINITY;
                 }
-                float mx = sc[0];
-#pragma unroll
-                for (int r = 1; r < 8; ++r) mx = fmaxf(mx, sc[r]);
-                mx = fmaxf(mx, shfl_xor_f(mx, 16));
-                mx = fmaxf(mx, shfl_xor_f(mx, 32));
+                float mx = fmaxf(fmaxf(fmaxf(sc[0], sc[1]), fmaxf(sc[2], sc[3])),
+                                 fmaxf(fmaxf(sc[4], sc[5]), fmaxf(sc[6], sc[7])));
+                mx = rows_pair<false, false>(mx);
+                mx = rows_pair<false, true>(mx);
                 const float m_new = fmaxf(m_i[i], mx);
                 const float mn = (m_new == -INFINITY) ? 0.f : m_new;
                 const float alpha = __builtin_amdgcn_exp2f(m_i[i] - mn);
@@ -936,33 +1005,32 @@ __global__ __launch_bounds__(64 * kPfWaves) void k_prefill_mfma(PfArgs pa) {
                 l_i[i] = l_i[i] * alpha + ps;
                 pb[i] = make_uint4(pack_bf16x2(sc[0], sc[1]), pack_bf16x2(sc[2], sc[3]),
                                    pack_bf16x2(sc[4], sc[5]), pack_bf16x2(sc[6], sc[7]));
+                // rescale only when some row's running max moved (exact skip)
+                if (__builtin_amdgcn_ballot_w64(alpha != 1.f)) {
 #pragma unroll
-                for (int dt = 0; dt < 8; ++dt) acc[i][dt] *= alpha;
+                    for (int dt = 0; dt < 8; ++dt) acc[i][dt] *= alpha;
+                }
             }
             // PV: V^T fragments read once per stage, shared by the tiles
 #pragma unroll
             for (int dt = 0; dt < 8; ++dt) {
                 const int d = dt * 16 + ln16;
-                uint2 va = *(const uint2 *)(sm + lds_v(0, d, lg));
-                uint2 vb = *(const uint2 *)(sm + lds_v(1, d, lg));
+                uint2 va = *(const uint2 *)(sm + lds_v8(0, d, lg));
+                uint2 vb = *(const uint2 *)(sm + lds_v8(1, d, lg));
                 uint4 vf = make_uint4(va.x, va.y, vb.x, vb.y);
 #pragma unroll
-                for (int i = 0; i < kPfTpw; ++i) {
-                    if (!live[i]) continue;
-                    acc[i][dt] = mfma16x16x32(vf, pb[i], acc[i][dt]);
-                }
+                for (int i = 0; i < kPfTpw; ++i) acc[i][dt] = mfma16x16x32(vf, pb[i], acc[i][dt]);
             }
-            if (st + 1 < n_stages) stage_store(buf ^ 1);
-            __syncthreads();
         }
+        __syncthreads();  // every wave is done with the ring before the next pass refills it
 
         // ---- epilogue: normalise and write rows of this pass
 #pragma unroll
         for (int i = 0; i < kPfTpw; ++i) {
             if (!live[i]) continue;
             float lt = l_i[i];
-            lt += shfl_xor_f(lt, 16);
-            lt += shfl_xor_f(lt, 32);
+            lt = rows_pair<true, false>(lt);
+            lt = rows_pair<true, true>(lt);
             const int r = pass_row0 + (wv + kPfWaves * i) * 16 + ln16;
             if (r >= n_rows) continue;
             const int j = r / G, gh = r % G;
@@ -1098,11 +1166,11 @@ hipError_t launch_merge(int dtype, const AttnArgs &a, hipStream_t s) {
     return hipGetLastError();
 }
 
-hipError_t launch_prefill_mfma(const AttnArgs &a, int32_t, const int32_t *seq_first,
-                               const int32_t *seq_ntok, int32_t n_seq, hipStream_t s) {
+hipError_t launch_prefill_mfma(const AttnArgs &a, const int32_t *seq_first, const int32_t *seq_ntok,
+                               int32_t n_seq, const uint8_t *zero_page, hipStream_t s) {
     const int G = a.g.hq / a.g.hkv;
-    if (!prefill_mfma_supported(1, a.g.d, G) || n_seq <= 0) return hipErrorInvalidValue;
-    PfArgs pa{a, seq_first, seq_ntok};
+    if (!prefill_mfma_supported(1, a.g.d, G) || n_seq <= 0 || !zero_page) return hipErrorInvalidValue;
+    PfArgs pa{a, seq_first, seq_ntok, zero_page};
     dim3 grid((unsigned)(n_seq * a.g.hkv)), block(64 * kPfWaves);
     switch (G) {
         case 1: hipLaunchKernelGGL(k_prefill_mfma<1>, grid, block, 0, s, pa); break;
