@@ -43,7 +43,7 @@ def build(verbose: bool = False, out: str = LIB, defines=()) -> str:
     """Compile every source for gfx950 and link libmtn.so next to this file
     (or at ``out``, with extra ``-D`` ``defines`` for tuning variants)."""
     objs = []
-    tag = "_".join(d.replace("=", "") for d in defines)
+    tag = "_".join("".join(ch for ch in d if ch.isalnum()) for d in defines)
     bdir = os.path.join(ROOT, "_build", tag) if tag else os.path.join(ROOT, "_build")
     os.makedirs(bdir, exist_ok=True)
     for src in SOURCES:

@@ -23,6 +23,7 @@ using namespace mtn;
 namespace {
 
 constexpr int kStages = 4;  // pinned staging buffers in flight
+constexpr size_t kZeroPage = 2 * kBlock * 128 * 4;  // 16 KiB
 
 // Lowest-free-first block allocator over a bitmap (bit set = free).
 class BlockAllocator {
@@ -103,7 +104,7 @@ struct mtn_pool {
     float2 *d_rope = nullptr;      // [max_tok][D/2]
     double *d_inv_freq = nullptr;  // [D/2]
     float *d_part = nullptr;       // decode split partials
-    uint8_t *d_zero = nullptr;     // 8 KiB of zeros (DMA source of absent blocks)
+    uint8_t *d_zero = nullptr;     // kZeroPage bytes of zeros (DMA source of absent blocks)
     size_t part_floats = 0;
     int32_t *h_stage[kStages] = {};
     hipEvent_t stage_ev[kStages] = {};
@@ -416,6 +417,7 @@ AttnArgs attn_args(mtn_pool *P, int32_t layer, const void *q, void *out, float *
     a.part = P->d_part;
     a.n_split = n_split;
     a.scale_log2 = P->scale * 1.4426950408889634f;
+    a.zero_page = P->d_zero;
     return a;
 }
 
@@ -590,8 +592,10 @@ mtn_status mtn_pool_create(const mtn_pool_config *cfg, void *kv_dev, size_t kv_b
         if ((e = hipMemcpy(P->d_inv_freq, inv.data(), sizeof(double) * half,
                            hipMemcpyHostToDevice)) != hipSuccess)
             return bail(e, "inv_freq upload");
-        if ((e = hipMalloc(&P->d_zero, 8192)) != hipSuccess) return bail(e, "zero page");
-        if ((e = hipMemsetAsync(P->d_zero, 0, 8192, (hipStream_t)stream)) != hipSuccess)
+        // zero page: at least one whole (block, head) pair, K + V^T, at the
+        // largest element size and head dim
+        if ((e = hipMalloc(&P->d_zero, kZeroPage)) != hipSuccess) return bail(e, "zero page");
+        if ((e = hipMemsetAsync(P->d_zero, 0, kZeroPage, (hipStream_t)stream)) != hipSuccess)
             return bail(e, "zero page clear");
         P->part_floats = (size_t)cfg->max_sessions * cfg->n_q_heads * 32 * (cfg->head_dim + 2);
         if ((e = hipMalloc(&P->d_part, sizeof(float) * P->part_floats)) != hipSuccess)

@@ -44,6 +44,7 @@ struct AttnArgs {
     float *part;             // split partials (acc [unit][G][D] then ml [unit][G][2])
     int32_t n_split;
     float scale_log2;        // softmax scale * log2(e)
+    const uint8_t *zero_page;  // 16 KiB of zeros (DMA source of absent blocks)
 };
 
 // dtype codes match the public MTN_F32 / MTN_BF16
@@ -60,7 +61,7 @@ hipError_t launch_append(int dtype, const PoolGeom &g, const PlanView &p, int32_
 hipError_t launch_attn_valu(int dtype, const AttnArgs &a, hipStream_t s);
 hipError_t launch_merge(int dtype, const AttnArgs &a, hipStream_t s);
 
-// MFMA chunk-prefill attention (bf16, D = 128).  zero_page: 8 KiB of device
+// MFMA chunk-prefill attention (bf16, D = 128).  zero_page: 16 KiB of device
 // zeros, the DMA source of blocks a chunk does not see.
 hipError_t launch_prefill_mfma(const AttnArgs &a, const int32_t *seq_first_tok,
                                const int32_t *seq_ntok, int32_t n_seq, const uint8_t *zero_page,
