@@ -32,6 +32,9 @@ if ROOT not in sys.path:
 
 HBM_PEAK_GBPS = 8000.0
 BF16_MFMA_PEAK_TFLOPS = 2500.0
+COPY_PROBE_BYTES = 4 << 30
+KERNEL_SRC = os.path.join(ROOT, "paper_2607_02640_amd", "csrc", "mtn_kernels.hip")
+TRAFFIC_SUMMARY = os.path.join(ROOT, "profiles", "decode_traffic_qwen3omni_128s.json")
 
 
 def log(*a):
@@ -49,7 +52,69 @@ def parse():
                     help="layers of one session-frame the oracle sample covers")
     ap.add_argument("--n-split", type=int, default=0)
     ap.add_argument("--json-out", default=None)
+    ap.add_argument("--traffic-summary", nargs=2, metavar=("FETCH_DIR", "WRITE_DIR"),
+                    help="summarise two rocprofv3 --pmc runs (FETCH_SIZE, WRITE_SIZE) of this "
+                         "bench into " + os.path.relpath(TRAFFIC_SUMMARY, ROOT) + " and exit")
     return ap.parse_args()
+
+
+def kernel_src_hash() -> str:
+    import hashlib
+    with open(KERNEL_SRC, "rb") as f:
+        return hashlib.sha256(f.read()).hexdigest()[:16]
+
+
+def traffic_summary(fetch_dir, write_dir):
+    """Per-dispatch HBM bytes of the decode kernel from FETCH_SIZE / WRITE_SIZE
+    (KiB per dispatch), each scaled by what the same counter reads for the
+    bench's own copy kernel (COPY_PROBE_BYTES read and written per dispatch)."""
+    import csv
+    import glob
+
+    def avg(d, counter, needle):
+        vals = []
+        for fn in glob.glob(os.path.join(d, "**", "*counter_collection.csv"), recursive=True):
+            for r in csv.DictReader(open(fn)):
+                if r["Counter_Name"] == counter and needle in r["Kernel_Name"]:
+                    vals.append(float(r["Counter_Value"]))
+        if not vals:
+            raise SystemExit(f"no {counter} samples for {needle} under {d}")
+        return sum(vals) / len(vals), len(vals)
+
+    kib = COPY_PROBE_BYTES / 1024
+    f_copy, _ = avg(fetch_dir, "FETCH_SIZE", "k_copy")
+    w_copy, _ = avg(write_dir, "WRITE_SIZE", "k_copy")
+    f_dec, nf = avg(fetch_dir, "FETCH_SIZE", "k_attn_valu")
+    w_dec, nw = avg(write_dir, "WRITE_SIZE", "k_attn_valu")
+    fs, ws = kib / f_copy, kib / w_copy
+    out = {
+        "kernel": "k_attn_valu (decode attention), 128-session Qwen3-Omni-shaped workload",
+        "kernel_src_sha256_16": kernel_src_hash(),
+        "copy_kernel_KiB_per_dispatch": {"FETCH_SIZE": f_copy, "WRITE_SIZE": w_copy,
+                                         "actual_read_KiB": kib, "actual_write_KiB": kib},
+        "scale": {"fetch": fs, "write": ws},
+        "decode_KiB_per_dispatch_raw": {"FETCH_SIZE": f_dec, "WRITE_SIZE": w_dec,
+                                        "dispatches": [nf, nw]},
+        "decode_bytes_per_launch": {"read": f_dec * fs * 1024, "write": w_dec * ws * 1024,
+                                    "total": (f_dec * fs + w_dec * ws) * 1024},
+    }
+    with open(TRAFFIC_SUMMARY, "w") as f:
+        json.dump(out, f, indent=1)
+        f.write("\n")
+    print(json.dumps(out, indent=1))
+
+
+def measured_traffic():
+    """HBM bytes per decode launch from the committed counter summary, or None
+    when the kernel source changed since the counters were taken."""
+    try:
+        with open(TRAFFIC_SUMMARY) as f:
+            t = json.load(f)
+    except OSError:
+        return None
+    if t.get("kernel_src_sha256_16") != kernel_src_hash():
+        return None
+    return t["decode_bytes_per_launch"]["total"]
 
 
 def pick(name):
@@ -126,8 +191,9 @@ def run_gpu(args, w):
     torch.cuda.synchronize()
     log(f"[bench] warmup {args.warmup} frames done")
 
-    # copy probe: achievable HBM bandwidth (read + write bytes / time)
-    probe_bytes = 4 << 30
+    # copy probe: achievable HBM bandwidth (read + write bytes / time); also
+    # the calibration kernel of the profiler's byte counters
+    probe_bytes = COPY_PROBE_BYTES
     src = torch.empty(probe_bytes, dtype=torch.uint8, device=dev)
     dst = torch.empty_like(src)
     mtn.hbm_copy(src, dst, probe_bytes)
@@ -233,6 +299,9 @@ def cpu_baseline(w, n_layers_sample):
 
 def main():
     args = parse()
+    if args.traffic_summary:
+        traffic_summary(*args.traffic_summary)
+        return
     if args.gpus != 1:
         print(f"bench.py runs on one GPU only (got --gpus {args.gpus}); the windowed-KV path "
               "shards by session with no exchange, so N GPUs run N independent copies",
@@ -272,7 +341,7 @@ def main():
             "peak": HBM_PEAK_GBPS,
             "unit": "GB/s",
             "frac": round(res["dec_gbps"] / HBM_PEAK_GBPS, 4),
-            "traffic": None,
+            "traffic": measured_traffic(),
             "bytes_per_launch": res["dec_bytes"],
             "avg_launch_ms": round(res["avg_dec_ms"], 4),
             "launches": res["dec_launches"],
