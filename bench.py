@@ -52,6 +52,12 @@ def parse():
                     help="layers of one session-frame the oracle sample covers")
     ap.add_argument("--n-split", type=int, default=0)
     ap.add_argument("--json-out", default=None)
+    ap.add_argument("--call", action="store_true",
+                    help="run a whole simulated call from empty sessions and report the "
+                         "per-frame tick latency and pool occupancy series")
+    ap.add_argument("--frames", type=int, default=0, help="--call: frames (0 = the workload's)")
+    ap.add_argument("--pool-blocks", type=int, default=0,
+                    help="--call: pool capacity in blocks (0 = exact windowed reservation)")
     ap.add_argument("--traffic-summary", nargs=2, metavar=("FETCH_DIR", "WRITE_DIR"),
                     help="summarise two rocprofv3 --pmc runs (FETCH_SIZE, WRITE_SIZE) of this "
                          "bench into " + os.path.relpath(TRAFFIC_SUMMARY, ROOT) + " and exit")
@@ -120,7 +126,8 @@ def measured_traffic():
 def pick(name):
     import workload as W
     table = {"qwen3-omni": W.QWEN3_OMNI, "moshi": W.MOSHI, "minicpm-o": W.MINICPM_O,
-             "tiny": W.TINY}
+             "tiny": W.TINY, "pool-stress-windowed": W.POOL_STRESS_WINDOWED,
+             "pool-stress-unbounded": W.POOL_STRESS_UNBOUNDED}
     return table[name]
 
 
@@ -257,6 +264,154 @@ def run_gpu(args, w):
     return res
 
 
+def run_call(args, w):
+    """A whole simulated call: sessions start empty and run `frames` frames
+    back to back (each tick serves every session: chunk prefill, then ragged
+    decode rounds).  Ragged workloads draw chunk / decode counts per
+    session-frame, start from mixed lengths (fast-forwarded by append-only
+    plans) and churn sessions.  Records the tick latency of every frame
+    (HIP events on the launch stream), pool occupancy, and the first frame a
+    plan fails (pool exhausted)."""
+    import numpy as np
+    import torch
+    import paper_2607_02640_amd as mtn
+    from workload import device_bank
+
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    tdt = torch.bfloat16 if w.dtype == "bf16" else torch.float32
+    N, Lyr, Hq, Hkv, D = w.n_sessions, w.n_layers, w.n_q_heads, w.n_kv_heads, w.head_dim
+    Cmax, Tmax = w.chunk[1], w.n_decode[1]
+    frames = args.frames or w.frames
+    ragged = w.chunk[0] != w.chunk[1] or w.n_decode[0] != w.n_decode[1]
+    if w.window is None:
+        # unbounded arm: the pool gets a fixed ~150 GB of HBM
+        max_len = frames * (Cmax + Tmax) + 64
+        block_bytes = Lyr * Hkv * 2 * 16 * D * (2 if w.dtype == "bf16" else 4)
+        n_blocks = args.pool_blocks or int(150e9 // block_bytes)
+    else:
+        max_len = 0
+        R = -(-(w.window + Cmax - 1) // 16) * 16
+        n_blocks = args.pool_blocks or N * (-(-w.n_sink // 16) + R // 16)
+    kw = dict(n_layers=Lyr, n_q_heads=Hq, n_kv_heads=Hkv, head_dim=D, n_sink=w.n_sink,
+              window=w.window, max_chunk=Cmax, max_sessions=N, n_blocks=n_blocks, dtype=w.dtype,
+              rope_theta=w.rope_theta, max_len=max_len)
+    nbytes = mtn.Pool.required(**kw)
+    log(f"[call] {w.name}: pool {nbytes / 1e9:.1f} GB ({n_blocks} blocks), {frames} frames")
+    kv = torch.empty(nbytes, dtype=torch.uint8, device=dev)
+    pool = mtn.Pool(**kw, kv=kv)
+    sids = [pool.session_open() for _ in range(N)]
+    s0 = 1000 * w.workload_id + 500
+    # chunk tensors are [layer][sum(chunk_len)][H][D] with the frame's own row
+    # count, so each frame views a prefix of one flat bank
+    rows = Lyr * N * Cmax
+    qc_flat = device_bank((rows, Hq, D), tdt, dev, s0 + 1, w.act_scale)
+    kc_flat = device_bank((rows, Hkv, D), tdt, dev, s0 + 2, w.act_scale)
+    vc_flat = device_bank((rows, Hkv, D), tdt, dev, s0 + 3, w.act_scale)
+    oc_flat = torch.empty_like(qc_flat)
+    qd = device_bank((Tmax, Lyr, N, Hq, D), tdt, dev, s0 + 4, w.act_scale)
+    kd = device_bank((Tmax, Lyr, N, Hkv, D), tdt, dev, s0 + 5, w.act_scale)
+    vd = device_bank((Tmax, Lyr, N, Hkv, D), tdt, dev, s0 + 6, w.act_scale)
+    od = torch.empty_like(qd)
+
+    def chunk_view(t, tc):
+        return t[:Lyr * tc].view(Lyr, tc, *t.shape[1:])
+    rng = np.random.Generator(np.random.PCG64(np.random.SeedSequence([w.workload_id, 77])))
+    churn = 0
+    if ragged:
+        # mixed lengths: 30 % still filling the window, 70 % wrapped
+        S_W = w.n_sink + w.window
+        target = np.where(rng.random(N) < 0.3, rng.integers(0, S_W, N),
+                          rng.integers(S_W, 4 * S_W, N))
+        have = np.zeros(N, dtype=np.int64)
+        while True:
+            idx = [i for i in range(N) if have[i] < target[i]]
+            if not idx:
+                break
+            ntok = [int(min(Cmax, target[i] - have[i])) for i in idx]
+            pool.plan_begin([sids[i] for i in idx], ntok)
+            kf, vf = chunk_view(kc_flat, sum(ntok)), chunk_view(vc_flat, sum(ntok))
+            for l in range(Lyr):
+                pool.frame_append_kv(l, kf[l], vf[l])
+            pool.plan_commit()
+            for i, n in zip(idx, ntok):
+                have[i] += n
+        churn = max(1, round(0.02 * N))
+        torch.cuda.synchronize()
+        log(f"[call] fast-forwarded to mixed lengths (mean {have.mean():.0f} tokens)")
+    evs = [torch.cuda.Event(enable_timing=True) for _ in range(2 * frames)]
+    occ, fail_frame, fail_code = [], None, None
+    stats0 = pool.stats()
+    for f in range(frames):
+        if ragged:
+            cl = rng.integers(w.chunk[0], w.chunk[1] + 1, N).tolist()
+            nd = rng.integers(w.n_decode[0], w.n_decode[1] + 1, N).tolist()
+        else:
+            cl, nd = [Cmax] * N, [Tmax] * N
+        tc = sum(cl)
+        evs[2 * f].record()
+        try:
+            pool.frame_step(sids, cl, nd, chunk_view(qc_flat, tc), chunk_view(kc_flat, tc),
+                            chunk_view(vc_flat, tc), chunk_view(oc_flat, tc), qd, kd, vd, od)
+        except mtn.MtnError as e:
+            fail_frame, fail_code = f + 1, e.code
+            log(f"[call] frame {f + 1}: {e}")
+            evs[2 * f + 1].record()
+            break
+        evs[2 * f + 1].record()
+        st = pool.stats()
+        occ.append(st["assigned"] / st["capacity"])
+        if churn:
+            for i in rng.choice(N, churn, replace=False):
+                pool.session_close(sids[i])
+                sids[i] = pool.session_open()
+        if (f + 1) % 50 == 0:
+            torch.cuda.synchronize()
+            log(f"[call] frame {f + 1}/{frames}")
+    torch.cuda.synchronize()
+    done = len(occ)
+    ticks = [evs[2 * f].elapsed_time(evs[2 * f + 1]) for f in range(done)]
+    pool.close()
+    return dict(ticks=ticks, occupancy=occ, fail_frame=fail_frame, fail_code=fail_code,
+                n_blocks=n_blocks, frames=frames, reserved0=stats0["reserved"])
+
+
+def call_report(args, w, r):
+    import numpy as np
+    t = np.array(r["ticks"])
+    buckets = [round(float(np.median(t[i:i + 10])), 3) for i in range(0, len(t), 10)]
+    fill = None
+    if w.window is not None and w.chunk[0] == w.chunk[1]:
+        per = w.chunk[1] + w.n_decode[1]
+        fill = -(-(w.n_sink + w.window) // per)     # frames until every query sees S + W keys
+    out = {
+        "metric": "per-frame tick latency over a simulated call",
+        "workload": w.name, "sessions": w.n_sessions, "frames_run": len(t),
+        "frames_planned": r["frames"], "frame_budget_ms": w.frame_period_s * 1e3,
+        "tick_ms_p50_per_10_frames": buckets,
+        "tick_ms_p50": round(float(np.median(t)), 3) if len(t) else None,
+        "tick_ms_p99": round(float(np.percentile(t, 99)), 3) if len(t) else None,
+        "tick_ms_max": round(float(t.max()), 3) if len(t) else None,
+        "deadline_misses": int((t > w.frame_period_s * 1e3).sum()),
+        "pool_blocks": r["n_blocks"],
+        "occupancy_first_last": [round(r["occupancy"][0], 4), round(r["occupancy"][-1], 4)]
+        if r["occupancy"] else None,
+        "occupancy_per_10_frames": [round(float(x), 4) for x in r["occupancy"][9::10]],
+        "pool_exhausted_in_frame": r["fail_frame"],
+    }
+    if fill is not None and len(t) > fill + 10:
+        steady = t[fill:]
+        mean = float(steady.mean())
+        post = [float(np.median(steady[i:i + 10])) for i in range(0, len(steady) - 9, 10)]
+        out["window_full_from_frame"] = fill + 1
+        out["steady_mean_ms"] = round(mean, 3)
+        out["steady_bucket_p50_max_dev_frac"] = round(max(abs(p / mean - 1) for p in post), 4)
+    print(json.dumps(out), flush=True)
+    if args.json_out:
+        with open(args.json_out, "w") as f:
+            f.write(json.dumps(out) + "\n")
+
+
 def cpu_baseline(w, n_layers_sample):
     """The float64 oracle (as it stands) on one session-frame at steady state,
     restricted to ``n_layers_sample`` layers and scaled to the full depth."""
@@ -308,6 +463,9 @@ def main():
               file=sys.stderr)
         sys.exit(2)
     w = pick(args.workload)
+    if args.call:
+        call_report(args, w, run_call(args, w))
+        return
     res = run_gpu(args, w)
     cpu = None
     if not args.no_cpu_baseline:
