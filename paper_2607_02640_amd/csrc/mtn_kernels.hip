@@ -270,10 +270,31 @@ struct QRegs<float, D, G> {
     float v[G][D / 4];
 };
 
-#ifndef MTN_DECODE_RING_KB
-#define MTN_DECODE_RING_KB 64
+// Decode launch shape per group size G: WPU waves share each K/V block (a
+// wave owns at most 4 of the G heads), NG wave groups split a unit's keys,
+// and each group double-buffers its blocks in LDS.  Measured at the
+// 128-session G = 8 (Hkv = 4), 64-session G = 1 and 256-session G = 4
+// shapes: small rings that let more workgroups stay resident beat deeper
+// rings, and two groups per unit where G = 8 put two waves on every SIMD
+// (6.1 TB/s vs 5.3 TB/s with one group and a 64 KiB ring).
+template <int G>
+struct DecodeShape {
+#ifdef MTN_DECODE_HEADS_PER_WAVE
+    static constexpr int WPU = G >= MTN_DECODE_HEADS_PER_WAVE ? G / MTN_DECODE_HEADS_PER_WAVE : 1;
+#else
+    static constexpr int WPU = G >= 4 ? G / 4 : 1;
 #endif
-constexpr int kRingBytes = MTN_DECODE_RING_KB * 1024;  // LDS ring of K/V^T blocks per unit
+#ifdef MTN_DECODE_GROUPS
+    static constexpr int NG = MTN_DECODE_GROUPS;
+#else
+    static constexpr int NG = WPU >= 2 ? 2 : 1;
+#endif
+#ifdef MTN_DECODE_NBUF
+    static constexpr int NBUF = MTN_DECODE_NBUF;
+#else
+    static constexpr int NBUF = 2;
+#endif
+};
 
 // Asynchronous 16-byte-per-lane copy global -> LDS (gfx950 LDS DMA).  Lane i
 // of the wave writes LDS bytes [lds + 16 i, lds + 16 i + 16).  Issued from
@@ -324,32 +345,41 @@ __device__ __forceinline__ int32_t scalar_ld(const int32_t *p, int idx) {
 __device__ __forceinline__ int swz(int x) { return x ^ ((x >> 3) & 3); }
 
 // One work unit = (query token, kv head, split segment), served by one
-// workgroup of WPU waves.  The waves share a ring of K/V^T blocks in LDS
-// (each issues 1/WPU of every block's DMA) and split the G query heads of the
-// group: wave w owns heads w*HW .. w*HW + HW - 1, HW = G / WPU <= 4, so every
+// workgroup of NG wave groups of WPU waves each.  The unit's keys are cut
+// into NG consecutive segments, one per group; each group streams its segment
+// through its own ring of K/V^T blocks in LDS (each wave issues 1/WPU of every
+// block's DMA) and its waves split the G query heads of the KV group: wave w
+// of a group owns heads w*HW .. w*HW + HW - 1, HW = G / WPU <= 4, so every
 // lane owns at most one head in the online softmax.  One barrier per block
-// publishes the landed block and frees the buffer consumed before it.
-template <typename T, int D, int G, int WPU>
-__global__ __launch_bounds__(64 * WPU) void k_attn_valu(AttnArgs a) {
+// step publishes the landed blocks and frees the buffers consumed before
+// them.  At the end the groups' (max, sum, acc) are merged through LDS by
+// log-sum-exp, so several waves per SIMD stream one unit with no second
+// launch.
+template <typename T, int D, int G, int WPU, int NG, int NBUF>
+__global__ __launch_bounds__(64 * WPU * NG) void k_attn_valu(AttnArgs a) {
     using L = Lay<T, D>;
     constexpr int HW = G / WPU;                     // heads per wave
     static_assert(HW * WPU == G && HW <= 4, "head split");
+    static_assert(NBUF >= 2 && NBUF <= 8, "ring depth");
     constexpr int BLK = 2 * kBlock * D * L::E;      // K + V^T bytes of one block (one head)
-    constexpr int NBUF = kRingBytes / BLK < 2 ? 2 : (kRingBytes / BLK < 8 ? kRingBytes / BLK : 8);
     constexpr int NCH = BLK / 16;                   // 16-byte chunks per block
     constexpr int NI = NCH / 64;                    // DMA instructions per block
     constexpr int NIW = NI / WPU;                   // ... issued by each wave
     static_assert(NIW * WPU == NI && NIW >= 1, "DMA split");
-    __shared__ __attribute__((aligned(16))) uint8_t ring[NBUF][BLK];
-    __shared__ __attribute__((aligned(16))) float sP[WPU][sizeof(T) == 2 ? 1 : 2][HW][kBlock];
-    __shared__ float sA[WPU][2][HW];
-    __shared__ float sM[WPU][HW], sL[WPU][HW];
+    static_assert(NG == 1 || NG * G * D * 4 <= NG * NBUF * BLK, "merge scratch fits the ring");
+    constexpr int NW = WPU * NG;                    // waves per workgroup
+    __shared__ __attribute__((aligned(16))) uint8_t ring[NG][NBUF][BLK];
+    __shared__ __attribute__((aligned(16))) float sP[NW][sizeof(T) == 2 ? 1 : 2][HW][kBlock];
+    __shared__ float sA[NW][2][HW];
+    __shared__ float sM[NW][HW], sL[NW][HW];
 
     const int lane = threadIdx.x & 63;
     // wave-uniform indices live in scalar registers: the block-table and plan
     // reads below become scalar loads, which do not share the vector-memory
     // counter the LDS ring is synchronised with
     const int wv = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+    const int grp = wv / WPU;                       // wave group (key segment)
+    const int wq = wv - grp * WPU;                  // wave inside the group
     const int64_t unit = blockIdx.x;
     const PoolGeom &g = a.g;
     const int split = __builtin_amdgcn_readfirstlane((int)(unit % a.n_split));
@@ -359,17 +389,29 @@ __global__ __launch_bounds__(64 * WPU) void k_attn_valu(AttnArgs a) {
     const int pos = __builtin_amdgcn_readfirstlane(a.p.tok_pos[t]);
     const int64_t row = __builtin_amdgcn_readfirstlane(a.p.tok_row[t]);
     const int key = lane >> 2, qtr = lane & 3;
-    const int h0 = wv * HW;  // first head of this wave inside the group
+    const int h0 = wq * HW;  // first head of this wave inside the KV group
 
     // ---- work range and the first prefetches (issued before the q prologue)
+    // segment seg = split * NG + grp of nseg = n_split * NG covers virtual
+    // blocks [v0, v1); sinks sit in virtual block 0, so only segment 0 reads them
     const VisRange vr = vis_range(g, pos);
     const int nv = vr.n_sb + vr.n_rb;
-    const int v0 = __builtin_amdgcn_readfirstlane((int)((int64_t)split * nv / a.n_split));
-    const int v1 = __builtin_amdgcn_readfirstlane((int)((int64_t)(split + 1) * nv / a.n_split));
+    const int64_t nseg = (int64_t)a.n_split * NG;
+    const int64_t seg = (int64_t)split * NG + grp;
+    const int v0 = __builtin_amdgcn_readfirstlane((int)(seg * nv / nseg));
+    const int v1 = __builtin_amdgcn_readfirstlane((int)((seg + 1) * nv / nseg));
     const int nblk = v1 - v0;
+    // the barrier is workgroup-wide: every group runs the longest group's steps
+    int nstep = 0;
+#pragma unroll
+    for (int q2 = 0; q2 < NG; ++q2) {
+        const int64_t s2 = (int64_t)split * NG + q2;
+        nstep = max(nstep, (int)((s2 + 1) * nv / nseg - s2 * nv / nseg));
+    }
+    nstep = __builtin_amdgcn_readfirstlane(nstep);
     const uint8_t *head_base = g.kv + (int64_t)a.layer * g.layer_stride + (int64_t)kvh * g.head_stride;
     const int32_t *trow = g.table + (int64_t)sid * g.row_len;
-    const uint32_t ring0 = lds_addr(&ring[0][0]);
+    const uint32_t ring0 = lds_addr(&ring[grp][0][0]);
 
     BlockIter it_issue(g, vr, v0), it_proc(g, vr, v0);
     auto issue = [&](int i) {  // next block of the range -> ring slot i % NBUF (this wave's share)
@@ -382,7 +424,7 @@ __global__ __launch_bounds__(64 * WPU) void k_attn_valu(AttnArgs a) {
         const uint32_t dst = ring0 + (uint32_t)((i % NBUF) * BLK);
 #pragma unroll
         for (int jj = 0; jj < NIW; ++jj) {
-            const int j = wv * NIW + jj;
+            const int j = wq * NIW + jj;
             dma16(src + swz(j * 64 + lane) * 16, dst + j * 1024);
         }
     };
@@ -447,15 +489,15 @@ __global__ __launch_bounds__(64 * WPU) void k_attn_valu(AttnArgs a) {
 #pragma unroll
         for (int r = 0; r < L::VD; ++r) acc[h][r] = 0.f;
 
-    for (int i = 0; i < nblk; ++i) {
+    for (int i = 0; i < nstep; ++i) {
         // this wave's share of block i has landed once at most the shares of
         // the blocks issued after it are outstanding; the barrier then covers
         // the other waves' shares and frees the buffer of block i - 1
-        const int after = min(NBUF - 2, nblk - 1 - i);
-        vm_wait_blocks<NIW, NBUF - 2>(after);
-        if constexpr (WPU > 1) __syncthreads();
+        if (i < nblk) vm_wait_blocks<NIW, NBUF - 2>(min(NBUF - 2, nblk - 1 - i));
+        if constexpr (NW > 1) __syncthreads();
+        if (i >= nblk) continue;  // a shorter segment idles through the last step
         if (i + NBUF - 1 < nblk) issue(i + NBUF - 1);
-        const uint8_t *blk = &ring[i % NBUF][0];
+        const uint8_t *blk = &ring[grp][i % NBUF][0];
         const int buf = i & 1;
         int lb, lo, hi;
         it_proc.get(&lb, &lo, &hi);
@@ -579,6 +621,44 @@ __global__ __launch_bounds__(64 * WPU) void k_attn_valu(AttnArgs a) {
         if (qtr < HW && key == 0) {
             sM[wv][qtr] = m;
             sL[wv][qtr] = lt;
+        }
+    }
+    if constexpr (NG > 1) {
+        // groups 1.. hand (m, l, acc) to group 0 through the (drained) ring
+        float *scr = (float *)&ring[0][0][0];  // [NG][G][D]
+        __syncthreads();
+        if (grp > 0) {
+#pragma unroll
+            for (int h = 0; h < HW; ++h)
+#pragma unroll
+                for (int r = 0; r < L::VD; ++r)
+                    scr[((int64_t)grp * G + h0 + h) * D + lane * L::VD + r] = acc[h][r];
+        }
+        __syncthreads();
+        if (grp > 0) return;
+#pragma unroll
+        for (int h = 0; h < HW; ++h) {
+            float M = sM[wq][h];
+#pragma unroll
+            for (int q2 = 1; q2 < NG; ++q2) M = fmaxf(M, sM[q2 * WPU + wq][h]);
+            const float Mn = (M == -INFINITY) ? 0.f : M;
+            float w0 = __builtin_amdgcn_exp2f(sM[wq][h] - Mn);
+            float Ls = sL[wq][h] * w0;
+#pragma unroll
+            for (int r = 0; r < L::VD; ++r) acc[h][r] *= w0;
+#pragma unroll
+            for (int q2 = 1; q2 < NG; ++q2) {
+                const float wg = __builtin_amdgcn_exp2f(sM[q2 * WPU + wq][h] - Mn);
+                Ls += sL[q2 * WPU + wq][h] * wg;
+#pragma unroll
+                for (int r = 0; r < L::VD; ++r)
+                    acc[h][r] = fmaf(wg, scr[((int64_t)q2 * G + h0 + h) * D + lane * L::VD + r], acc[h][r]);
+            }
+            // only group 0's waves read these from here on
+            if (lane == 0) {
+                sM[wv][h] = M;
+                sL[wv][h] = Ls;
+            }
         }
     }
     wave_sync();
@@ -708,10 +788,19 @@ __global__ void k_copy(const u32x4_t *__restrict__ src, u32x4_t *__restrict__ ds
 typedef __attribute__((ext_vector_type(8))) __bf16 bf16x8_t;
 typedef __attribute__((ext_vector_type(4))) float f32x4_t;
 
-constexpr int kPfWaves = 8;   // waves per workgroup
-constexpr int kPfTpw = 2;     // 16-row query tiles per wave per pass
+#ifndef MTN_PF_WAVES
+#define MTN_PF_WAVES 8
+#endif
+#ifndef MTN_PF_TILES_PER_WAVE
+#define MTN_PF_TILES_PER_WAVE 2
+#endif
+#ifndef MTN_PF_STAGES
+#define MTN_PF_STAGES 8
+#endif
+constexpr int kPfWaves = MTN_PF_WAVES;          // waves per workgroup
+constexpr int kPfTpw = MTN_PF_TILES_PER_WAVE;   // 16-row query tiles per wave per pass
 constexpr int kPfRowsPerPass = kPfWaves * kPfTpw * 16;
-constexpr int kPfStages = 8;  // LDS ring depth in stages of two blocks (16 KiB each)
+constexpr int kPfStages = MTN_PF_STAGES;        // LDS ring depth in stages of two blocks (16 KiB each)
 constexpr int kPfStageBytes = 16384;
 
 struct PfArgs {
@@ -799,10 +888,14 @@ struct PfIter {
     }
 };
 
+#ifndef MTN_PF_WAVES_PER_EU
+#define MTN_PF_WAVES_PER_EU 1
+#endif
 template <int G>
-__global__ __launch_bounds__(64 * kPfWaves) void k_prefill_mfma(PfArgs pa) {
+__global__ __launch_bounds__(64 * kPfWaves, MTN_PF_WAVES_PER_EU) void k_prefill_mfma(PfArgs pa) {
     constexpr int D = 128;
     constexpr int NIW = kPfStageBytes / 1024 / kPfWaves;  // DMA instructions per wave per stage
+    static_assert(NIW * kPfWaves * 1024 == kPfStageBytes, "stage DMA split");
     __shared__ __attribute__((aligned(16))) uint8_t ring[kPfStages][kPfStageBytes];
     const AttnArgs &a = pa.a;
     const PoolGeom &g = a.g;
@@ -939,20 +1032,23 @@ __global__ __launch_bounds__(64 * kPfWaves) void k_prefill_mfma(PfArgs pa) {
             const bool part1 = m1.phys >= 0 && m1.lo < m1.hi && (m1.lo > 0 || m1.hi < kBlock);
             if (part0 || part1) {
                 // values of slots outside the union may be NaN: zero them in LDS
-                const int b = tid >> 8;            // 512 threads: 256 per block
-                const int d = (tid & 255) >> 1, half = tid & 1;
-                const int lo = b ? m1.lo : m0.lo, hi = b ? m1.hi : m0.hi;
-                if (b ? part1 : part0) {
-                    uint4 *pv = (uint4 *)(sm + lds_v16(b, d, half));
-                    uint4 x = *pv;
-                    uint32_t w[4] = {x.x, x.y, x.z, x.w};
+                // (512 16-byte V^T chunks per stage: 256 per block, two per d)
+                for (int e = tid; e < 512; e += 64 * kPfWaves) {
+                    const int b = e >> 8;
+                    const int d = (e & 255) >> 1, half = e & 1;
+                    const int lo = b ? m1.lo : m0.lo, hi = b ? m1.hi : m0.hi;
+                    if (b ? part1 : part0) {
+                        uint4 *pv = (uint4 *)(sm + lds_v16(b, d, half));
+                        uint4 x = *pv;
+                        uint32_t w[4] = {x.x, x.y, x.z, x.w};
 #pragma unroll
-                    for (int e = 0; e < 4; ++e) {
-                        const int ka = half * 8 + 2 * e, kb = ka + 1;
-                        w[e] &= ((ka >= lo && ka < hi) ? 0x0000FFFFu : 0u) |
-                                ((kb >= lo && kb < hi) ? 0xFFFF0000u : 0u);
+                        for (int q4 = 0; q4 < 4; ++q4) {
+                            const int ka = half * 8 + 2 * q4, kb = ka + 1;
+                            w[q4] &= ((ka >= lo && ka < hi) ? 0x0000FFFFu : 0u) |
+                                     ((kb >= lo && kb < hi) ? 0xFFFF0000u : 0u);
+                        }
+                        *pv = make_uint4(w[0], w[1], w[2], w[3]);
                     }
-                    *pv = make_uint4(w[0], w[1], w[2], w[3]);
                 }
                 __syncthreads();
             }
@@ -1058,16 +1154,13 @@ __global__ __launch_bounds__(64 * kPfWaves) void k_prefill_mfma(PfArgs pa) {
     }
 }
 
-#ifndef MTN_DECODE_HEADS_PER_WAVE
-#define MTN_DECODE_HEADS_PER_WAVE 4
-#endif
 template <typename T, int D, int G>
 hipError_t launch_valu_t(const AttnArgs &a, hipStream_t s) {
-    constexpr int HPW = MTN_DECODE_HEADS_PER_WAVE;
-    constexpr int WPU = G >= HPW ? G / HPW : 1;
+    using DS = DecodeShape<G>;
     int64_t units = (int64_t)a.p.n_tok * a.g.hkv * a.n_split;
     if (units == 0) return hipSuccess;
-    hipLaunchKernelGGL((k_attn_valu<T, D, G, WPU>), dim3((unsigned)units), dim3(64 * WPU), 0, s, a);
+    hipLaunchKernelGGL((k_attn_valu<T, D, G, DS::WPU, DS::NG, DS::NBUF>), dim3((unsigned)units),
+                       dim3(64 * DS::WPU * DS::NG), 0, s, a);
     return hipGetLastError();
 }
 
@@ -1084,10 +1177,10 @@ hipError_t launch_valu_d(const AttnArgs &a, int G, hipStream_t s) {
 
 template <typename T, int D, int G>
 int resident_t() {
-    constexpr int HPW = MTN_DECODE_HEADS_PER_WAVE;
-    constexpr int WPU = G >= HPW ? G / HPW : 1;
+    using DS = DecodeShape<G>;
     int n = 0;
-    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, k_attn_valu<T, D, G, WPU>, 64 * WPU, 0) !=
+    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(
+            &n, k_attn_valu<T, D, G, DS::WPU, DS::NG, DS::NBUF>, 64 * DS::WPU * DS::NG, 0) !=
         hipSuccess)
         return 1;
     return n > 0 ? n : 1;
