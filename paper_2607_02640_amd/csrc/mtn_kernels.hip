@@ -339,10 +339,12 @@ __device__ __forceinline__ int32_t scalar_ld(const int32_t *p, int idx) {
     return ((const __attribute__((address_space(4))) int32_t *)p)[idx];
 }
 
-// 16-byte chunk permutation of a block buffer (an involution that keeps each
-// aligned group of four chunks together): a lane's 64-byte slice lands
-// rotated so that eight consecutive lanes read eight distinct LDS bank groups.
-__device__ __forceinline__ int swz(int x) { return x ^ ((x >> 3) & 3); }
+// 16-byte chunk permutation of a block buffer: an involution that XORs the
+// low four chunk bits with the next four, so every 16-byte read instruction of
+// the ring (lane l takes chunk 4 l + c) spreads its lanes over all LDS banks.
+// Chosen by measurement: 255 B/clk/CU of ds_read_b128 against 203 for a
+// two-bit rotation and 117 unswizzled.
+__device__ __forceinline__ int swz(int x) { return x ^ ((x >> 4) & 15); }
 
 // One work unit = (query token, kv head, split segment), served by one
 // workgroup of NG wave groups of WPU waves each.  The unit's keys are cut
@@ -780,11 +782,13 @@ __global__ void k_copy(const u32x4_t *__restrict__ src, u32x4_t *__restrict__ ds
 //   S^T[key][row] = K[key][:] . Qrot[row][:]      (A = K, B = Q^T)
 //   O^T[d][row]  += V^T[d][key] . P^T[key][row]   (A = V^T, B = P^T)
 // With the 16x16x32 MFMA output layout, lane l holds column (row) l % 16 of
-// both S^T and O^T, so the softmax state and the accumulators of a row live
-// in the same lane.  The B operand of the PV product is the lane's own eight
-// probabilities: keys 4g..4g+3 of the first block and 4g..4g+3 of the second
-// (g = l / 16) take the k slots 8g..8g+7, and the V^T operand uses the same
-// key order.
+// both S^T and O^T, so a row's softmax state and its accumulators share a
+// lane.  The QK product of a stage is two MFMAs per 32-wide slice of d whose
+// A rows are permuted keys: row i of MFMA mf holds stage key
+// 8 (i / 4) + 4 mf + i % 4.  Lane l (g = l / 16) then holds the scores of the
+// eight consecutive stage keys 8g .. 8g + 7, all in block g / 2, which are
+// exactly the k slots 8g .. 8g + 7 of its PV B operand; the matching V^T
+// A operand is one aligned 16-byte chunk per lane.
 typedef __attribute__((ext_vector_type(8))) __bf16 bf16x8_t;
 typedef __attribute__((ext_vector_type(4))) float f32x4_t;
 
@@ -814,26 +818,52 @@ __device__ __forceinline__ f32x4_t mfma16x16x32(const uint4 &a, const uint4 &b, 
     return __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8_t, a),
                                                     __builtin_bit_cast(bf16x8_t, b), c, 0, 0, 0);
 }
+// Plain v_max3_f32 / v_max_f32.  Scores are finite or -inf (masked), never
+// NaN, so the NaN-quieting the compiler adds around fmaxf is not needed.
+__device__ __forceinline__ float vmax3(float a, float b, float c) {
+    float r;
+    asm("v_max3_f32 %0, %1, %2, %3" : "=v"(r) : "v"(a), "v"(b), "v"(c));
+    return r;
+}
+__device__ __forceinline__ float vmax2(float a, float b) {
+    float r;
+    asm("v_max_f32 %0, %1, %2" : "=v"(r) : "v"(a), "v"(b));
+    return r;
+}
+// max over the four 16-lane rows (lanes with equal lane % 16)
+__device__ __forceinline__ float rows_max(float x) {
+    const unsigned u = __builtin_bit_cast(unsigned, x);
+    auto r = __builtin_amdgcn_permlane16_swap(u, opaque_copy(u), false, false);
+    x = vmax2(__builtin_bit_cast(float, (unsigned)r[0]), __builtin_bit_cast(float, (unsigned)r[1]));
+    const unsigned w = __builtin_bit_cast(unsigned, x);
+    auto q = __builtin_amdgcn_permlane32_swap(w, opaque_copy(w), false, false);
+    return vmax2(__builtin_bit_cast(float, (unsigned)q[0]), __builtin_bit_cast(float, (unsigned)q[1]));
+}
 
-// LDS addressing (bytes) inside one stage: K tiles of blocks 0, 1 (16-byte
-// chunks swizzled by key), then V^T tiles (16-byte chunks swizzled by d).
+// LDS layout of one stage: K tiles of blocks 0, 1 (the 16-byte chunks of a
+// key row permuted by kswz(b, key)), then V^T tiles (the two 16-byte halves of
+// a d row swapped on bit 2 of d).  A K read instruction has lanes 0..15 on
+// keys {0..3, 8..11} (or {4..7, 12..15}) of both blocks; kswz gives those 16
+// (block, key) pairs 16 distinct chunk positions and ignores key bit 2, so
+// the second MFMA's rows sit exactly 4 rows (1 KiB) further.  Both patterns
+// read at the full LDS rate (measured: 228 and 240 B/clk/CU against 178 for
+// a swizzle without the block bit).
+__device__ __forceinline__ int kswz(int b, int key) {
+    return (key & 3) | ((key & 8) >> 1) | (b << 3);
+}
 __device__ __forceinline__ int lds_k(int b, int key, int chunk16) {
-    return b * 4096 + key * 256 + ((chunk16 ^ (key & 7)) << 4);
+    return b * 4096 + key * 256 + ((chunk16 ^ kswz(b, key)) << 4);
 }
-__device__ __forceinline__ int lds_v16(int b, int d, int chunk16) {
-    return 8192 + b * 4096 + d * 32 + ((chunk16 ^ ((d >> 2) & 1)) << 4);
+__device__ __forceinline__ int lds_v16(int b, int d, int half) {
+    return 8192 + b * 4096 + d * 32 + ((half ^ ((d >> 2) & 1)) << 4);
 }
-// 8 bytes V^T[d][keys 4g .. 4g+3] of block b
-__device__ __forceinline__ int lds_v8(int b, int d, int g) {
-    return lds_v16(b, d, g >> 1) + ((g & 1) << 3);
-}
-// Global byte offset (inside the block's 8 KiB K + V^T pair) of the 16-byte
-// chunk that lands at stage byte offset `off` (block b = which of the two).
+// Byte offset, inside a block's 8 KiB (K tile, V^T tile) pair, of the 16-byte
+// chunk that lands at stage byte offset `off`; *b = which block of the stage.
 __device__ __forceinline__ int stage_src(int off, int *b) {
     if (off < 8192) {
         *b = off >> 12;
         const int r = off & 4095, key = r >> 8, pos = (r >> 4) & 15;
-        return key * 256 + ((pos ^ (key & 7)) << 4);
+        return key * 256 + ((pos ^ kswz(*b, key)) << 4);
     }
     const int o2 = off - 8192;
     *b = o2 >> 12;
@@ -841,61 +871,19 @@ __device__ __forceinline__ int stage_src(int off, int *b) {
     return 4096 + d * 32 + ((pos ^ ((d >> 2) & 1)) << 4);
 }
 
-// Walks the union's virtual blocks 0, 1, ... of a chunk (sinks, then the
-// ring run) without division: logical block, valid slots [lo, hi), the
-// absolute position of slot 0 and whether the block holds sinks.
-struct PfIter {
-    int v, nvb, n_sb, sink_tokens, n_rb, first_off, last_hi, rb, ring_blocks, nsb, ring_p0;
-    __device__ __forceinline__ void init(const PoolGeom &g, int n_sb_, int sink_tokens_, int n_rb_,
-                                         int first, int ring_n, int A) {
-        v = 0;
-        n_sb = n_sb_;
-        sink_tokens = sink_tokens_;
-        n_rb = n_rb_;
-        nvb = n_sb + n_rb;
-        first_off = first % kBlock;
-        last_hi = (first_off + ring_n - 1) % kBlock + 1;
-        ring_blocks = g.ring / kBlock;
-        nsb = g.n_sink_blocks;
-        rb = first / kBlock;
-        ring_p0 = A - first_off;
-    }
-    // returns false for a block past the end of the union
-    __device__ __forceinline__ bool get(int *lb, int *lo, int *hi, int *p0, bool *sink) const {
-        if (v >= nvb) return false;
-        if (v < n_sb) {
-            *lb = v;
-            *lo = 0;
-            *hi = min(kBlock, sink_tokens - v * kBlock);
-            *p0 = v * kBlock;
-            *sink = true;
-        } else {
-            const int u = v - n_sb;
-            *lb = nsb + rb;
-            *lo = (u == 0) ? first_off : 0;
-            *hi = (u == n_rb - 1) ? last_hi : kBlock;
-            *p0 = ring_p0;
-            *sink = false;
-        }
-        return true;
-    }
-    __device__ __forceinline__ void next() {
-        if (v >= n_sb) {
-            rb = (rb + 1 == ring_blocks) ? 0 : rb + 1;
-            ring_p0 += kBlock;
-        }
-        ++v;
-    }
+// A virtual block of a chunk's key union (sinks first, then the ring run):
+// logical block, valid slots [lo, hi), absolute position of slot 0.
+struct PfBlock {
+    int lb, lo, hi, p0;
+    bool sink;
 };
 
-#ifndef MTN_PF_WAVES_PER_EU
-#define MTN_PF_WAVES_PER_EU 1
-#endif
 template <int G>
-__global__ __launch_bounds__(64 * kPfWaves, MTN_PF_WAVES_PER_EU) void k_prefill_mfma(PfArgs pa) {
+__global__ __launch_bounds__(64 * kPfWaves) void k_prefill_mfma(PfArgs pa) {
     constexpr int D = 128;
     constexpr int NIW = kPfStageBytes / 1024 / kPfWaves;  // DMA instructions per wave per stage
     static_assert(NIW * kPfWaves * 1024 == kPfStageBytes, "stage DMA split");
+    static_assert(kPfStages >= 2 && kPfStages <= 8, "ring depth");
     __shared__ __attribute__((aligned(16))) uint8_t ring[kPfStages][kPfStageBytes];
     const AttnArgs &a = pa.a;
     const PoolGeom &g = a.g;
@@ -922,55 +910,126 @@ __global__ __launch_bounds__(64 * kPfWaves, MTN_PF_WAVES_PER_EU) void k_prefill_
     const int A = g.window < 0 ? 0 : max(g.n_sink, pos0 - g.window + 1);
     const int ring_n = pos_last - A + 1;  // >= 1: the chunk itself is in the run
     const int first = g.window < 0 ? A : (A - g.n_sink) % g.ring;
-    const int n_rb = ((first % kBlock) + ring_n + kBlock - 1) / kBlock;
+    const int first_off = first % kBlock;
+    const int rb_start = first / kBlock;
+    const int ring_blocks = g.ring / kBlock;
+    const int n_rb = (first_off + ring_n + kBlock - 1) / kBlock;
+    const int last_hi = (first_off + ring_n - 1) % kBlock + 1;
+    const int ring_p0 = A - first_off;
     const int nvb = n_sb + n_rb;
     const int n_stages = (nvb + 1) / 2;
 
-    // block metadata of the stage being issued / processed
-    struct BlockMeta {
-        int phys, lo, hi, p0;
-        bool sink;
-    };
-    auto meta = [&](PfIter &it, BlockMeta &m) {
-        int lb;
-        if (it.get(&lb, &m.lo, &m.hi, &m.p0, &m.sink)) {
-            m.phys = scalar_ld(trow, __builtin_amdgcn_readfirstlane(lb));
-            if (m.phys < 0) m.hi = m.lo;
+    auto vblock = [&](int v) {
+        PfBlock m;
+        if (v < n_sb) {
+            m.lb = v;
+            m.lo = 0;
+            m.hi = min(kBlock, sink_tokens - v * kBlock);
+            m.p0 = v * kBlock;
+            m.sink = true;
+        } else if (v < nvb) {
+            const int u = v - n_sb;
+            int rb = rb_start + u;
+            rb = rb >= ring_blocks ? rb - ring_blocks : rb;
+            m.lb = g.n_sink_blocks + rb;
+            m.lo = u == 0 ? first_off : 0;
+            m.hi = u == n_rb - 1 ? last_hi : kBlock;
+            m.p0 = ring_p0 + u * kBlock;
+            m.sink = false;
         } else {
-            m.phys = -1;
+            m.lb = -1;
             m.lo = m.hi = m.p0 = 0;
             m.sink = false;
         }
-        it.next();
+        return m;
     };
-    PfIter it_issue, it_proc;
 
-    // DMA of the next stage into ring slot st % kPfStages; each wave moves NIW KiB
-    auto issue_stage = [&](int st) {
-        BlockMeta m0, m1;
-        meta(it_issue, m0);
-        meta(it_issue, m1);
-        const uint8_t *b0 = (m0.phys < 0 || m0.lo >= m0.hi) ? pa.zero_page
-                                                            : layer_base + (int64_t)m0.phys * g.block_stride;
-        const uint8_t *b1 = (m1.phys < 0 || m1.lo >= m1.hi) ? pa.zero_page
-                                                            : layer_base + (int64_t)m1.phys * g.block_stride;
-        const uint32_t dst = ring0 + (uint32_t)((st % kPfStages) * kPfStageBytes);
+    // per-lane DMA source offsets (fixed for every stage): instruction j of
+    // this wave moves stage bytes [j * 1024, j * 1024 + 1024), block j_b
+    int src_off[NIW];
+#pragma unroll
+    for (int jj = 0; jj < NIW; ++jj) {
+        int b;
+        src_off[jj] = stage_src((wv * NIW + jj) * 1024 + lane * 16, &b);
+    }
+    // logical block of virtual block v < nvb (branch-free: sinks, then the ring)
+    auto vlb = [&](int v) {
+        int rb = rb_start + v - n_sb;
+        rb = rb >= ring_blocks ? rb - ring_blocks : rb;
+        return v < n_sb ? v : g.n_sink_blocks + rb;
+    };
+    // bit 2 (st % kPfStages) + b: block b of stage st holds assigned data.
+    // Every virtual block below nvb holds at least one valid slot.
+    uint32_t have_bits = 0;
+    auto load_phys = [&](int st, int &ph0, int &ph1) {
+        const int va = 2 * st, vb = va + 1;
+        ph0 = scalar_ld(trow, vlb(va));                      // va < nvb always
+        ph1 = vb < nvb ? scalar_ld(trow, vlb(vb)) : -1;
+    };
+    auto issue_dma = [&](int st, int ph0, int ph1) {
+        const bool h0 = ph0 >= 0, h1 = ph1 >= 0;
+        const uint8_t *b0 = h0 ? layer_base + (int64_t)ph0 * g.block_stride : pa.zero_page;
+        const uint8_t *b1 = h1 ? layer_base + (int64_t)ph1 * g.block_stride : pa.zero_page;
+        const int slot = st % kPfStages;
+        have_bits = (have_bits & ~(3u << (2 * slot))) | ((h0 ? 1u : 0u) << (2 * slot)) |
+                    ((h1 ? 2u : 0u) << (2 * slot));
+        const uint32_t dst = ring0 + (uint32_t)(slot * kPfStageBytes);
 #pragma unroll
         for (int jj = 0; jj < NIW; ++jj) {
-            const int j = wv * NIW + jj;
-            int b;
-            const int src = stage_src(j * 1024 + lane * 16, &b);
-            dma16((b ? b1 : b0) + src, dst + j * 1024);
+            const int j = wv * NIW + jj;  // uniform; block of the instruction below
+            const int jb = j < 8 ? (j >> 2) : ((j - 8) >> 2);
+            dma16((jb ? b1 : b0) + src_off[jj], dst + j * 1024);
         }
     };
 
+    // per-lane LDS offsets inside a stage: K rows of the two QK MFMAs
+    // (permuted keys), and the lane's V^T chunk
+    // (the two MFMAs' keys differ by 4, which kswz ignores: MFMA 1's row is
+    // MFMA 0's plus 4 * 256 bytes)
+    int koff[4];
+    {
+        const int kap = 8 * (ln16 >> 2) + (ln16 & 3);
+#pragma unroll
+        for (int s = 0; s < 4; ++s) koff[s] = lds_k(kap >> 4, kap & 15, s * 4 + lg);
+    }
+    const int lblk = lg >> 1;          // the block of this lane's eight keys
+    const int lkey0 = 8 * (lg & 1);    // ... and the first of them
+    const int voff = lds_v16(lblk, ln16, lg & 1);  // + dt * 16 * 32 for d tile dt
+
     const int hq0 = kvh * G;
     for (int pass_row0 = 0; pass_row0 < n_rows; pass_row0 += kPfRowsPerPass) {
-        // ---- per-wave query tiles: rows r = pass_row0 + (wv + 8 i) * 16 + ln16
+        // query positions spanned by this pass (the unmasked test below)
+        const int tq_min = pos0 + pass_row0 / G;
+        const int tq_max = pos0 + (min(n_rows, pass_row0 + kPfRowsPerPass) - 1) / G;
+        // virtual blocks every row of the pass sees whole: sink blocks
+        // [0, fs_hi) and ring blocks [fr_lo, fr_hi) (as virtual indices)
+        const int fs_hi = min(sink_tokens / kBlock, (tq_min + 1) / kBlock);
+        int fr_lo, fr_hi;
+        {
+            // ring block u spans positions ring_p0 + 16u .. + 15; it is whole
+            // when u > 0 or first_off == 0, u < n_rb - 1 or last_hi == 16,
+            // its end is at most tq_min and (windowed) its start is at least
+            // tq_max - W + 1
+            int ulo = first_off == 0 ? 0 : 1;
+            if (g.window >= 0) {
+                const int need = tq_max - g.window + 1 - ring_p0;  // p0 offset >= need
+                ulo = max(ulo, need <= 0 ? 0 : (need + kBlock - 1) / kBlock);
+            }
+            const int lim = tq_min - (kBlock - 1) - ring_p0;      // 16u <= lim
+            int uhi = lim < 0 ? 0 : lim / kBlock + 1;
+            uhi = min(uhi, last_hi == kBlock ? n_rb : n_rb - 1);
+            fr_lo = n_sb + ulo;
+            fr_hi = n_sb + max(uhi, ulo);
+        }
+        auto whole_v = [&](int v) { return v < fs_hi || (v >= fr_lo && v < fr_hi); };
+        // ---- per-wave query tiles: rows r = pass_row0 + (wv + kPfWaves i) * 16 + ln16
         uint4 qf[kPfTpw][4];
         f32x4_t acc[kPfTpw][8];
-        float m_i[kPfTpw], l_i[kPfTpw];
-        int trow_tok[kPfTpw];
+        // row reference max (log2 units) and the row sum of the probabilities,
+        // accumulated by an MFMA against all-ones (every entry = the row sum)
+        float m_ref[kPfTpw];
+        f32x4_t l_i[kPfTpw];
+        int tq_i[kPfTpw];
         bool live[kPfTpw];
 #pragma unroll
         for (int i = 0; i < kPfTpw; ++i) {
@@ -980,9 +1039,9 @@ __global__ __launch_bounds__(64 * kPfWaves, MTN_PF_WAVES_PER_EU) void k_prefill_
             const bool rv_ = r < n_rows;
             const int j = rv_ ? r / G : 0;
             const int gh = rv_ ? r % G : 0;
-            trow_tok[i] = j;
-            m_i[i] = -INFINITY;
-            l_i[i] = 0.f;
+            tq_i[i] = pos0 + j;
+            m_ref[i] = -INFINITY;
+            l_i[i] = f32x4_t{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
             for (int dt = 0; dt < 8; ++dt) acc[i][dt] = f32x4_t{0.f, 0.f, 0.f, 0.f};
             const int t = tok0 + j;
@@ -1012,117 +1071,157 @@ __global__ __launch_bounds__(64 * kPfWaves, MTN_PF_WAVES_PER_EU) void k_prefill_
             }
         }
 
-        it_issue.init(g, n_sb, sink_tokens, n_rb, first, ring_n, A);
-        it_proc.init(g, n_sb, sink_tokens, n_rb, first, ring_n, A);
+        // One stage: two blocks of keys against every tile of this wave.
+        // FULL stages (every row sees every key) skip all masking.  The
+        // softmax keeps a per-row reference max that moves only when a score
+        // exceeds it by more than 2^8 (probabilities stay <= 256), so the
+        // accumulator rescale is rare; the result is the same softmax.
+        auto stage_body = [&](auto full_c, const uint8_t *sm, int st, uint32_t hb) {
+            constexpr bool FULL = decltype(full_c)::value;
+            constexpr float kLazy = 8.f;
+            int bp0 = 0, blo = 0, bhi = 0;
+            bool bsink = false;
+            if constexpr (!FULL) {
+                const PfBlock m0 = vblock(2 * st), m1 = vblock(2 * st + 1);
+                // values of slots outside a block's valid range may be NaN:
+                // zero them in LDS (512 16-byte V^T chunks: 256 per block)
+                const bool part0 = (hb & 1u) && (m0.lo > 0 || m0.hi < kBlock);
+                const bool part1 = (hb & 2u) && (m1.lo > 0 || m1.hi < kBlock);
+                if (part0 || part1) {
+                    for (int e = tid; e < 512; e += 64 * kPfWaves) {
+                        const int b = e >> 8;
+                        const int d = (e & 255) >> 1, half = e & 1;
+                        const int lo = b ? m1.lo : m0.lo, hi = b ? m1.hi : m0.hi;
+                        if (b ? part1 : part0) {
+                            uint4 *pv = (uint4 *)(sm + lds_v16(b, d, half));
+                            uint4 x = *pv;
+                            uint32_t w[4] = {x.x, x.y, x.z, x.w};
+#pragma unroll
+                            for (int q4 = 0; q4 < 4; ++q4) {
+                                const int ka = half * 8 + 2 * q4, kb = ka + 1;
+                                w[q4] &= ((ka >= lo && ka < hi) ? 0x0000FFFFu : 0u) |
+                                         ((kb >= lo && kb < hi) ? 0xFFFF0000u : 0u);
+                            }
+                            *pv = make_uint4(w[0], w[1], w[2], w[3]);
+                        }
+                    }
+                    __syncthreads();
+                }
+                // this lane's eight keys lie in block lblk
+                const PfBlock &mb = lblk ? m1 : m0;
+                const bool hv = lblk ? (hb & 2u) : (hb & 1u);
+                bp0 = mb.p0;
+                bsink = mb.sink;
+                blo = mb.lo;
+                bhi = hv ? mb.hi : mb.lo;
+            }
+            // QK, tile by tile (K fragments read once per stage, shared; tiles
+            // past the last row compute on zero queries and are dropped)
+            f32x4_t sa[kPfTpw], sb[kPfTpw];
+#pragma unroll
+            for (int i = 0; i < kPfTpw; ++i) {
+                sa[i] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+                sb[i] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+            }
+#pragma unroll
+            for (int s = 0; s < 4; ++s) {
+                const uint4 k0 = *(const uint4 *)(sm + koff[s]);
+                const uint4 k1 = *(const uint4 *)(sm + koff[s] + 1024);
+#pragma unroll
+                for (int i = 0; i < kPfTpw; ++i) {
+                    sa[i] = mfma16x16x32(k0, qf[i][s], sa[i]);
+                    sb[i] = mfma16x16x32(k1, qf[i][s], sb[i]);
+                }
+            }
+            // row max per tile: lane holds row ln16, stage keys 8 lg + e
+            // (e < 8) = slots lkey0 + e of block lblk
+            float sc[kPfTpw][8], mx[kPfTpw];
+            bool bump = false;
+#pragma unroll
+            for (int i = 0; i < kPfTpw; ++i) {
+#pragma unroll
+                for (int r = 0; r < 4; ++r) {
+                    sc[i][r] = sa[i][r];
+                    sc[i][4 + r] = sb[i][r];
+                }
+                if constexpr (!FULL) {
+                    // visible slots of the block for query position tq: one range
+                    const int tq = tq_i[i];
+                    const int wl = g.window < 0 ? -(1 << 30) : tq - g.window + 1;
+                    const int vlo = bsink ? blo : max(blo, wl - bp0);
+                    const int vhi = min(bhi, tq + 1 - bp0);
+#pragma unroll
+                    for (int e = 0; e < 8; ++e) {
+                        const int o = lkey0 + e;
+                        sc[i][e] = (o >= vlo && o < vhi) ? sc[i][e] : -INFINITY;
+                    }
+                }
+                const float m8 = vmax3(vmax3(sc[i][0], sc[i][1], sc[i][2]),
+                                       vmax3(sc[i][3], sc[i][4], sc[i][5]), vmax2(sc[i][6], sc[i][7]));
+                mx[i] = rows_max(m8);
+                bump = bump || mx[i] > m_ref[i] + kLazy;
+            }
+            if (__builtin_amdgcn_ballot_w64(bump)) {
+#pragma unroll
+                for (int i = 0; i < kPfTpw; ++i) {
+                    const float mnew = mx[i] > m_ref[i] + kLazy ? mx[i] : m_ref[i];
+                    const float alpha = mnew == m_ref[i] ? 1.f : __builtin_amdgcn_exp2f(m_ref[i] - mnew);
+                    m_ref[i] = mnew;
+                    l_i[i] *= alpha;  // all four entries
+#pragma unroll
+                    for (int dt = 0; dt < 8; ++dt) acc[i][dt] *= alpha;
+                }
+            }
+            // probabilities against the reference, then PV (one 16-byte V^T
+            // chunk per lane per d tile, shared by the tiles)
+            uint4 pb[kPfTpw];
+#pragma unroll
+            for (int i = 0; i < kPfTpw; ++i) {
+                const float mr = FULL ? m_ref[i] : (m_ref[i] == -INFINITY ? 0.f : m_ref[i]);
+#pragma unroll
+                for (int r = 0; r < 8; ++r) sc[i][r] = __builtin_amdgcn_exp2f(sc[i][r] - mr);
+                pb[i] = make_uint4(pack_bf16x2(sc[i][0], sc[i][1]), pack_bf16x2(sc[i][2], sc[i][3]),
+                                   pack_bf16x2(sc[i][4], sc[i][5]), pack_bf16x2(sc[i][6], sc[i][7]));
+            }
+            // row sums of the (bf16) probabilities: all-ones A operand
+            const uint4 ones = make_uint4(0x3F803F80u, 0x3F803F80u, 0x3F803F80u, 0x3F803F80u);
+#pragma unroll
+            for (int i = 0; i < kPfTpw; ++i) l_i[i] = mfma16x16x32(ones, pb[i], l_i[i]);
+#pragma unroll
+            for (int dt = 0; dt < 8; ++dt) {
+                const uint4 vf = *(const uint4 *)(sm + voff + dt * 16 * 32);
+#pragma unroll
+                for (int i = 0; i < kPfTpw; ++i) acc[i][dt] = mfma16x16x32(vf, pb[i], acc[i][dt]);
+            }
+        };
+
         const int pre = n_stages < kPfStages - 1 ? n_stages : kPfStages - 1;
-        for (int st = 0; st < pre; ++st) issue_stage(st);
+        for (int st = 0; st < pre; ++st) {
+            int ph0, ph1;
+            load_phys(st, ph0, ph1);
+            issue_dma(st, ph0, ph1);
+        }
+        // block-table entries of the next stage to issue, loaded a stage ahead
+        int nx0 = -1, nx1 = -1;
+        if (pre < n_stages) load_phys(pre, nx0, nx1);
         for (int st = 0; st < n_stages; ++st) {
             // this wave's share of stage st landed; the barrier covers the other
             // waves' shares and frees the slot consumed at st - 1
             const int after = min(kPfStages - 2, n_stages - 1 - st);
             vm_wait_blocks<NIW, kPfStages - 2>(after);
             __syncthreads();
-            if (st + kPfStages - 1 < n_stages) issue_stage(st + kPfStages - 1);
-            uint8_t *sm = &ring[st % kPfStages][0];
-            // key metadata of the two blocks of this stage (uniform)
-            BlockMeta m0, m1;
-            meta(it_proc, m0);
-            meta(it_proc, m1);
-            const bool part0 = m0.phys >= 0 && m0.lo < m0.hi && (m0.lo > 0 || m0.hi < kBlock);
-            const bool part1 = m1.phys >= 0 && m1.lo < m1.hi && (m1.lo > 0 || m1.hi < kBlock);
-            if (part0 || part1) {
-                // values of slots outside the union may be NaN: zero them in LDS
-                // (512 16-byte V^T chunks per stage: 256 per block, two per d)
-                for (int e = tid; e < 512; e += 64 * kPfWaves) {
-                    const int b = e >> 8;
-                    const int d = (e & 255) >> 1, half = e & 1;
-                    const int lo = b ? m1.lo : m0.lo, hi = b ? m1.hi : m0.hi;
-                    if (b ? part1 : part0) {
-                        uint4 *pv = (uint4 *)(sm + lds_v16(b, d, half));
-                        uint4 x = *pv;
-                        uint32_t w[4] = {x.x, x.y, x.z, x.w};
-#pragma unroll
-                        for (int q4 = 0; q4 < 4; ++q4) {
-                            const int ka = half * 8 + 2 * q4, kb = ka + 1;
-                            w[q4] &= ((ka >= lo && ka < hi) ? 0x0000FFFFu : 0u) |
-                                     ((kb >= lo && kb < hi) ? 0xFFFF0000u : 0u);
-                        }
-                        *pv = make_uint4(w[0], w[1], w[2], w[3]);
-                    }
-                }
-                __syncthreads();
+            const uint32_t hb = (have_bits >> (2 * (st % kPfStages))) & 3u;
+            const int nst = st + kPfStages - 1;
+            if (nst < n_stages) {
+                issue_dma(nst, nx0, nx1);
+                if (nst + 1 < n_stages) load_phys(nst + 1, nx0, nx1);
             }
-            // QK: K fragments are read once per stage and shared by the tiles
-            // (tiles past the last row compute on zero queries and are dropped)
-            f32x4_t s0[kPfTpw], s1[kPfTpw];
-#pragma unroll
-            for (int i = 0; i < kPfTpw; ++i) {
-                s0[i] = f32x4_t{0.f, 0.f, 0.f, 0.f};
-                s1[i] = f32x4_t{0.f, 0.f, 0.f, 0.f};
-            }
-#pragma unroll
-            for (int s = 0; s < 4; ++s) {
-                uint4 k0 = *(const uint4 *)(sm + lds_k(0, ln16, s * 4 + lg));
-                uint4 k1 = *(const uint4 *)(sm + lds_k(1, ln16, s * 4 + lg));
-#pragma unroll
-                for (int i = 0; i < kPfTpw; ++i) {
-                    s0[i] = mfma16x16x32(k0, qf[i][s], s0[i]);
-                    s1[i] = mfma16x16x32(k1, qf[i][s], s1[i]);
-                }
-            }
-            // online softmax per row (lane holds row ln16, keys 4*lg + r).  The
-            // visible slots of a block for query position tq are one range:
-            // [max(lo, tq - W + 1 - p0), min(hi, tq + 1 - p0)), sinks exempt
-            // from the window bound.
-            uint4 pb[kPfTpw];
-#pragma unroll
-            for (int i = 0; i < kPfTpw; ++i) {
-                const int tq = pos0 + trow_tok[i];
-                const int wl = g.window < 0 ? -(1 << 30) : tq - g.window + 1;
-                const int ol0 = m0.sink ? m0.lo : max(m0.lo, wl - m0.p0);
-                const int oh0 = min(m0.hi, tq + 1 - m0.p0);
-                const int ol1 = m1.sink ? m1.lo : max(m1.lo, wl - m1.p0);
-                const int oh1 = min(m1.hi, tq + 1 - m1.p0);
-                float sc[8];
-#pragma unroll
-                for (int r = 0; r < 4; ++r) {
-                    const int o = 4 * lg + r;
-                    sc[r] = (o >= ol0 && o < oh0) ? s0[i][r] : -INFINITY;
-                    sc[4 + r] = (o >= ol1 && o < oh1) ? s1[i][r] : -INFINITY;
-                }
-                float mx = fmaxf(fmaxf(fmaxf(sc[0], sc[1]), fmaxf(sc[2], sc[3])),
-                                 fmaxf(fmaxf(sc[4], sc[5]), fmaxf(sc[6], sc[7])));
-                mx = rows_pair<false, false>(mx);
-                mx = rows_pair<false, true>(mx);
-                const float m_new = fmaxf(m_i[i], mx);
-                const float mn = (m_new == -INFINITY) ? 0.f : m_new;
-                const float alpha = __builtin_amdgcn_exp2f(m_i[i] - mn);
-                m_i[i] = m_new;
-                float ps = 0.f;
-#pragma unroll
-                for (int r = 0; r < 8; ++r) {
-                    sc[r] = __builtin_amdgcn_exp2f(sc[r] - mn);
-                    ps += sc[r];
-                }
-                l_i[i] = l_i[i] * alpha + ps;
-                pb[i] = make_uint4(pack_bf16x2(sc[0], sc[1]), pack_bf16x2(sc[2], sc[3]),
-                                   pack_bf16x2(sc[4], sc[5]), pack_bf16x2(sc[6], sc[7]));
-                // rescale only when some row's running max moved (exact skip)
-                if (__builtin_amdgcn_ballot_w64(alpha != 1.f)) {
-#pragma unroll
-                    for (int dt = 0; dt < 8; ++dt) acc[i][dt] *= alpha;
-                }
-            }
-            // PV: V^T fragments read once per stage, shared by the tiles
-#pragma unroll
-            for (int dt = 0; dt < 8; ++dt) {
-                const int d = dt * 16 + ln16;
-                uint2 va = *(const uint2 *)(sm + lds_v8(0, d, lg));
-                uint2 vb = *(const uint2 *)(sm + lds_v8(1, d, lg));
-                uint4 vf = make_uint4(va.x, va.y, vb.x, vb.y);
-#pragma unroll
-                for (int i = 0; i < kPfTpw; ++i) acc[i][dt] = mfma16x16x32(vf, pb[i], acc[i][dt]);
-            }
+            const uint8_t *sm = &ring[st % kPfStages][0];
+            // every row of the pass sees every key of the stage: no masking
+            if (hb == 3u && whole_v(2 * st) && whole_v(2 * st + 1))
+                stage_body(std::true_type{}, sm, st, hb);
+            else
+                stage_body(std::false_type{}, sm, st, hb);
         }
         __syncthreads();  // every wave is done with the ring before the next pass refills it
 
@@ -1130,9 +1229,7 @@ __global__ __launch_bounds__(64 * kPfWaves, MTN_PF_WAVES_PER_EU) void k_prefill_
 #pragma unroll
         for (int i = 0; i < kPfTpw; ++i) {
             if (!live[i]) continue;
-            float lt = l_i[i];
-            lt = rows_pair<true, false>(lt);
-            lt = rows_pair<true, true>(lt);
+            const float lt = l_i[i][0];
             const int r = pass_row0 + (wv + kPfWaves * i) * 16 + ln16;
             if (r >= n_rows) continue;
             const int j = r / G, gh = r % G;
@@ -1149,7 +1246,7 @@ __global__ __launch_bounds__(64 * kPfWaves, MTN_PF_WAVES_PER_EU) void k_prefill_
             }
             if (a.lse && lg == 0)
                 a.lse[row * g.hq + hq0 + gh] =
-                    (m_i[i] + __builtin_amdgcn_logf(lt)) * 0.6931471805599453f;
+                    (m_ref[i] + __builtin_amdgcn_logf(lt)) * 0.6931471805599453f;
         }
     }
 }
