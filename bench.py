@@ -96,6 +96,13 @@ def traffic_summary(fetch_dir, write_dir):
     out = {
         "kernel": "k_attn_valu (decode attention), 128-session Qwen3-Omni-shaped workload",
         "kernel_src_sha256_16": kernel_src_hash(),
+        "commands": [
+            "rocprofv3 --pmc FETCH_SIZE --output-format csv -d " + fetch_dir +
+            " -o f -- python3 bench.py --steps 1 --warmup 0 --no-cpu-baseline",
+            "rocprofv3 --pmc WRITE_SIZE --output-format csv -d " + write_dir +
+            " -o w -- python3 bench.py --steps 1 --warmup 0 --no-cpu-baseline",
+            "python3 bench.py --traffic-summary " + fetch_dir + " " + write_dir,
+        ],
         "copy_kernel_KiB_per_dispatch": {"FETCH_SIZE": f_copy, "WRITE_SIZE": w_copy,
                                          "actual_read_KiB": kib, "actual_write_KiB": kib},
         "scale": {"fetch": fs, "write": ws},
@@ -110,9 +117,13 @@ def traffic_summary(fetch_dir, write_dir):
     print(json.dumps(out, indent=1))
 
 
-def measured_traffic():
+def measured_traffic(workload_name: str):
     """HBM bytes per decode launch from the committed counter summary, or None
-    when the kernel source changed since the counters were taken."""
+    when the kernel source changed since the counters were taken or the
+    counters cover another workload (they are taken on the 128-session
+    Qwen3-Omni-shaped frame step)."""
+    if workload_name != "qwen3-omni":
+        return None
     try:
         with open(TRAFFIC_SUMMARY) as f:
             t = json.load(f)
@@ -499,7 +510,7 @@ def main():
             "peak": HBM_PEAK_GBPS,
             "unit": "GB/s",
             "frac": round(res["dec_gbps"] / HBM_PEAK_GBPS, 4),
-            "traffic": measured_traffic(),
+            "traffic": measured_traffic(args.workload),
             "bytes_per_launch": res["dec_bytes"],
             "avg_launch_ms": round(res["avg_dec_ms"], 4),
             "launches": res["dec_launches"],
