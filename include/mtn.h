@@ -264,6 +264,57 @@ mtn_status mtn_pool_kernel_times(mtn_pool *pool, int64_t *launches, double *ms);
  * profiler's byte counters.                                                   */
 mtn_status mtn_hbm_copy(const void *src, void *dst, size_t bytes, void *stream);
 
+/* ---- deadline-aware admission (host only) ------------------------------ */
+
+/*
+ * An AIMD admission controller on the measured per-frame latency (§4.2: the
+ * schedulable concurrency depends on model, window, hardware and arrivals, so
+ * it is discovered from feedback instead of set by hand; arrivals beyond the
+ * cap get a clean rejection).  The caller offers each arriving session, opens
+ * a pool session only when it is admitted, releases it when the session ends,
+ * and reports every tick's latency (e.g. the time of one mtn_frame_step over
+ * all admitted sessions).  Per observed tick:
+ *   - during `hold` observations after a cut, nothing changes (the cut must
+ *     reach the signal first);
+ *   - latency >= target_ms: cap = max(min_cap, min(cap, floor(backoff *
+ *     admitted))) -- a multiplicative cut relative to the load that produced
+ *     the latency; admitted sessions are never evicted;
+ *   - otherwise, if since the previous observation an offer was rejected or
+ *     the admitted count reached the cap: cap = min(max_cap, cap + increase).
+ * An offer is admitted iff admitted < cap.  All arithmetic is IEEE double and
+ * int32; the controller is deterministic given the call sequence.
+ * A controller is used from one host thread.
+ */
+typedef struct mtn_admission mtn_admission; /* opaque; owned by the library */
+
+typedef struct {
+    double  target_ms;    /* latency target, > 0 (e.g. 0.3 x the frame budget)   */
+    double  backoff;      /* multiplicative factor, 0 < backoff < 1               */
+    int32_t increase;     /* additive step per observation, >= 1                  */
+    int32_t initial_cap;  /* min_cap <= initial_cap <= max_cap                    */
+    int32_t min_cap;      /* >= 1                                                 */
+    int32_t max_cap;
+    int32_t hold_ticks;   /* observations without a decision after a cut, >= 0   */
+} mtn_admission_config;
+
+typedef struct {
+    int32_t cap;          /* current admission cap                                */
+    int32_t admitted;     /* admitted and not yet released                        */
+    int32_t hold;         /* observations left before the next decision           */
+    int64_t offered, rejected, ticks, decreases, increases;
+} mtn_admission_state;
+
+/* MTN_ERR_INVALID_ARG for a config outside the ranges above. */
+mtn_status mtn_admission_create(const mtn_admission_config *cfg, mtn_admission **out);
+void       mtn_admission_destroy(mtn_admission *a);          /* NULL accepted   */
+/* One arriving session: *admitted = 1 (admitted, counted) or 0 (rejected).    */
+mtn_status mtn_admission_offer(mtn_admission *a, int32_t *admitted);
+/* An admitted session ended.  MTN_ERR_BAD_STATE when none is admitted.        */
+mtn_status mtn_admission_release(mtn_admission *a);
+/* One tick's latency in ms (finite, >= 0): the AIMD update above.             */
+mtn_status mtn_admission_observe(mtn_admission *a, double tick_ms);
+mtn_status mtn_admission_get(const mtn_admission *a, mtn_admission_state *out);
+
 const char *mtn_status_string(mtn_status s);
 const char *mtn_pool_last_error(const mtn_pool *pool);
 

@@ -18,6 +18,11 @@ Modules
     The pool/block/ring index arithmetic (block pinning of App. A "Sink half",
     free-behind-window of App. A "Window half", the pool-fill law of §3.1 Eq. 1)
     as an independent pure-Python model, compared bit-exactly with the library.
+``admission``
+    The deadline-aware admission loop of §4.2 (AIMD on the per-frame latency:
+    multiplicative cut near the target, additive probe with headroom, clean
+    rejection beyond the cap), compared call by call with the library's
+    host-only controller.
 
 Parity status of each function is stated in its module header.
 """

@@ -39,6 +39,8 @@ EXPORTS = [
     "mtn_frame_step", "mtn_pool_stats", "mtn_session_info", "mtn_session_block_table",
     "mtn_plan_info", "mtn_debug_poison_dead", "mtn_pool_set_timing",
     "mtn_pool_kernel_times", "mtn_hbm_copy", "mtn_status_string", "mtn_pool_last_error",
+    "mtn_admission_create", "mtn_admission_destroy", "mtn_admission_offer",
+    "mtn_admission_release", "mtn_admission_observe", "mtn_admission_get",
 ]
 
 
@@ -58,6 +60,22 @@ class PoolStats(C.Structure):
         ("capacity", C.c_int64), ("assigned", C.c_int64), ("reserved", C.c_int64),
         ("open_sessions", C.c_int32), ("blocks_per_session", C.c_int32),
         ("ring_tokens", C.c_int32), ("sink_blocks", C.c_int32),
+    ]
+
+
+class AdmissionConfig(C.Structure):
+    _fields_ = [
+        ("target_ms", C.c_double), ("backoff", C.c_double), ("increase", C.c_int32),
+        ("initial_cap", C.c_int32), ("min_cap", C.c_int32), ("max_cap", C.c_int32),
+        ("hold_ticks", C.c_int32),
+    ]
+
+
+class AdmissionState(C.Structure):
+    _fields_ = [
+        ("cap", C.c_int32), ("admitted", C.c_int32), ("hold", C.c_int32),
+        ("offered", C.c_int64), ("rejected", C.c_int64), ("ticks", C.c_int64),
+        ("decreases", C.c_int64), ("increases", C.c_int64),
     ]
 
 
@@ -109,6 +127,12 @@ def load() -> C.CDLL:
         "mtn_pool_set_timing": (i32, [vp, i32]),
         "mtn_pool_kernel_times": (i32, [vp, P64, C.POINTER(C.c_double)]),
         "mtn_hbm_copy": (i32, [vp, vp, C.c_size_t, vp]),
+        "mtn_admission_create": (i32, [C.POINTER(AdmissionConfig), C.POINTER(vp)]),
+        "mtn_admission_destroy": (None, [vp]),
+        "mtn_admission_offer": (i32, [vp, P32]),
+        "mtn_admission_release": (i32, [vp]),
+        "mtn_admission_observe": (i32, [vp, C.c_double]),
+        "mtn_admission_get": (i32, [vp, C.POINTER(AdmissionState)]),
         "mtn_status_string": (C.c_char_p, [i32]),
         "mtn_pool_last_error": (C.c_char_p, [vp]),
     }
@@ -306,3 +330,54 @@ def hbm_copy(src, dst, nbytes: int, stream=None) -> None:
     st = lib.mtn_hbm_copy(_ptr(src), _ptr(dst), C.c_size_t(nbytes), _stream(stream))
     if st != MTN_OK:
         raise MtnError(st, "hbm_copy")
+
+
+class Admission:
+    """AIMD admission controller on the per-frame latency (host only; see
+    mtn_admission_* in include/mtn.h)."""
+
+    def __init__(self, *, target_ms, backoff, increase, initial_cap, min_cap, max_cap,
+                 hold_ticks):
+        self._lib = load()
+        cfg = AdmissionConfig(float(target_ms), float(backoff), int(increase), int(initial_cap),
+                              int(min_cap), int(max_cap), int(hold_ticks))
+        h = C.c_void_p()
+        st = self._lib.mtn_admission_create(C.byref(cfg), C.byref(h))
+        if st != MTN_OK:
+            raise MtnError(st, "mtn_admission_create")
+        self._h = h
+
+    def close(self):
+        if getattr(self, "_h", None):
+            self._lib.mtn_admission_destroy(self._h)
+            self._h = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+    def offer(self) -> bool:
+        out = C.c_int32()
+        st = self._lib.mtn_admission_offer(self._h, C.byref(out))
+        if st != MTN_OK:
+            raise MtnError(st, "mtn_admission_offer")
+        return bool(out.value)
+
+    def release(self) -> None:
+        st = self._lib.mtn_admission_release(self._h)
+        if st != MTN_OK:
+            raise MtnError(st, "mtn_admission_release")
+
+    def observe(self, tick_ms: float) -> None:
+        st = self._lib.mtn_admission_observe(self._h, C.c_double(tick_ms))
+        if st != MTN_OK:
+            raise MtnError(st, "mtn_admission_observe")
+
+    def state(self) -> dict:
+        s = AdmissionState()
+        st = self._lib.mtn_admission_get(self._h, C.byref(s))
+        if st != MTN_OK:
+            raise MtnError(st, "mtn_admission_get")
+        return {k: getattr(s, k) for k, _ in AdmissionState._fields_}
