@@ -58,6 +58,16 @@ def parse():
     ap.add_argument("--frames", type=int, default=0, help="--call: frames (0 = the workload's)")
     ap.add_argument("--pool-blocks", type=int, default=0,
                     help="--call: pool capacity in blocks (0 = exact windowed reservation)")
+    ap.add_argument("--admission", choices=["windowed", "unbounded"], default=None,
+                    help="open-system admission ramp: sessions arrive at a fixed rate, an "
+                         "AIMD controller on the measured tick latency admits or rejects "
+                         "them, every tick runs one frame for all admitted sessions")
+    ap.add_argument("--offered", type=int, default=512, help="--admission: sessions offered")
+    ap.add_argument("--arrivals", type=int, default=12,
+                    help="--admission: arrivals per tick (8/s at a 1.5 s frame)")
+    ap.add_argument("--target-frac", type=float, default=0.3,
+                    help="--admission: latency target as a fraction of the frame budget")
+    ap.add_argument("--max-ticks", type=int, default=70, help="--admission: ticks to run")
     ap.add_argument("--traffic-summary", nargs=2, metavar=("FETCH_DIR", "WRITE_DIR"),
                     help="summarise two rocprofv3 --pmc runs (FETCH_SIZE, WRITE_SIZE) of this "
                          "bench into " + os.path.relpath(TRAFFIC_SUMMARY, ROOT) + " and exit")
@@ -423,6 +433,130 @@ def call_report(args, w, r):
             f.write(json.dumps(out) + "\n")
 
 
+def run_admission(args):
+    """Open-system admission ramp on the Qwen3-Omni shapes (the paper's run
+    offers 512 sessions at 8/s with a latency target of 0.3 of the budget).
+    Every tick: offer the tick's arrivals to the AIMD controller, open the
+    admitted ones (each arrives with S + W tokens of history, appended
+    untimed, so a windowed session costs its steady-state work from its
+    first tick), run one frame for every admitted session, and feed the
+    tick's latency (HIP events) back to the controller.  The windowed arm
+    sizes its pool to the controller's max cap; the unbounded arm gets the
+    pool-stress capacity (150 GB) and keeps growing every session."""
+    import numpy as np
+    import torch
+    import paper_2607_02640_amd as mtn
+    from workload import device_bank, QWEN3_OMNI as W
+
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    bf = torch.bfloat16
+    Lyr, Hq, Hkv, D = W.n_layers, W.n_q_heads, W.n_kv_heads, W.head_dim
+    C, tau = W.chunk[1], W.n_decode[1]
+    max_cap = 448
+    windowed = args.admission == "windowed"
+    hist = W.n_sink + W.window                       # history each arrival brings
+    if windowed:
+        R = -(-(W.window + C - 1) // 16) * 16
+        n_blocks = max_cap * (-(-W.n_sink // 16) + R // 16)
+        window, max_len = W.window, 0
+    else:
+        block_bytes = Lyr * Hkv * 2 * 16 * D * 2
+        n_blocks = int(150e9 // block_bytes)
+        window, max_len = None, hist + args.max_ticks * (C + tau) + 64
+    kw = dict(n_layers=Lyr, n_q_heads=Hq, n_kv_heads=Hkv, head_dim=D, n_sink=W.n_sink,
+              window=window, max_chunk=C, max_sessions=max_cap, n_blocks=n_blocks, dtype="bf16",
+              rope_theta=W.rope_theta, max_len=max_len)
+    nbytes = mtn.Pool.required(**kw)
+    log(f"[admission] {args.admission}: pool {nbytes / 1e9:.1f} GB ({n_blocks} blocks)")
+    kv = torch.empty(nbytes, dtype=torch.uint8, device=dev)
+    pool = mtn.Pool(**kw, kv=kv)
+    budget_ms = W.frame_period_s * 1e3
+    ctrl = mtn.Admission(target_ms=args.target_frac * budget_ms, backoff=0.8, increase=16,
+                         initial_cap=16, min_cap=1, max_cap=max_cap, hold_ticks=2)
+    s0 = 1000 * W.workload_id + 900
+    # flat banks sized for max_cap sessions; each tick views a prefix
+    qc = device_bank((Lyr * max_cap * C, Hq, D), bf, dev, s0 + 1)
+    kc = device_bank((Lyr * max_cap * C, Hkv, D), bf, dev, s0 + 2)
+    vc = device_bank((Lyr * max_cap * C, Hkv, D), bf, dev, s0 + 3)
+    oc = torch.empty_like(qc)
+    qd = device_bank((tau * Lyr * max_cap, Hq, D), bf, dev, s0 + 4)
+    kd = device_bank((tau * Lyr * max_cap, Hkv, D), bf, dev, s0 + 5)
+    vd = device_bank((tau * Lyr * max_cap, Hkv, D), bf, dev, s0 + 6)
+    od = torch.empty_like(qd)
+
+    def cview(t, n):
+        return t[:Lyr * n * C].view(Lyr, n * C, *t.shape[1:])
+
+    def dview(t, n):
+        return t[:tau * Lyr * n].view(tau, Lyr, n, *t.shape[1:])
+
+    sids, offered, rows = [], 0, []
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    wall_tick = None
+    for tick in range(1, args.max_ticks + 1):
+        new = []
+        for _ in range(args.arrivals):
+            if offered >= args.offered:
+                break
+            offered += 1
+            if ctrl.offer():
+                new.append(pool.session_open())
+        # arrivals bring their history (untimed); an unbounded pool can run
+        # out here too, which is the same wall
+        try:
+            for p in range(-(-hist // C)) if new else []:
+                pool.plan_begin(new, [C] * len(new))
+                for l in range(Lyr):
+                    pool.frame_append_kv(l, cview(kc, len(new))[l], cview(vc, len(new))[l])
+                pool.plan_commit()
+        except mtn.MtnError as e:
+            wall_tick = tick
+            log(f"[admission] tick {tick} (arrivals' history): {e}")
+            break
+        sids += new
+        n = len(sids)
+        torch.cuda.synchronize()
+        e0.record()
+        try:
+            pool.frame_step(sids, [C] * n, [tau] * n, cview(qc, n), cview(kc, n), cview(vc, n),
+                            cview(oc, n), dview(qd, n), dview(kd, n), dview(vd, n), dview(od, n))
+        except mtn.MtnError as e:
+            wall_tick = tick
+            log(f"[admission] tick {tick}: {e}")
+            break
+        e1.record()
+        torch.cuda.synchronize()
+        ms = e0.elapsed_time(e1)
+        ctrl.observe(ms)
+        st, ps = ctrl.state(), pool.stats()
+        rows.append(dict(tick=tick, offered=offered, admitted=st["admitted"], cap=st["cap"],
+                         rejected=st["rejected"], tick_ms=round(ms, 3),
+                         occupancy=round(ps["assigned"] / ps["capacity"], 4)))
+        if tick % 10 == 0:
+            log(f"[admission] tick {tick}: {rows[-1]}")
+    pool.close()
+    last = rows[-20:]
+    ticks = np.array([r["tick_ms"] for r in last]) if last else np.array([0.0])
+    out = {
+        "metric": "open-system admission ramp under AIMD on the per-frame latency",
+        "arm": args.admission, "workload": W.name, "offered": args.offered,
+        "arrivals_per_tick": args.arrivals, "frame_budget_ms": budget_ms,
+        "target_ms": args.target_frac * budget_ms,
+        "controller": dict(backoff=0.8, increase=16, initial_cap=16, max_cap=max_cap, hold_ticks=2),
+        "ticks_run": len(rows), "pool_exhausted_at_tick": wall_tick,
+        "final": rows[-1] if rows else None,
+        "last20_admitted_mean": float(np.mean([r["admitted"] for r in last])) if last else None,
+        "last20_tick_ms_p50": float(np.median(ticks)), "last20_tick_ms_p99": float(np.percentile(ticks, 99)),
+        "max_tick_ms": max(r["tick_ms"] for r in rows) if rows else None,
+        "series": rows,
+    }
+    print(json.dumps(out), flush=True)
+    if args.json_out:
+        with open(args.json_out, "w") as f:
+            f.write(json.dumps(out) + "\n")
+
+
 def cpu_baseline(w, n_layers_sample):
     """The float64 oracle (as it stands) on one session-frame at steady state,
     restricted to ``n_layers_sample`` layers and scaled to the full depth."""
@@ -473,6 +607,9 @@ def main():
               "shards by session with no exchange, so N GPUs run N independent copies",
               file=sys.stderr)
         sys.exit(2)
+    if args.admission:
+        run_admission(args)
+        return
     w = pick(args.workload)
     if args.call:
         call_report(args, w, run_call(args, w))
