@@ -252,10 +252,11 @@ def run_gpu(args, w):
     total_ms = evs[0].elapsed_time(evs[-1])
     log(f"[bench] {args.steps} frames in {total_ms:.1f} ms (wall {wall:.2f}s); kernels {kt}")
 
-    # algorithmic bytes (steady state: every query sees S + W keys)
+    # algorithmic bytes (steady state: every query sees S + W keys).  A decode
+    # launch also appends its token (read k, v; write the pool copy)
     vis = w.n_sink + w.window
     beta = 2 * Hkv * D * esz
-    dec_bytes = N * (vis * beta + Hq * D * 2 * esz)          # per decode launch
+    dec_bytes = N * (vis * beta + Hq * D * 2 * esz + 2 * beta)   # per decode launch
     dec_flops = N * 4 * Hq * D * vis
     chunk_union = vis + C - 1                                 # keys a chunk reads
     pre_bytes = N * (chunk_union * beta + C * Hq * D * 2 * esz)

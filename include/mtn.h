@@ -188,11 +188,25 @@ mtn_status mtn_attend_decode(mtn_pool *pool, int32_t layer, const void *q, void 
                              float *lse, int32_t n_split, void *stream);
 
 /*
+ * mtn_frame_append_kv followed by mtn_attend_decode for one layer of an open
+ * plan whose every sequence has n_tok == 1, in one launch: each planned token
+ * is the newest key of its own query, so the workgroup that attends to the
+ * end of that query's window takes the new key and value from k / v
+ * (rotated and rounded exactly as the stored copy) and writes the stored
+ * copy for later calls.  Same arguments and layouts as the two calls; the
+ * layer must not have been appended yet in this plan (MTN_ERR_BAD_STATE).
+ * mtn_frame_step uses this form for its decode rounds.
+ */
+mtn_status mtn_attend_decode_append(mtn_pool *pool, int32_t layer, const void *k, const void *v,
+                                    const void *q, void *out, float *lse, int32_t n_split,
+                                    void *stream);
+
+/*
  * One whole frame for a batch of sessions (§2 task model): plan the chunk,
  * then for each layer append + chunk-prefill attend, commit; then for each
  * decode round j (only sessions with n_decode[i] > j) plan one token, for each
- * layer append + decode attend, commit.  Chunks of one token everywhere use the
- * decode kernel.
+ * layer append + decode attend (one launch, as mtn_attend_decode_append),
+ * commit.  Chunks of one token everywhere use the decode kernel the same way.
  */
 typedef struct {
     int32_t        n_seq;

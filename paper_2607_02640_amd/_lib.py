@@ -36,6 +36,7 @@ EXPORTS = [
     "mtn_pool_required_bytes", "mtn_pool_create", "mtn_pool_destroy",
     "mtn_session_open", "mtn_session_close", "mtn_plan_begin", "mtn_plan_commit",
     "mtn_frame_append_kv", "mtn_attend_chunk_prefill", "mtn_attend_decode",
+    "mtn_attend_decode_append",
     "mtn_frame_step", "mtn_pool_stats", "mtn_session_info", "mtn_session_block_table",
     "mtn_plan_info", "mtn_debug_poison_dead", "mtn_pool_set_timing",
     "mtn_pool_kernel_times", "mtn_hbm_copy", "mtn_status_string", "mtn_pool_last_error",
@@ -118,6 +119,7 @@ def load() -> C.CDLL:
         "mtn_frame_append_kv": (i32, [vp, i32, vp, vp, vp]),
         "mtn_attend_chunk_prefill": (i32, [vp, i32, vp, vp, vp, vp]),
         "mtn_attend_decode": (i32, [vp, i32, vp, vp, vp, i32, vp]),
+        "mtn_attend_decode_append": (i32, [vp, i32, vp, vp, vp, vp, vp, i32, vp]),
         "mtn_frame_step": (i32, [vp, C.POINTER(FrameBatch), vp]),
         "mtn_pool_stats": (i32, [vp, C.POINTER(PoolStats)]),
         "mtn_session_info": (i32, [vp, i32, P64, P32]),
@@ -266,6 +268,12 @@ class Pool:
     def attend_decode(self, layer, q, out, lse=None, n_split=0, stream=None) -> None:
         self._check(self.lib.mtn_attend_decode(self.h, layer, _ptr(q), _ptr(out), _ptr(lse),
                                                n_split, _stream(stream)), "attend_decode")
+
+    def attend_decode_append(self, layer, k, v, q, out, lse=None, n_split=0,
+                             stream=None) -> None:
+        self._check(self.lib.mtn_attend_decode_append(self.h, layer, _ptr(k), _ptr(v), _ptr(q),
+                                                      _ptr(out), _ptr(lse), n_split,
+                                                      _stream(stream)), "attend_decode_append")
 
     def frame_step(self, sids, chunk_len, n_decode, q_chunk, k_chunk, v_chunk, out_chunk,
                    q_dec=None, k_dec=None, v_dec=None, out_dec=None, lse_chunk=None,

@@ -418,6 +418,8 @@ AttnArgs attn_args(mtn_pool *P, int32_t layer, const void *q, void *out, float *
     a.n_split = n_split;
     a.scale_log2 = P->scale * 1.4426950408889634f;
     a.zero_page = P->d_zero;
+    a.k_new = nullptr;
+    a.v_new = nullptr;
     return a;
 }
 
@@ -438,8 +440,11 @@ int32_t auto_split(const mtn_pool *P, int32_t n_items) {
     return (int32_t)std::max<int64_t>(1, std::min<int64_t>(sp, kMaxSplit));
 }
 
+// k_new / v_new non-null: the decode also appends the planned tokens of this
+// layer (each is the newest key of its own query), in the same launch.
 mtn_status decode_impl(mtn_pool *P, int32_t layer, const void *q, void *out, float *lse,
-                       int32_t n_split, void *stream) {
+                       int32_t n_split, void *stream, const void *k_new = nullptr,
+                       const void *v_new = nullptr) {
     hipStream_t s = (hipStream_t)stream;
     if (n_split == 0) n_split = auto_split(P, P->T);
     int64_t need = (int64_t)P->T * P->cfg.n_q_heads * n_split * (P->cfg.head_dim + 2);
@@ -451,12 +456,15 @@ mtn_status decode_impl(mtn_pool *P, int32_t layer, const void *q, void *out, flo
         n_split = std::min(n_split, kMaxSplit);
     }
     AttnArgs a = attn_args(P, layer, q, out, lse, n_split);
+    a.k_new = k_new;
+    a.v_new = v_new;
     hipEvent_t e0;
     mtn_status st = timing_begin(P, s, &e0);
     if (st) return st;
     HIP_TRY(P, launch_attn_valu(P->cfg.kv_dtype, a, s));
     st = timing_end(P, 2, e0, s);
     if (st) return st;
+    if (k_new) P->layer_done[layer] = 1;
     if (n_split > 1) {
         st = timing_begin(P, s, &e0);
         if (st) return st;
@@ -724,6 +732,18 @@ mtn_status mtn_attend_decode(mtn_pool *P, int32_t layer, const void *q, void *ou
     return decode_impl(P, layer, q, out, lse, n_split, stream);
 }
 
+mtn_status mtn_attend_decode_append(mtn_pool *P, int32_t layer, const void *k, const void *v,
+                                    const void *q, void *out, float *lse, int32_t n_split,
+                                    void *stream) {
+    mtn_status st = check_call(P, layer, stream);
+    if (st) return st;
+    if (!k || !v || !q || !out) return fail(P, MTN_ERR_INVALID_ARG, "null k, v, q or out");
+    if (!P->all_single) return fail(P, MTN_ERR_BAD_STATE, "decode needs n_tok == 1 everywhere");
+    if (n_split < 0 || n_split > kMaxSplit) return fail(P, MTN_ERR_INVALID_ARG, "bad n_split");
+    if (P->layer_done[layer]) return fail(P, MTN_ERR_BAD_STATE, "layer already appended");
+    return decode_impl(P, layer, q, out, lse, n_split, stream, k, v);
+}
+
 mtn_status mtn_frame_step(mtn_pool *P, const mtn_frame_batch *b, void *stream) {
     if (!P || !b) return MTN_ERR_INVALID_ARG;
     if (P->host_only) return fail(P, MTN_ERR_BAD_STATE, "host-only pool has no device path");
@@ -771,15 +791,16 @@ mtn_status mtn_frame_step(mtn_pool *P, const mtn_frame_batch *b, void *stream) {
     if (st) return st;
     for (int32_t l = 0; l < L; ++l) {
         size_t rq = (size_t)l * Tc * Hq * D, rk = (size_t)l * Tc * Hkv * D;
-        st = append_impl(P, l, off(b->k_chunk, rk), off(b->v_chunk, rk), stream);
-        if (st) return st;
         float *lse = b->lse_chunk ? b->lse_chunk + (size_t)l * Tc * Hq : nullptr;
-        if (P->all_single)
+        if (P->all_single) {  // one-token chunks: decode with the append fused in
             st = decode_impl(P, l, off(b->q_chunk, rq), (void *)off(b->out_chunk, rq), lse,
-                             b->n_split, stream);
-        else
+                             b->n_split, stream, off(b->k_chunk, rk), off(b->v_chunk, rk));
+        } else {
+            st = append_impl(P, l, off(b->k_chunk, rk), off(b->v_chunk, rk), stream);
+            if (st) return st;
             st = prefill_impl(P, l, off(b->q_chunk, rq), (void *)off(b->out_chunk, rq), lse,
                               stream);
+        }
         if (st) return st;
     }
     st = plan_commit(P);
@@ -798,12 +819,10 @@ mtn_status mtn_frame_step(mtn_pool *P, const mtn_frame_batch *b, void *stream) {
         if (st) return st;
         for (int32_t l = 0; l < L; ++l) {
             size_t base = ((size_t)j * L + l) * n;
-            st = append_impl(P, l, off(b->k_dec, base * Hkv * D), off(b->v_dec, base * Hkv * D),
-                             stream);
-            if (st) return st;
             float *lse = b->lse_dec ? b->lse_dec + base * Hq : nullptr;
             st = decode_impl(P, l, off(b->q_dec, base * Hq * D),
-                             (void *)off(b->out_dec, base * Hq * D), lse, b->n_split, stream);
+                             (void *)off(b->out_dec, base * Hq * D), lse, b->n_split, stream,
+                             off(b->k_dec, base * Hkv * D), off(b->v_dec, base * Hkv * D));
             if (st) return st;
         }
         st = plan_commit(P);

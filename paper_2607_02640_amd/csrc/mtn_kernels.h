@@ -45,6 +45,10 @@ struct AttnArgs {
     int32_t n_split;
     float scale_log2;        // softmax scale * log2(e)
     const uint8_t *zero_page;  // 16 KiB of zeros (DMA source of absent blocks)
+    // decode with a fused append (or null): [rows][Hkv][D] keys / values of
+    // the planned tokens, each the newest position of its own query
+    const void *k_new;
+    const void *v_new;
 };
 
 // dtype codes match the public MTN_F32 / MTN_BF16

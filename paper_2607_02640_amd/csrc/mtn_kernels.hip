@@ -392,6 +392,12 @@ __global__ __launch_bounds__(64 * WPU * NG) void k_attn_valu(AttnArgs a) {
     const int64_t row = __builtin_amdgcn_readfirstlane(a.p.tok_row[t]);
     const int key = lane >> 2, qtr = lane & 3;
     const int h0 = wq * HW;  // first head of this wave inside the KV group
+    // Decode with a fused append: the group holding the unit's last segment
+    // (it always ends at the query's own position, the newest key) takes that
+    // key from the inputs instead of the pool -- masking its slot out of the
+    // ring scan -- and writes the key and value into the pool at the end, for
+    // later launches.  No wave of this launch reads that slot as a key.
+    const bool own_new = a.k_new != nullptr && split == a.n_split - 1 && grp == NG - 1;
 
     // ---- work range and the first prefetches (issued before the q prologue)
     // segment seg = split * NG + grp of nseg = n_split * NG covers virtual
@@ -433,8 +439,22 @@ __global__ __launch_bounds__(64 * WPU * NG) void k_attn_valu(AttnArgs a) {
     const int pre = nblk < NBUF - 1 ? nblk : NBUF - 1;
     for (int i = 0; i < pre; ++i) issue(i);
 
-    // ---- q prologue: rotate at pos, fold the softmax scale (log2 domain)
+    // fused append: the newest key's score for the owned head, this lane's
+    // value dims of it (set in the q prologue by the owning group)
+    float s_new = 0.f;
+    float v_new[L::VD];
+#pragma unroll
+    for (int r = 0; r < L::VD; ++r) v_new[r] = 0.f;
+
+    // ---- q prologue: rotate at pos, fold the softmax scale (log2 domain).
+    // With a fused append, the owning group also rotates the newest key's
+    // quarter with the same RoPE values, exactly as the append kernel does
+    // (fp32, then rounded to the stored type), and accumulates its scores for
+    // this wave's heads as the q pairs come out.  The pool copy is written
+    // after the ring loop (nothing in this launch reads it, and no ring wait
+    // then covers the stores).
     QRegs<T, D, HW> q;
+    uint32_t knew[(D / 4) * sizeof(T) / 4];  // the rotated key quarter, stored layout
     {
         // each lane reads its quarter and the RoPE partner quarter of every
         // head as whole 16-byte vectors
@@ -445,45 +465,87 @@ __global__ __launch_bounds__(64 * WPU * NG) void k_attn_valu(AttnArgs a) {
         const float sgn = (qtr < 2) ? -1.f : 1.f;
         constexpr int EPV = 16 / L::E;        // elements per 16-byte vector
         constexpr int NVQ = L::QD / EPV;      // vectors per quarter
+        const T *kb = own_new ? (const T *)a.k_new + (row * g.hkv + kvh) * D : nullptr;
+        float sn[HW];
 #pragma unroll
-        for (int h = 0; h < HW; ++h) {
-            const uint4 *qa = (const uint4 *)(qb + (int64_t)h * D + d0);
-            const uint4 *qp = (const uint4 *)(qb + (int64_t)h * D + dp);
+        for (int h = 0; h < HW; ++h) sn[h] = 0.f;
+        // element pairs of a 16-byte vector: (lo, hi) floats of dword e/2
+        auto unpack = [](const uint4 &v, float *x) {
+            const uint32_t w[4] = {v.x, v.y, v.z, v.w};
 #pragma unroll
-            for (int vq = 0; vq < NVQ; ++vq) {
-                uint4 xa = qa[vq], xp = qp[vq];
-                const uint32_t wa[4] = {xa.x, xa.y, xa.z, xa.w};
-                const uint32_t wp[4] = {xp.x, xp.y, xp.z, xp.w};
+            for (int e = 0; e < EPV; ++e) {
+                if constexpr (sizeof(T) == 2)
+                    x[e] = __uint_as_float((e & 1) ? (w[e / 2] & 0xFFFF0000u) : (w[e / 2] << 16));
+                else
+                    x[e] = __uint_as_float(w[e]);
+            }
+        };
+#pragma unroll
+        for (int vq = 0; vq < NVQ; ++vq) {
+            float2 cs[EPV];
+#pragma unroll
+            for (int e = 0; e < EPV; ++e) cs[e] = rp[vq * EPV + e];
+            uint32_t kv4[4];  // the newest key's rotated vector (stored layout)
+            if (own_new) {
                 float xs[EPV], ys[EPV];
+                unpack(((const uint4 *)(kb + d0))[vq], xs);
+                unpack(((const uint4 *)(kb + dp))[vq], ys);
 #pragma unroll
-                for (int e = 0; e < EPV; ++e) {
+                for (int e = 0; e < EPV; e += 2) {
+                    const float k0 = fmaf(xs[e], cs[e].x, sgn * ys[e] * cs[e].y);
+                    const float k1 = fmaf(xs[e + 1], cs[e + 1].x, sgn * ys[e + 1] * cs[e + 1].y);
                     if constexpr (sizeof(T) == 2) {
-                        xs[e] = __uint_as_float((e & 1) ? (wa[e / 2] & 0xFFFF0000u) : (wa[e / 2] << 16));
-                        ys[e] = __uint_as_float((e & 1) ? (wp[e / 2] & 0xFFFF0000u) : (wp[e / 2] << 16));
+                        kv4[e / 2] = pack_bf16x2(k0, k1);
                     } else {
-                        xs[e] = __uint_as_float(wa[e]);
-                        ys[e] = __uint_as_float(wp[e]);
+                        kv4[e] = __float_as_uint(k0);
+                        kv4[e + 1] = __float_as_uint(k1);
                     }
                 }
+#pragma unroll
+                for (int c = 0; c < 4; ++c) knew[vq * 4 + c] = kv4[c];
+            }
+#pragma unroll
+            for (int h = 0; h < HW; ++h) {
+                float xs[EPV], ys[EPV];
+                unpack(((const uint4 *)(qb + (int64_t)h * D + d0))[vq], xs);
+                unpack(((const uint4 *)(qb + (int64_t)h * D + dp))[vq], ys);
 #pragma unroll
                 for (int e = 0; e < EPV; e += 2) {
                     const int i = vq * EPV + e;
-                    float2 c0 = rp[i], c1 = rp[i + 1];
-                    float r0 = fmaf(xs[e], c0.x, sgn * ys[e] * c0.y) * a.scale_log2;
-                    float r1 = fmaf(xs[e + 1], c1.x, sgn * ys[e + 1] * c1.y) * a.scale_log2;
+                    const float r0 = fmaf(xs[e], cs[e].x, sgn * ys[e] * cs[e].y) * a.scale_log2;
+                    const float r1 = fmaf(xs[e + 1], cs[e + 1].x, sgn * ys[e + 1] * cs[e + 1].y) * a.scale_log2;
                     if constexpr (sizeof(T) == 2) {
                         q.v[h][i / 2] = pack_bf16x2(r0, r1);
+                        if (own_new) sn[h] = dot2_bf16(q.v[h][i / 2], kv4[e / 2], sn[h]);
                     } else {
                         q.v[h][i] = r0;
                         q.v[h][i + 1] = r1;
+                        if (own_new) {
+                            sn[h] = fmaf(r0, __uint_as_float(kv4[e]), sn[h]);
+                            sn[h] = fmaf(r1, __uint_as_float(kv4[e + 1]), sn[h]);
+                        }
                     }
                 }
             }
+        }
+        if (own_new) {
+#pragma unroll
+            for (int h = 0; h < HW; ++h) sn[h] += dpp<kQuadXor1>(sn[h]);
+#pragma unroll
+            for (int h = 0; h < HW; ++h) sn[h] += dpp<kQuadXor2>(sn[h]);
+            const int hsel = qtr < HW ? qtr : qtr % HW;
+            s_new = sn[0];
+#pragma unroll
+            for (int c = 1; c < HW; ++c) s_new = (hsel == c) ? sn[c] : s_new;
+            const T *vb = (const T *)a.v_new + (row * g.hkv + kvh) * D;
+#pragma unroll
+            for (int r = 0; r < L::VD; ++r) v_new[r] = to_f32(vb[lane * L::VD + r]);
         }
     }
 
     // the head this lane owns in the softmax (lanes with qtr >= HW duplicate)
     const int hown = qtr < HW ? qtr : qtr % HW;
+
     float m = -INFINITY, lsum = 0.f;
     float acc[HW][L::VD];
 #pragma unroll
@@ -505,6 +567,7 @@ __global__ __launch_bounds__(64 * WPU * NG) void k_attn_valu(AttnArgs a) {
         it_proc.get(&lb, &lo, &hi);
         it_proc.next();
         if (scalar_ld(trow, __builtin_amdgcn_readfirstlane(lb)) < 0) hi = lo;  // unassigned: nothing visible
+        if (own_new && i == nblk - 1 && hi > lo) --hi;  // the newest key comes from registers
 
         // QK: this lane's quarter of key `key`, then the quad all-reduce
         uint32_t kw[L::NV4 * 4];
@@ -614,6 +677,43 @@ __global__ __launch_bounds__(64 * WPU * NG) void k_attn_valu(AttnArgs a) {
 #pragma unroll
                     for (int r = 0; r < L::VD; ++r) acc[h][r] = fmaf(pc, __uint_as_float(vv[r][c]), acc[h][r]);
                 }
+        }
+    }
+
+    if (own_new && wq == 0) {
+        // ---- the pool copy of the newest key and value, for later launches:
+        // lanes 0..3 write the four quarters of the key row, every lane its
+        // value dims (the V^T column)
+        const int64_t tb = __builtin_amdgcn_readfirstlane(a.p.tok_block[t]);
+        const int toff = __builtin_amdgcn_readfirstlane(a.p.tok_off[t]);
+        uint8_t *ktile = (uint8_t *)g.kv + (int64_t)a.layer * g.layer_stride + tb * g.block_stride +
+                         (int64_t)kvh * g.head_stride;
+        if (key == 0) {
+            uint4 *kd = (uint4 *)(ktile + ((int64_t)toff * D + qtr * L::QD) * L::E);
+#pragma unroll
+            for (int c = 0; c < (int)(sizeof(knew) / 16); ++c)
+                kd[c] = make_uint4(knew[4 * c], knew[4 * c + 1], knew[4 * c + 2], knew[4 * c + 3]);
+        }
+        T *VTp = (T *)(ktile + g.tile_bytes);
+#pragma unroll
+        for (int r = 0; r < L::VD; ++r)
+            VTp[(lane * L::VD + r) * kBlock + toff] = from_f32<T>(v_new[r]);
+    }
+    if (own_new) {
+        // ---- the newest key (score from the prologue): one more online-softmax step
+        const float m_new = fmaxf(m, s_new);  // s_new is finite
+        const float alpha = __builtin_amdgcn_exp2f(m - m_new);
+        const float pn = __builtin_amdgcn_exp2f(s_new - m_new);
+        lsum = lsum * alpha + (key == 0 ? pn : 0.f);
+        m = m_new;
+#pragma unroll
+        for (int h = 0; h < HW; ++h) {
+            // lane h holds head h's softmax state (key 0, quarter h)
+            const float al = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, alpha), h));
+            float ph = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, pn), h));
+            if constexpr (sizeof(T) == 2) ph = to_f32(from_f32<bf16_t>(ph));  // as the PV operand
+#pragma unroll
+            for (int r = 0; r < L::VD; ++r) acc[h][r] = fmaf(ph, v_new[r], acc[h][r] * al);
         }
     }
 

@@ -81,7 +81,7 @@ class Harness:
         assert err <= tol, f"{what}: max abs err {err:.3e} > {tol}"
         assert lerr <= max(tol, 1e-4), f"{what}: lse err {lerr:.3e}"
 
-    def frame(self, chunk_len, n_dec, n_split=0, check=True, use_frame_step=True):
+    def frame(self, chunk_len, n_dec, n_split=0, check=True, use_frame_step=True, fused=False):
         n = len(self.sids)
         draws_c = [self._draw(i, chunk_len[i]) for i in range(n)]
         tc = sum(chunk_len)
@@ -110,7 +110,8 @@ class Harness:
             self.pool.frame_step(self.sids, chunk_len, n_dec, qc, kc, vc, oc, qd, kd, vd, od,
                                  lse_chunk=lc, lse_dec=ld, n_split=n_split)
         else:
-            self._per_layer(chunk_len, n_dec, qc, kc, vc, oc, lc, qd, kd, vd, od, ld, n_split)
+            self._per_layer(chunk_len, n_dec, qc, kc, vc, oc, lc, qd, kd, vd, od, ld, n_split,
+                            fused)
         torch.cuda.synchronize()
         if not check:
             for i in range(n):
@@ -135,10 +136,16 @@ class Harness:
                 ref, rl = self._oracle_step(i, *dec_draws[j][i])
                 self._cmp(od_h[j, :, i:i + 1], ref, ld_h[j, :, i:i + 1], rl, f"decode{j} s{i}")
 
-    def _per_layer(self, chunk_len, n_dec, qc, kc, vc, oc, lc, qd, kd, vd, od, ld, n_split):
+    def _per_layer(self, chunk_len, n_dec, qc, kc, vc, oc, lc, qd, kd, vd, od, ld, n_split,
+                   fused=False):
+        """Per-layer calls; fused=True uses mtn_attend_decode_append for every
+        one-token plan instead of mtn_frame_append_kv + mtn_attend_decode."""
         p = self.pool
         p.plan_begin(self.sids, chunk_len)
         for l in range(self.L):
+            if max(chunk_len) == 1 and fused:
+                p.attend_decode_append(l, kc[l], vc[l], qc[l], oc[l], lc[l], n_split=n_split)
+                continue
             p.frame_append_kv(l, kc[l], vc[l])
             if max(chunk_len) == 1:
                 p.attend_decode(l, qc[l], oc[l], lc[l], n_split=n_split)
@@ -156,8 +163,11 @@ class Harness:
                 v = vd[j, l].index_select(0, ii).contiguous()
                 o = torch.empty_like(q)
                 lse = torch.empty((len(idx), self.hq), dtype=torch.float32, device="cuda")
-                p.frame_append_kv(l, k, v)
-                p.attend_decode(l, q, o, lse, n_split=n_split)
+                if fused:
+                    p.attend_decode_append(l, k, v, q, o, lse, n_split=n_split)
+                else:
+                    p.frame_append_kv(l, k, v)
+                    p.attend_decode(l, q, o, lse, n_split=n_split)
                 od[j, l].index_copy_(0, ii, o)
                 ld[j, l].index_copy_(0, ii, lse)
             p.plan_commit()

@@ -132,3 +132,46 @@ def test_session_churn_reuses_blocks():
     pool.poison_dead()
     for f in range(8):
         h.frame([8, 2, 5], [2, 2, 2])
+
+
+@pytest.mark.parametrize("dtype,d,hq,hkv,S,W,cmax", [
+    ("bf16", 128, 16, 2, 4, 70, 25),   # G = 8: two wave groups, the owner is the second
+    ("bf16", 128, 4, 4, 3, 48, 1),     # G = 1, C_max = 1: ring R = W, so the window wraps
+    ("f32", 64, 8, 2, 4, 37, 6),       # fp32 path, G = 4
+])
+def test_fused_decode_append_matches_oracle(dtype, d, hq, hkv, S, W, cmax):
+    """mtn_attend_decode_append (one launch: the newest key from the inputs,
+    the pool copy written for later calls) against the oracle, per-layer
+    calls over ragged frames, dead slots NaN-poisoned between frames."""
+    say(f"fused decode+append {dtype} d{d} {hq}/{hkv} S={S} W={W} cmax={cmax}")
+    n = 3
+    R = -(-(W + cmax - 1) // 16) * 16
+    pool, h = _tiny(dtype=dtype, d=d, hq=hq, hkv=hkv, S=S, W=W, cmax=cmax, n=n, L=2,
+                    blocks=n * (-(-S // 16) + R // 16))
+    rnd = random.Random(11)
+    for f in range(14):
+        h.frame([rnd.randint(1, cmax) for _ in range(n)], [rnd.randint(0, 5) for _ in range(n)],
+                use_frame_step=False, fused=True)
+        pool.poison_dead()
+    say(f"max err {h.max_err:.2e}")
+
+
+def test_fused_and_separate_calls_store_identical_pools():
+    """The fused call stores exactly what mtn_frame_append_kv stores: two
+    pools, NaN-poisoned end to end, fed the same frames through the two call
+    sequences, hold bit-identical bytes after every frame."""
+    say("fused vs separate pool bytes")
+    n, L = 3, 2
+    cfg = dict(dtype="bf16", d=128, hq=16, hkv=2, S=4, W=40, cmax=9, n=n, L=L, blocks=n * 4)
+    pa, ha = _tiny(**cfg)
+    pb, hb = _tiny(**cfg)
+    pa.poison_dead()
+    pb.poison_dead()
+    rnd = random.Random(5)
+    for f in range(10):
+        cl = [rnd.randint(1, 9) for _ in range(n)]
+        nd = [rnd.randint(0, 4) for _ in range(n)]
+        ha.frame(cl, nd, use_frame_step=False, fused=True)
+        hb.frame(cl, nd, use_frame_step=False, fused=False)
+        torch.cuda.synchronize()
+        assert torch.equal(pa.kv, pb.kv), f"pool bytes differ after frame {f}"
