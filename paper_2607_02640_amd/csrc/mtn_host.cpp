@@ -95,6 +95,7 @@ struct mtn_pool {
     std::vector<int64_t> seq_pos0;
     std::vector<int32_t> tok_sid, tok_pos, tok_row, tok_block, tok_off;
     std::vector<int32_t> upd_idx, upd_val;
+    std::vector<int32_t> pf_items;  // prefill (sequence, row pass) pairs
     std::vector<uint8_t> layer_done;
 
     // device
@@ -111,7 +112,7 @@ struct mtn_pool {
     bool stage_used[kStages] = {};
     int stage_i = 0;
     PlanView view{};
-    int32_t *d_seq_first = nullptr, *d_seq_ntok = nullptr;
+    int32_t *d_seq_first = nullptr, *d_seq_ntok = nullptr, *d_pf_items = nullptr;
     int32_t resident_units = 0;    // decode work units resident on the whole GPU
 
     // timing
@@ -312,6 +313,15 @@ mtn_status plan_begin(mtn_pool *P, int32_t n_seq, const int32_t *sids, const int
     }
     if (P->unbounded) P->reserved = P->assigned;
     P->all_single = (P->max_ntok == 1);
+    P->pf_items.clear();
+    {
+        const int64_t rpp = prefill_rows_per_pass();
+        for (int32_t i = 0; i < n_seq; ++i)
+            for (int64_t p = 0; p * rpp < (int64_t)n_tok[i] * P->G; ++p) {
+                P->pf_items.push_back(i);
+                P->pf_items.push_back((int32_t)p);
+            }
+    }
     P->layer_done.assign((size_t)P->cfg.n_layers, 0);
     P->plan_open = true;
     P->plan_stream = stream;
@@ -334,6 +344,7 @@ mtn_status plan_begin(mtn_pool *P, int32_t n_seq, const int32_t *sids, const int
     put(P->seq_ntok.data(), n_seq);
     put(P->upd_idx.data(), U);
     put(P->upd_val.data(), U);
+    put(P->pf_items.data(), (int32_t)P->pf_items.size());
     hipStream_t s = (hipStream_t)stream;
     int32_t *d = P->d_meta;
     HIP_TRY(P, hipMemcpyAsync(d, h, o * sizeof(int32_t), hipMemcpyHostToDevice, s));
@@ -350,6 +361,7 @@ mtn_status plan_begin(mtn_pool *P, int32_t n_seq, const int32_t *sids, const int
     P->view.rope = P->d_rope;
     P->view.n_tok = (int32_t)T;
     const int32_t *d_upd_idx = d + 5 * T + 2 * n_seq;
+    P->d_pf_items = d + 5 * T + 2 * n_seq + 2 * U;
     HIP_TRY(P, launch_plan_apply(d_upd_idx, d_upd_idx + U, U, P->d_table, P->view.tok_pos,
                                  (int32_t)T, P->d_inv_freq, P->cfg.head_dim / 2, P->d_rope, s));
     return MTN_OK;
@@ -484,7 +496,8 @@ mtn_status prefill_impl(mtn_pool *P, int32_t layer, const void *q, void *out, fl
     mtn_status st = timing_begin(P, s, &e0);
     if (st) return st;
     if (prefill_mfma_supported(P->cfg.kv_dtype, P->cfg.head_dim, P->G)) {
-        HIP_TRY(P, launch_prefill_mfma(a, P->d_seq_first, P->d_seq_ntok, P->n_seq, P->d_zero, s));
+        HIP_TRY(P, launch_prefill_mfma(a, P->d_seq_first, P->d_seq_ntok, P->d_pf_items,
+                                       (int32_t)(P->pf_items.size() / 2), P->d_zero, s));
     } else {
         HIP_TRY(P, launch_attn_valu(P->cfg.kv_dtype, a, s));
     }
@@ -581,7 +594,11 @@ mtn_status mtn_pool_create(const mtn_pool_config *cfg, void *kv_dev, size_t kv_b
         if ((e = hipMemcpyAsync(P->d_table, P->table.data(), tbl, hipMemcpyHostToDevice,
                                 (hipStream_t)stream)) != hipSuccess)
             return bail(e, "table upload");
-        size_t meta = sizeof(int32_t) * ((size_t)P->max_tok * 7 + 2 * (size_t)cfg->max_sessions + 64);
+        // per plan: 5 T token fields, 2 n_seq sequence fields, 2 U table updates
+        // (U <= T), and 2 per prefill pass (<= T G / 256 + n_seq passes, G <= 8)
+        size_t meta = sizeof(int32_t) * ((size_t)P->max_tok * 7 + 2 * (size_t)cfg->max_sessions +
+                                         2 * ((size_t)P->max_tok / 32 + (size_t)cfg->max_sessions) +
+                                         64);
         if ((e = hipMalloc(&P->d_meta, meta)) != hipSuccess) return bail(e, "meta");
         for (int i = 0; i < kStages; ++i) {
             if ((e = hipHostMalloc(&P->h_stage[i], meta, hipHostMallocDefault)) != hipSuccess)

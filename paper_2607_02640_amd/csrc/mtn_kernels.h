@@ -65,11 +65,15 @@ hipError_t launch_append(int dtype, const PoolGeom &g, const PlanView &p, int32_
 hipError_t launch_attn_valu(int dtype, const AttnArgs &a, hipStream_t s);
 hipError_t launch_merge(int dtype, const AttnArgs &a, hipStream_t s);
 
-// MFMA chunk-prefill attention (bf16, D = 128).  zero_page: 16 KiB of device
-// zeros, the DMA source of blocks a chunk does not see.
+// MFMA chunk-prefill attention (bf16, D = 128): one workgroup per (sequence,
+// row pass, kv head).  items: n_items (sequence, pass) pairs, pass p of a
+// sequence covering its query rows [p, p + 1) * prefill_rows_per_pass() (rows
+// are token * G + group head).  zero_page: 16 KiB of device zeros, the DMA
+// source of blocks a pass does not see.
+int prefill_rows_per_pass();
 hipError_t launch_prefill_mfma(const AttnArgs &a, const int32_t *seq_first_tok,
-                               const int32_t *seq_ntok, int32_t n_seq, const uint8_t *zero_page,
-                               hipStream_t s);
+                               const int32_t *seq_ntok, const int32_t *items, int32_t n_items,
+                               const uint8_t *zero_page, hipStream_t s);
 
 hipError_t launch_poison(int dtype, const PoolGeom &g, int32_t n_layers, int64_t n_blocks,
                          const uint16_t *live_mask, hipStream_t s);

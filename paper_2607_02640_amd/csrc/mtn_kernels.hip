@@ -911,6 +911,7 @@ struct PfArgs {
     AttnArgs a;
     const int32_t *seq_first;  // first planned token of each sequence
     const int32_t *seq_ntok;
+    const int32_t *items;      // (sequence, row pass) pairs: one workgroup row each
     const uint8_t *zero_page;  // 16 KiB of zeros: the DMA source of absent blocks
 };
 
@@ -987,8 +988,12 @@ __global__ __launch_bounds__(64 * kPfWaves) void k_prefill_mfma(PfArgs pa) {
     __shared__ __attribute__((aligned(16))) uint8_t ring[kPfStages][kPfStageBytes];
     const AttnArgs &a = pa.a;
     const PoolGeom &g = a.g;
-    const int seq = blockIdx.x / g.hkv;
+    // one workgroup per (sequence, row pass, kv head): a long chunk's passes
+    // run in parallel, each over the keys its own rows can see
+    const int item = blockIdx.x / g.hkv;
     const int kvh = blockIdx.x % g.hkv;
+    const int seq = __builtin_amdgcn_readfirstlane(pa.items[2 * item]);
+    const int pass = __builtin_amdgcn_readfirstlane(pa.items[2 * item + 1]);
     const int tid = threadIdx.x;
     const int lane = tid & 63;
     const int wv = __builtin_amdgcn_readfirstlane(tid >> 6);
@@ -997,24 +1002,28 @@ __global__ __launch_bounds__(64 * kPfWaves) void k_prefill_mfma(PfArgs pa) {
     const int ntok = __builtin_amdgcn_readfirstlane(pa.seq_ntok[seq]);
     const int sid = __builtin_amdgcn_readfirstlane(a.p.tok_sid[tok0]);
     const int pos0 = __builtin_amdgcn_readfirstlane(a.p.tok_pos[tok0]);
-    const int pos_last = pos0 + ntok - 1;
     const int n_rows = ntok * G;
+    const int pass_row0 = pass * kPfRowsPerPass;
+    // query positions spanned by this pass's rows
+    const int tq_min = pos0 + pass_row0 / G;
+    const int tq_max = pos0 + (min(n_rows, pass_row0 + kPfRowsPerPass) - 1) / G;
     const int32_t *trow = g.table + (int64_t)sid * g.row_len;
     const uint8_t *layer_base = g.kv + (int64_t)a.layer * g.layer_stride + (int64_t)kvh * g.head_stride;
     const uint32_t ring0 = lds_addr(&ring[0][0]);
 
-    // union of the visible sets of the chunk's queries: sinks, then the ring
-    // run [A, pos_last] with A = max(S, pos0 - W + 1)
-    const int sink_tokens = min(g.n_sink, pos_last + 1);
+    // union of the visible sets of the pass's queries: sinks, then the ring
+    // run [A, tq_max] with A = max(S, tq_min - W + 1) (empty while every
+    // query position is still below S)
+    const int sink_tokens = min(g.n_sink, tq_max + 1);
     const int n_sb = (sink_tokens + kBlock - 1) / kBlock;
-    const int A = g.window < 0 ? 0 : max(g.n_sink, pos0 - g.window + 1);
-    const int ring_n = pos_last - A + 1;  // >= 1: the chunk itself is in the run
+    const int A = g.window < 0 ? 0 : max(g.n_sink, tq_min - g.window + 1);
+    const int ring_n = max(0, tq_max - A + 1);
     const int first = g.window < 0 ? A : (A - g.n_sink) % g.ring;
     const int first_off = first % kBlock;
     const int rb_start = first / kBlock;
     const int ring_blocks = g.ring / kBlock;
-    const int n_rb = (first_off + ring_n + kBlock - 1) / kBlock;
-    const int last_hi = (first_off + ring_n - 1) % kBlock + 1;
+    const int n_rb = ring_n > 0 ? (first_off + ring_n + kBlock - 1) / kBlock : 0;
+    const int last_hi = ring_n > 0 ? (first_off + ring_n - 1) % kBlock + 1 : kBlock;
     const int ring_p0 = A - first_off;
     const int nvb = n_sb + n_rb;
     const int n_stages = (nvb + 1) / 2;
@@ -1097,10 +1106,7 @@ __global__ __launch_bounds__(64 * kPfWaves) void k_prefill_mfma(PfArgs pa) {
     const int voff = lds_v16(lblk, ln16, lg & 1);  // + dt * 16 * 32 for d tile dt
 
     const int hq0 = kvh * G;
-    for (int pass_row0 = 0; pass_row0 < n_rows; pass_row0 += kPfRowsPerPass) {
-        // query positions spanned by this pass (the unmasked test below)
-        const int tq_min = pos0 + pass_row0 / G;
-        const int tq_max = pos0 + (min(n_rows, pass_row0 + kPfRowsPerPass) - 1) / G;
+    {
         // virtual blocks every row of the pass sees whole: sink blocks
         // [0, fs_hi) and ring blocks [fr_lo, fr_hi) (as virtual indices)
         const int fs_hi = min(sink_tokens / kBlock, (tq_min + 1) / kBlock);
@@ -1323,7 +1329,6 @@ __global__ __launch_bounds__(64 * kPfWaves) void k_prefill_mfma(PfArgs pa) {
             else
                 stage_body(std::false_type{}, sm, st, hb);
         }
-        __syncthreads();  // every wave is done with the ring before the next pass refills it
 
         // ---- epilogue: normalise and write rows of this pass
 #pragma unroll
@@ -1462,12 +1467,16 @@ hipError_t launch_merge(int dtype, const AttnArgs &a, hipStream_t s) {
     return hipGetLastError();
 }
 
+int prefill_rows_per_pass() { return kPfRowsPerPass; }
+
 hipError_t launch_prefill_mfma(const AttnArgs &a, const int32_t *seq_first, const int32_t *seq_ntok,
-                               int32_t n_seq, const uint8_t *zero_page, hipStream_t s) {
+                               const int32_t *items, int32_t n_items, const uint8_t *zero_page,
+                               hipStream_t s) {
     const int G = a.g.hq / a.g.hkv;
-    if (!prefill_mfma_supported(1, a.g.d, G) || n_seq <= 0 || !zero_page) return hipErrorInvalidValue;
-    PfArgs pa{a, seq_first, seq_ntok, zero_page};
-    dim3 grid((unsigned)(n_seq * a.g.hkv)), block(64 * kPfWaves);
+    if (!prefill_mfma_supported(1, a.g.d, G) || n_items <= 0 || !zero_page || !items)
+        return hipErrorInvalidValue;
+    PfArgs pa{a, seq_first, seq_ntok, items, zero_page};
+    dim3 grid((unsigned)(n_items * a.g.hkv)), block(64 * kPfWaves);
     switch (G) {
         case 1: hipLaunchKernelGGL(k_prefill_mfma<1>, grid, block, 0, s, pa); break;
         case 2: hipLaunchKernelGGL(k_prefill_mfma<2>, grid, block, 0, s, pa); break;
