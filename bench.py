@@ -68,6 +68,10 @@ def parse():
     ap.add_argument("--target-frac", type=float, default=0.3,
                     help="--admission: latency target as a fraction of the frame budget")
     ap.add_argument("--max-ticks", type=int, default=70, help="--admission: ticks to run")
+    ap.add_argument("--recycle", action="store_true",
+                    help="application-level recycling arm: an unbounded engine whose sessions "
+                         "are dropped and re-prefilled with their sinks plus last W tokens "
+                         "whenever the context would pass S + 2W")
     ap.add_argument("--traffic-summary", nargs=2, metavar=("FETCH_DIR", "WRITE_DIR"),
                     help="summarise two rocprofv3 --pmc runs (FETCH_SIZE, WRITE_SIZE) of this "
                          "bench into " + os.path.relpath(TRAFFIC_SUMMARY, ROOT) + " and exit")
@@ -558,6 +562,115 @@ def run_admission(args):
             f.write(json.dumps(out) + "\n")
 
 
+def run_recycle(args):
+    """Application-level recycling (the paper's alternative to the in-engine
+    window, at the Qwen3-Omni shapes): the engine keeps every token (no
+    window), and the application bounds the context itself -- when a
+    session's context would pass S + 2W it closes the session, opens a fresh
+    one and re-prefills the sinks plus the last W tokens as one S + W chunk
+    (positions start again at 0), in that frame's batch.  Initial lengths are
+    staggered over [S + W, S + 2W) so the re-encodes spread over frames.
+    Inputs are synthetic draws like the other runs; the re-prefill costs
+    what re-encoding the retained context costs this attention path."""
+    import numpy as np
+    import torch
+    import paper_2607_02640_amd as mtn
+    from workload import device_bank, QWEN3_OMNI as W
+
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    bf = torch.bfloat16
+    N, Lyr, Hq, Hkv, D = W.n_sessions, W.n_layers, W.n_q_heads, W.n_kv_heads, W.head_dim
+    C, tau, S, Wn = W.chunk[1], W.n_decode[1], W.n_sink, W.window
+    keep, limit = S + Wn, S + 2 * Wn
+    frames = args.frames or W.frames
+    max_len = limit + C + tau + 64
+    n_blocks = N * -(-max_len // 16)
+    kw = dict(n_layers=Lyr, n_q_heads=Hq, n_kv_heads=Hkv, head_dim=D, n_sink=S, window=None,
+              max_chunk=keep, max_sessions=N, n_blocks=n_blocks, dtype="bf16",
+              rope_theta=W.rope_theta, max_len=max_len)
+    nbytes = mtn.Pool.required(**kw)
+    log(f"[recycle] pool {nbytes / 1e9:.1f} GB ({n_blocks} blocks), {frames} frames")
+    kv = torch.empty(nbytes, dtype=torch.uint8, device=dev)
+    pool = mtn.Pool(**kw, kv=kv)
+    sids = [pool.session_open() for _ in range(N)]
+    r_max = 4                                   # re-encodes per frame; later ones wait a frame
+    rows = Lyr * ((N - r_max) * C + r_max * keep)
+    s0 = 1000 * W.workload_id + 700
+    qc = device_bank((rows, Hq, D), bf, dev, s0 + 1)
+    kc = device_bank((rows, Hkv, D), bf, dev, s0 + 2)
+    vc = device_bank((rows, Hkv, D), bf, dev, s0 + 3)
+    oc = torch.empty_like(qc)
+    qd = device_bank((tau, Lyr, N, Hq, D), bf, dev, s0 + 4)
+    kd = device_bank((tau, Lyr, N, Hkv, D), bf, dev, s0 + 5)
+    vd = device_bank((tau, Lyr, N, Hkv, D), bf, dev, s0 + 6)
+    od = torch.empty_like(qd)
+
+    def cview(t, tc):
+        return t[:Lyr * tc].view(Lyr, tc, *t.shape[1:])
+
+    # staggered start: session i at keep + i * W / N tokens (append-only plans)
+    target = [keep + (i * Wn) // N for i in range(N)]
+    have = [0] * N
+    while True:
+        idx = [i for i in range(N) if have[i] < target[i]]
+        if not idx:
+            break
+        ntok = [min(C, target[i] - have[i]) for i in idx]
+        pool.plan_begin([sids[i] for i in idx], ntok)
+        for l in range(Lyr):
+            pool.frame_append_kv(l, cview(kc, sum(ntok))[l], cview(vc, sum(ntok))[l])
+        pool.plan_commit()
+        for i, n in zip(idx, ntok):
+            have[i] += n
+    length = list(have)
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    ticks, recycled = [], []
+    for f in range(frames):
+        due = [i for i in range(N) if length[i] + C + tau > limit][:r_max]
+        for i in due:                           # drop the cache; the chunk re-encodes
+            pool.session_close(sids[i])
+            sids[i] = pool.session_open()
+        cl = [keep if i in due else C for i in range(N)]
+        tc = sum(cl)
+        e0.record()
+        pool.frame_step(sids, cl, [tau] * N, cview(qc, tc), cview(kc, tc), cview(vc, tc),
+                        cview(oc, tc), qd, kd, vd, od)
+        e1.record()
+        torch.cuda.synchronize()
+        ticks.append(e0.elapsed_time(e1))
+        recycled.append(len(due))
+        for i in range(N):
+            length[i] = (keep if i in due else length[i] + C) + tau
+        if (f + 1) % 50 == 0:
+            log(f"[recycle] frame {f + 1}/{frames}")
+    pool.close()
+    t = np.array(ticks)
+    rec = np.array(recycled)
+    out = {
+        "metric": "per-frame tick latency, application-level recycling arm",
+        "workload": W.name + "-app-recycle", "sessions": N, "frames_run": len(t),
+        "frame_budget_ms": W.frame_period_s * 1e3, "keep_tokens": keep, "recycle_at": limit,
+        "tick_ms_p50": round(float(np.median(t)), 3),
+        "tick_ms_p90": round(float(np.percentile(t, 90)), 3),
+        "tick_ms_p99": round(float(np.percentile(t, 99)), 3),
+        "tick_ms_max": round(float(t.max()), 3),
+        "tick_ms_mean": round(float(t.mean()), 3),
+        "tick_ms_mean_with_reencode": round(float(t[rec > 0].mean()), 3) if (rec > 0).any() else None,
+        "tick_ms_mean_without": round(float(t[rec == 0].mean()), 3) if (rec == 0).any() else None,
+        "reencodes": int(rec.sum()),
+        "tick_ms_p50_per_10_frames": [round(float(np.median(t[i:i + 10])), 3)
+                                      for i in range(0, len(t), 10)],
+        "tick_ms": [round(float(x), 3) for x in t],
+        "reencodes_per_frame": [int(x) for x in rec],
+    }
+    print(json.dumps(out), flush=True)
+    if args.json_out:
+        with open(args.json_out, "w") as f:
+            f.write(json.dumps(out) + "\n")
+
+
 def cpu_baseline(w, n_layers_sample):
     """The float64 oracle (as it stands) on one session-frame at steady state,
     restricted to ``n_layers_sample`` layers and scaled to the full depth."""
@@ -610,6 +723,9 @@ def main():
         sys.exit(2)
     if args.admission:
         run_admission(args)
+        return
+    if args.recycle:
+        run_recycle(args)
         return
     w = pick(args.workload)
     if args.call:
