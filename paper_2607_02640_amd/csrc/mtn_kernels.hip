@@ -439,9 +439,8 @@ __global__ __launch_bounds__(64 * WPU * NG) void k_attn_valu(AttnArgs a) {
     const int pre = nblk < NBUF - 1 ? nblk : NBUF - 1;
     for (int i = 0; i < pre; ++i) issue(i);
 
-    // fused append: the newest key's score for the owned head, this lane's
-    // value dims of it (set in the q prologue by the owning group)
-    float s_new = 0.f;
+    // fused append: this lane's value dims of the newest key (set in the q
+    // prologue by the owning group)
     float v_new[L::VD];
 #pragma unroll
     for (int r = 0; r < L::VD; ++r) v_new[r] = 0.f;
@@ -466,9 +465,6 @@ __global__ __launch_bounds__(64 * WPU * NG) void k_attn_valu(AttnArgs a) {
         constexpr int EPV = 16 / L::E;        // elements per 16-byte vector
         constexpr int NVQ = L::QD / EPV;      // vectors per quarter
         const T *kb = own_new ? (const T *)a.k_new + (row * g.hkv + kvh) * D : nullptr;
-        float sn[HW];
-#pragma unroll
-        for (int h = 0; h < HW; ++h) sn[h] = 0.f;
         // element pairs of a 16-byte vector: (lo, hi) floats of dword e/2
         auto unpack = [](const uint4 &v, float *x) {
             const uint32_t w[4] = {v.x, v.y, v.z, v.w};
@@ -516,27 +512,14 @@ __global__ __launch_bounds__(64 * WPU * NG) void k_attn_valu(AttnArgs a) {
                     const float r1 = fmaf(xs[e + 1], cs[e + 1].x, sgn * ys[e + 1] * cs[e + 1].y) * a.scale_log2;
                     if constexpr (sizeof(T) == 2) {
                         q.v[h][i / 2] = pack_bf16x2(r0, r1);
-                        if (own_new) sn[h] = dot2_bf16(q.v[h][i / 2], kv4[e / 2], sn[h]);
                     } else {
                         q.v[h][i] = r0;
                         q.v[h][i + 1] = r1;
-                        if (own_new) {
-                            sn[h] = fmaf(r0, __uint_as_float(kv4[e]), sn[h]);
-                            sn[h] = fmaf(r1, __uint_as_float(kv4[e + 1]), sn[h]);
-                        }
                     }
                 }
             }
         }
         if (own_new) {
-#pragma unroll
-            for (int h = 0; h < HW; ++h) sn[h] += dpp<kQuadXor1>(sn[h]);
-#pragma unroll
-            for (int h = 0; h < HW; ++h) sn[h] += dpp<kQuadXor2>(sn[h]);
-            const int hsel = qtr < HW ? qtr : qtr % HW;
-            s_new = sn[0];
-#pragma unroll
-            for (int c = 1; c < HW; ++c) s_new = (hsel == c) ? sn[c] : s_new;
             const T *vb = (const T *)a.v_new + (row * g.hkv + kvh) * D;
 #pragma unroll
             for (int r = 0; r < L::VD; ++r) v_new[r] = to_f32(vb[lane * L::VD + r]);
@@ -680,27 +663,31 @@ __global__ __launch_bounds__(64 * WPU * NG) void k_attn_valu(AttnArgs a) {
         }
     }
 
-    if (own_new && wq == 0) {
-        // ---- the pool copy of the newest key and value, for later launches:
-        // lanes 0..3 write the four quarters of the key row, every lane its
-        // value dims (the V^T column)
-        const int64_t tb = __builtin_amdgcn_readfirstlane(a.p.tok_block[t]);
-        const int toff = __builtin_amdgcn_readfirstlane(a.p.tok_off[t]);
-        uint8_t *ktile = (uint8_t *)g.kv + (int64_t)a.layer * g.layer_stride + tb * g.block_stride +
-                         (int64_t)kvh * g.head_stride;
-        if (key == 0) {
-            uint4 *kd = (uint4 *)(ktile + ((int64_t)toff * D + qtr * L::QD) * L::E);
-#pragma unroll
-            for (int c = 0; c < (int)(sizeof(knew) / 16); ++c)
-                kd[c] = make_uint4(knew[4 * c], knew[4 * c + 1], knew[4 * c + 2], knew[4 * c + 3]);
-        }
-        T *VTp = (T *)(ktile + g.tile_bytes);
-#pragma unroll
-        for (int r = 0; r < L::VD; ++r)
-            VTp[(lane * L::VD + r) * kBlock + toff] = from_f32<T>(v_new[r]);
-    }
     if (own_new) {
-        // ---- the newest key (score from the prologue): one more online-softmax step
+        // ---- the newest key (rotated in the prologue): its score for the
+        // owned head, then one more online-softmax step
+        float sn[HW];
+#pragma unroll
+        for (int h = 0; h < HW; ++h) sn[h] = 0.f;
+        constexpr int KW = (int)(sizeof(knew) / 4);
+        if constexpr (sizeof(T) == 2) {
+#pragma unroll
+            for (int c = 0; c < KW; ++c)
+#pragma unroll
+                for (int h = 0; h < HW; ++h) sn[h] = dot2_bf16(q.v[h][c], knew[c], sn[h]);
+        } else {
+#pragma unroll
+            for (int c = 0; c < KW; ++c)
+#pragma unroll
+                for (int h = 0; h < HW; ++h) sn[h] = fmaf(q.v[h][c], __uint_as_float(knew[c]), sn[h]);
+        }
+#pragma unroll
+        for (int h = 0; h < HW; ++h) sn[h] += dpp<kQuadXor1>(sn[h]);
+#pragma unroll
+        for (int h = 0; h < HW; ++h) sn[h] += dpp<kQuadXor2>(sn[h]);
+        float s_new = sn[0];
+#pragma unroll
+        for (int c = 1; c < HW; ++c) s_new = (hown == c) ? sn[c] : s_new;
         const float m_new = fmaxf(m, s_new);  // s_new is finite
         const float alpha = __builtin_amdgcn_exp2f(m - m_new);
         const float pn = __builtin_amdgcn_exp2f(s_new - m_new);
@@ -716,6 +703,27 @@ __global__ __launch_bounds__(64 * WPU * NG) void k_attn_valu(AttnArgs a) {
             for (int r = 0; r < L::VD; ++r) acc[h][r] = fmaf(ph, v_new[r], acc[h][r] * al);
         }
     }
+
+    // the pool copy of the newest key and value, for later launches: lanes
+    // 0..3 write the four quarters of the key row, every lane its value dims
+    // (the V^T column).  Issued after the wave's last barrier -- a barrier's
+    // release fence would wait for these scattered stores.
+    auto store_new = [&]() {
+        const int64_t tb = __builtin_amdgcn_readfirstlane(a.p.tok_block[t]);
+        const int toff = __builtin_amdgcn_readfirstlane(a.p.tok_off[t]);
+        uint8_t *ktile = (uint8_t *)g.kv + (int64_t)a.layer * g.layer_stride + tb * g.block_stride +
+                         (int64_t)kvh * g.head_stride;
+        if (key == 0) {
+            uint4 *kd = (uint4 *)(ktile + ((int64_t)toff * D + qtr * L::QD) * L::E);
+#pragma unroll
+            for (int c = 0; c < (int)(sizeof(knew) / 16); ++c)
+                kd[c] = make_uint4(knew[4 * c], knew[4 * c + 1], knew[4 * c + 2], knew[4 * c + 3]);
+        }
+        T *VTp = (T *)(ktile + g.tile_bytes);
+#pragma unroll
+        for (int r = 0; r < L::VD; ++r)
+            VTp[(lane * L::VD + r) * kBlock + toff] = from_f32<T>(v_new[r]);
+    };
 
     // ---- finish: reduce the per-lane partial sums, publish (m, l) per head
     {
@@ -737,7 +745,10 @@ __global__ __launch_bounds__(64 * WPU * NG) void k_attn_valu(AttnArgs a) {
                     scr[((int64_t)grp * G + h0 + h) * D + lane * L::VD + r] = acc[h][r];
         }
         __syncthreads();
-        if (grp > 0) return;
+        if (grp > 0) {
+            if (own_new && wq == 0) store_new();
+            return;
+        }
 #pragma unroll
         for (int h = 0; h < HW; ++h) {
             float M = sM[wq][h];
@@ -791,6 +802,9 @@ __global__ __launch_bounds__(64 * WPU * NG) void k_attn_valu(AttnArgs a) {
             pml[base * 2] = sM[wv][lane];
             pml[base * 2 + 1] = sL[wv][lane];
         }
+    }
+    if constexpr (NG == 1) {
+        if (own_new && wq == 0) store_new();  // one group: it owns the newest key
     }
 }
 
