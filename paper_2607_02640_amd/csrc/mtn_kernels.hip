@@ -7,6 +7,7 @@
 // position t attends to keys k <= t with k < S or k in the W positions ending
 // at t; sinks are visited first, segments of a split decode are merged once.
 #include "mtn_kernels.h"
+#include "mtn_device.h"
 
 #include <hip/hip_runtime.h>
 #include <math.h>
@@ -17,181 +18,6 @@
 
 namespace mtn {
 namespace {
-
-typedef __attribute__((ext_vector_type(2))) __bf16 bf16x2_t;
-
-// ---------------------------------------------------------------------------
-// element helpers
-// ---------------------------------------------------------------------------
-struct bf16_t {
-    uint16_t bits;
-};
-
-__device__ __forceinline__ float to_f32(float x) { return x; }
-__device__ __forceinline__ float to_f32(bf16_t x) {
-    return __uint_as_float((uint32_t)x.bits << 16);
-}
-template <typename T>
-__device__ __forceinline__ T from_f32(float x);
-template <>
-__device__ __forceinline__ float from_f32<float>(float x) {
-    return x;
-}
-template <>
-__device__ __forceinline__ bf16_t from_f32<bf16_t>(float x) {
-    __bf16 b = (__bf16)x;  // round to nearest even (hardware cvt on gfx950)
-    return bf16_t{__builtin_bit_cast(uint16_t, b)};
-}
-__device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
-    bf16x2_t v = {(__bf16)lo, (__bf16)hi};
-    return __builtin_bit_cast(uint32_t, v);
-}
-__device__ __forceinline__ float dot2_bf16(uint32_t a, uint32_t b, float c) {
-    return __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2_t, a),
-                                           __builtin_bit_cast(bf16x2_t, b), c, false);
-}
-
-// DPP helpers (row = 16 lanes, quad = 4 lanes)
-template <int CTRL>
-__device__ __forceinline__ float dpp(float x) {
-    return __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(
-                                         0, __builtin_bit_cast(int, x), CTRL, 0xf, 0xf, false));
-}
-constexpr int kQuadXor1 = 0xB1;  // quad_perm [1,0,3,2]
-constexpr int kQuadXor2 = 0x4E;  // quad_perm [2,3,0,1]
-constexpr int kRowRor4 = 0x124;  // row_ror:4
-constexpr int kRowRor8 = 0x128;  // row_ror:8
-constexpr int kRowShr4 = 0x114;  // row_shr:4 (lane i takes lane i - 4 of its row)
-
-__device__ __forceinline__ float shfl_xor_f(float x, int m) {
-    return __shfl_xor(x, m, 64);
-}
-
-// Exchange between rows (16-lane groups) with the gfx950 permlane swaps: the
-// two results hold x of row pairs (0,1),(2,3) resp. of the two half-waves,
-// so combining them reduces across the pair.  Pure VALU, no LDS round trip.
-// The second operand is an opaque copy of x: given one value for both
-// operands the compiler folds the two results into one.
-__device__ __forceinline__ unsigned opaque_copy(unsigned x) {
-    unsigned y;
-    asm volatile("v_mov_b32 %0, %1" : "=v"(y) : "v"(x));
-    return y;
-}
-template <bool SUM, bool HALF>
-__device__ __forceinline__ float rows_pair(float x) {
-    const unsigned u = __builtin_bit_cast(unsigned, x);
-    unsigned a, b;
-    if constexpr (HALF) {
-        auto r = __builtin_amdgcn_permlane32_swap(u, opaque_copy(u), false, false);
-        a = r[0];
-        b = r[1];
-    } else {
-        auto r = __builtin_amdgcn_permlane16_swap(u, opaque_copy(u), false, false);
-        a = r[0];
-        b = r[1];
-    }
-    const float fa = __builtin_bit_cast(float, a), fb = __builtin_bit_cast(float, b);
-    return SUM ? fa + fb : fmaxf(fa, fb);
-}
-
-// max / sum over the 16 lanes that share (lane & 3) -- i.e. over the 16 keys
-// of a block for one quarter index
-__device__ __forceinline__ float keys_max(float x) {
-    x = fmaxf(x, dpp<kRowRor4>(x));
-    x = fmaxf(x, dpp<kRowRor8>(x));
-    x = rows_pair<false, false>(x);
-    return rows_pair<false, true>(x);
-}
-__device__ __forceinline__ float keys_sum(float x) {
-    x += dpp<kRowRor4>(x);
-    x += dpp<kRowRor8>(x);
-    x = rows_pair<true, false>(x);
-    return rows_pair<true, true>(x);
-}
-
-__device__ __forceinline__ void wave_sync() {
-    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
-    __builtin_amdgcn_wave_barrier();
-    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
-}
-
-// ---------------------------------------------------------------------------
-// visible-range geometry of one query (sinks first, then the ring run)
-// ---------------------------------------------------------------------------
-struct VisRange {
-    int sink_tokens;  // min(S, t+1)
-    int n_sb;         // sink blocks read
-    int first;        // ring slot of the first window position
-    int ring_n;       // window positions (0 = none)
-    int n_rb;         // ring blocks read (a block may appear twice on a wrap)
-};
-
-__device__ __forceinline__ VisRange vis_range(const PoolGeom &g, int t) {
-    VisRange r;
-    r.sink_tokens = min(g.n_sink, t + 1);
-    r.n_sb = (r.sink_tokens + kBlock - 1) / kBlock;
-    int a = g.window < 0 ? 0 : max(g.n_sink, t - g.window + 1);
-    if (a <= t) {
-        r.ring_n = t - a + 1;
-        r.first = g.window < 0 ? a : (a - g.n_sink) % g.ring;
-        r.n_rb = ((r.first % kBlock) + r.ring_n + kBlock - 1) / kBlock;
-    } else {
-        r.ring_n = 0;
-        r.first = 0;
-        r.n_rb = 0;
-    }
-    return r;
-}
-
-// logical block and valid slot range [lo, hi) of virtual block v
-__device__ __forceinline__ void vblock(const PoolGeom &g, const VisRange &r, int v, int *lb,
-                                       int *lo, int *hi) {
-    if (v < r.n_sb) {
-        *lb = v;
-        *lo = 0;
-        *hi = min(kBlock, r.sink_tokens - v * kBlock);
-        return;
-    }
-    int u = v - r.n_sb;
-    int ring_blocks = g.ring / kBlock;
-    *lb = g.n_sink_blocks + (r.first / kBlock + u) % ring_blocks;
-    *lo = (u == 0) ? r.first % kBlock : 0;
-    *hi = (u == r.n_rb - 1) ? ((r.first % kBlock) + r.ring_n - 1) % kBlock + 1 : kBlock;
-}
-
-// Walks the virtual blocks v0, v0 + 1, ... of one query without integer
-// division inside the loop (one modulo at construction).
-struct BlockIter {
-    int v, n_sb, sink_tokens, n_rb, first_off, last_hi, rb, ring_blocks, nsb, rb_start;
-    __device__ __forceinline__ BlockIter(const PoolGeom &g, const VisRange &r, int v0) {
-        v = v0;
-        n_sb = r.n_sb;
-        sink_tokens = r.sink_tokens;
-        n_rb = r.n_rb;
-        first_off = r.first % kBlock;
-        last_hi = r.ring_n > 0 ? (first_off + r.ring_n - 1) % kBlock + 1 : 0;
-        ring_blocks = g.ring / kBlock;
-        nsb = g.n_sink_blocks;
-        rb_start = r.first / kBlock;
-        rb = v0 > n_sb ? (rb_start + (v0 - n_sb)) % ring_blocks : rb_start;
-    }
-    __device__ __forceinline__ void get(int *lb, int *lo, int *hi) const {
-        if (v < n_sb) {
-            *lb = v;
-            *lo = 0;
-            *hi = min(kBlock, sink_tokens - v * kBlock);
-        } else {
-            const int u = v - n_sb;
-            *lb = nsb + rb;
-            *lo = (u == 0) ? first_off : 0;
-            *hi = (u == n_rb - 1) ? last_hi : kBlock;
-        }
-    }
-    __device__ __forceinline__ void next() {
-        if (v >= n_sb) rb = (rb + 1 == ring_blocks) ? 0 : rb + 1;
-        ++v;
-    }
-};
 
 // ---------------------------------------------------------------------------
 // plan apply: block-table updates + RoPE (cos, sin) table in fp64
@@ -295,56 +121,6 @@ struct DecodeShape {
     static constexpr int NBUF = 2;
 #endif
 };
-
-// Asynchronous 16-byte-per-lane copy global -> LDS (gfx950 LDS DMA).  Lane i
-// of the wave writes LDS bytes [lds + 16 i, lds + 16 i + 16).  Issued from
-// inline assembly so that the compiler does not guard later LDS reads with a
-// full vmcnt(0); completion is awaited explicitly with vm_wait<N>().
-// The K/V stream is read exactly once per launch: non-temporal ("nt") loads
-// keep it from displacing reused lines in the caches (measured +2 % on the
-// 128-session decode).
-#ifndef MTN_DMA_POLICY
-#define MTN_DMA_POLICY "nt"
-#endif
-__device__ __forceinline__ void dma16(const void *gptr, uint32_t lds) {
-    asm volatile(
-        "s_mov_b32 m0, %1\n\t"
-        "global_load_lds_dwordx4 %0, off " MTN_DMA_POLICY
-        :
-        : "v"(gptr), "s"(__builtin_amdgcn_readfirstlane(lds))
-        : "memory", "m0");
-}
-template <int N>
-__device__ __forceinline__ void vm_wait() {
-    asm volatile("s_waitcnt vmcnt(%0)" : : "n"(N) : "memory");
-}
-// wait until at most `after` blocks of NIW DMA instructions are outstanding
-template <int NIW, int MAXA>
-__device__ __forceinline__ void vm_wait_blocks(int after) {
-    if constexpr (MAXA >= 6) { if (after >= 6) { vm_wait<6 * NIW>(); return; } }
-    if constexpr (MAXA >= 5) { if (after == 5) { vm_wait<5 * NIW>(); return; } }
-    if constexpr (MAXA >= 4) { if (after == 4) { vm_wait<4 * NIW>(); return; } }
-    if constexpr (MAXA >= 3) { if (after == 3) { vm_wait<3 * NIW>(); return; } }
-    if constexpr (MAXA >= 2) { if (after == 2) { vm_wait<2 * NIW>(); return; } }
-    if constexpr (MAXA >= 1) { if (after == 1) { vm_wait<NIW>(); return; } }
-    vm_wait<0>();
-}
-__device__ __forceinline__ uint32_t lds_addr(const void *p) {
-    return (uint32_t)(uintptr_t)(const __attribute__((address_space(3))) void *)p;
-}
-// Read-only metadata (block table) fetched through the scalar unit: the
-// table is never written while a kernel runs, so the constant address space
-// is exact, and its loads are tracked apart from the vector-memory counter.
-__device__ __forceinline__ int32_t scalar_ld(const int32_t *p, int idx) {
-    return ((const __attribute__((address_space(4))) int32_t *)p)[idx];
-}
-
-// 16-byte chunk permutation of a block buffer: an involution that XORs the
-// low four chunk bits with the next four, so every 16-byte read instruction of
-// the ring (lane l takes chunk 4 l + c) spreads its lanes over all LDS banks.
-// Chosen by measurement: 255 B/clk/CU of ds_read_b128 against 203 for a
-// two-bit rotation and 117 unswizzled.
-__device__ __forceinline__ int swz(int x) { return x ^ ((x >> 4) & 15); }
 
 // One work unit = (query token, kv head, split segment), served by one
 // workgroup of NG wave groups of WPU waves each.  The unit's keys are cut
@@ -903,8 +679,6 @@ __global__ void k_copy(const u32x4_t *__restrict__ src, u32x4_t *__restrict__ ds
 // eight consecutive stage keys 8g .. 8g + 7, all in block g / 2, which are
 // exactly the k slots 8g .. 8g + 7 of its PV B operand; the matching V^T
 // A operand is one aligned 16-byte chunk per lane.
-typedef __attribute__((ext_vector_type(8))) __bf16 bf16x8_t;
-typedef __attribute__((ext_vector_type(4))) float f32x4_t;
 
 #ifndef MTN_PF_WAVES
 #define MTN_PF_WAVES 8
@@ -928,32 +702,6 @@ struct PfArgs {
     const int32_t *items;      // (sequence, row pass) pairs: one workgroup row each
     const uint8_t *zero_page;  // 16 KiB of zeros: the DMA source of absent blocks
 };
-
-__device__ __forceinline__ f32x4_t mfma16x16x32(const uint4 &a, const uint4 &b, f32x4_t c) {
-    return __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8_t, a),
-                                                    __builtin_bit_cast(bf16x8_t, b), c, 0, 0, 0);
-}
-// Plain v_max3_f32 / v_max_f32.  Scores are finite or -inf (masked), never
-// NaN, so the NaN-quieting the compiler adds around fmaxf is not needed.
-__device__ __forceinline__ float vmax3(float a, float b, float c) {
-    float r;
-    asm("v_max3_f32 %0, %1, %2, %3" : "=v"(r) : "v"(a), "v"(b), "v"(c));
-    return r;
-}
-__device__ __forceinline__ float vmax2(float a, float b) {
-    float r;
-    asm("v_max_f32 %0, %1, %2" : "=v"(r) : "v"(a), "v"(b));
-    return r;
-}
-// max over the four 16-lane rows (lanes with equal lane % 16)
-__device__ __forceinline__ float rows_max(float x) {
-    const unsigned u = __builtin_bit_cast(unsigned, x);
-    auto r = __builtin_amdgcn_permlane16_swap(u, opaque_copy(u), false, false);
-    x = vmax2(__builtin_bit_cast(float, (unsigned)r[0]), __builtin_bit_cast(float, (unsigned)r[1]));
-    const unsigned w = __builtin_bit_cast(unsigned, x);
-    auto q = __builtin_amdgcn_permlane32_swap(w, opaque_copy(w), false, false);
-    return vmax2(__builtin_bit_cast(float, (unsigned)q[0]), __builtin_bit_cast(float, (unsigned)q[1]));
-}
 
 // LDS layout of one stage: K tiles of blocks 0, 1 (the 16-byte chunks of a
 // key row permuted by kswz(b, key)), then V^T tiles (the two 16-byte halves of
