@@ -23,6 +23,11 @@ Modules
     multiplicative cut near the target, additive probe with headroom, clean
     rejection beyond the cap), compared call by call with the library's
     host-only controller.
+``fp8_kv``
+    The OCP E4M3 codec and the per-(token, head) power-of-two scale rule of
+    the FP8 KV cache (per-token KV reduction composes with the window, §4.1
+    and §6), written from the format's definition; ``OracleSession`` applies
+    it to every stored row when ``kv_quant="fp8_e4m3"``.
 
 Parity status of each function is stated in its module header.
 """

@@ -33,7 +33,10 @@ Readings where the paper is silent or ambiguous (each is listed in the design doc):
   the sink count is irrelevant.
 
 Nothing is rounded: inputs are widened to float64 exactly (bf16 and fp32 are
-both exactly representable) and every step runs in float64.
+both exactly representable) and every step runs in float64.  The one
+exception is opt-in: ``kv_quant="fp8_e4m3"`` stores every K/V row through the
+E4M3 codec of ``fp8_kv`` (per-token KV reduction, §4.1 / §6), and attention
+reads the exact dequantized values.
 """
 from __future__ import annotations
 
@@ -41,6 +44,8 @@ import math
 from typing import Dict, List, Optional, Sequence, Tuple
 
 import numpy as np
+
+from .fp8_kv import roundtrip_row
 
 UNBOUNDED = None  # window value that means "no window" (the vanilla policy)
 
@@ -161,7 +166,8 @@ class OracleSession:
     def __init__(self, n_q_heads: int, n_kv_heads: int, head_dim: int,
                  n_sink: int, window: Optional[int], theta: float = 10000.0,
                  scale: Optional[float] = None, n_layers: int = 1,
-                 literal_window: bool = False, check_psum: bool = True):
+                 literal_window: bool = False, check_psum: bool = True,
+                 kv_quant: Optional[str] = None):
         if n_q_heads % n_kv_heads:
             raise ValueError("n_q_heads must be a multiple of n_kv_heads")
         self.hq, self.hkv, self.d = n_q_heads, n_kv_heads, head_dim
@@ -173,6 +179,9 @@ class OracleSession:
         self.n_layers = n_layers
         self.literal = literal_window
         self.check_psum = check_psum
+        if kv_quant not in (None, "fp8_e4m3"):
+            raise ValueError("kv_quant must be None or 'fp8_e4m3'")
+        self.kv_quant = kv_quant
         self.length = 0
         self.state: List[Dict[int, Tuple[np.ndarray, np.ndarray]]] = [
             {} for _ in range(n_layers)]
@@ -208,7 +217,15 @@ class OracleSession:
         # Insert every chunk token first: each query then sees the earlier
         # tokens of its own chunk (causal inside the chunk).
         for i in range(c):
-            st[base + i] = (rope_rotate(k[i], base + i, self.theta), v[i].copy())
+            kr = rope_rotate(k[i], base + i, self.theta)
+            vi = v[i].copy()
+            if self.kv_quant == "fp8_e4m3":
+                # the cache holds what the quantized pool returns: each
+                # (token, head) row of the rotated key and of the value
+                # through the E4M3 codec with its own power-of-two scale
+                kr = np.stack([roundtrip_row(kr[h], True) for h in range(self.hkv)])
+                vi = np.stack([roundtrip_row(vi[h], True) for h in range(self.hkv)])
+            st[base + i] = (kr, vi)
         self._done.add(layer)
         if not attend:
             return None
