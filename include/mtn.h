@@ -30,8 +30,16 @@
  *     stream; a pool is driven from one host thread at a time.
  *   - Layouts are row-major with the last index fastest.
  *   - Element types: MTN_F32 is IEEE binary32, MTN_BF16 is bfloat16.  The KV
- *     cache and q/k/v/out share one element type (kv_dtype == io_dtype).
- *     Accumulation is fp32; bf16 results are rounded to nearest-even.
+ *     cache and q/k/v/out share one element type (kv_dtype == io_dtype),
+ *     except for the FP8 cache: kv_dtype MTN_FP8_E4M3 stores every (token,
+ *     kv head) row of the rotated key and of the value as OCP E4M3 codes
+ *     (bias 7, max 448, round to nearest even) with its own power-of-two
+ *     scale 2^e, e the smallest integer with max|row| <= 448 * 2^e (clamped
+ *     to [-126, 127], 0 for an all-zero row); its q/k/v/out are bf16
+ *     (io_dtype MTN_BF16) and it needs head_dim 128.  Per-token KV
+ *     reduction composes with the window bound (Metronome §4.1, closing
+ *     remark; §6).  Accumulation is fp32; bf16 results are rounded to
+ *     nearest-even.
  */
 #ifndef MTN_H
 #define MTN_H
@@ -58,7 +66,7 @@ typedef int32_t mtn_status;
                                          layer not appended, ...)              */
 #define MTN_ERR_UNSUPPORTED     (-9)  /* shape/dtype with no compiled kernel   */
 
-enum { MTN_F32 = 0, MTN_BF16 = 1 };
+enum { MTN_F32 = 0, MTN_BF16 = 1, MTN_FP8_E4M3 = 2 };
 
 /* window value selecting the unbounded (vanilla) policy: no window, no
  * eviction, sinks ignored, linear block table up to max_len tokens.          */
@@ -84,8 +92,8 @@ typedef struct {
     int32_t  max_sessions;  /* >= 1 concurrently open sessions                 */
     int32_t  max_len;       /* unbounded only: per-session token cap (>= 1)    */
     int64_t  n_blocks;      /* pool capacity in blocks (>= 1)                  */
-    int32_t  kv_dtype;      /* MTN_F32 | MTN_BF16                              */
-    int32_t  io_dtype;      /* must equal kv_dtype                             */
+    int32_t  kv_dtype;      /* MTN_F32 | MTN_BF16 | MTN_FP8_E4M3               */
+    int32_t  io_dtype;      /* kv_dtype, or MTN_BF16 for an MTN_FP8_E4M3 cache */
     double   rope_theta;    /* RoPE base (> 1)                                 */
     float    softmax_scale; /* 0 selects 1/sqrt(head_dim)                      */
     uint32_t flags;         /* MTN_POOL_* flags                                */
@@ -101,6 +109,15 @@ typedef struct {
  *
  * K rows hold RoPE-rotated keys; the V tile is stored transposed (dimension-
  * major) so that consecutive tokens of one dimension are adjacent.
+ *
+ * MTN_FP8_E4M3 (D = 128): each (l, b, h) region is 4224 bytes at
+ * ((l * n_blocks + b) * Hkv + h) * 4224 and holds
+ *   K codes  [16][128]                       bytes [0, 2048)
+ *   V codes  in key quads: byte ((key / 4) * 128 + d) * 4 + key % 4,
+ *                                            bytes [2048, 4096)
+ *   K exponents e + 127, one byte per key    bytes [4096, 4112)
+ *   V exponents e + 127                      bytes [4112, 4128)
+ * and 96 bytes of padding; a stored value is code * 2^e.
  */
 mtn_status mtn_pool_required_bytes(const mtn_pool_config *cfg, size_t *kv_bytes);
 

@@ -28,6 +28,10 @@ MTN_ERR_UNSUPPORTED = -9
 
 MTN_F32 = 0
 MTN_BF16 = 1
+MTN_FP8_E4M3 = 2
+# pool dtype name -> (kv_dtype, io_dtype); "fp8" keeps E4M3 codes with bf16 io
+DTYPES = {"f32": (MTN_F32, MTN_F32), "bf16": (MTN_BF16, MTN_BF16),
+          "fp8": (MTN_FP8_E4M3, MTN_BF16)}
 MTN_WINDOW_UNBOUNDED = -1
 MTN_POOL_HOST_ONLY = 1
 
@@ -185,11 +189,11 @@ class Pool:
                  rope_theta=10000.0, softmax_scale=0.0, block_size=16, host_only=False,
                  kv=None, stream=None):
         self.lib = load()
-        dt = MTN_BF16 if dtype == "bf16" else MTN_F32
+        kvt, iot = DTYPES[dtype]
         self.cfg = PoolConfig(
             n_layers, n_q_heads, n_kv_heads, head_dim, block_size, n_sink,
             MTN_WINDOW_UNBOUNDED if window is None else window, max_chunk, max_sessions,
-            max_len, n_blocks, dt, dt, rope_theta, softmax_scale,
+            max_len, n_blocks, kvt, iot, rope_theta, softmax_scale,
             MTN_POOL_HOST_ONLY if host_only else 0)
         self.dtype = dtype
         self.host_only = host_only
@@ -208,12 +212,12 @@ class Pool:
     @staticmethod
     def required(**kw) -> int:
         lib = load()
-        dt = MTN_BF16 if kw.get("dtype", "bf16") == "bf16" else MTN_F32
+        kvt, iot = DTYPES[kw.get("dtype", "bf16")]
         w = kw["window"]
         cfg = PoolConfig(kw["n_layers"], kw["n_q_heads"], kw["n_kv_heads"], kw["head_dim"],
                          kw.get("block_size", 16), kw["n_sink"],
                          MTN_WINDOW_UNBOUNDED if w is None else w, kw["max_chunk"],
-                         kw["max_sessions"], kw.get("max_len", 0), kw["n_blocks"], dt, dt,
+                         kw["max_sessions"], kw.get("max_len", 0), kw["n_blocks"], kvt, iot,
                          kw.get("rope_theta", 1e4), 0.0, 0)
         n = C.c_size_t()
         st = lib.mtn_pool_required_bytes(C.byref(cfg), C.byref(n))

@@ -12,6 +12,13 @@
 namespace mtn {
 namespace {
 
+// FP8 KV region of one (layer, block, kv head), D = 128: K codes [16][128],
+// V codes in key quads, then 16 K and 16 V scale-exponent bytes
+constexpr int kF8D = 128;                 // head dim of the fp8 path
+constexpr int kF8Tile = kBlock * kF8D;    // bytes of one K (or V) code tile
+constexpr int kF8Exp = 2 * kF8Tile;       // offset of the exponent bytes
+constexpr int kF8Read = 2 * kF8Tile + 32; // bytes a kernel reads per (block, head)
+
 typedef __attribute__((ext_vector_type(2))) __bf16 bf16x2_t;
 
 // ---------------------------------------------------------------------------

@@ -1,0 +1,588 @@
+// gfx950 kernels of the FP8 KV cache: E4M3 codes with one power-of-two scale
+// per (token, kv head) and tensor.  Fused RoPE + quantize + append, and the
+// decode attention (with or without the append fused in) as MFMA tiles over
+// blocks streamed through LDS.
+//
+// Method: Metronome (arXiv 2607.02640) §4.1 / App. A for what a query sees
+// (sinks ∪ the W positions ending at it, causal).  Per-token KV reduction
+// composes with that bound (§4.1, closing remark; §6): the window bounds how
+// many tokens stay resident, the 8-bit codes how many bytes each one holds.
+//
+// Layout of one (layer, block, kv head) region, D = 128, head stride 4224:
+//   [0, 2048)     K codes, [16 keys][128 dims]
+//   [2048, 4096)  V codes in key quads: byte ((key / 4) * 128 + d) * 4 + key % 4
+//   [4096, 4112)  K scale exponents (e + 127), one byte per key
+//   [4112, 4128)  V scale exponents
+// A stored value is code * 2^e; code * 2^e is exact in bf16, so the kernels
+// convert codes to bf16 unscaled and apply the scales to scores (K) and to
+// probabilities (V).
+#include "mtn_kernels.h"
+#include "mtn_device.h"
+
+#include <hip/hip_runtime.h>
+#include <math.h>
+#include <stdint.h>
+
+#include <algorithm>
+
+namespace mtn {
+namespace {
+
+typedef __attribute__((ext_vector_type(4))) short s16x4_t;
+
+// smallest e with amax <= 448 * 2^e, clamped to [-126, 127]; 0 for amax = 0
+__device__ __forceinline__ int f8_scale_exp(float amax) {
+    if (!(amax > 0.f)) return 0;
+    int e = __builtin_amdgcn_frexp_expf(amax) - 9;  // amax * 2^-e in [256, 512)
+    if (ldexpf(amax, -e) > 448.f) ++e;
+    return min(max(e, -126), 127);
+}
+// E4M3 codes of (a, b) into bytes 0, 1 (hi = false) or 2, 3 of `old`;
+// round to nearest even, |a|, |b| <= 448
+template <bool HI>
+__device__ __forceinline__ uint32_t f8_pack(float a, float b, uint32_t old) {
+    return (uint32_t)__builtin_amdgcn_cvt_pk_fp8_f32(a, b, (int)old, HI);
+}
+// two E4M3 codes (bytes 0, 1 or 2, 3 of w) -> two bf16, exact
+template <bool HI>
+__device__ __forceinline__ uint32_t f8_bf16x2(uint32_t w) {
+    return __builtin_bit_cast(uint32_t, __builtin_amdgcn_cvt_scalef32_pk_bf16_fp8(w, 1.0f, HI));
+}
+// 2^(byte r of w - 127) as a float (stored exponents are in [1, 254])
+__device__ __forceinline__ float f8_scale(uint32_t w, int r) {
+    return __uint_as_float(((w >> (8 * r)) & 0xFFu) << 23);
+}
+__device__ __forceinline__ f32x4_t mfma16x16x16(const uint2 &a, const uint2 &b, f32x4_t c) {
+    return __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(__builtin_bit_cast(s16x4_t, a),
+                                                      __builtin_bit_cast(s16x4_t, b), c, 0, 0, 0);
+}
+// sum over the four 16-lane rows (lanes with equal lane % 16)
+__device__ __forceinline__ float rows_sum(float x) {
+    return rows_pair<true, true>(rows_pair<true, false>(x));
+}
+// 16 bytes of bf16 as 8 floats
+__device__ __forceinline__ void unpack8(const uint4 &v, float *x) {
+    const uint32_t w[4] = {v.x, v.y, v.z, v.w};
+#pragma unroll
+    for (int e = 0; e < 8; ++e)
+        x[e] = __uint_as_float((e & 1) ? (w[e / 2] & 0xFFFF0000u) : (w[e / 2] << 16));
+}
+
+// ---------------------------------------------------------------------------
+// fused RoPE + quantize + append: one wave per (token, kv head); lane i holds
+// the rotation pair (i, i + 64)
+// ---------------------------------------------------------------------------
+__global__ __launch_bounds__(256) void k_append_fp8(PoolGeom g, PlanView p, int32_t layer,
+                                                    const bf16_t *__restrict__ k,
+                                                    const bf16_t *__restrict__ v) {
+    const int lane = threadIdx.x & 63;
+    const int64_t item = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
+    if (item >= (int64_t)p.n_tok * g.hkv) return;  // whole waves
+    const int h = (int)(item % g.hkv);
+    const int t = (int)(item / g.hkv);
+    const int64_t row = p.tok_row[t];
+    const bf16_t *kr = k + (row * g.hkv + h) * kF8D;
+    const bf16_t *vr = v + (row * g.hkv + h) * kF8D;
+    const float2 cs = p.rope[(int64_t)t * (kF8D / 2) + lane];
+    const float x0 = to_f32(kr[lane]), x1 = to_f32(kr[lane + 64]);
+    const float y0 = fmaf(x0, cs.x, -x1 * cs.y);
+    const float y1 = fmaf(x1, cs.x, x0 * cs.y);
+    const float v0 = to_f32(vr[lane]), v1 = to_f32(vr[lane + 64]);
+    float ak = fmaxf(fabsf(y0), fabsf(y1)), av = fmaxf(fabsf(v0), fabsf(v1));
+#pragma unroll
+    for (int m = 32; m >= 1; m >>= 1) {
+        ak = fmaxf(ak, __shfl_xor(ak, m, 64));
+        av = fmaxf(av, __shfl_xor(av, m, 64));
+    }
+    const int ek = f8_scale_exp(ak), ev = f8_scale_exp(av);
+    const uint32_t kc = f8_pack<false>(ldexpf(y0, -ek), ldexpf(y1, -ek), 0u);
+    const uint32_t vc = f8_pack<false>(ldexpf(v0, -ev), ldexpf(v1, -ev), 0u);
+    uint8_t *tile = (uint8_t *)g.kv + (int64_t)layer * g.layer_stride +
+                    (int64_t)p.tok_block[t] * g.block_stride + (int64_t)h * g.head_stride;
+    const int off = p.tok_off[t];
+    tile[off * kF8D + lane] = (uint8_t)kc;
+    tile[off * kF8D + lane + 64] = (uint8_t)(kc >> 8);
+    uint8_t *vq = tile + kF8Tile + (off >> 2) * (4 * kF8D) + (off & 3);
+    vq[lane * 4] = (uint8_t)vc;
+    vq[(lane + 64) * 4] = (uint8_t)(vc >> 8);
+    if (lane == 0) {
+        tile[kF8Exp + off] = (uint8_t)(ek + 127);
+        tile[kF8Exp + kBlock + off] = (uint8_t)(ev + 127);
+    }
+}
+
+// ---------------------------------------------------------------------------
+// decode attention over fp8 blocks
+// ---------------------------------------------------------------------------
+// One work unit = (query token, kv head, split segment), one workgroup of NG
+// waves; the unit's keys are cut into NG consecutive segments and each wave
+// streams its own segment through its own LDS ring of NBUF blocks (no
+// barrier inside the loop).  Per block, one wave computes all G heads:
+//   S[key][head]  = K[key][:] . Q^T   four 16x16x32 MFMAs (A = K codes as bf16)
+//   O^T[d][head] += V^T[d][key] . P'  eight 16x16x16 MFMAs (A = V codes as bf16)
+// Lane l (n = l % 16, g4 = l / 16) holds head n (heads >= G are zero
+// queries): its QK B operand covers dims 32 g4 .. 32 g4 + 31, its scores are
+// keys 4 g4 .. 4 g4 + 3, which is exactly its PV B operand, and its output
+// accumulators are dims 32 g4 + 8 i + j (i < 4, j < 8) -- the PV MFMA j
+// takes dims 8 m + j on its rows m.  The online softmax keeps a per-head
+// reference max that moves only when a block's max exceeds it by more than
+// 2^8, so the accumulator rescale is rare.  At the end the waves' (max, sum,
+// acc) are merged through LDS by log-sum-exp.
+template <int G>
+struct F8Shape {
+#ifdef MTN_FP8_GROUPS
+    static constexpr int NG = MTN_FP8_GROUPS;
+#else
+    static constexpr int NG = 4;
+#endif
+#ifdef MTN_FP8_NBUF
+    static constexpr int NBUF = MTN_FP8_NBUF;
+#else
+    static constexpr int NBUF = 3;  // three workgroups per CU: LDS and registers agree
+#endif
+};
+
+template <int G, int NG, int NBUF>
+__global__ __launch_bounds__(64 * NG) void k_attn_fp8(AttnArgs a) {
+    constexpr int D = kF8D;
+    constexpr int BLK = kF8Read;   // one block's ring slot
+    constexpr int NIW = 5;         // DMA instructions per block: 4 x 1 KiB + the 32 exponent bytes
+    static_assert(G >= 1 && G <= 16, "heads per kv group");
+    static_assert(NBUF >= 2 && NBUF <= 8, "ring depth");
+    static_assert(NBUF * BLK >= 16 * D * 4, "merge scratch fits one wave's ring");
+    __shared__ __attribute__((aligned(16))) uint8_t ring[NG][NBUF][BLK];
+    __shared__ float sM[NG][16], sL[NG][16];
+    __shared__ __attribute__((aligned(16))) uint8_t snew[2][D];  // newest key / value codes
+
+    const int lane = threadIdx.x & 63;
+    const int n = lane & 15, g4 = lane >> 4;
+    const int wv = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+    const int64_t unit = blockIdx.x;
+    const PoolGeom &g = a.g;
+    const int split = __builtin_amdgcn_readfirstlane((int)(unit % a.n_split));
+    const int kvh = __builtin_amdgcn_readfirstlane((int)((unit / a.n_split) % g.hkv));
+    const int t = __builtin_amdgcn_readfirstlane((int)(unit / ((int64_t)a.n_split * g.hkv)));
+    const int sid = __builtin_amdgcn_readfirstlane(a.p.tok_sid[t]);
+    const int pos = __builtin_amdgcn_readfirstlane(a.p.tok_pos[t]);
+    const int64_t row = __builtin_amdgcn_readfirstlane(a.p.tok_row[t]);
+    // the wave holding the unit's last segment (which ends at the query's own
+    // position) takes the newest key from the inputs when the append is fused
+    const bool own_new = a.k_new != nullptr && split == a.n_split - 1 && wv == NG - 1;
+
+    const VisRange vr = vis_range(g, pos);
+    const int nv = vr.n_sb + vr.n_rb;
+    const int64_t nseg = (int64_t)a.n_split * NG;
+    const int64_t seg = (int64_t)split * NG + wv;
+    const int v0 = __builtin_amdgcn_readfirstlane((int)(seg * nv / nseg));
+    const int v1 = __builtin_amdgcn_readfirstlane((int)((seg + 1) * nv / nseg));
+    const int nblk = v1 - v0;
+    const uint8_t *head_base = g.kv + (int64_t)a.layer * g.layer_stride + (int64_t)kvh * g.head_stride;
+    const int32_t *trow = g.table + (int64_t)sid * g.row_len;
+    const uint32_t ring0 = lds_addr(&ring[wv][0][0]);
+
+    BlockIter it_issue(g, vr, v0), it_proc(g, vr, v0);
+    auto issue = [&](int i) {
+        int lb, lo, hi;
+        it_issue.get(&lb, &lo, &hi);
+        it_issue.next();
+        int phys = scalar_ld(trow, __builtin_amdgcn_readfirstlane(lb));
+        phys = phys < 0 ? 0 : phys;  // unassigned: any valid block, every slot masked
+        const uint8_t *src = head_base + (int64_t)phys * g.block_stride;
+        const uint32_t dst = ring0 + (uint32_t)((i % NBUF) * BLK);
+#pragma unroll
+        for (int j = 0; j < 4; ++j) dma16(src + swz(j * 64 + lane) * 16, dst + j * 1024);
+        if (lane < 2) dma16(src + kF8Exp + lane * 16, dst + kF8Exp);
+    };
+    const int pre = nblk < NBUF - 1 ? nblk : NBUF - 1;
+    for (int i = 0; i < pre; ++i) issue(i);
+
+    // ---- q prologue: rotate at pos, fold the softmax scale (log2 domain);
+    // the B operand of QK MFMA s holds dims 32 g4 + 8 s .. + 7 of head n.
+    const int d0 = 32 * g4;
+    const int dp = d0 ^ 64;  // RoPE partner dims
+    uint4 qb[4];
+    const float2 *rp = a.p.rope + (int64_t)t * (D / 2) + (d0 & 63);
+    const float sgn = g4 < 2 ? -1.f : 1.f;
+    {
+        const bool hv = n < G;
+        const bf16_t *qh = (const bf16_t *)a.q + (row * g.hq + (int64_t)kvh * G + (hv ? n : 0)) * D;
+#pragma unroll
+        for (int s = 0; s < 4; ++s) {
+            float x[8], y[8];
+            unpack8(((const uint4 *)(qh + d0))[s], x);
+            unpack8(((const uint4 *)(qh + dp))[s], y);
+            uint32_t w[4];
+#pragma unroll
+            for (int e = 0; e < 8; e += 2) {
+                const float2 c0 = rp[8 * s + e], c1 = rp[8 * s + e + 1];
+                const float r0 = fmaf(x[e], c0.x, sgn * y[e] * c0.y) * a.scale_log2;
+                const float r1 = fmaf(x[e + 1], c1.x, sgn * y[e + 1] * c1.y) * a.scale_log2;
+                w[e / 2] = hv ? pack_bf16x2(r0, r1) : 0u;
+            }
+            qb[s] = make_uint4(w[0], w[1], w[2], w[3]);
+        }
+    }
+    // The owner rotates and quantizes the newest key and value two dims per
+    // lane (dims d0 + 2 n, d0 + 2 n + 1), publishes the codes in LDS for the
+    // score and value step after the ring loop, and keeps its own two codes
+    // for the pool copy.
+    uint32_t kc2 = 0, vc2 = 0;
+    int ek_new = 0, ev_new = 0;
+    const int dd = d0 + 2 * n;
+    if (own_new) {
+        const bf16_t *kh = (const bf16_t *)a.k_new + (row * g.hkv + kvh) * D;
+        const bf16_t *vh = (const bf16_t *)a.v_new + (row * g.hkv + kvh) * D;
+        const uint32_t kx = *(const uint32_t *)(kh + dd), ky = *(const uint32_t *)(kh + (dd ^ 64));
+        const uint32_t vx = *(const uint32_t *)(vh + dd);
+        const float4 cs = *(const float4 *)(rp + 2 * n);  // (cos, sin) of dims dd, dd + 1
+        // rotated exactly as the append kernel does
+        const float k0 = fmaf(__uint_as_float(kx << 16), cs.x, sgn * __uint_as_float(ky << 16) * cs.y);
+        const float k1 = fmaf(__uint_as_float(kx & 0xFFFF0000u), cs.z,
+                              sgn * __uint_as_float(ky & 0xFFFF0000u) * cs.w);
+        const float v0 = __uint_as_float(vx << 16), v1 = __uint_as_float(vx & 0xFFFF0000u);
+        float ak = fmaxf(fabsf(k0), fabsf(k1)), av = fmaxf(fabsf(v0), fabsf(v1));
+#pragma unroll
+        for (int m = 1; m < 16; m <<= 1) {  // the 16 lanes of a row, then the rows
+            ak = fmaxf(ak, __shfl_xor(ak, m, 64));
+            av = fmaxf(av, __shfl_xor(av, m, 64));
+        }
+        ek_new = __builtin_amdgcn_readfirstlane(f8_scale_exp(rows_max(ak)));
+        ev_new = __builtin_amdgcn_readfirstlane(f8_scale_exp(rows_max(av)));
+        kc2 = f8_pack<false>(ldexpf(k0, -ek_new), ldexpf(k1, -ek_new), 0u);
+        vc2 = f8_pack<false>(ldexpf(v0, -ev_new), ldexpf(v1, -ev_new), 0u);
+        *(uint16_t *)&snew[0][dd] = (uint16_t)kc2;
+        *(uint16_t *)&snew[1][dd] = (uint16_t)vc2;
+    }
+
+    float m_ref = -INFINITY, lsum = 0.f;
+    f32x4_t acc[8];
+#pragma unroll
+    for (int j = 0; j < 8; ++j) acc[j] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+    // per-lane LDS offsets of the K and V fragments inside a ring slot
+    const int ko0 = swz(8 * n + 2 * g4) * 16, ko1 = swz(8 * n + 2 * g4 + 1) * 16;
+    const int vo0 = swz(128 + 32 * g4 + 2 * n) * 16, vo1 = swz(128 + 32 * g4 + 2 * n + 1) * 16;
+
+    for (int i = 0; i < nblk; ++i) {
+        // block i has landed once at most the blocks issued after it are in flight
+        vm_wait_blocks<NIW, NBUF - 2>(min(NBUF - 2, nblk - 1 - i));
+        if (i + NBUF - 1 < nblk) issue(i + NBUF - 1);
+        const uint8_t *blk = &ring[wv][i % NBUF][0];
+        int lb, lo, hi;
+        it_proc.get(&lb, &lo, &hi);
+        it_proc.next();
+        if (scalar_ld(trow, __builtin_amdgcn_readfirstlane(lb)) < 0) hi = lo;  // unassigned
+        if (own_new && i == nblk - 1 && hi > lo) --hi;  // the newest key comes from registers
+        const bool full = lo == 0 && hi == kBlock;
+
+        const uint4 k0 = *(const uint4 *)(blk + ko0);
+        const uint4 k1 = *(const uint4 *)(blk + ko1);
+        const uint4 w0 = *(const uint4 *)(blk + vo0);
+        const uint4 w1 = *(const uint4 *)(blk + vo1);
+        const uint32_t eks = *(const uint32_t *)(blk + kF8Exp + 4 * g4);
+        const uint32_t evs = *(const uint32_t *)(blk + kF8Exp + kBlock + 4 * g4);
+
+        // QK: S[key][head] for keys 4 g4 + r, head n
+        const uint32_t kw[8] = {k0.x, k0.y, k0.z, k0.w, k1.x, k1.y, k1.z, k1.w};
+        f32x4_t c = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+        for (int s = 0; s < 4; ++s) {
+            const uint4 af = make_uint4(f8_bf16x2<false>(kw[2 * s]), f8_bf16x2<true>(kw[2 * s]),
+                                        f8_bf16x2<false>(kw[2 * s + 1]), f8_bf16x2<true>(kw[2 * s + 1]));
+            c = mfma16x16x32(af, qb[s], c);
+        }
+        float sc[4];
+#pragma unroll
+        for (int r = 0; r < 4; ++r) sc[r] = c[r] * f8_scale(eks, r);
+        if (!full) {
+#pragma unroll
+            for (int r = 0; r < 4; ++r) {
+                const int key = 4 * g4 + r;
+                sc[r] = (key >= lo && key < hi) ? sc[r] : -INFINITY;
+            }
+        }
+        const float mx = rows_max(vmax2(vmax2(sc[0], sc[1]), vmax2(sc[2], sc[3])));
+        const bool bump = mx > m_ref + 8.f;
+        if (__builtin_amdgcn_ballot_w64(bump)) {
+            const float mnew = bump ? mx : m_ref;
+            const float alpha = mnew == m_ref ? 1.f : __builtin_amdgcn_exp2f(m_ref - mnew);
+            m_ref = mnew;
+            lsum *= alpha;
+#pragma unroll
+            for (int j = 0; j < 8; ++j) acc[j] *= alpha;
+        }
+        const float mr = m_ref == -INFINITY ? 0.f : m_ref;
+        float pv[4];
+#pragma unroll
+        for (int r = 0; r < 4; ++r) pv[r] = __builtin_amdgcn_exp2f(sc[r] - mr);
+        lsum += (pv[0] + pv[1]) + (pv[2] + pv[3]);
+        // fold the value scales into the probabilities
+#pragma unroll
+        for (int r = 0; r < 4; ++r) pv[r] *= f8_scale(evs, r);
+        uint32_t vw[8] = {w0.x, w0.y, w0.z, w0.w, w1.x, w1.y, w1.z, w1.w};
+        if (!full) {
+            // invisible slots: zero probability, and zero codes (they may be NaN)
+            uint32_t bm = 0;
+#pragma unroll
+            for (int r = 0; r < 4; ++r) {
+                const int key = 4 * g4 + r;
+                const bool ok = key >= lo && key < hi;
+                pv[r] = ok ? pv[r] : 0.f;
+                bm |= ok ? (0xFFu << (8 * r)) : 0u;
+            }
+#pragma unroll
+            for (int j = 0; j < 8; ++j) vw[j] &= bm;
+        }
+        const uint2 pb = make_uint2(pack_bf16x2(pv[0], pv[1]), pack_bf16x2(pv[2], pv[3]));
+#pragma unroll
+        for (int j = 0; j < 8; ++j)
+            acc[j] = mfma16x16x16(make_uint2(f8_bf16x2<false>(vw[j]), f8_bf16x2<true>(vw[j])), pb, acc[j]);
+    }
+
+    float L = rows_sum(lsum);
+    if (own_new) {
+        wave_sync();
+        uint32_t kcode[8], vcode[8];  // codes of this lane's dims d0 .. d0 + 31
+        {
+            const uint4 a0 = *(const uint4 *)&snew[0][d0], a1 = *(const uint4 *)&snew[0][d0 + 16];
+            const uint4 b0 = *(const uint4 *)&snew[1][d0], b1 = *(const uint4 *)&snew[1][d0 + 16];
+            kcode[0] = a0.x; kcode[1] = a0.y; kcode[2] = a0.z; kcode[3] = a0.w;
+            kcode[4] = a1.x; kcode[5] = a1.y; kcode[6] = a1.z; kcode[7] = a1.w;
+            vcode[0] = b0.x; vcode[1] = b0.y; vcode[2] = b0.z; vcode[3] = b0.w;
+            vcode[4] = b1.x; vcode[5] = b1.y; vcode[6] = b1.z; vcode[7] = b1.w;
+        }
+        // ---- the newest key: its score for head n (this lane's 32 dims, then
+        // the sum over the four lane rows), one exact online-softmax step
+        float sn = 0.f;
+#pragma unroll
+        for (int s = 0; s < 4; ++s) {
+            const uint32_t qw[4] = {qb[s].x, qb[s].y, qb[s].z, qb[s].w};
+#pragma unroll
+            for (int p2 = 0; p2 < 4; ++p2) {
+                const uint32_t kc = kcode[2 * s + p2 / 2];
+                sn = dot2_bf16(qw[p2], (p2 & 1) ? f8_bf16x2<true>(kc) : f8_bf16x2<false>(kc), sn);
+            }
+        }
+        sn = rows_sum(sn) * __uint_as_float((uint32_t)(ek_new + 127) << 23);
+        const float m_new = fmaxf(m_ref, sn);  // sn is finite
+        const float alpha = __builtin_amdgcn_exp2f(m_ref - m_new);
+        const float pn = __builtin_amdgcn_exp2f(sn - m_new);
+        L = L * alpha + pn;
+        m_ref = m_new;
+        // the PV operand precision: bf16 of p * 2^e_v
+        const float pvn = to_f32(from_f32<bf16_t>(pn * __uint_as_float((uint32_t)(ev_new + 127) << 23)));
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+#pragma unroll
+            for (int hw = 0; hw < 2; ++hw) {  // dims d0 + 8 i + 4 hw .. + 3
+                const uint32_t vc = vcode[2 * i + hw];
+                const auto lo2 = __builtin_amdgcn_cvt_pk_f32_fp8(vc, false);
+                const auto hi2 = __builtin_amdgcn_cvt_pk_f32_fp8(vc, true);
+                const float vf[4] = {lo2[0], lo2[1], hi2[0], hi2[1]};
+#pragma unroll
+                for (int q = 0; q < 4; ++q) {
+                    const int j = 4 * hw + q;
+                    acc[j][i] = fmaf(pvn, vf[q], acc[j][i] * alpha);
+                }
+            }
+        }
+    }
+
+    // the pool copy of the newest key and value, for later launches; issued
+    // after the wave's last barrier (a barrier's release fence would wait for
+    // these scattered stores)
+    auto store_new = [&]() {
+        const int64_t tb = __builtin_amdgcn_readfirstlane(a.p.tok_block[t]);
+        const int toff = __builtin_amdgcn_readfirstlane(a.p.tok_off[t]);
+        uint8_t *tile = (uint8_t *)g.kv + (int64_t)a.layer * g.layer_stride + tb * g.block_stride +
+                        (int64_t)kvh * g.head_stride;
+        *(uint16_t *)(tile + toff * D + dd) = (uint16_t)kc2;  // K row bytes dd, dd + 1
+        uint8_t *vq = tile + kF8Tile + (toff >> 2) * (4 * D) + (toff & 3);
+        vq[dd * 4] = (uint8_t)vc2;
+        vq[(dd + 1) * 4] = (uint8_t)(vc2 >> 8);
+        if (lane == 0) {
+            tile[kF8Exp + toff] = (uint8_t)(ek_new + 127);
+            tile[kF8Exp + kBlock + toff] = (uint8_t)(ev_new + 127);
+        }
+    };
+
+    if constexpr (NG > 1) {
+        // waves 1.. hand (m, l, acc) to wave 0 through their own drained rings
+        if (wv > 0) {
+            float *scr = (float *)&ring[wv][0][0] + n * D + d0;  // [16][D]
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+                *(float4 *)(scr + 8 * i) = make_float4(acc[0][i], acc[1][i], acc[2][i], acc[3][i]);
+                *(float4 *)(scr + 8 * i + 4) = make_float4(acc[4][i], acc[5][i], acc[6][i], acc[7][i]);
+            }
+            if (g4 == 0) {
+                sM[wv][n] = m_ref;
+                sL[wv][n] = L;
+            }
+        }
+        __syncthreads();
+        if (wv > 0) {
+            if (own_new) store_new();
+            return;
+        }
+        float M = m_ref;
+#pragma unroll
+        for (int q = 1; q < NG; ++q) M = fmaxf(M, sM[q][n]);
+        const float Mn = M == -INFINITY ? 0.f : M;
+        const float w0 = __builtin_amdgcn_exp2f(m_ref - Mn);
+        L *= w0;
+#pragma unroll
+        for (int j = 0; j < 8; ++j) acc[j] *= w0;
+#pragma unroll
+        for (int q = 1; q < NG; ++q) {
+            const float wq = __builtin_amdgcn_exp2f(sM[q][n] - Mn);
+            L = fmaf(sL[q][n], wq, L);
+            const float *scr = (const float *)&ring[q][0][0] + n * D + d0;
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+                const float4 lo4 = *(const float4 *)(scr + 8 * i);
+                const float4 hi4 = *(const float4 *)(scr + 8 * i + 4);
+                acc[0][i] = fmaf(wq, lo4.x, acc[0][i]);
+                acc[1][i] = fmaf(wq, lo4.y, acc[1][i]);
+                acc[2][i] = fmaf(wq, lo4.z, acc[2][i]);
+                acc[3][i] = fmaf(wq, lo4.w, acc[3][i]);
+                acc[4][i] = fmaf(wq, hi4.x, acc[4][i]);
+                acc[5][i] = fmaf(wq, hi4.y, acc[5][i]);
+                acc[6][i] = fmaf(wq, hi4.z, acc[6][i]);
+                acc[7][i] = fmaf(wq, hi4.w, acc[7][i]);
+            }
+        }
+        m_ref = M;
+    }
+
+    const int hq0 = kvh * G;
+    if (n < G) {
+        if (a.n_split == 1) {
+            const float inv = 1.f / L;
+            bf16_t *ob = (bf16_t *)a.out + (row * g.hq + hq0 + n) * D + d0;
+#pragma unroll
+            for (int i = 0; i < 4; ++i)
+                *(uint4 *)(ob + 8 * i) =
+                    make_uint4(pack_bf16x2(acc[0][i] * inv, acc[1][i] * inv),
+                               pack_bf16x2(acc[2][i] * inv, acc[3][i] * inv),
+                               pack_bf16x2(acc[4][i] * inv, acc[5][i] * inv),
+                               pack_bf16x2(acc[6][i] * inv, acc[7][i] * inv));
+            if (a.lse && g4 == 0)
+                a.lse[row * g.hq + hq0 + n] = (m_ref + __builtin_amdgcn_logf(L)) * 0.6931471805599453f;
+        } else {
+            const int64_t ns = a.n_split;
+            const int64_t base = ((int64_t)t * g.hq + hq0 + n) * ns + split;
+            float *pacc = a.part + base * D + d0;
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+                *(float4 *)(pacc + 8 * i) = make_float4(acc[0][i], acc[1][i], acc[2][i], acc[3][i]);
+                *(float4 *)(pacc + 8 * i + 4) = make_float4(acc[4][i], acc[5][i], acc[6][i], acc[7][i]);
+            }
+            if (g4 == 0) {
+                float *pml = a.part + (int64_t)a.p.n_tok * g.hq * ns * D;
+                pml[base * 2] = m_ref;
+                pml[base * 2 + 1] = L;
+            }
+        }
+    }
+    if constexpr (NG == 1) {
+        if (own_new) store_new();  // one wave: it owns the newest key
+    }
+}
+
+// ---------------------------------------------------------------------------
+// debug poison: NaN codes and infinite scales into every slot whose live bit
+// is clear
+// ---------------------------------------------------------------------------
+__global__ void k_poison_fp8(PoolGeom g, int32_t n_layers, int64_t n_blocks,
+                             const uint16_t *__restrict__ live) {
+    const int64_t n_items = (int64_t)n_layers * n_blocks * g.hkv;
+    for (int64_t it = blockIdx.x; it < n_items; it += gridDim.x) {
+        const int h = (int)(it % g.hkv);
+        const int64_t b = (it / g.hkv) % n_blocks;
+        const int l = (int)(it / ((int64_t)g.hkv * n_blocks));
+        const uint16_t lm = live[b];
+        if (lm == 0xFFFF) continue;
+        uint8_t *tile = (uint8_t *)g.kv + (int64_t)l * g.layer_stride + b * g.block_stride +
+                        (int64_t)h * g.head_stride;
+        for (int e = threadIdx.x; e < kF8Tile; e += blockDim.x) {
+            const int key = e / kF8D, d = e % kF8D;
+            if (!((lm >> key) & 1)) {
+                tile[e] = 0x7F;
+                tile[kF8Tile + ((key >> 2) * kF8D + d) * 4 + (key & 3)] = 0x7F;
+            }
+        }
+        if (threadIdx.x < 2 * kBlock) {
+            const int key = threadIdx.x % kBlock;
+            if (!((lm >> key) & 1)) tile[kF8Exp + threadIdx.x] = 0xFF;
+        }
+    }
+}
+
+template <int G>
+hipError_t launch_fp8_g(const AttnArgs &a, hipStream_t s) {
+    using S = F8Shape<G>;
+    const int64_t units = (int64_t)a.p.n_tok * a.g.hkv * a.n_split;
+    if (units == 0) return hipSuccess;
+    hipLaunchKernelGGL((k_attn_fp8<G, S::NG, S::NBUF>), dim3((unsigned)units), dim3(64 * S::NG), 0,
+                       s, a);
+    return hipGetLastError();
+}
+template <int G>
+int resident_fp8_g() {
+    using S = F8Shape<G>;
+    int n = 0;
+    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, k_attn_fp8<G, S::NG, S::NBUF>, 64 * S::NG,
+                                                     0) != hipSuccess)
+        return 1;
+    return n > 0 ? n : 1;
+}
+
+}  // namespace
+
+int fp8_head_stride(int d) {
+    // codes + exponents, rounded up to 128 bytes so every region starts on a
+    // line boundary
+    return d == kF8D ? ((kF8Read + 127) / 128) * 128 : 0;
+}
+
+bool attn_fp8_supported(int d, int g) {
+    return d == kF8D && (g == 1 || g == 2 || g == 4 || g == 8);
+}
+
+int attn_fp8_resident_per_cu(int g) {
+    switch (g) {
+        case 1: return resident_fp8_g<1>();
+        case 2: return resident_fp8_g<2>();
+        case 4: return resident_fp8_g<4>();
+        default: return resident_fp8_g<8>();
+    }
+}
+
+hipError_t launch_append_fp8(const PoolGeom &g, const PlanView &p, int32_t layer, const void *k,
+                             const void *v, hipStream_t s) {
+    if (g.d != kF8D) return hipErrorInvalidValue;
+    const int64_t waves = (int64_t)p.n_tok * g.hkv;
+    if (waves == 0) return hipSuccess;
+    hipLaunchKernelGGL(k_append_fp8, dim3((unsigned)((waves + 3) / 4)), dim3(256), 0, s, g, p, layer,
+                       (const bf16_t *)k, (const bf16_t *)v);
+    return hipGetLastError();
+}
+
+hipError_t launch_attn_fp8(const AttnArgs &a, hipStream_t s) {
+    const int G = a.g.hq / a.g.hkv;
+    if (!attn_fp8_supported(a.g.d, G)) return hipErrorInvalidValue;
+    switch (G) {
+        case 1: return launch_fp8_g<1>(a, s);
+        case 2: return launch_fp8_g<2>(a, s);
+        case 4: return launch_fp8_g<4>(a, s);
+        default: return launch_fp8_g<8>(a, s);
+    }
+}
+
+hipError_t launch_poison_fp8(const PoolGeom &g, int32_t n_layers, int64_t n_blocks,
+                             const uint16_t *live, hipStream_t s) {
+    hipLaunchKernelGGL(k_poison_fp8, dim3(8192), dim3(256), 0, s, g, n_layers, n_blocks, live);
+    return hipGetLastError();
+}
+
+}  // namespace mtn

@@ -147,6 +147,13 @@ mtn_status hip_fail(mtn_pool *p, hipError_t e, const char *where) {
 
 int64_t ceil_div(int64_t a, int64_t b) { return (a + b - 1) / b; }
 
+// Bytes of one (layer, block, kv head) region: K tile + V^T tile of 16 x D
+// elements, or for fp8 the code tiles plus 32 exponent bytes, padded to 128.
+int64_t kv_head_stride(const mtn_pool_config *c) {
+    if (c->kv_dtype == MTN_FP8_E4M3) return fp8_head_stride(c->head_dim);
+    return 2 * (int64_t)kBlock * c->head_dim * (c->kv_dtype == MTN_BF16 ? 2 : 4);
+}
+
 mtn_status validate(const mtn_pool_config *c) {
     if (!c) return MTN_ERR_INVALID_ARG;
     if (c->n_layers < 1 || c->n_q_heads < 1 || c->n_kv_heads < 1) return MTN_ERR_INVALID_ARG;
@@ -162,8 +169,13 @@ mtn_status validate(const mtn_pool_config *c) {
         if ((int64_t)c->window + c->max_chunk + c->n_sink > (int64_t)1 << 30)
             return MTN_ERR_INVALID_ARG;
     }
-    if (c->kv_dtype != MTN_F32 && c->kv_dtype != MTN_BF16) return MTN_ERR_INVALID_ARG;
-    if (c->io_dtype != c->kv_dtype) return MTN_ERR_UNSUPPORTED;
+    if (c->kv_dtype == MTN_FP8_E4M3) {
+        // E4M3 codes in the pool, bf16 queries / keys / values / outputs
+        if (c->io_dtype != MTN_BF16 || c->head_dim != 128) return MTN_ERR_UNSUPPORTED;
+    } else {
+        if (c->kv_dtype != MTN_F32 && c->kv_dtype != MTN_BF16) return MTN_ERR_INVALID_ARG;
+        if (c->io_dtype != c->kv_dtype) return MTN_ERR_UNSUPPORTED;
+    }
     if (!(c->rope_theta > 1.0)) return MTN_ERR_INVALID_ARG;
     if (c->softmax_scale < 0.f || !std::isfinite(c->softmax_scale)) return MTN_ERR_INVALID_ARG;
     if ((int64_t)c->max_sessions * c->max_chunk > (int64_t)1 << 24) return MTN_ERR_INVALID_ARG;
@@ -410,7 +422,10 @@ mtn_status append_impl(mtn_pool *P, int32_t layer, const void *k, const void *v,
     hipEvent_t e0;
     mtn_status st = timing_begin(P, s, &e0);
     if (st) return st;
-    HIP_TRY(P, launch_append(P->cfg.kv_dtype, geom(P), P->view, layer, k, v, s));
+    if (P->cfg.kv_dtype == MTN_FP8_E4M3)
+        HIP_TRY(P, launch_append_fp8(geom(P), P->view, layer, k, v, s));
+    else
+        HIP_TRY(P, launch_append(P->cfg.kv_dtype, geom(P), P->view, layer, k, v, s));
     st = timing_end(P, 0, e0, s);
     if (st) return st;
     P->layer_done[layer] = 1;
@@ -473,14 +488,17 @@ mtn_status decode_impl(mtn_pool *P, int32_t layer, const void *q, void *out, flo
     hipEvent_t e0;
     mtn_status st = timing_begin(P, s, &e0);
     if (st) return st;
-    HIP_TRY(P, launch_attn_valu(P->cfg.kv_dtype, a, s));
+    if (P->cfg.kv_dtype == MTN_FP8_E4M3)
+        HIP_TRY(P, launch_attn_fp8(a, s));
+    else
+        HIP_TRY(P, launch_attn_valu(P->cfg.kv_dtype, a, s));
     st = timing_end(P, 2, e0, s);
     if (st) return st;
     if (k_new) P->layer_done[layer] = 1;
     if (n_split > 1) {
         st = timing_begin(P, s, &e0);
         if (st) return st;
-        HIP_TRY(P, launch_merge(P->cfg.kv_dtype, a, s));
+        HIP_TRY(P, launch_merge(P->cfg.io_dtype, a, s));  // writes io rows
         st = timing_end(P, 3, e0, s);
         if (st) return st;
     }
@@ -496,7 +514,7 @@ mtn_status prefill_impl(mtn_pool *P, int32_t layer, const void *q, void *out, fl
     mtn_status st = timing_begin(P, s, &e0);
     if (st) return st;
     if (prefill_mfma_supported(P->cfg.kv_dtype, P->cfg.head_dim, P->G)) {
-        HIP_TRY(P, launch_prefill_mfma(a, P->d_seq_first, P->d_seq_ntok, P->d_pf_items,
+        HIP_TRY(P, launch_prefill_mfma(P->cfg.kv_dtype, a, P->d_seq_first, P->d_seq_ntok, P->d_pf_items,
                                        (int32_t)(P->pf_items.size() / 2), P->d_zero, s));
     } else {
         HIP_TRY(P, launch_attn_valu(P->cfg.kv_dtype, a, s));
@@ -532,8 +550,7 @@ mtn_status mtn_pool_required_bytes(const mtn_pool_config *cfg, size_t *kv_bytes)
     mtn_status st = validate(cfg);
     if (st) return st;
     if (!kv_bytes) return MTN_ERR_INVALID_ARG;
-    size_t e = cfg->kv_dtype == MTN_BF16 ? 2 : 4;
-    size_t per_block = (size_t)cfg->n_kv_heads * 2 * kBlock * cfg->head_dim * e;
+    size_t per_block = (size_t)cfg->n_kv_heads * (size_t)kv_head_stride(cfg);
     *kv_bytes = per_block * (size_t)cfg->n_blocks * (size_t)cfg->n_layers;
     return MTN_OK;
 }
@@ -547,7 +564,9 @@ mtn_status mtn_pool_create(const mtn_pool_config *cfg, void *kv_dev, size_t kv_b
     bool host_only = cfg->flags & MTN_POOL_HOST_ONLY;
     if (!host_only) {
         if (!kv_dev || kv_bytes < need || ((uintptr_t)kv_dev & 255)) return MTN_ERR_INVALID_ARG;
-        if (!attn_valu_supported(cfg->kv_dtype, cfg->head_dim, cfg->n_q_heads / cfg->n_kv_heads))
+        const int g = cfg->n_q_heads / cfg->n_kv_heads;
+        if (cfg->kv_dtype == MTN_FP8_E4M3 ? !attn_fp8_supported(cfg->head_dim, g)
+                                          : !attn_valu_supported(cfg->kv_dtype, cfg->head_dim, g))
             return MTN_ERR_UNSUPPORTED;
     }
     mtn_pool *P = new mtn_pool();
@@ -555,7 +574,7 @@ mtn_status mtn_pool_create(const mtn_pool_config *cfg, void *kv_dev, size_t kv_b
     P->host_only = host_only;
     P->unbounded = cfg->window == MTN_WINDOW_UNBOUNDED;
     P->G = cfg->n_q_heads / cfg->n_kv_heads;
-    P->elt = cfg->kv_dtype == MTN_BF16 ? 2 : 4;
+    P->elt = cfg->io_dtype == MTN_BF16 ? 2 : 4;  // io element size
     if (P->unbounded) {
         P->S = 0;
         P->W = -1;
@@ -568,8 +587,8 @@ mtn_status mtn_pool_create(const mtn_pool_config *cfg, void *kv_dev, size_t kv_b
         P->R = (int32_t)(ceil_div((int64_t)cfg->window + cfg->max_chunk - 1, kBlock) * kBlock);
     }
     P->row_len = P->nsb + P->R / kBlock;
-    P->tile_bytes = (int64_t)kBlock * cfg->head_dim * (int64_t)P->elt;
-    P->head_stride = 2 * P->tile_bytes;
+    P->tile_bytes = (int64_t)kBlock * cfg->head_dim * (cfg->kv_dtype == MTN_FP8_E4M3 ? 1 : (int64_t)P->elt);
+    P->head_stride = kv_head_stride(cfg);
     P->block_stride = P->head_stride * cfg->n_kv_heads;
     P->layer_stride = P->block_stride * cfg->n_blocks;
     P->scale = cfg->softmax_scale > 0.f ? cfg->softmax_scale
@@ -631,7 +650,9 @@ mtn_status mtn_pool_create(const mtn_pool_config *cfg, void *kv_dev, size_t kv_b
             hipSuccess)
             return bail(e, "cu count");
         P->resident_units =
-            n_cu * attn_valu_resident_per_cu(cfg->kv_dtype, cfg->head_dim, P->G);
+            n_cu * (cfg->kv_dtype == MTN_FP8_E4M3
+                        ? attn_fp8_resident_per_cu(P->G)
+                        : attn_valu_resident_per_cu(cfg->kv_dtype, cfg->head_dim, P->G));
         if ((e = hipStreamSynchronize((hipStream_t)stream)) != hipSuccess)
             return bail(e, "sync");
     }
@@ -927,7 +948,10 @@ mtn_status mtn_debug_poison_dead(mtn_pool *P, void *stream) {
     HIP_TRY(P, hipMalloc(&d_live, sizeof(uint16_t) * live.size()));
     HIP_TRY(P, hipMemcpy(d_live, live.data(), sizeof(uint16_t) * live.size(),
                          hipMemcpyHostToDevice));
-    HIP_TRY(P, launch_poison(P->cfg.kv_dtype, geom(P), P->cfg.n_layers, P->cfg.n_blocks, d_live, s));
+    if (P->cfg.kv_dtype == MTN_FP8_E4M3)
+        HIP_TRY(P, launch_poison_fp8(geom(P), P->cfg.n_layers, P->cfg.n_blocks, d_live, s));
+    else
+        HIP_TRY(P, launch_poison(P->cfg.kv_dtype, geom(P), P->cfg.n_layers, P->cfg.n_blocks, d_live, s));
     HIP_TRY(P, hipStreamSynchronize(s));
     HIP_TRY(P, hipFree(d_live));
     return MTN_OK;

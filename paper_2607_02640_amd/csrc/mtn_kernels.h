@@ -51,7 +51,7 @@ struct AttnArgs {
     const void *v_new;
 };
 
-// dtype codes match the public MTN_F32 / MTN_BF16
+// dtype codes match the public MTN_F32 / MTN_BF16 / MTN_FP8_E4M3
 hipError_t launch_plan_apply(const int32_t *upd_idx, const int32_t *upd_val, int32_t n_upd,
                              int32_t *table, const int32_t *tok_pos, int32_t n_tok,
                              const double *inv_freq, int32_t half_d, float2 *rope,
@@ -65,13 +65,13 @@ hipError_t launch_append(int dtype, const PoolGeom &g, const PlanView &p, int32_
 hipError_t launch_attn_valu(int dtype, const AttnArgs &a, hipStream_t s);
 hipError_t launch_merge(int dtype, const AttnArgs &a, hipStream_t s);
 
-// MFMA chunk-prefill attention (bf16, D = 128): one workgroup per (sequence,
+// MFMA chunk-prefill attention (bf16 or fp8 pool, D = 128): one workgroup per (sequence,
 // row pass, kv head).  items: n_items (sequence, pass) pairs, pass p of a
 // sequence covering its query rows [p, p + 1) * prefill_rows_per_pass() (rows
 // are token * G + group head).  zero_page: 16 KiB of device zeros, the DMA
 // source of blocks a pass does not see.
 int prefill_rows_per_pass();
-hipError_t launch_prefill_mfma(const AttnArgs &a, const int32_t *seq_first_tok,
+hipError_t launch_prefill_mfma(int dtype, const AttnArgs &a, const int32_t *seq_first_tok,
                                const int32_t *seq_ntok, const int32_t *items, int32_t n_items,
                                const uint8_t *zero_page, hipStream_t s);
 
@@ -79,6 +79,19 @@ hipError_t launch_poison(int dtype, const PoolGeom &g, int32_t n_layers, int64_t
                          const uint16_t *live_mask, hipStream_t s);
 
 hipError_t launch_copy(const void *src, void *dst, size_t bytes, hipStream_t s);
+
+// FP8 (E4M3) KV cache, D = 128, bf16 io: bytes per (layer, block, kv head)
+// region (0 for an unsupported head dim), the fused RoPE + quantize + append,
+// the MFMA decode (k_new / v_new in AttnArgs select the fused append) and the
+// debug poison.
+int fp8_head_stride(int d);
+bool attn_fp8_supported(int d, int g);
+int attn_fp8_resident_per_cu(int g);
+hipError_t launch_append_fp8(const PoolGeom &g, const PlanView &p, int32_t layer, const void *k,
+                             const void *v, hipStream_t s);
+hipError_t launch_attn_fp8(const AttnArgs &a, hipStream_t s);
+hipError_t launch_poison_fp8(const PoolGeom &g, int32_t n_layers, int64_t n_blocks,
+                             const uint16_t *live_mask, hipStream_t s);
 
 bool attn_valu_supported(int dtype, int d, int g);
 // workgroups of the vector attention kernel resident per CU (occupancy query)

@@ -741,13 +741,58 @@ struct PfBlock {
     bool sink;
 };
 
-template <int G>
+// An fp8 stage as the DMA lands it (two block regions of kF8Read bytes: K
+// codes, V codes in key quads, exponents) -> the bf16 stage layout above, each
+// value code * 2^e exactly.  512 threads: thread tid converts, in block
+// tid >> 8, K dims 8 (tid & 15) .. + 7 of key (tid >> 4) & 15, and V dims
+// 2 (tid & 63), 2 (tid & 63) + 1 of keys 4 ((tid >> 6) & 3) .. + 3.
+__device__ __forceinline__ void f8_stage_to_bf16(const uint8_t *src, uint8_t *dst, int tid) {
+    const int b = tid >> 8;
+    const uint8_t *blk = src + b * kF8Read;
+    {
+        const int key = (tid >> 4) & 15, hc = tid & 15;
+        const uint2 c = *(const uint2 *)(blk + key * kF8D + hc * 8);
+        const float sk = __uint_as_float((uint32_t)blk[kF8Exp + key] << 23);
+        const auto a0 = __builtin_amdgcn_cvt_pk_f32_fp8(c.x, false);
+        const auto a1 = __builtin_amdgcn_cvt_pk_f32_fp8(c.x, true);
+        const auto a2 = __builtin_amdgcn_cvt_pk_f32_fp8(c.y, false);
+        const auto a3 = __builtin_amdgcn_cvt_pk_f32_fp8(c.y, true);
+        *(uint4 *)(dst + lds_k(b, key, hc)) =
+            make_uint4(pack_bf16x2(a0[0] * sk, a0[1] * sk), pack_bf16x2(a1[0] * sk, a1[1] * sk),
+                       pack_bf16x2(a2[0] * sk, a2[1] * sk), pack_bf16x2(a3[0] * sk, a3[1] * sk));
+    }
+    {
+        const int kg = (tid >> 6) & 3, dp = tid & 63;
+        const uint2 c = *(const uint2 *)(blk + kF8Tile + (kg * kF8D + 2 * dp) * 4);
+        const uint32_t ew = *(const uint32_t *)(blk + kF8Exp + kBlock + 4 * kg);
+        float sv[4];
+#pragma unroll
+        for (int r = 0; r < 4; ++r) sv[r] = __uint_as_float(((ew >> (8 * r)) & 0xFFu) << 23);
+        const uint32_t w[2] = {c.x, c.y};
+#pragma unroll
+        for (int x = 0; x < 2; ++x) {  // dim 2 dp + x: keys 4 kg .. 4 kg + 3
+            const auto lo = __builtin_amdgcn_cvt_pk_f32_fp8(w[x], false);
+            const auto hi = __builtin_amdgcn_cvt_pk_f32_fp8(w[x], true);
+            *(uint2 *)(dst + lds_v16(b, 2 * dp + x, kg >> 1) + (kg & 1) * 8) =
+                make_uint2(pack_bf16x2(lo[0] * sv[0], lo[1] * sv[1]),
+                           pack_bf16x2(hi[0] * sv[2], hi[1] * sv[3]));
+        }
+    }
+}
+
+// F8: the pool holds E4M3 codes.  Each stage then lands as two kF8Read-byte
+// regions (one 1 KiB DMA instruction per wave, plus the 32 exponent bytes
+// from waves 0 and 4), and every stage is converted into one bf16 stage
+// buffer (a second barrier) before the same MFMA stage body runs on it.
+template <int G, bool F8>
 __global__ __launch_bounds__(64 * kPfWaves) void k_prefill_mfma(PfArgs pa) {
     constexpr int D = 128;
-    constexpr int NIW = kPfStageBytes / 1024 / kPfWaves;  // DMA instructions per wave per stage
-    static_assert(NIW * kPfWaves * 1024 == kPfStageBytes, "stage DMA split");
+    constexpr int SB = F8 ? 2 * kF8Read : kPfStageBytes;  // bytes of a ring stage
+    constexpr int NIW = F8 ? 1 : kPfStageBytes / 1024 / kPfWaves;  // full DMA instructions per wave per stage
+    static_assert(F8 ? kPfWaves == 8 : NIW * kPfWaves * 1024 == kPfStageBytes, "stage DMA split");
     static_assert(kPfStages >= 2 && kPfStages <= 8, "ring depth");
-    __shared__ __attribute__((aligned(16))) uint8_t ring[kPfStages][kPfStageBytes];
+    __shared__ __attribute__((aligned(16))) uint8_t ring[kPfStages][SB];
+    __shared__ __attribute__((aligned(16))) uint8_t bfs[F8 ? kPfStageBytes : 16];
     const AttnArgs &a = pa.a;
     const PoolGeom &g = a.g;
     // one workgroup per (sequence, row pass, kv head): a long chunk's passes
@@ -821,7 +866,8 @@ __global__ __launch_bounds__(64 * kPfWaves) void k_prefill_mfma(PfArgs pa) {
 #pragma unroll
     for (int jj = 0; jj < NIW; ++jj) {
         int b;
-        src_off[jj] = stage_src((wv * NIW + jj) * 1024 + lane * 16, &b);
+        src_off[jj] = F8 ? (wv & 3) * 1024 + lane * 16
+                         : stage_src((wv * NIW + jj) * 1024 + lane * 16, &b);
     }
     // logical block of virtual block v < nvb (branch-free: sinks, then the ring)
     auto vlb = [&](int v) {
@@ -844,12 +890,20 @@ __global__ __launch_bounds__(64 * kPfWaves) void k_prefill_mfma(PfArgs pa) {
         const int slot = st % kPfStages;
         have_bits = (have_bits & ~(3u << (2 * slot))) | ((h0 ? 1u : 0u) << (2 * slot)) |
                     ((h1 ? 2u : 0u) << (2 * slot));
-        const uint32_t dst = ring0 + (uint32_t)(slot * kPfStageBytes);
+        const uint32_t dst = ring0 + (uint32_t)(slot * SB);
+        if constexpr (F8) {
+            const int jb = wv >> 2;  // block of this wave's instruction
+            const uint8_t *src = jb ? b1 : b0;
+            const uint32_t bdst = dst + jb * kF8Read;
+            dma16(src + src_off[0], bdst + (wv & 3) * 1024);
+            if ((wv & 3) == 0 && lane < 2) dma16(src + kF8Exp + lane * 16, bdst + kF8Exp);
+        } else {
 #pragma unroll
-        for (int jj = 0; jj < NIW; ++jj) {
-            const int j = wv * NIW + jj;  // uniform; block of the instruction below
-            const int jb = j < 8 ? (j >> 2) : ((j - 8) >> 2);
-            dma16((jb ? b1 : b0) + src_off[jj], dst + j * 1024);
+            for (int jj = 0; jj < NIW; ++jj) {
+                const int j = wv * NIW + jj;  // uniform; block of the instruction below
+                const int jb = j < 8 ? (j >> 2) : ((j - 8) >> 2);
+                dma16((jb ? b1 : b0) + src_off[jj], dst + j * 1024);
+            }
         }
     };
 
@@ -1076,7 +1130,14 @@ __global__ __launch_bounds__(64 * kPfWaves) void k_prefill_mfma(PfArgs pa) {
             // this wave's share of stage st landed; the barrier covers the other
             // waves' shares and frees the slot consumed at st - 1
             const int after = min(kPfStages - 2, n_stages - 1 - st);
-            vm_wait_blocks<NIW, kPfStages - 2>(after);
+            if constexpr (F8) {
+                if ((wv & 3) == 0)
+                    vm_wait_blocks<2, kPfStages - 2>(after);
+                else
+                    vm_wait_blocks<1, kPfStages - 2>(after);
+            } else {
+                vm_wait_blocks<NIW, kPfStages - 2>(after);
+            }
             __syncthreads();
             const uint32_t hb = (have_bits >> (2 * (st % kPfStages))) & 3u;
             const int nst = st + kPfStages - 1;
@@ -1085,6 +1146,12 @@ __global__ __launch_bounds__(64 * kPfWaves) void k_prefill_mfma(PfArgs pa) {
                 if (nst + 1 < n_stages) load_phys(nst + 1, nx0, nx1);
             }
             const uint8_t *sm = &ring[st % kPfStages][0];
+            if constexpr (F8) {
+                // the previous stage's readers all passed the barrier above
+                f8_stage_to_bf16(sm, bfs, tid);
+                __syncthreads();
+                sm = bfs;
+            }
             // every row of the pass sees every key of the stage: no masking
             if (hb == 3u && whole_v(2 * st) && whole_v(2 * st + 1))
                 stage_body(std::true_type{}, sm, st, hb);
@@ -1174,7 +1241,7 @@ bool attn_valu_supported(int dtype, int d, int g) {
 }
 
 bool prefill_mfma_supported(int dtype, int d, int g) {
-    return dtype == 1 && d == 128 && (g == 1 || g == 2 || g == 4 || g == 8);
+    return (dtype == 1 || dtype == 2) && d == 128 && (g == 1 || g == 2 || g == 4 || g == 8);
 }
 
 hipError_t launch_plan_apply(const int32_t *upd_idx, const int32_t *upd_val, int32_t n_upd,
@@ -1231,20 +1298,28 @@ hipError_t launch_merge(int dtype, const AttnArgs &a, hipStream_t s) {
 
 int prefill_rows_per_pass() { return kPfRowsPerPass; }
 
-hipError_t launch_prefill_mfma(const AttnArgs &a, const int32_t *seq_first, const int32_t *seq_ntok,
-                               const int32_t *items, int32_t n_items, const uint8_t *zero_page,
-                               hipStream_t s) {
+template <bool F8>
+void launch_prefill_g(int G, dim3 grid, dim3 block, hipStream_t s, const PfArgs &pa) {
+    switch (G) {
+        case 1: hipLaunchKernelGGL((k_prefill_mfma<1, F8>), grid, block, 0, s, pa); break;
+        case 2: hipLaunchKernelGGL((k_prefill_mfma<2, F8>), grid, block, 0, s, pa); break;
+        case 4: hipLaunchKernelGGL((k_prefill_mfma<4, F8>), grid, block, 0, s, pa); break;
+        default: hipLaunchKernelGGL((k_prefill_mfma<8, F8>), grid, block, 0, s, pa); break;
+    }
+}
+
+hipError_t launch_prefill_mfma(int dtype, const AttnArgs &a, const int32_t *seq_first,
+                               const int32_t *seq_ntok, const int32_t *items, int32_t n_items,
+                               const uint8_t *zero_page, hipStream_t s) {
     const int G = a.g.hq / a.g.hkv;
-    if (!prefill_mfma_supported(1, a.g.d, G) || n_items <= 0 || !zero_page || !items)
+    if (!prefill_mfma_supported(dtype, a.g.d, G) || n_items <= 0 || !zero_page || !items)
         return hipErrorInvalidValue;
     PfArgs pa{a, seq_first, seq_ntok, items, zero_page};
     dim3 grid((unsigned)(n_items * a.g.hkv)), block(64 * kPfWaves);
-    switch (G) {
-        case 1: hipLaunchKernelGGL(k_prefill_mfma<1>, grid, block, 0, s, pa); break;
-        case 2: hipLaunchKernelGGL(k_prefill_mfma<2>, grid, block, 0, s, pa); break;
-        case 4: hipLaunchKernelGGL(k_prefill_mfma<4>, grid, block, 0, s, pa); break;
-        default: hipLaunchKernelGGL(k_prefill_mfma<8>, grid, block, 0, s, pa); break;
-    }
+    if (dtype == 2)
+        launch_prefill_g<true>(G, grid, block, s, pa);
+    else
+        launch_prefill_g<false>(G, grid, block, s, pa);
     return hipGetLastError();
 }
 

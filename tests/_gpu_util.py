@@ -10,8 +10,10 @@ import paper_2607_02640_amd as mtn
 from oracle import windowed_attention as wa
 from workload import session_rng, draw_qkv
 
-TDT = {"f32": torch.float32, "bf16": torch.bfloat16}
-TOL = {"f32": 1e-5, "bf16": 2e-2}
+# io element type and output tolerance per pool dtype (the fp8 pool takes bf16
+# io; its oracle holds the E4M3 round trip of every stored row)
+TDT = {"f32": torch.float32, "bf16": torch.bfloat16, "fp8": torch.bfloat16}
+TOL = {"f32": 1e-5, "bf16": 2e-2, "fp8": 2e-2}
 
 
 def say(*a):
@@ -49,7 +51,8 @@ class Harness:
         self.L, self.hq, self.hkv, self.d = n_layers, hq, hkv, d
         self.dtype = dtype
         self.sids = [pool.session_open() for _ in range(n_sessions)]
-        self.orc = [wa.OracleSession(hq, hkv, d, S, W, theta=theta, n_layers=n_layers)
+        self.orc = [wa.OracleSession(hq, hkv, d, S, W, theta=theta, n_layers=n_layers,
+                                     kv_quant="fp8_e4m3" if dtype == "fp8" else None)
                     for _ in range(n_sessions)]
         self.rng = [session_rng(1000 + seed, i) for i in range(n_sessions)]
         self.max_err = 0.0
