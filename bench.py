@@ -33,7 +33,9 @@ if ROOT not in sys.path:
 HBM_PEAK_GBPS = 8000.0
 BF16_MFMA_PEAK_TFLOPS = 2500.0
 COPY_PROBE_BYTES = 4 << 30
-KERNEL_SRC = os.path.join(ROOT, "paper_2607_02640_amd", "csrc", "mtn_kernels.hip")
+# sources of the bf16 decode kernel (the counters go stale when these change)
+KERNEL_SRC = [os.path.join(ROOT, "paper_2607_02640_amd", "csrc", f)
+              for f in ("mtn_kernels.hip", "mtn_device.h")]
 TRAFFIC_SUMMARY = os.path.join(ROOT, "profiles", "decode_traffic_qwen3omni_128s.json")
 
 
@@ -51,6 +53,9 @@ def parse():
     ap.add_argument("--cpu-layers", type=int, default=48,
                     help="layers of one session-frame the oracle sample covers")
     ap.add_argument("--n-split", type=int, default=0)
+    ap.add_argument("--kv-dtype", choices=["bf16", "fp8"], default=None,
+                    help="KV cache element type (default: the workload's); fp8 keeps E4M3 "
+                         "codes with per-token power-of-two scales and bf16 io")
     ap.add_argument("--json-out", default=None)
     ap.add_argument("--call", action="store_true",
                     help="run a whole simulated call from empty sessions and report the "
@@ -80,8 +85,11 @@ def parse():
 
 def kernel_src_hash() -> str:
     import hashlib
-    with open(KERNEL_SRC, "rb") as f:
-        return hashlib.sha256(f.read()).hexdigest()[:16]
+    h = hashlib.sha256()
+    for fn in KERNEL_SRC:
+        with open(fn, "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()[:16]
 
 
 def traffic_summary(fetch_dir, write_dir):
@@ -168,8 +176,9 @@ def run_gpu(args, w):
 
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
-    tdt = torch.bfloat16 if w.dtype == "bf16" else torch.float32
-    esz = 2 if w.dtype == "bf16" else 4
+    kvd = args.kv_dtype or w.dtype
+    tdt = torch.float32 if kvd == "f32" else torch.bfloat16   # io element type
+    esz = 4 if kvd == "f32" else 2
     N, Lyr, Hq, Hkv, D = w.n_sessions, w.n_layers, w.n_q_heads, w.n_kv_heads, w.head_dim
     C, tau = w.chunk[1], w.n_decode[1]
     if w.chunk[0] != w.chunk[1] or w.n_decode[0] != w.n_decode[1]:
@@ -178,10 +187,10 @@ def run_gpu(args, w):
     blocks_per = -(-w.n_sink // 16) + R // 16
     n_blocks = N * blocks_per
     kw = dict(n_layers=Lyr, n_q_heads=Hq, n_kv_heads=Hkv, head_dim=D, n_sink=w.n_sink,
-              window=w.window, max_chunk=C, max_sessions=N, n_blocks=n_blocks, dtype=w.dtype,
+              window=w.window, max_chunk=C, max_sessions=N, n_blocks=n_blocks, dtype=kvd,
               rope_theta=w.rope_theta)
     nbytes = mtn.Pool.required(**kw)
-    log(f"[bench] pool {nbytes / 1e9:.1f} GB ({n_blocks} blocks), workload {w.name}")
+    log(f"[bench] pool {nbytes / 1e9:.1f} GB ({n_blocks} blocks), workload {w.name}, kv {kvd}")
     kv = torch.empty(nbytes, dtype=torch.uint8, device=dev)
     pool = mtn.Pool(**kw, kv=kv)
     sids = [pool.session_open() for _ in range(N)]
@@ -258,9 +267,13 @@ def run_gpu(args, w):
 
     # algorithmic bytes (steady state: every query sees S + W keys).  A decode
     # launch also appends its token (read k, v; write the pool copy)
+    # pool bytes of one token (all kv heads): K and V rows, plus the two scale
+    # exponent bytes per head of the fp8 cache
     vis = w.n_sink + w.window
-    beta = 2 * Hkv * D * esz
-    dec_bytes = N * (vis * beta + Hq * D * 2 * esz + 2 * beta)   # per decode launch
+    beta = Hkv * (2 * D + 2) if kvd == "fp8" else 2 * Hkv * D * esz
+    # per decode launch: the visible keys, q in and out, the new token's k and v
+    # in (io type) and its pool copy out
+    dec_bytes = N * (vis * beta + Hq * D * 2 * esz + 2 * Hkv * D * esz + beta)
     dec_flops = N * 4 * Hq * D * vis
     chunk_union = vis + C - 1                                 # keys a chunk reads
     pre_bytes = N * (chunk_union * beta + C * Hq * D * 2 * esz)
@@ -285,7 +298,7 @@ def run_gpu(args, w):
         dec_bytes=dec_bytes, dec_launches=n_dec, dec_flops=dec_flops,
         merge_ms_avg=ms_mrg / max(n_mrg, 1), append_ms_avg=ms_app / max(n_app, 1),
         pre_gbps=pre_gbps, pre_tflops=pre_tflops, avg_pre_ms=avg_pre, pre_bytes=pre_bytes,
-        copy_gbps=copy_gbps, n_blocks=n_blocks, pool_gb=nbytes / 1e9)
+        copy_gbps=copy_gbps, n_blocks=n_blocks, pool_gb=nbytes / 1e9, kv_dtype=kvd)
     pool.close()
     return res
 
@@ -756,15 +769,18 @@ def main():
             "sinks": w.n_sink, "window": w.window, "block": 16, "chunk": w.chunk[1],
             "decode_steps": w.n_decode[1], "frame_budget_s": w.frame_period_s,
             "steady_state": "every query sees S + W keys", "parallelism": "single GPU",
+            "kv_cache": {"bf16": "bf16", "f32": "fp32",
+                         "fp8": "fp8-e4m3, per-token power-of-two scales"}[res["kv_dtype"]],
         },
         "roofline": {
             "bound": "hbm",
-            "kernel": "decode attention (k_attn_valu)",
+            "kernel": ("decode attention (k_attn_fp8)" if res["kv_dtype"] == "fp8"
+                       else "decode attention (k_attn_valu)"),
             "achieved": round(res["dec_gbps"], 1),
             "peak": HBM_PEAK_GBPS,
             "unit": "GB/s",
             "frac": round(res["dec_gbps"] / HBM_PEAK_GBPS, 4),
-            "traffic": measured_traffic(args.workload),
+            "traffic": measured_traffic(args.workload) if res["kv_dtype"] == w.dtype else None,
             "bytes_per_launch": res["dec_bytes"],
             "avg_launch_ms": round(res["avg_dec_ms"], 4),
             "launches": res["dec_launches"],
