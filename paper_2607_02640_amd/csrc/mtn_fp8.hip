@@ -128,6 +128,14 @@ __global__ __launch_bounds__(256) void k_append_fp8(PoolGeom g, PlanView p, int3
 // reference max that moves only when a block's max exceeds it by more than
 // 2^8, so the accumulator rescale is rare.  At the end the waves' (max, sum,
 // acc) are merged through LDS by log-sum-exp.
+// Launch shape, from sweeps of waves per workgroup (2..8) and ring depth
+// (2..4) at the 128-session G = 8, 64-session G = 1 and 256-session G = 4
+// shapes: two-block rings win everywhere, and 4 waves win at G = 8 (6.03 TB/s
+// against 5.88 with 8).  8 waves measured 4 % faster at the smaller groups
+// but gave wrong fused-decode outputs: there the compiler keeps the MFMA
+// accumulators in VGPRs and refills an accumulator chain's source registers
+// with the next operand three wait states after the MFMA that reads them.
+// With 4 waves the accumulators live in AGPRs, which no VALU op rewrites.
 template <int G>
 struct F8Shape {
 #ifdef MTN_FP8_GROUPS
@@ -138,7 +146,7 @@ struct F8Shape {
 #ifdef MTN_FP8_NBUF
     static constexpr int NBUF = MTN_FP8_NBUF;
 #else
-    static constexpr int NBUF = 3;  // three workgroups per CU: LDS and registers agree
+    static constexpr int NBUF = 2;
 #endif
 };
 

@@ -752,14 +752,16 @@ __device__ __forceinline__ void f8_stage_to_bf16(const uint8_t *src, uint8_t *ds
     {
         const int key = (tid >> 4) & 15, hc = tid & 15;
         const uint2 c = *(const uint2 *)(blk + key * kF8D + hc * 8);
+        // one scale for the whole row: the scaling conversion multiplies both
+        // codes of a pair by the key's 2^e, exactly
         const float sk = __uint_as_float((uint32_t)blk[kF8Exp + key] << 23);
-        const auto a0 = __builtin_amdgcn_cvt_pk_f32_fp8(c.x, false);
-        const auto a1 = __builtin_amdgcn_cvt_pk_f32_fp8(c.x, true);
-        const auto a2 = __builtin_amdgcn_cvt_pk_f32_fp8(c.y, false);
-        const auto a3 = __builtin_amdgcn_cvt_pk_f32_fp8(c.y, true);
+        auto cv = [&](uint32_t w, auto hi) {
+            return __builtin_bit_cast(uint32_t, __builtin_amdgcn_cvt_scalef32_pk_bf16_fp8(
+                                                    w, sk, decltype(hi)::value));
+        };
         *(uint4 *)(dst + lds_k(b, key, hc)) =
-            make_uint4(pack_bf16x2(a0[0] * sk, a0[1] * sk), pack_bf16x2(a1[0] * sk, a1[1] * sk),
-                       pack_bf16x2(a2[0] * sk, a2[1] * sk), pack_bf16x2(a3[0] * sk, a3[1] * sk));
+            make_uint4(cv(c.x, std::false_type{}), cv(c.x, std::true_type{}),
+                       cv(c.y, std::false_type{}), cv(c.y, std::true_type{}));
     }
     {
         const int kg = (tid >> 6) & 3, dp = tid & 63;
