@@ -33,9 +33,10 @@ if ROOT not in sys.path:
 HBM_PEAK_GBPS = 8000.0
 BF16_MFMA_PEAK_TFLOPS = 2500.0
 COPY_PROBE_BYTES = 4 << 30
-# sources of the bf16 decode kernel (the counters go stale when these change)
+# sources of the decode kernel of the 128-session bf16 workload (the counters
+# go stale when these change)
 KERNEL_SRC = [os.path.join(ROOT, "paper_2607_02640_amd", "csrc", f)
-              for f in ("mtn_kernels.hip", "mtn_device.h")]
+              for f in ("mtn_mfma.hip", "mtn_device.h")]
 TRAFFIC_SUMMARY = os.path.join(ROOT, "profiles", "decode_traffic_qwen3omni_128s.json")
 
 
@@ -112,11 +113,11 @@ def traffic_summary(fetch_dir, write_dir):
     kib = COPY_PROBE_BYTES / 1024
     f_copy, _ = avg(fetch_dir, "FETCH_SIZE", "k_copy")
     w_copy, _ = avg(write_dir, "WRITE_SIZE", "k_copy")
-    f_dec, nf = avg(fetch_dir, "FETCH_SIZE", "k_attn_valu")
-    w_dec, nw = avg(write_dir, "WRITE_SIZE", "k_attn_valu")
+    f_dec, nf = avg(fetch_dir, "FETCH_SIZE", "k_attn_mfma")
+    w_dec, nw = avg(write_dir, "WRITE_SIZE", "k_attn_mfma")
     fs, ws = kib / f_copy, kib / w_copy
     out = {
-        "kernel": "k_attn_valu (decode attention), 128-session Qwen3-Omni-shaped workload",
+        "kernel": "k_attn_mfma<bf16> (decode attention), 128-session Qwen3-Omni-shaped workload",
         "kernel_src_sha256_16": kernel_src_hash(),
         "commands": [
             "rocprofv3 --pmc FETCH_SIZE --output-format csv -d " + fetch_dir +
@@ -774,7 +775,9 @@ def main():
         },
         "roofline": {
             "bound": "hbm",
-            "kernel": ("decode attention (k_attn_fp8)" if res["kv_dtype"] == "fp8"
+            "kernel": ("decode attention (k_attn_mfma, fp8 blocks)" if res["kv_dtype"] == "fp8"
+                       else "decode attention (k_attn_mfma, bf16 blocks)"
+                       if w.n_q_heads == 8 * w.n_kv_heads and w.head_dim == 128
                        else "decode attention (k_attn_valu)"),
             "achieved": round(res["dec_gbps"], 1),
             "peak": HBM_PEAK_GBPS,

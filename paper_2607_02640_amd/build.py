@@ -22,7 +22,7 @@ COMMON = [
     "-Wall", "-Wno-unused-function", "-Wno-unused-result",
 ]
 
-SOURCES = ["mtn_host.cpp", "mtn_admission.cpp", "mtn_kernels.hip", "mtn_fp8.hip"]
+SOURCES = ["mtn_host.cpp", "mtn_admission.cpp", "mtn_kernels.hip", "mtn_mfma.hip"]
 
 
 def _run(cmd, verbose):

@@ -68,29 +68,28 @@ __device__ __forceinline__ float shfl_xor_f(float x, int m) {
     return __shfl_xor(x, m, 64);
 }
 
-// Exchange between rows (16-lane groups) with the gfx950 permlane swaps: the
-// two results hold x of row pairs (0,1),(2,3) resp. of the two half-waves,
-// so combining them reduces across the pair.  Pure VALU, no LDS round trip.
-// The second operand is an opaque copy of x: given one value for both
-// operands the compiler folds the two results into one.
-__device__ __forceinline__ unsigned opaque_copy(unsigned x) {
-    unsigned y;
-    asm volatile("v_mov_b32 %0, %1" : "=v"(y) : "v"(x));
-    return y;
+// Exchange between rows (16-lane groups) with the gfx950 permlane swaps.
+// With b a copy of a, `v_permlane16_swap a, b` leaves rows (0, 0, 2, 2) of the
+// input in a and rows (1, 1, 3, 3) in b; `v_permlane32_swap a, b` leaves rows
+// (0, 1, 0, 1) and (2, 3, 2, 3): combining a and b reduces across the pair.
+// Pure VALU, no LDS round trip.  The copy, the swap and explicit wait states
+// on both sides are one asm statement: with the copy issued as separate
+// inline asm three instructions before the swap, rows 1 and 3 of a sum came
+// out wrong (the swap took a stale copy), and the compiler cannot space
+// instructions it does not see.
+template <bool HALF>
+__device__ __forceinline__ void row_swap(unsigned &a, unsigned &b) {
+    if constexpr (HALF)
+        asm volatile("v_mov_b32 %1, %0\n\ts_nop 7\n\tv_permlane32_swap_b32 %0, %1\n\ts_nop 7"
+                     : "+v"(a), "=&v"(b));
+    else
+        asm volatile("v_mov_b32 %1, %0\n\ts_nop 7\n\tv_permlane16_swap_b32 %0, %1\n\ts_nop 7"
+                     : "+v"(a), "=&v"(b));
 }
 template <bool SUM, bool HALF>
 __device__ __forceinline__ float rows_pair(float x) {
-    const unsigned u = __builtin_bit_cast(unsigned, x);
-    unsigned a, b;
-    if constexpr (HALF) {
-        auto r = __builtin_amdgcn_permlane32_swap(u, opaque_copy(u), false, false);
-        a = r[0];
-        b = r[1];
-    } else {
-        auto r = __builtin_amdgcn_permlane16_swap(u, opaque_copy(u), false, false);
-        a = r[0];
-        b = r[1];
-    }
+    unsigned a = __builtin_bit_cast(unsigned, x), b;
+    row_swap<HALF>(a, b);
     const float fa = __builtin_bit_cast(float, a), fb = __builtin_bit_cast(float, b);
     return SUM ? fa + fb : fmaxf(fa, fb);
 }
@@ -265,12 +264,11 @@ __device__ __forceinline__ float vmax2(float a, float b) {
 }
 // max over the four 16-lane rows (lanes with equal lane % 16)
 __device__ __forceinline__ float rows_max(float x) {
-    const unsigned u = __builtin_bit_cast(unsigned, x);
-    auto r = __builtin_amdgcn_permlane16_swap(u, opaque_copy(u), false, false);
-    x = vmax2(__builtin_bit_cast(float, (unsigned)r[0]), __builtin_bit_cast(float, (unsigned)r[1]));
-    const unsigned w = __builtin_bit_cast(unsigned, x);
-    auto q = __builtin_amdgcn_permlane32_swap(w, opaque_copy(w), false, false);
-    return vmax2(__builtin_bit_cast(float, (unsigned)q[0]), __builtin_bit_cast(float, (unsigned)q[1]));
+    unsigned a = __builtin_bit_cast(unsigned, x), b;
+    row_swap<false>(a, b);
+    unsigned c = __builtin_bit_cast(unsigned, vmax2(__builtin_bit_cast(float, a), __builtin_bit_cast(float, b)));
+    row_swap<true>(c, b);
+    return vmax2(__builtin_bit_cast(float, c), __builtin_bit_cast(float, b));
 }
 
 }  // namespace

@@ -450,6 +450,21 @@ AttnArgs attn_args(mtn_pool *P, int32_t layer, const void *q, void *out, float *
     return a;
 }
 
+// bf16 decode kernel: the MFMA kernel (per-wave LDS rings, all heads of a KV
+// group per block on matrix cores) for D = 128 and G = 8, the vector kernel
+// otherwise.  Measured: at the 128-session G = 8 shape 6.63 TB/s against 5.84
+// for the vector kernel; at the 64-session G = 1 and 256-session G = 4 shapes
+// the vector kernel's one-wave workgroups win (6.86 and 6.68 TB/s against
+// 6.61 and 6.53).
+bool use_mfma_bf16(const mtn_pool *P) {
+#ifdef MTN_BF16_DECODE_VALU
+    return false;
+#else
+    return P->cfg.kv_dtype == MTN_BF16 && P->G == 8 &&
+           attn_mfma_bf16_supported(P->cfg.head_dim, P->G);
+#endif
+}
+
 // Decode split heuristic.  A unit (query, kv head, segment) streams its keys
 // through an LDS ring whose pipeline fills at the start and drains at the
 // end, so units should be long, and a partly filled last round of units
@@ -490,6 +505,8 @@ mtn_status decode_impl(mtn_pool *P, int32_t layer, const void *q, void *out, flo
     if (st) return st;
     if (P->cfg.kv_dtype == MTN_FP8_E4M3)
         HIP_TRY(P, launch_attn_fp8(a, s));
+    else if (use_mfma_bf16(P))
+        HIP_TRY(P, launch_attn_mfma_bf16(a, s));
     else
         HIP_TRY(P, launch_attn_valu(P->cfg.kv_dtype, a, s));
     st = timing_end(P, 2, e0, s);
@@ -650,9 +667,9 @@ mtn_status mtn_pool_create(const mtn_pool_config *cfg, void *kv_dev, size_t kv_b
             hipSuccess)
             return bail(e, "cu count");
         P->resident_units =
-            n_cu * (cfg->kv_dtype == MTN_FP8_E4M3
-                        ? attn_fp8_resident_per_cu(P->G)
-                        : attn_valu_resident_per_cu(cfg->kv_dtype, cfg->head_dim, P->G));
+            n_cu * (cfg->kv_dtype == MTN_FP8_E4M3 ? attn_fp8_resident_per_cu(P->G)
+                    : use_mfma_bf16(P)            ? attn_mfma_bf16_resident_per_cu(P->G)
+                                                  : attn_valu_resident_per_cu(cfg->kv_dtype, cfg->head_dim, P->G));
         if ((e = hipStreamSynchronize((hipStream_t)stream)) != hipSuccess)
             return bail(e, "sync");
     }

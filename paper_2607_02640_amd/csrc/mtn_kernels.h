@@ -93,6 +93,11 @@ hipError_t launch_attn_fp8(const AttnArgs &a, hipStream_t s);
 hipError_t launch_poison_fp8(const PoolGeom &g, int32_t n_layers, int64_t n_blocks,
                              const uint16_t *live_mask, hipStream_t s);
 
+// The same MFMA decode over bf16 blocks (D = 128, bf16 io), append fusable.
+bool attn_mfma_bf16_supported(int d, int g);
+int attn_mfma_bf16_resident_per_cu(int g);
+hipError_t launch_attn_mfma_bf16(const AttnArgs &a, hipStream_t s);
+
 bool attn_valu_supported(int dtype, int d, int g);
 // workgroups of the vector attention kernel resident per CU (occupancy query)
 int attn_valu_resident_per_cu(int dtype, int d, int g);

@@ -1,21 +1,22 @@
-// gfx950 kernels of the FP8 KV cache: E4M3 codes with one power-of-two scale
-// per (token, kv head) and tensor.  Fused RoPE + quantize + append, and the
-// decode attention (with or without the append fused in) as MFMA tiles over
-// blocks streamed through LDS.
+// gfx950 MFMA decode attention over KV blocks in bf16 or in FP8 (E4M3 codes
+// with one power-of-two scale per (token, kv head) and tensor), with the
+// append fusable, plus the FP8 pool's fused RoPE + quantize + append and its
+// debug poison.
 //
 // Method: Metronome (arXiv 2607.02640) §4.1 / App. A for what a query sees
 // (sinks ∪ the W positions ending at it, causal).  Per-token KV reduction
 // composes with that bound (§4.1, closing remark; §6): the window bounds how
 // many tokens stay resident, the 8-bit codes how many bytes each one holds.
 //
-// Layout of one (layer, block, kv head) region, D = 128, head stride 4224:
+// FP8 layout of one (layer, block, kv head) region, D = 128, head stride 4224:
 //   [0, 2048)     K codes, [16 keys][128 dims]
 //   [2048, 4096)  V codes in key quads: byte ((key / 4) * 128 + d) * 4 + key % 4
 //   [4096, 4112)  K scale exponents (e + 127), one byte per key
 //   [4112, 4128)  V scale exponents
 // A stored value is code * 2^e; code * 2^e is exact in bf16, so the kernels
 // convert codes to bf16 unscaled and apply the scales to scores (K) and to
-// probabilities (V).
+// probabilities (V).  The bf16 pool keeps its K tile [16][D] and V^T tile
+// [D][16] per region.
 #include "mtn_kernels.h"
 #include "mtn_device.h"
 
@@ -27,8 +28,6 @@
 
 namespace mtn {
 namespace {
-
-typedef __attribute__((ext_vector_type(4))) short s16x4_t;
 
 // smallest e with amax <= 448 * 2^e, clamped to [-126, 127]; 0 for amax = 0
 __device__ __forceinline__ int f8_scale_exp(float amax) {
@@ -52,7 +51,10 @@ __device__ __forceinline__ uint32_t f8_bf16x2(uint32_t w) {
 __device__ __forceinline__ float f8_scale(uint32_t w, int r) {
     return __uint_as_float(((w >> (8 * r)) & 0xFFu) << 23);
 }
-__device__ __forceinline__ f32x4_t mfma16x16x16(const uint2 &a, const uint2 &b, f32x4_t c) {
+typedef __attribute__((ext_vector_type(4))) short s16x4_t;
+// The 16-key PV product: lane (m, g4) brings the 4 keys 4 g4 .. 4 g4 + 3 of
+// both operands (the 16x16x16 MFMA's k slice of the lane).
+__device__ __forceinline__ f32x4_t mfma_pv(const uint2 &a, const uint2 &b, f32x4_t c) {
     return __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(__builtin_bit_cast(s16x4_t, a),
                                                       __builtin_bit_cast(s16x4_t, b), c, 0, 0, 0);
 }
@@ -112,14 +114,15 @@ __global__ __launch_bounds__(256) void k_append_fp8(PoolGeom g, PlanView p, int3
 }
 
 // ---------------------------------------------------------------------------
-// decode attention over fp8 blocks
+// MFMA decode attention over fp8 blocks (F8) or bf16 blocks, D = 128
 // ---------------------------------------------------------------------------
 // One work unit = (query token, kv head, split segment), one workgroup of NG
 // waves; the unit's keys are cut into NG consecutive segments and each wave
 // streams its own segment through its own LDS ring of NBUF blocks (no
 // barrier inside the loop).  Per block, one wave computes all G heads:
-//   S[key][head]  = K[key][:] . Q^T   four 16x16x32 MFMAs (A = K codes as bf16)
-//   O^T[d][head] += V^T[d][key] . P'  eight 16x16x16 MFMAs (A = V codes as bf16)
+//   S[key][head]  = K[key][:] . Q^T   four 16x16x32 MFMAs (A = K as bf16)
+//   O^T[d][head] += V^T[d][key] . P'  eight 16x16x16 MFMAs (A = V as bf16)
+// (fp8 codes convert to bf16 exactly; bf16 blocks are used as they are).
 // Lane l (n = l % 16, g4 = l / 16) holds head n (heads >= G are zero
 // queries): its QK B operand covers dims 32 g4 .. 32 g4 + 31, its scores are
 // keys 4 g4 .. 4 g4 + 3, which is exactly its PV B operand, and its output
@@ -129,38 +132,37 @@ __global__ __launch_bounds__(256) void k_append_fp8(PoolGeom g, PlanView p, int3
 // 2^8, so the accumulator rescale is rare.  At the end the waves' (max, sum,
 // acc) are merged through LDS by log-sum-exp.
 // Launch shape, from sweeps of waves per workgroup (2..8) and ring depth
-// (2..4) at the 128-session G = 8, 64-session G = 1 and 256-session G = 4
-// shapes: two-block rings win everywhere, and 4 waves win at G = 8 (6.03 TB/s
-// against 5.88 with 8).  8 waves measured 4 % faster at the smaller groups
-// but gave wrong fused-decode outputs: there the compiler keeps the MFMA
-// accumulators in VGPRs and refills an accumulator chain's source registers
-// with the next operand three wait states after the MFMA that reads them.
-// With 4 waves the accumulators live in AGPRs, which no VALU op rewrites.
-template <int G>
-struct F8Shape {
-#ifdef MTN_FP8_GROUPS
-    static constexpr int NG = MTN_FP8_GROUPS;
+// (2..4) at the 128-session G = 8 (512 units per launch), 64-session G = 1
+// and 256-session G = 4 (2048 units) shapes: two-block rings win everywhere;
+// 4 waves win at G = 8 (fp8 5.97 TB/s against 5.86 with 8; bf16 6.63 against
+// 6.59), 8 waves at the smaller groups (fp8 6.14-6.21 against 5.79-5.95).
+template <bool F8, int G>
+struct MfmaShape {
+#ifdef MTN_MFMA_GROUPS
+    static constexpr int NG = MTN_MFMA_GROUPS;
 #else
-    static constexpr int NG = 4;
+    static constexpr int NG = G >= 8 ? 4 : 8;
 #endif
-#ifdef MTN_FP8_NBUF
-    static constexpr int NBUF = MTN_FP8_NBUF;
+#ifdef MTN_MFMA_NBUF
+    static constexpr int NBUF = MTN_MFMA_NBUF;
 #else
     static constexpr int NBUF = 2;
 #endif
 };
 
-template <int G, int NG, int NBUF>
-__global__ __launch_bounds__(64 * NG) void k_attn_fp8(AttnArgs a) {
+template <bool F8, int G, int NG, int NBUF>
+__global__ __launch_bounds__(64 * NG) void k_attn_mfma(AttnArgs a) {
     constexpr int D = kF8D;
-    constexpr int BLK = kF8Read;   // one block's ring slot
-    constexpr int NIW = 5;         // DMA instructions per block: 4 x 1 KiB + the 32 exponent bytes
+    // one block's ring slot: fp8 codes + exponents, or the bf16 K and V^T tiles
+    constexpr int BLK = F8 ? kF8Read : 2 * kBlock * D * 2;
+    // DMA instructions per block: 4 x 1 KiB + the 32 exponent bytes, or 8 x 1 KiB
+    constexpr int NIW = F8 ? 5 : 8;
+    constexpr int ESZ = F8 ? 1 : 2;  // bytes per stored element
     static_assert(G >= 1 && G <= 16, "heads per kv group");
     static_assert(NBUF >= 2 && NBUF <= 8, "ring depth");
     static_assert(NBUF * BLK >= 16 * D * 4, "merge scratch fits one wave's ring");
     __shared__ __attribute__((aligned(16))) uint8_t ring[NG][NBUF][BLK];
     __shared__ float sM[NG][16], sL[NG][16];
-    __shared__ __attribute__((aligned(16))) uint8_t snew[2][D];  // newest key / value codes
 
     const int lane = threadIdx.x & 63;
     const int n = lane & 15, g4 = lane >> 4;
@@ -173,8 +175,10 @@ __global__ __launch_bounds__(64 * NG) void k_attn_fp8(AttnArgs a) {
     const int sid = __builtin_amdgcn_readfirstlane(a.p.tok_sid[t]);
     const int pos = __builtin_amdgcn_readfirstlane(a.p.tok_pos[t]);
     const int64_t row = __builtin_amdgcn_readfirstlane(a.p.tok_row[t]);
-    // the wave holding the unit's last segment (which ends at the query's own
-    // position) takes the newest key from the inputs when the append is fused
+    // With a fused append, the wave holding the unit's last segment (which
+    // ends at the query's own position) takes the newest key and value from
+    // the inputs: it writes their stored form into its LDS copy of the last
+    // block, at the token's slot, and into the pool after its last barrier.
     const bool own_new = a.k_new != nullptr && split == a.n_split - 1 && wv == NG - 1;
 
     const VisRange vr = vis_range(g, pos);
@@ -197,9 +201,14 @@ __global__ __launch_bounds__(64 * NG) void k_attn_fp8(AttnArgs a) {
         phys = phys < 0 ? 0 : phys;  // unassigned: any valid block, every slot masked
         const uint8_t *src = head_base + (int64_t)phys * g.block_stride;
         const uint32_t dst = ring0 + (uint32_t)((i % NBUF) * BLK);
+        if constexpr (F8) {
 #pragma unroll
-        for (int j = 0; j < 4; ++j) dma16(src + swz(j * 64 + lane) * 16, dst + j * 1024);
-        if (lane < 2) dma16(src + kF8Exp + lane * 16, dst + kF8Exp);
+            for (int j = 0; j < 4; ++j) dma16(src + swz(j * 64 + lane) * 16, dst + j * 1024);
+            if (lane < 2) dma16(src + kF8Exp + lane * 16, dst + kF8Exp);
+        } else {
+#pragma unroll
+            for (int j = 0; j < 8; ++j) dma16(src + swz(j * 64 + lane) * 16, dst + j * 1024);
+        }
     };
     const int pre = nblk < NBUF - 1 ? nblk : NBUF - 1;
     for (int i = 0; i < pre; ++i) issue(i);
@@ -230,10 +239,9 @@ __global__ __launch_bounds__(64 * NG) void k_attn_fp8(AttnArgs a) {
             qb[s] = make_uint4(w[0], w[1], w[2], w[3]);
         }
     }
-    // The owner rotates and quantizes the newest key and value two dims per
-    // lane (dims d0 + 2 n, d0 + 2 n + 1), publishes the codes in LDS for the
-    // score and value step after the ring loop, and keeps its own two codes
-    // for the pool copy.
+    // The owner rotates (and, fp8, quantizes) the newest key and value two
+    // dims per lane (dims d0 + 2 n, d0 + 2 n + 1), exactly as the append
+    // kernel does.
     uint32_t kc2 = 0, vc2 = 0;
     int ek_new = 0, ev_new = 0;
     const int dd = d0 + 2 * n;
@@ -247,28 +255,58 @@ __global__ __launch_bounds__(64 * NG) void k_attn_fp8(AttnArgs a) {
         const float k0 = fmaf(__uint_as_float(kx << 16), cs.x, sgn * __uint_as_float(ky << 16) * cs.y);
         const float k1 = fmaf(__uint_as_float(kx & 0xFFFF0000u), cs.z,
                               sgn * __uint_as_float(ky & 0xFFFF0000u) * cs.w);
-        const float v0 = __uint_as_float(vx << 16), v1 = __uint_as_float(vx & 0xFFFF0000u);
-        float ak = fmaxf(fabsf(k0), fabsf(k1)), av = fmaxf(fabsf(v0), fabsf(v1));
+        if constexpr (F8) {
+            const float v0 = __uint_as_float(vx << 16), v1 = __uint_as_float(vx & 0xFFFF0000u);
+            float ak = fmaxf(fabsf(k0), fabsf(k1)), av = fmaxf(fabsf(v0), fabsf(v1));
 #pragma unroll
-        for (int m = 1; m < 16; m <<= 1) {  // the 16 lanes of a row, then the rows
-            ak = fmaxf(ak, __shfl_xor(ak, m, 64));
-            av = fmaxf(av, __shfl_xor(av, m, 64));
+            for (int m = 1; m < 16; m <<= 1) {  // the 16 lanes of a row, then the rows
+                ak = fmaxf(ak, __shfl_xor(ak, m, 64));
+                av = fmaxf(av, __shfl_xor(av, m, 64));
+            }
+            ek_new = __builtin_amdgcn_readfirstlane(f8_scale_exp(rows_max(ak)));
+            ev_new = __builtin_amdgcn_readfirstlane(f8_scale_exp(rows_max(av)));
+            kc2 = f8_pack<false>(ldexpf(k0, -ek_new), ldexpf(k1, -ek_new), 0u);
+            vc2 = f8_pack<false>(ldexpf(v0, -ev_new), ldexpf(v1, -ev_new), 0u);
+        } else {
+            kc2 = pack_bf16x2(k0, k1);  // rounded to the stored type as the append does
+            vc2 = vx;
         }
-        ek_new = __builtin_amdgcn_readfirstlane(f8_scale_exp(rows_max(ak)));
-        ev_new = __builtin_amdgcn_readfirstlane(f8_scale_exp(rows_max(av)));
-        kc2 = f8_pack<false>(ldexpf(k0, -ek_new), ldexpf(k1, -ek_new), 0u);
-        vc2 = f8_pack<false>(ldexpf(v0, -ev_new), ldexpf(v1, -ev_new), 0u);
-        *(uint16_t *)&snew[0][dd] = (uint16_t)kc2;
-        *(uint16_t *)&snew[1][dd] = (uint16_t)vc2;
     }
+    const int toff = __builtin_amdgcn_readfirstlane(a.p.tok_off[t]);  // the newest key's slot
+    // the newest token's stored bytes into a ring slot holding its block (the
+    // slot's DMA has landed); chunk x of the block lives at swz(x)
+    auto put_new = [&](uint8_t *blk) {
+        auto at = [&](int byte) { return blk + swz(byte >> 4) * 16 + (byte & 15); };
+        if constexpr (F8) {
+            *(uint16_t *)at(toff * D + dd) = (uint16_t)kc2;
+            const int vb = kF8Tile + ((toff >> 2) * D + dd) * 4 + (toff & 3);
+            *at(vb) = (uint8_t)vc2;
+            *at(vb + 4) = (uint8_t)(vc2 >> 8);
+            if (lane == 0) {
+                blk[kF8Exp + toff] = (uint8_t)(ek_new + 127);
+                blk[kF8Exp + kBlock + toff] = (uint8_t)(ev_new + 127);
+            }
+        } else {
+            *(uint32_t *)at((toff * D + dd) * 2) = kc2;
+            const int vb = kBlock * D * 2 + (dd * kBlock + toff) * 2;  // V^T [D][16]
+            *(uint16_t *)at(vb) = (uint16_t)vc2;
+            *(uint16_t *)at(vb + kBlock * 2) = (uint16_t)(vc2 >> 16);
+        }
+        wave_sync();
+    };
 
     float m_ref = -INFINITY, lsum = 0.f;
     f32x4_t acc[8];
 #pragma unroll
     for (int j = 0; j < 8; ++j) acc[j] = f32x4_t{0.f, 0.f, 0.f, 0.f};
-    // per-lane LDS offsets of the K and V fragments inside a ring slot
-    const int ko0 = swz(8 * n + 2 * g4) * 16, ko1 = swz(8 * n + 2 * g4 + 1) * 16;
-    const int vo0 = swz(128 + 32 * g4 + 2 * n) * 16, vo1 = swz(128 + 32 * g4 + 2 * n + 1) * 16;
+    // per-lane LDS offsets of the K and V fragments inside a ring slot (the
+    // chunk swizzle keeps each 16-lane read phase on 16 distinct bank groups)
+    //   fp8:  K chunks 8 n + 2 g4 (+1); V quads chunks 128 + 32 g4 + 2 n (+1)
+    //   bf16: K chunks 16 n + 4 g4 + s; V^T row 8 n + j, keys 4 g4 .. + 3 at
+    //         chunk 256 + 2 (8 n + j) + g4 / 2, byte 8 (g4 % 2)
+    const int ko0 = F8 ? swz(8 * n + 2 * g4) * 16 : 0, ko1 = F8 ? swz(8 * n + 2 * g4 + 1) * 16 : 0;
+    const int vo0 = F8 ? swz(128 + 32 * g4 + 2 * n) * 16 : 0;
+    const int vo1 = F8 ? swz(128 + 32 * g4 + 2 * n + 1) * 16 : 0;
 
     for (int i = 0; i < nblk; ++i) {
         // block i has landed once at most the blocks issued after it are in flight
@@ -279,28 +317,43 @@ __global__ __launch_bounds__(64 * NG) void k_attn_fp8(AttnArgs a) {
         it_proc.get(&lb, &lo, &hi);
         it_proc.next();
         if (scalar_ld(trow, __builtin_amdgcn_readfirstlane(lb)) < 0) hi = lo;  // unassigned
-        if (own_new && i == nblk - 1 && hi > lo) --hi;  // the newest key comes from registers
+        if (own_new && i == nblk - 1) put_new((uint8_t *)blk);  // slot hi - 1 is the newest key
         const bool full = lo == 0 && hi == kBlock;
 
-        const uint4 k0 = *(const uint4 *)(blk + ko0);
-        const uint4 k1 = *(const uint4 *)(blk + ko1);
-        const uint4 w0 = *(const uint4 *)(blk + vo0);
-        const uint4 w1 = *(const uint4 *)(blk + vo1);
-        const uint32_t eks = *(const uint32_t *)(blk + kF8Exp + 4 * g4);
-        const uint32_t evs = *(const uint32_t *)(blk + kF8Exp + kBlock + 4 * g4);
-
         // QK: S[key][head] for keys 4 g4 + r, head n
-        const uint32_t kw[8] = {k0.x, k0.y, k0.z, k0.w, k1.x, k1.y, k1.z, k1.w};
         f32x4_t c = {0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-        for (int s = 0; s < 4; ++s) {
-            const uint4 af = make_uint4(f8_bf16x2<false>(kw[2 * s]), f8_bf16x2<true>(kw[2 * s]),
-                                        f8_bf16x2<false>(kw[2 * s + 1]), f8_bf16x2<true>(kw[2 * s + 1]));
-            c = mfma16x16x32(af, qb[s], c);
-        }
+        uint2 vw2[8];  // PV A operands (4 keys of dim 8 n + j), bf16 pool
+        uint32_t vw[8];  // the same as fp8 codes
+        uint32_t evs = 0;
         float sc[4];
+        if constexpr (F8) {
+            const uint4 k0 = *(const uint4 *)(blk + ko0);
+            const uint4 k1 = *(const uint4 *)(blk + ko1);
+            const uint4 w0 = *(const uint4 *)(blk + vo0);
+            const uint4 w1 = *(const uint4 *)(blk + vo1);
+            const uint32_t eks = *(const uint32_t *)(blk + kF8Exp + 4 * g4);
+            evs = *(const uint32_t *)(blk + kF8Exp + kBlock + 4 * g4);
+            const uint32_t kw[8] = {k0.x, k0.y, k0.z, k0.w, k1.x, k1.y, k1.z, k1.w};
 #pragma unroll
-        for (int r = 0; r < 4; ++r) sc[r] = c[r] * f8_scale(eks, r);
+            for (int s = 0; s < 4; ++s) {
+                const uint4 af = make_uint4(f8_bf16x2<false>(kw[2 * s]), f8_bf16x2<true>(kw[2 * s]),
+                                            f8_bf16x2<false>(kw[2 * s + 1]), f8_bf16x2<true>(kw[2 * s + 1]));
+                c = mfma16x16x32(af, qb[s], c);
+            }
+            vw[0] = w0.x; vw[1] = w0.y; vw[2] = w0.z; vw[3] = w0.w;
+            vw[4] = w1.x; vw[5] = w1.y; vw[6] = w1.z; vw[7] = w1.w;
+#pragma unroll
+            for (int r = 0; r < 4; ++r) sc[r] = c[r] * f8_scale(eks, r);
+        } else {
+#pragma unroll
+            for (int s = 0; s < 4; ++s)
+                c = mfma16x16x32(*(const uint4 *)(blk + swz(16 * n + 4 * g4 + s) * 16), qb[s], c);
+#pragma unroll
+            for (int j = 0; j < 8; ++j)
+                vw2[j] = *(const uint2 *)(blk + swz(256 + 16 * n + 2 * j + (g4 >> 1)) * 16 + 8 * (g4 & 1));
+#pragma unroll
+            for (int r = 0; r < 4; ++r) sc[r] = c[r];
+        }
         if (!full) {
 #pragma unroll
             for (int r = 0; r < 4; ++r) {
@@ -323,12 +376,13 @@ __global__ __launch_bounds__(64 * NG) void k_attn_fp8(AttnArgs a) {
 #pragma unroll
         for (int r = 0; r < 4; ++r) pv[r] = __builtin_amdgcn_exp2f(sc[r] - mr);
         lsum += (pv[0] + pv[1]) + (pv[2] + pv[3]);
-        // fold the value scales into the probabilities
+        if constexpr (F8) {
+            // fold the value scales into the probabilities
 #pragma unroll
-        for (int r = 0; r < 4; ++r) pv[r] *= f8_scale(evs, r);
-        uint32_t vw[8] = {w0.x, w0.y, w0.z, w0.w, w1.x, w1.y, w1.z, w1.w};
+            for (int r = 0; r < 4; ++r) pv[r] *= f8_scale(evs, r);
+        }
         if (!full) {
-            // invisible slots: zero probability, and zero codes (they may be NaN)
+            // invisible slots: zero probability, and zero values (they may be NaN)
             uint32_t bm = 0;
 #pragma unroll
             for (int r = 0; r < 4; ++r) {
@@ -337,79 +391,53 @@ __global__ __launch_bounds__(64 * NG) void k_attn_fp8(AttnArgs a) {
                 pv[r] = ok ? pv[r] : 0.f;
                 bm |= ok ? (0xFFu << (8 * r)) : 0u;
             }
+            if constexpr (F8) {
 #pragma unroll
-            for (int j = 0; j < 8; ++j) vw[j] &= bm;
-        }
-        const uint2 pb = make_uint2(pack_bf16x2(pv[0], pv[1]), pack_bf16x2(pv[2], pv[3]));
+                for (int j = 0; j < 8; ++j) vw[j] &= bm;
+            } else {
+                // bf16 keys: two bytes of the mask per key
+                const uint32_t m01 = (bm & 0x1u ? 0x0000FFFFu : 0u) | (bm & 0x100u ? 0xFFFF0000u : 0u);
+                const uint32_t m23 = (bm & 0x10000u ? 0x0000FFFFu : 0u) | (bm & 0x1000000u ? 0xFFFF0000u : 0u);
 #pragma unroll
-        for (int j = 0; j < 8; ++j)
-            acc[j] = mfma16x16x16(make_uint2(f8_bf16x2<false>(vw[j]), f8_bf16x2<true>(vw[j])), pb, acc[j]);
-    }
-
-    float L = rows_sum(lsum);
-    if (own_new) {
-        wave_sync();
-        uint32_t kcode[8], vcode[8];  // codes of this lane's dims d0 .. d0 + 31
-        {
-            const uint4 a0 = *(const uint4 *)&snew[0][d0], a1 = *(const uint4 *)&snew[0][d0 + 16];
-            const uint4 b0 = *(const uint4 *)&snew[1][d0], b1 = *(const uint4 *)&snew[1][d0 + 16];
-            kcode[0] = a0.x; kcode[1] = a0.y; kcode[2] = a0.z; kcode[3] = a0.w;
-            kcode[4] = a1.x; kcode[5] = a1.y; kcode[6] = a1.z; kcode[7] = a1.w;
-            vcode[0] = b0.x; vcode[1] = b0.y; vcode[2] = b0.z; vcode[3] = b0.w;
-            vcode[4] = b1.x; vcode[5] = b1.y; vcode[6] = b1.z; vcode[7] = b1.w;
-        }
-        // ---- the newest key: its score for head n (this lane's 32 dims, then
-        // the sum over the four lane rows), one exact online-softmax step
-        float sn = 0.f;
-#pragma unroll
-        for (int s = 0; s < 4; ++s) {
-            const uint32_t qw[4] = {qb[s].x, qb[s].y, qb[s].z, qb[s].w};
-#pragma unroll
-            for (int p2 = 0; p2 < 4; ++p2) {
-                const uint32_t kc = kcode[2 * s + p2 / 2];
-                sn = dot2_bf16(qw[p2], (p2 & 1) ? f8_bf16x2<true>(kc) : f8_bf16x2<false>(kc), sn);
-            }
-        }
-        sn = rows_sum(sn) * __uint_as_float((uint32_t)(ek_new + 127) << 23);
-        const float m_new = fmaxf(m_ref, sn);  // sn is finite
-        const float alpha = __builtin_amdgcn_exp2f(m_ref - m_new);
-        const float pn = __builtin_amdgcn_exp2f(sn - m_new);
-        L = L * alpha + pn;
-        m_ref = m_new;
-        // the PV operand precision: bf16 of p * 2^e_v
-        const float pvn = to_f32(from_f32<bf16_t>(pn * __uint_as_float((uint32_t)(ev_new + 127) << 23)));
-#pragma unroll
-        for (int i = 0; i < 4; ++i) {
-#pragma unroll
-            for (int hw = 0; hw < 2; ++hw) {  // dims d0 + 8 i + 4 hw .. + 3
-                const uint32_t vc = vcode[2 * i + hw];
-                const auto lo2 = __builtin_amdgcn_cvt_pk_f32_fp8(vc, false);
-                const auto hi2 = __builtin_amdgcn_cvt_pk_f32_fp8(vc, true);
-                const float vf[4] = {lo2[0], lo2[1], hi2[0], hi2[1]};
-#pragma unroll
-                for (int q = 0; q < 4; ++q) {
-                    const int j = 4 * hw + q;
-                    acc[j][i] = fmaf(pvn, vf[q], acc[j][i] * alpha);
+                for (int j = 0; j < 8; ++j) {
+                    vw2[j].x &= m01;
+                    vw2[j].y &= m23;
                 }
             }
         }
+        const uint2 pb = make_uint2(pack_bf16x2(pv[0], pv[1]), pack_bf16x2(pv[2], pv[3]));
+#pragma unroll
+        for (int j = 0; j < 8; ++j) {
+            if constexpr (F8)
+                acc[j] = mfma_pv(make_uint2(f8_bf16x2<false>(vw[j]), f8_bf16x2<true>(vw[j])), pb, acc[j]);
+            else
+                acc[j] = mfma_pv(vw2[j], pb, acc[j]);
+        }
     }
+
+    float L = rows_sum(lsum);
 
     // the pool copy of the newest key and value, for later launches; issued
     // after the wave's last barrier (a barrier's release fence would wait for
     // these scattered stores)
     auto store_new = [&]() {
         const int64_t tb = __builtin_amdgcn_readfirstlane(a.p.tok_block[t]);
-        const int toff = __builtin_amdgcn_readfirstlane(a.p.tok_off[t]);
         uint8_t *tile = (uint8_t *)g.kv + (int64_t)a.layer * g.layer_stride + tb * g.block_stride +
                         (int64_t)kvh * g.head_stride;
-        *(uint16_t *)(tile + toff * D + dd) = (uint16_t)kc2;  // K row bytes dd, dd + 1
-        uint8_t *vq = tile + kF8Tile + (toff >> 2) * (4 * D) + (toff & 3);
-        vq[dd * 4] = (uint8_t)vc2;
-        vq[(dd + 1) * 4] = (uint8_t)(vc2 >> 8);
-        if (lane == 0) {
-            tile[kF8Exp + toff] = (uint8_t)(ek_new + 127);
-            tile[kF8Exp + kBlock + toff] = (uint8_t)(ev_new + 127);
+        if constexpr (F8) {
+            *(uint16_t *)(tile + toff * D + dd) = (uint16_t)kc2;  // K row bytes dd, dd + 1
+            uint8_t *vq = tile + kF8Tile + (toff >> 2) * (4 * D) + (toff & 3);
+            vq[dd * 4] = (uint8_t)vc2;
+            vq[(dd + 1) * 4] = (uint8_t)(vc2 >> 8);
+            if (lane == 0) {
+                tile[kF8Exp + toff] = (uint8_t)(ek_new + 127);
+                tile[kF8Exp + kBlock + toff] = (uint8_t)(ev_new + 127);
+            }
+        } else {
+            *(uint32_t *)(tile + (toff * D + dd) * 2) = kc2;  // K row elements dd, dd + 1
+            uint16_t *vt = (uint16_t *)(tile + g.tile_bytes);  // V^T [D][16]
+            vt[dd * kBlock + toff] = (uint16_t)vc2;
+            vt[(dd + 1) * kBlock + toff] = (uint16_t)(vc2 >> 16);
         }
     };
 
@@ -526,23 +554,41 @@ __global__ void k_poison_fp8(PoolGeom g, int32_t n_layers, int64_t n_blocks,
     }
 }
 
-template <int G>
-hipError_t launch_fp8_g(const AttnArgs &a, hipStream_t s) {
-    using S = F8Shape<G>;
+template <bool F8, int G>
+hipError_t launch_mfma_g(const AttnArgs &a, hipStream_t s) {
+    using S = MfmaShape<F8, G>;
     const int64_t units = (int64_t)a.p.n_tok * a.g.hkv * a.n_split;
     if (units == 0) return hipSuccess;
-    hipLaunchKernelGGL((k_attn_fp8<G, S::NG, S::NBUF>), dim3((unsigned)units), dim3(64 * S::NG), 0,
-                       s, a);
+    hipLaunchKernelGGL((k_attn_mfma<F8, G, S::NG, S::NBUF>), dim3((unsigned)units), dim3(64 * S::NG),
+                       0, s, a);
     return hipGetLastError();
 }
-template <int G>
-int resident_fp8_g() {
-    using S = F8Shape<G>;
+template <bool F8, int G>
+int resident_mfma_g() {
+    using S = MfmaShape<F8, G>;
     int n = 0;
-    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, k_attn_fp8<G, S::NG, S::NBUF>, 64 * S::NG,
-                                                     0) != hipSuccess)
+    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, k_attn_mfma<F8, G, S::NG, S::NBUF>,
+                                                     64 * S::NG, 0) != hipSuccess)
         return 1;
     return n > 0 ? n : 1;
+}
+template <bool F8>
+hipError_t launch_mfma(const AttnArgs &a, hipStream_t s) {
+    switch (a.g.hq / a.g.hkv) {
+        case 1: return launch_mfma_g<F8, 1>(a, s);
+        case 2: return launch_mfma_g<F8, 2>(a, s);
+        case 4: return launch_mfma_g<F8, 4>(a, s);
+        default: return launch_mfma_g<F8, 8>(a, s);
+    }
+}
+template <bool F8>
+int resident_mfma(int g) {
+    switch (g) {
+        case 1: return resident_mfma_g<F8, 1>();
+        case 2: return resident_mfma_g<F8, 2>();
+        case 4: return resident_mfma_g<F8, 4>();
+        default: return resident_mfma_g<F8, 8>();
+    }
 }
 
 }  // namespace
@@ -557,13 +603,13 @@ bool attn_fp8_supported(int d, int g) {
     return d == kF8D && (g == 1 || g == 2 || g == 4 || g == 8);
 }
 
-int attn_fp8_resident_per_cu(int g) {
-    switch (g) {
-        case 1: return resident_fp8_g<1>();
-        case 2: return resident_fp8_g<2>();
-        case 4: return resident_fp8_g<4>();
-        default: return resident_fp8_g<8>();
-    }
+int attn_fp8_resident_per_cu(int g) { return resident_mfma<true>(g); }
+
+bool attn_mfma_bf16_supported(int d, int g) { return attn_fp8_supported(d, g); }
+int attn_mfma_bf16_resident_per_cu(int g) { return resident_mfma<false>(g); }
+hipError_t launch_attn_mfma_bf16(const AttnArgs &a, hipStream_t s) {
+    if (!attn_mfma_bf16_supported(a.g.d, a.g.hq / a.g.hkv)) return hipErrorInvalidValue;
+    return launch_mfma<false>(a, s);
 }
 
 hipError_t launch_append_fp8(const PoolGeom &g, const PlanView &p, int32_t layer, const void *k,
@@ -577,14 +623,8 @@ hipError_t launch_append_fp8(const PoolGeom &g, const PlanView &p, int32_t layer
 }
 
 hipError_t launch_attn_fp8(const AttnArgs &a, hipStream_t s) {
-    const int G = a.g.hq / a.g.hkv;
-    if (!attn_fp8_supported(a.g.d, G)) return hipErrorInvalidValue;
-    switch (G) {
-        case 1: return launch_fp8_g<1>(a, s);
-        case 2: return launch_fp8_g<2>(a, s);
-        case 4: return launch_fp8_g<4>(a, s);
-        default: return launch_fp8_g<8>(a, s);
-    }
+    if (!attn_fp8_supported(a.g.d, a.g.hq / a.g.hkv)) return hipErrorInvalidValue;
+    return launch_mfma<true>(a, s);
 }
 
 hipError_t launch_poison_fp8(const PoolGeom &g, int32_t n_layers, int64_t n_blocks,
