@@ -31,7 +31,9 @@ Parity status: pinned (tests/test_fp8_pins.py) against torch's float8_e4m3fn
 conversion (every code, every rounding midpoint, random values), the format's
 closed forms (448, smallest normal / subnormal, ties to even), brute-force
 nearest-value search, the scale rule's closed form, and the error bound of
-quantized attention against the exact float64 oracle.
+quantized attention against the exact float64 oracle.  The rows are encoded
+by ``e4m3_encode_array``, the same steps on arrays, pinned element by element
+against the scalar ``e4m3_encode``.
 """
 from __future__ import annotations
 
@@ -84,6 +86,39 @@ def e4m3_encode(x: float) -> int:
     return sign | ((ex2 + E4M3_BIAS) << 3) | man
 
 
+_DECODE_TABLE = None
+
+
+def e4m3_decode_array(codes: np.ndarray) -> np.ndarray:
+    """e4m3_decode of every code (a lookup in the 256 values it defines)."""
+    global _DECODE_TABLE
+    if _DECODE_TABLE is None:
+        _DECODE_TABLE = np.array([e4m3_decode(c) for c in range(256)], dtype=np.float64)
+    return _DECODE_TABLE[np.asarray(codes, dtype=np.uint8)]
+
+
+def e4m3_encode_array(x: np.ndarray) -> np.ndarray:
+    """e4m3_encode of every element, the same steps on arrays: the binade
+    exponent from frexp, the quantum 2^(e - 3) (2^-9 below the normal range),
+    the ratio rounded half to even (exact: a power-of-two division), then the
+    fields of the rounded magnitude."""
+    x = np.asarray(x, dtype=np.float64)
+    if not np.all(np.isfinite(x)) or np.any(np.abs(x) > E4M3_MAX):
+        raise ValueError("outside the finite E4M3 range")
+    sign = np.where(np.signbit(x), 0x80, 0).astype(np.int64)
+    a = np.abs(x)
+    _, k = np.frexp(a)
+    ex = np.maximum(k - 1, 1 - E4M3_BIAS)
+    mag = np.rint(np.ldexp(a, -(ex - 3))) * np.ldexp(1.0, ex - 3)
+    _, k2 = np.frexp(mag)
+    ex2 = k2 - 1
+    sub = mag < 2.0 ** (1 - E4M3_BIAS)
+    sub_code = np.ldexp(mag, 9).astype(np.int64)
+    norm_code = ((ex2 + E4M3_BIAS) << 3) + (np.ldexp(mag, -(ex2 - 3)).astype(np.int64) - 8)
+    code = np.where(sub, sub_code, norm_code)
+    return (sign | code).astype(np.uint8)
+
+
 def scale_exponent(amax: float) -> int:
     """Smallest e with amax <= 448 * 2^e, clamped to [-126, 127]; 0 for 0."""
     amax = float(amax)
@@ -105,12 +140,11 @@ def quantize_row(x: np.ndarray) -> Tuple[np.ndarray, int]:
     """Codes (uint8[D]) and scale exponent e of one (token, head) row."""
     x = np.asarray(x, dtype=np.float64)
     e = scale_exponent(float(np.max(np.abs(x))) if x.size else 0.0)
-    s = 2.0 ** (-e)
-    return np.array([e4m3_encode(v * s) for v in x], dtype=np.uint8), e
+    return e4m3_encode_array(np.ldexp(x, -e)), e
 
 
 def dequantize_row(codes: np.ndarray, e: int) -> np.ndarray:
-    return np.array([e4m3_decode(c) for c in codes], dtype=np.float64) * 2.0 ** e
+    return e4m3_decode_array(codes) * 2.0 ** e
 
 
 def roundtrip_row(x: np.ndarray, as_float32: bool) -> np.ndarray:

@@ -9,7 +9,8 @@ import pytest
 import torch
 
 from oracle import fp8_kv
-from oracle.fp8_kv import e4m3_decode, e4m3_encode, quantize_row, scale_exponent
+from oracle.fp8_kv import (e4m3_decode, e4m3_decode_array, e4m3_encode, e4m3_encode_array,
+                           quantize_row, scale_exponent)
 from oracle.windowed_attention import OracleSession, rope_rotate
 
 ALL = np.arange(256, dtype=np.uint8)
@@ -53,6 +54,25 @@ def test_encode_matches_torch_on_codes_midpoints_and_random():
     assert np.array_equal(x32.astype(np.float64), np.asarray(vals, np.float64))  # all exact in fp32
     mine = np.array([e4m3_encode(v) for v in vals], np.uint8)
     assert np.array_equal(mine, torch_encode(x32))
+
+
+def test_array_codec_equals_scalar_codec():
+    """The vectorised encoder the oracle's rows use is the scalar definition
+    element by element (and so torch's cast): every code, every midpoint,
+    random and tiny values, signed zeros."""
+    mids = _midpoints()
+    rng = np.random.default_rng(17)
+    vals = ([e4m3_decode(c) for c in FINITE] + mids + [-m for m in mids] + [0.0, -0.0]
+            + list(rng.uniform(-448, 448, 3000)) + list(rng.standard_normal(3000) * 1e-3))
+    x = np.array(vals)
+    got = e4m3_encode_array(x)
+    ref = np.array([e4m3_encode(v) for v in vals], np.uint8)
+    assert np.array_equal(got, ref)
+    dec = e4m3_decode_array(ALL)
+    ok = ~np.isnan(dec)
+    assert np.array_equal(dec[ok], np.array([e4m3_decode(c) for c in ALL])[ok])
+    with pytest.raises(ValueError):
+        e4m3_encode_array(np.array([1.0, 449.0]))
 
 
 # ---- closed forms of the format ---------------------------------------------

@@ -1,6 +1,7 @@
 """Full-size parity at the Qwen3-Omni-shaped workload, in the launch
 configuration the bench times: 128 sessions, 48 layers, GQA 32/4, D = 128,
-bf16, S = 4, W = 4096, 25-token chunks + 16 decodes, pool sized to the exact
+bf16 (and the FP8 KV cache, against the oracle holding the same E4M3 round
+trip), S = 4, W = 4096, 25-token chunks + 16 decodes, pool sized to the exact
 windowed reservation.  Sessions are fast-forwarded to a full window by
 append-only plans, then one whole frame runs through mtn_frame_step.
 Sampled (session, layer) pairs are recomputed one by one by the float64
@@ -21,15 +22,15 @@ def _f64(t):
     return t.detach().to("cpu", torch.float64).numpy()
 
 
-@pytest.mark.parametrize("n_split", [0, 2])
-def test_qwen3_omni_shape_sampled_parity(n_split):
+@pytest.mark.parametrize("dtype,n_split", [("bf16", 0), ("bf16", 2), ("fp8", 0)])
+def test_qwen3_omni_shape_sampled_parity(dtype, n_split):
     N, Lyr, Hq, Hkv, D = W.n_sessions, W.n_layers, W.n_q_heads, W.n_kv_heads, W.head_dim
     C, tau = W.chunk[1], W.n_decode[1]
     R = -(-(W.window + C - 1) // 16) * 16
     n_blocks = N * (-(-W.n_sink // 16) + R // 16)
-    say(f"full-size pool: {n_blocks} blocks, n_split={n_split}")
+    say(f"full-size pool: {n_blocks} blocks, {dtype}, n_split={n_split}")
     pool = make_pool(n_layers=Lyr, hq=Hq, hkv=Hkv, d=D, S=W.n_sink, W=W.window, cmax=C,
-                     max_sessions=N, n_blocks=n_blocks, dtype="bf16", theta=W.rope_theta)
+                     max_sessions=N, n_blocks=n_blocks, dtype=dtype, theta=W.rope_theta)
     sids = [pool.session_open() for _ in range(N)]
     dev = torch.device("cuda")
     bf = torch.bfloat16
@@ -55,7 +56,8 @@ def test_qwen3_omni_shape_sampled_parity(n_split):
     say("frame done; oracle samples")
     worst = 0.0
     for (i, l) in [(0, 0), (77, 23), (127, 47)]:
-        o = wa.OracleSession(Hq, Hkv, D, W.n_sink, W.window, theta=W.rope_theta, n_layers=1)
+        o = wa.OracleSession(Hq, Hkv, D, W.n_sink, W.window, theta=W.rope_theta, n_layers=1,
+                             kv_quant="fp8_e4m3" if dtype == "fp8" else None)
         k_rows = _f64(ff_k[l, i * C:(i + 1) * C])
         v_rows = _f64(ff_v[l, i * C:(i + 1) * C])
         for _ in range(n_ff):
