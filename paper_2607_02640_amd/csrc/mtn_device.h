@@ -211,6 +211,17 @@ __device__ __forceinline__ void dma16(const void *gptr, uint32_t lds) {
         : "v"(gptr), "s"(__builtin_amdgcn_readfirstlane(lds))
         : "memory", "m0");
 }
+// The same copy from a uniform 64-bit base held in SGPRs plus a 32-bit lane
+// offset (the global "saddr" form): a stream whose base changes per block but
+// whose lane offsets stay fixed needs no per-lane 64-bit address arithmetic.
+__device__ __forceinline__ void dma16_s(uint32_t voff, const void *sbase, uint32_t lds) {
+    asm volatile(
+        "s_mov_b32 m0, %2\n\t"
+        "global_load_lds_dwordx4 %0, %1 " MTN_DMA_POLICY
+        :
+        : "v"(voff), "s"(sbase), "s"(__builtin_amdgcn_readfirstlane(lds))
+        : "memory", "m0");
+}
 template <int N>
 __device__ __forceinline__ void vm_wait() {
     asm volatile("s_waitcnt vmcnt(%0)" : : "n"(N) : "memory");

@@ -783,18 +783,17 @@ __device__ __forceinline__ void f8_stage_to_bf16(const uint8_t *src, uint8_t *ds
 }
 
 // F8: the pool holds E4M3 codes.  Each stage then lands as two kF8Read-byte
-// regions (one 1 KiB DMA instruction per wave, plus the 32 exponent bytes
-// from waves 0 and 4), and every stage is converted into one bf16 stage
-// buffer (a second barrier) before the same MFMA stage body runs on it.
+// regions (per block four 1 KiB DMA instructions plus the 32 exponent
+// bytes), and every stage is converted into one of two bf16 stage buffers (a
+// second barrier) before the same MFMA stage body runs on it.
 template <int G, bool F8>
 __global__ __launch_bounds__(64 * kPfWaves) void k_prefill_mfma(PfArgs pa) {
     constexpr int D = 128;
     constexpr int SB = F8 ? 2 * kF8Read : kPfStageBytes;  // bytes of a ring stage
-    constexpr int NIW = F8 ? 1 : kPfStageBytes / 1024 / kPfWaves;  // full DMA instructions per wave per stage
-    static_assert(F8 ? kPfWaves == 8 : NIW * kPfWaves * 1024 == kPfStageBytes, "stage DMA split");
-    static_assert(kPfStages >= 2 && kPfStages <= 8, "ring depth");
+    static_assert(kPfWaves >= 2, "two DMA waves");
+    static_assert(kPfStages >= 3 && kPfStages <= 8, "ring depth (the DMA waits count at most 63)");
     __shared__ __attribute__((aligned(16))) uint8_t ring[kPfStages][SB];
-    __shared__ __attribute__((aligned(16))) uint8_t bfs[F8 ? kPfStageBytes : 16];
+    __shared__ __attribute__((aligned(16))) uint8_t bfs[F8 ? 2 : 1][F8 ? kPfStageBytes : 16];
     const AttnArgs &a = pa.a;
     const PoolGeom &g = a.g;
     // one workgroup per (sequence, row pass, kv head): a long chunk's passes
@@ -862,14 +861,27 @@ __global__ __launch_bounds__(64 * kPfWaves) void k_prefill_mfma(PfArgs pa) {
         return m;
     };
 
-    // per-lane DMA source offsets (fixed for every stage): instruction j of
-    // this wave moves stage bytes [j * 1024, j * 1024 + 1024), block j_b
-    int src_off[NIW];
+    // The DMA of every stage is issued by two waves: wave b (b < 2) moves
+    // block b, the other waves only meet them at the barrier.  Its lane
+    // source offsets inside the block and the LDS offsets of its instructions
+    // inside a ring slot are the same for every stage.  bf16: 4 instructions
+    // for the K tile, 4 for the V^T tile; F8: 4 for the K and V codes, one
+    // 2-lane instruction for the 32 exponent bytes.
+    constexpr int NDI = F8 ? 5 : 8;  // DMA instructions per block
+    const bool dma_wave = wv < 2;
+    const int db = wv & 1;
+    uint32_t dsrc[NDI], ddst[NDI];
 #pragma unroll
-    for (int jj = 0; jj < NIW; ++jj) {
-        int b;
-        src_off[jj] = F8 ? (wv & 3) * 1024 + lane * 16
-                         : stage_src((wv * NIW + jj) * 1024 + lane * 16, &b);
+    for (int j = 0; j < NDI; ++j) {
+        if constexpr (F8) {
+            dsrc[j] = j < 4 ? j * 1024 + lane * 16 : kF8Exp + (lane & 1) * 16;
+            ddst[j] = db * kF8Read + (j < 4 ? j * 1024 : kF8Exp);
+        } else {
+            const int off = j < 4 ? db * 4096 + j * 1024 : 8192 + db * 4096 + (j - 4) * 1024;
+            int bb;
+            dsrc[j] = stage_src(off + lane * 16, &bb);
+            ddst[j] = off;
+        }
     }
     // logical block of virtual block v < nvb (branch-free: sinks, then the ring)
     auto vlb = [&](int v) {
@@ -877,34 +889,21 @@ __global__ __launch_bounds__(64 * kPfWaves) void k_prefill_mfma(PfArgs pa) {
         rb = rb >= ring_blocks ? rb - ring_blocks : rb;
         return v < n_sb ? v : g.n_sink_blocks + rb;
     };
-    // bit 2 (st % kPfStages) + b: block b of stage st holds assigned data.
-    // Every virtual block below nvb holds at least one valid slot.
-    uint32_t have_bits = 0;
-    auto load_phys = [&](int st, int &ph0, int &ph1) {
-        const int va = 2 * st, vb = va + 1;
-        ph0 = scalar_ld(trow, vlb(va));                      // va < nvb always
-        ph1 = vb < nvb ? scalar_ld(trow, vlb(vb)) : -1;
-    };
-    auto issue_dma = [&](int st, int ph0, int ph1) {
-        const bool h0 = ph0 >= 0, h1 = ph1 >= 0;
-        const uint8_t *b0 = h0 ? layer_base + (int64_t)ph0 * g.block_stride : pa.zero_page;
-        const uint8_t *b1 = h1 ? layer_base + (int64_t)ph1 * g.block_stride : pa.zero_page;
-        const int slot = st % kPfStages;
-        have_bits = (have_bits & ~(3u << (2 * slot))) | ((h0 ? 1u : 0u) << (2 * slot)) |
-                    ((h1 ? 2u : 0u) << (2 * slot));
-        const uint32_t dst = ring0 + (uint32_t)(slot * SB);
-        if constexpr (F8) {
-            const int jb = wv >> 2;  // block of this wave's instruction
-            const uint8_t *src = jb ? b1 : b0;
-            const uint32_t bdst = dst + jb * kF8Read;
-            dma16(src + src_off[0], bdst + (wv & 3) * 1024);
-            if ((wv & 3) == 0 && lane < 2) dma16(src + kF8Exp + lane * 16, bdst + kF8Exp);
-        } else {
+    // physical block of virtual block v; -1 past the key union.  Every block
+    // of the union holds appended tokens, so the planner has assigned it.
+    auto phys = [&](int v) { return v < nvb ? scalar_ld(trow, vlb(v)) : -1; };
+    // this wave's block of stage st into the stage's ring slot; stages past
+    // the last (and absent blocks) move the zero page, so every stage costs
+    // a DMA wave the same NDI instructions and its waits are constant
+    auto issue_block = [&](int st, int ph) {
+        const uint8_t *src = ph >= 0 ? layer_base + (int64_t)ph * g.block_stride : pa.zero_page;
+        const uint32_t dst = ring0 + (uint32_t)((st % kPfStages) * SB);
 #pragma unroll
-            for (int jj = 0; jj < NIW; ++jj) {
-                const int j = wv * NIW + jj;  // uniform; block of the instruction below
-                const int jb = j < 8 ? (j >> 2) : ((j - 8) >> 2);
-                dma16((jb ? b1 : b0) + src_off[jj], dst + j * 1024);
+        for (int j = 0; j < NDI; ++j) {
+            if (F8 && j == 4) {
+                if (lane < 2) dma16_s(dsrc[j], src, dst + ddst[j]);
+            } else {
+                dma16_s(dsrc[j], src, dst + ddst[j]);
             }
         }
     };
@@ -925,9 +924,8 @@ __global__ __launch_bounds__(64 * kPfWaves) void k_prefill_mfma(PfArgs pa) {
 
     const int hq0 = kvh * G;
     {
-        // virtual blocks every row of the pass sees whole: sink blocks
-        // [0, fs_hi) and ring blocks [fr_lo, fr_hi) (as virtual indices)
-        const int fs_hi = min(sink_tokens / kBlock, (tq_min + 1) / kBlock);
+        // ring blocks every row of the pass sees whole: [fr_lo, fr_hi) (as
+        // virtual indices)
         int fr_lo, fr_hi;
         {
             // ring block u spans positions ring_p0 + 16u .. + 15; it is whole
@@ -945,12 +943,14 @@ __global__ __launch_bounds__(64 * kPfWaves) void k_prefill_mfma(PfArgs pa) {
             fr_lo = n_sb + ulo;
             fr_hi = n_sb + max(uhi, ulo);
         }
-        auto whole_v = [&](int v) { return v < fs_hi || (v >= fr_lo && v < fr_hi); };
         // ---- per-wave query tiles: rows r = pass_row0 + (wv + kPfWaves i) * 16 + ln16
         uint4 qf[kPfTpw][4];
         f32x4_t acc[kPfTpw][8];
         // row reference max (log2 units) and the row sum of the probabilities,
-        // accumulated by an MFMA against all-ones (every entry = the row sum)
+        // accumulated by an MFMA against all-ones (every entry = the row sum).
+        // The reference starts at the lowest finite float: the first finite
+        // score of a row exceeds it by more than 2^8 and sets it, while
+        // masked (-inf) scores give probability 0 against it.
         float m_ref[kPfTpw];
         f32x4_t l_i[kPfTpw];
         int tq_i[kPfTpw];
@@ -964,7 +964,7 @@ __global__ __launch_bounds__(64 * kPfWaves) void k_prefill_mfma(PfArgs pa) {
             const int j = rv_ ? r / G : 0;
             const int gh = rv_ ? r % G : 0;
             tq_i[i] = pos0 + j;
-            m_ref[i] = -INFINITY;
+            m_ref[i] = -3.402823466e38f;
             l_i[i] = f32x4_t{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
             for (int dt = 0; dt < 8; ++dt) acc[i][dt] = f32x4_t{0.f, 0.f, 0.f, 0.f};
@@ -995,53 +995,64 @@ __global__ __launch_bounds__(64 * kPfWaves) void k_prefill_mfma(PfArgs pa) {
             }
         }
 
-        // One stage: two blocks of keys against every tile of this wave.
-        // FULL stages (every row sees every key) skip all masking.  The
-        // softmax keeps a per-row reference max that moves only when a score
-        // exceeds it by more than 2^8 (probabilities stay <= 256), so the
-        // accumulator rescale is rare; the result is the same softmax.
-        auto stage_body = [&](auto full_c, const uint8_t *sm, int st, uint32_t hb) {
-            constexpr bool FULL = decltype(full_c)::value;
-            constexpr float kLazy = 8.f;
-            int bp0 = 0, blo = 0, bhi = 0;
-            bool bsink = false;
-            if constexpr (!FULL) {
-                const PfBlock m0 = vblock(2 * st), m1 = vblock(2 * st + 1);
-                // values of slots outside a block's valid range may be NaN:
-                // zero them in LDS (512 16-byte V^T chunks: 256 per block)
-                const bool part0 = (hb & 1u) && (m0.lo > 0 || m0.hi < kBlock);
-                const bool part1 = (hb & 2u) && (m1.lo > 0 || m1.hi < kBlock);
-                if (part0 || part1) {
-                    for (int e = tid; e < 512; e += 64 * kPfWaves) {
-                        const int b = e >> 8;
-                        const int d = (e & 255) >> 1, half = e & 1;
-                        const int lo = b ? m1.lo : m0.lo, hi = b ? m1.hi : m0.hi;
-                        if (b ? part1 : part0) {
-                            uint4 *pv = (uint4 *)(sm + lds_v16(b, d, half));
-                            uint4 x = *pv;
-                            uint32_t w[4] = {x.x, x.y, x.z, x.w};
+        // The stage loop is software-pipelined by one stage: iteration st
+        // masks and softmaxes the scores of stage st (computed by the previous
+        // iteration) while the QK MFMAs of stage st + 1 run, then accumulates
+        // PV of stage st.  The softmax keeps a per-row reference max that
+        // moves only when a score exceeds it by more than 2^8 (probabilities
+        // stay <= 256), so the accumulator rescale is rare; the result is the
+        // same softmax.  Whether any lane holds such a score is checked on
+        // the lane's own eight scores; only then is the row max formed across
+        // the four lanes of a row.
+        constexpr float kLazy = 8.f;
+        // the bf16 stage buffer the MFMAs read for stage st
+        auto stage_buf = [&](int st) -> uint8_t * {
+            if constexpr (F8)
+                return &bfs[st & 1][0];
+            else
+                return &ring[st % kPfStages][0];
+        };
+        // FULL stages: both blocks in the key union and inside the ring blocks
+        // every row sees whole
+        const int full_r_lo = (fr_lo + 1) / 2, full_r_hi = min(fr_hi, nvb) / 2;
+        // V^T words of slots outside a block's valid range (they may hold
+        // NaN, and 0 * NaN is NaN) are zeroed in registers: the lane's V
+        // chunk holds slots lkey0 .. lkey0 + 7 of block lblk for one d, two
+        // per dword (the even slot in the low half)
+        auto v_slot_mask = [&](int st, uint32_t (&vm)[4]) {
+            const PfBlock mb = vblock(2 * st + lblk);
 #pragma unroll
-                            for (int q4 = 0; q4 < 4; ++q4) {
-                                const int ka = half * 8 + 2 * q4, kb = ka + 1;
-                                w[q4] &= ((ka >= lo && ka < hi) ? 0x0000FFFFu : 0u) |
-                                         ((kb >= lo && kb < hi) ? 0xFFFF0000u : 0u);
-                            }
-                            *pv = make_uint4(w[0], w[1], w[2], w[3]);
-                        }
-                    }
-                    __syncthreads();
-                }
-                // this lane's eight keys lie in block lblk
-                const PfBlock &mb = lblk ? m1 : m0;
-                const bool hv = lblk ? (hb & 2u) : (hb & 1u);
-                bp0 = mb.p0;
-                bsink = mb.sink;
-                blo = mb.lo;
-                bhi = hv ? mb.hi : mb.lo;
+            for (int q4 = 0; q4 < 4; ++q4) {
+                const int ka = lkey0 + 2 * q4, kb = ka + 1;
+                vm[q4] = ((ka >= mb.lo && ka < mb.hi) ? 0x0000FFFFu : 0u) |
+                         ((kb >= mb.lo && kb < mb.hi) ? 0xFFFF0000u : 0u);
             }
-            // QK, tile by tile (K fragments read once per stage, shared; tiles
-            // past the last row compute on zero queries and are dropped)
-            f32x4_t sa[kPfTpw], sb[kPfTpw];
+        };
+        // lane l holds row ln16 and stage keys 8 lg + r (sa) and 8 lg + 4 + r
+        // (sb), r < 4: slots lkey0 + r and lkey0 + 4 + r of block lblk.
+        // Scores of slots the row's query cannot see become -inf.
+        auto mask_scores = [&](int st, f32x4_t (&sa)[kPfTpw], f32x4_t (&sb)[kPfTpw]) {
+            const PfBlock mb = vblock(2 * st + lblk);
+            const int bp0 = mb.p0, blo = mb.lo, bhi = mb.hi;
+#pragma unroll
+            for (int i = 0; i < kPfTpw; ++i) {
+                // visible slots of the block for query position tq: one range
+                const int tq = tq_i[i];
+                const int wl = g.window < 0 ? -(1 << 30) : tq - g.window + 1;
+                const int vlo = mb.sink ? blo : max(blo, wl - bp0);
+                const int vhi = min(bhi, tq + 1 - bp0);
+#pragma unroll
+                for (int r = 0; r < 4; ++r) {
+                    const int oa = lkey0 + r, ob = oa + 4;
+                    sa[i][r] = (oa >= vlo && oa < vhi) ? sa[i][r] : -INFINITY;
+                    sb[i][r] = (ob >= vlo && ob < vhi) ? sb[i][r] : -INFINITY;
+                }
+            }
+        };
+        // S^T of a stage for every tile of this wave (K fragments read once,
+        // shared by the tiles; tiles past the last row compute on zero
+        // queries and are dropped)
+        auto qk = [&](const uint8_t *sm, f32x4_t (&sa)[kPfTpw], f32x4_t (&sb)[kPfTpw]) {
 #pragma unroll
             for (int i = 0; i < kPfTpw; ++i) {
                 sa[i] = f32x4_t{0.f, 0.f, 0.f, 0.f};
@@ -1057,38 +1068,68 @@ __global__ __launch_bounds__(64 * kPfWaves) void k_prefill_mfma(PfArgs pa) {
                     sb[i] = mfma16x16x32(k1, qf[i][s], sb[i]);
                 }
             }
-            // row max per tile: lane holds row ln16, stage keys 8 lg + e
-            // (e < 8) = slots lkey0 + e of block lblk
-            float sc[kPfTpw][8], mx[kPfTpw];
+        };
+        // ring prologue: stages 0 .. kPfStages - 2 in flight
+        int nph = -1;  // DMA waves: physical block of the next stage to issue
+        if (dma_wave) {
+#pragma unroll
+            for (int st = 0; st < kPfStages - 1; ++st) issue_block(st, phys(2 * st + db));
+            nph = phys(2 * (kPfStages - 1) + db);
+        }
+        f32x4_t sa[kPfTpw], sb[kPfTpw];  // scores of the stage being consumed
+        if (dma_wave) vm_wait<NDI * (kPfStages - 2)>();  // stage 0 landed
+        __syncthreads();
+        if constexpr (F8) {
+            f8_stage_to_bf16(&ring[0][0], stage_buf(0), tid);
+            __syncthreads();
+        }
+        qk(stage_buf(0), sa, sb);
+        // one stage; MASKED: the stage may hold keys some row cannot see
+        auto step = [&](int st, auto masked_c) {
+            constexpr bool MASKED = decltype(masked_c)::value;
+            const uint8_t *sm = stage_buf(st);
+            // V^T chunks of stage st (visible since the previous barrier):
+            // their LDS latency overlaps the wait below
+            uint4 vf[8];
+#pragma unroll
+            for (int dt = 0; dt < 8; ++dt) vf[dt] = *(const uint4 *)(sm + voff + dt * 16 * 32);
+            if constexpr (MASKED) {
+                mask_scores(st, sa, sb);
+                uint32_t vm[4];
+                v_slot_mask(st, vm);
+#pragma unroll
+                for (int dt = 0; dt < 8; ++dt)
+                    vf[dt] = make_uint4(vf[dt].x & vm[0], vf[dt].y & vm[1], vf[dt].z & vm[2], vf[dt].w & vm[3]);
+            }
+            // stage st + 1 landed (a zero-page stage after the last); the
+            // barrier covers both DMA waves and frees the ring slot last read
+            // at st - 1, which takes stage st + kPfStages - 1
+            if (dma_wave) vm_wait<NDI * (kPfStages - 3)>();
+            __syncthreads();
+            if (dma_wave) {
+                const int nst = st + kPfStages - 1;
+                issue_block(nst, nph);
+                nph = phys(2 * (nst + 1) + db);
+            }
+            if constexpr (F8) {
+                // the other bf16 buffer: its stage (st - 1) is consumed
+                f8_stage_to_bf16(&ring[(st + 1) % kPfStages][0], stage_buf(st + 1), tid);
+                __syncthreads();
+            }
+            // lazy reference max: lane-local test, row max only on a bump
+            float m8[kPfTpw];
             bool bump = false;
 #pragma unroll
             for (int i = 0; i < kPfTpw; ++i) {
-#pragma unroll
-                for (int r = 0; r < 4; ++r) {
-                    sc[i][r] = sa[i][r];
-                    sc[i][4 + r] = sb[i][r];
-                }
-                if constexpr (!FULL) {
-                    // visible slots of the block for query position tq: one range
-                    const int tq = tq_i[i];
-                    const int wl = g.window < 0 ? -(1 << 30) : tq - g.window + 1;
-                    const int vlo = bsink ? blo : max(blo, wl - bp0);
-                    const int vhi = min(bhi, tq + 1 - bp0);
-#pragma unroll
-                    for (int e = 0; e < 8; ++e) {
-                        const int o = lkey0 + e;
-                        sc[i][e] = (o >= vlo && o < vhi) ? sc[i][e] : -INFINITY;
-                    }
-                }
-                const float m8 = vmax3(vmax3(sc[i][0], sc[i][1], sc[i][2]),
-                                       vmax3(sc[i][3], sc[i][4], sc[i][5]), vmax2(sc[i][6], sc[i][7]));
-                mx[i] = rows_max(m8);
-                bump = bump || mx[i] > m_ref[i] + kLazy;
+                m8[i] = vmax3(vmax3(sa[i][0], sa[i][1], sa[i][2]), vmax3(sa[i][3], sb[i][0], sb[i][1]),
+                              vmax2(sb[i][2], sb[i][3]));
+                bump = bump || m8[i] > m_ref[i] + kLazy;
             }
             if (__builtin_amdgcn_ballot_w64(bump)) {
 #pragma unroll
                 for (int i = 0; i < kPfTpw; ++i) {
-                    const float mnew = mx[i] > m_ref[i] + kLazy ? mx[i] : m_ref[i];
+                    const float mx = rows_max(m8[i]);
+                    const float mnew = mx > m_ref[i] + kLazy ? mx : m_ref[i];
                     const float alpha = mnew == m_ref[i] ? 1.f : __builtin_amdgcn_exp2f(m_ref[i] - mnew);
                     m_ref[i] = mnew;
                     l_i[i] *= alpha;  // all four entries
@@ -1096,70 +1137,76 @@ __global__ __launch_bounds__(64 * kPfWaves) void k_prefill_mfma(PfArgs pa) {
                     for (int dt = 0; dt < 8; ++dt) acc[i][dt] *= alpha;
                 }
             }
-            // probabilities against the reference, then PV (one 16-byte V^T
-            // chunk per lane per d tile, shared by the tiles)
+            // QK of the next stage (at the last stage it reads a stale
+            // buffer and its scores are dropped), interleaved with this
+            // stage's probabilities: in each of four groups, one MFMA then
+            // two VALU instructions, so the exponentials run while the matrix
+            // core works
+            const uint8_t *nsm = stage_buf(st + 1);
+            uint4 kf[4][2];
+#pragma unroll
+            for (int s = 0; s < 4; ++s) {
+                kf[s][0] = *(const uint4 *)(nsm + koff[s]);
+                kf[s][1] = *(const uint4 *)(nsm + koff[s] + 1024);
+            }
+            f32x4_t na[kPfTpw], nb[kPfTpw];
+            float p[kPfTpw][8];
+            constexpr int kEpg = 2 * kPfTpw;  // probabilities per group
+            const f32x4_t zero4 = f32x4_t{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+            for (int s = 0; s < 4; ++s) {
+#pragma unroll
+                for (int i = 0; i < kPfTpw; ++i) {
+                    na[i] = mfma16x16x32(kf[s][0], qf[i][s], s ? na[i] : zero4);
+                    nb[i] = mfma16x16x32(kf[s][1], qf[i][s], s ? nb[i] : zero4);
+                }
+#pragma unroll
+                for (int u = 0; u < kEpg; ++u) {
+                    const int f = s * kEpg + u, i = f >> 3, e = f & 7;
+                    p[i][e] = __builtin_amdgcn_exp2f((e < 4 ? sa[i][e] : sb[i][e - 4]) - m_ref[i]);
+                }
+#ifndef MTN_PF_NO_SCHED
+                if (s == 0) __builtin_amdgcn_sched_group_barrier(0x100, 8, 0);  // all K reads first
+#pragma unroll
+                for (int k = 0; k < 2 * kPfTpw; ++k) {
+                    __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+                    __builtin_amdgcn_sched_group_barrier(0x002, 2, 0);
+                }
+                __builtin_amdgcn_sched_barrier(0);
+#endif
+            }
             uint4 pb[kPfTpw];
 #pragma unroll
-            for (int i = 0; i < kPfTpw; ++i) {
-                const float mr = FULL ? m_ref[i] : (m_ref[i] == -INFINITY ? 0.f : m_ref[i]);
-#pragma unroll
-                for (int r = 0; r < 8; ++r) sc[i][r] = __builtin_amdgcn_exp2f(sc[i][r] - mr);
-                pb[i] = make_uint4(pack_bf16x2(sc[i][0], sc[i][1]), pack_bf16x2(sc[i][2], sc[i][3]),
-                                   pack_bf16x2(sc[i][4], sc[i][5]), pack_bf16x2(sc[i][6], sc[i][7]));
-            }
+            for (int i = 0; i < kPfTpw; ++i)
+                pb[i] = make_uint4(pack_bf16x2(p[i][0], p[i][1]), pack_bf16x2(p[i][2], p[i][3]),
+                                   pack_bf16x2(p[i][4], p[i][5]), pack_bf16x2(p[i][6], p[i][7]));
             // row sums of the (bf16) probabilities: all-ones A operand
             const uint4 ones = make_uint4(0x3F803F80u, 0x3F803F80u, 0x3F803F80u, 0x3F803F80u);
 #pragma unroll
             for (int i = 0; i < kPfTpw; ++i) l_i[i] = mfma16x16x32(ones, pb[i], l_i[i]);
 #pragma unroll
             for (int dt = 0; dt < 8; ++dt) {
-                const uint4 vf = *(const uint4 *)(sm + voff + dt * 16 * 32);
 #pragma unroll
-                for (int i = 0; i < kPfTpw; ++i) acc[i][dt] = mfma16x16x32(vf, pb[i], acc[i][dt]);
+                for (int i = 0; i < kPfTpw; ++i) acc[i][dt] = mfma16x16x32(vf[dt], pb[i], acc[i][dt]);
+            }
+#pragma unroll
+            for (int i = 0; i < kPfTpw; ++i) {
+                sa[i] = na[i];
+                sb[i] = nb[i];
             }
         };
-
-        const int pre = n_stages < kPfStages - 1 ? n_stages : kPfStages - 1;
-        for (int st = 0; st < pre; ++st) {
-            int ph0, ph1;
-            load_phys(st, ph0, ph1);
-            issue_dma(st, ph0, ph1);
-        }
-        // block-table entries of the next stage to issue, loaded a stage ahead
-        int nx0 = -1, nx1 = -1;
-        if (pre < n_stages) load_phys(pre, nx0, nx1);
-        for (int st = 0; st < n_stages; ++st) {
-            // this wave's share of stage st landed; the barrier covers the other
-            // waves' shares and frees the slot consumed at st - 1
-            const int after = min(kPfStages - 2, n_stages - 1 - st);
-            if constexpr (F8) {
-                if ((wv & 3) == 0)
-                    vm_wait_blocks<2, kPfStages - 2>(after);
-                else
-                    vm_wait_blocks<1, kPfStages - 2>(after);
-            } else {
-                vm_wait_blocks<NIW, kPfStages - 2>(after);
-            }
-            __syncthreads();
-            const uint32_t hb = (have_bits >> (2 * (st % kPfStages))) & 3u;
-            const int nst = st + kPfStages - 1;
-            if (nst < n_stages) {
-                issue_dma(nst, nx0, nx1);
-                if (nst + 1 < n_stages) load_phys(nst + 1, nx0, nx1);
-            }
-            const uint8_t *sm = &ring[st % kPfStages][0];
-            if constexpr (F8) {
-                // the previous stage's readers all passed the barrier above
-                f8_stage_to_bf16(sm, bfs, tid);
-                __syncthreads();
-                sm = bfs;
-            }
-            // every row of the pass sees every key of the stage: no masking
-            if (hb == 3u && whole_v(2 * st) && whole_v(2 * st + 1))
-                stage_body(std::true_type{}, sm, st, hb);
-            else
-                stage_body(std::false_type{}, sm, st, hb);
-        }
+        // the FULL stages inside the whole ring blocks run without masking;
+        // every other stage (sinks, the window's left edge, the causal edge)
+        // takes the masked step (exact for FULL stages too).  Three loops, so
+        // each keeps its scores and accumulators in fixed registers.
+        const int st_a = min(full_r_lo, n_stages);
+        const int st_b = max(st_a, min(full_r_hi, n_stages));
+        int st = 0;
+        for (; st < st_a; ++st) step(st, std::true_type{});
+        for (; st < st_b; ++st) step(st, std::false_type{});
+        for (; st < n_stages; ++st) step(st, std::true_type{});
+        // no DMA may land in LDS after the workgroup has ended
+        if (dma_wave) vm_wait<0>();
 
         // ---- epilogue: normalise and write rows of this pass
 #pragma unroll
