@@ -689,6 +689,9 @@ __global__ void k_copy(const u32x4_t *__restrict__ src, u32x4_t *__restrict__ ds
 #ifndef MTN_PF_STAGES
 #define MTN_PF_STAGES 8
 #endif
+#ifndef MTN_PF_DMA_WAVES
+#define MTN_PF_DMA_WAVES 2
+#endif
 constexpr int kPfWaves = MTN_PF_WAVES;          // waves per workgroup
 constexpr int kPfTpw = MTN_PF_TILES_PER_WAVE;   // 16-row query tiles per wave per pass
 constexpr int kPfRowsPerPass = kPfWaves * kPfTpw * 16;
@@ -861,26 +864,31 @@ __global__ __launch_bounds__(64 * kPfWaves) void k_prefill_mfma(PfArgs pa) {
         return m;
     };
 
-    // The DMA of every stage is issued by two waves: wave b (b < 2) moves
-    // block b, the other waves only meet them at the barrier.  Its lane
-    // source offsets inside the block and the LDS offsets of its instructions
-    // inside a ring slot are the same for every stage.  bf16: 4 instructions
-    // for the K tile, 4 for the V^T tile; F8: 4 for the K and V codes, one
-    // 2-lane instruction for the 32 exponent bytes.
+    // The DMA of every stage is issued by DW waves: wave w < DW moves part
+    // of block w & 1, the other waves only meet them at the barrier.  Lane
+    // source offsets inside the block and the LDS offsets of the
+    // instructions inside a ring slot are the same for every stage.  A block
+    // takes NDI instructions -- bf16: 4 for the K tile, 4 for the V^T tile;
+    // F8: 4 for the K and V codes, one 2-lane instruction for the 32 exponent
+    // bytes -- and wave w issues those k = (w >> 1) + (DW / 2) m, m < NPW.
     constexpr int NDI = F8 ? 5 : 8;  // DMA instructions per block
-    const bool dma_wave = wv < 2;
+    constexpr int DW = F8 ? 2 : MTN_PF_DMA_WAVES;
+    constexpr int NPW = NDI / (DW / 2);  // DMA instructions per DMA wave per stage
+    static_assert(DW >= 2 && DW <= kPfWaves && NPW * (DW / 2) == NDI, "DMA split");
+    const bool dma_wave = wv < DW;
     const int db = wv & 1;
-    uint32_t dsrc[NDI], ddst[NDI];
+    uint32_t dsrc[NPW], ddst[NPW];
 #pragma unroll
-    for (int j = 0; j < NDI; ++j) {
+    for (int m = 0; m < NPW; ++m) {
+        const int j = (wv >> 1) + (DW / 2) * m;
         if constexpr (F8) {
-            dsrc[j] = j < 4 ? j * 1024 + lane * 16 : kF8Exp + (lane & 1) * 16;
-            ddst[j] = db * kF8Read + (j < 4 ? j * 1024 : kF8Exp);
+            dsrc[m] = j < 4 ? j * 1024 + lane * 16 : kF8Exp + (lane & 1) * 16;
+            ddst[m] = db * kF8Read + (j < 4 ? j * 1024 : kF8Exp);
         } else {
             const int off = j < 4 ? db * 4096 + j * 1024 : 8192 + db * 4096 + (j - 4) * 1024;
             int bb;
-            dsrc[j] = stage_src(off + lane * 16, &bb);
-            ddst[j] = off;
+            dsrc[m] = stage_src(off + lane * 16, &bb);
+            ddst[m] = off;
         }
     }
     // logical block of virtual block v < nvb (branch-free: sinks, then the ring)
@@ -894,16 +902,16 @@ __global__ __launch_bounds__(64 * kPfWaves) void k_prefill_mfma(PfArgs pa) {
     auto phys = [&](int v) { return v < nvb ? scalar_ld(trow, vlb(v)) : -1; };
     // this wave's block of stage st into the stage's ring slot; stages past
     // the last (and absent blocks) move the zero page, so every stage costs
-    // a DMA wave the same NDI instructions and its waits are constant
+    // a DMA wave the same NPW instructions and its waits are constant
     auto issue_block = [&](int st, int ph) {
         const uint8_t *src = ph >= 0 ? layer_base + (int64_t)ph * g.block_stride : pa.zero_page;
         const uint32_t dst = ring0 + (uint32_t)((st % kPfStages) * SB);
 #pragma unroll
-        for (int j = 0; j < NDI; ++j) {
-            if (F8 && j == 4) {
-                if (lane < 2) dma16_s(dsrc[j], src, dst + ddst[j]);
+        for (int m = 0; m < NPW; ++m) {
+            if (F8 && m == 4) {
+                if (lane < 2) dma16_s(dsrc[m], src, dst + ddst[m]);
             } else {
-                dma16_s(dsrc[j], src, dst + ddst[j]);
+                dma16_s(dsrc[m], src, dst + ddst[m]);
             }
         }
     };
@@ -1077,7 +1085,7 @@ __global__ __launch_bounds__(64 * kPfWaves) void k_prefill_mfma(PfArgs pa) {
             nph = phys(2 * (kPfStages - 1) + db);
         }
         f32x4_t sa[kPfTpw], sb[kPfTpw];  // scores of the stage being consumed
-        if (dma_wave) vm_wait<NDI * (kPfStages - 2)>();  // stage 0 landed
+        if (dma_wave) vm_wait<NPW * (kPfStages - 2)>();  // stage 0 landed
         __syncthreads();
         if constexpr (F8) {
             f8_stage_to_bf16(&ring[0][0], stage_buf(0), tid);
@@ -1104,7 +1112,7 @@ __global__ __launch_bounds__(64 * kPfWaves) void k_prefill_mfma(PfArgs pa) {
             // stage st + 1 landed (a zero-page stage after the last); the
             // barrier covers both DMA waves and frees the ring slot last read
             // at st - 1, which takes stage st + kPfStages - 1
-            if (dma_wave) vm_wait<NDI * (kPfStages - 3)>();
+            if (dma_wave) vm_wait<NPW * (kPfStages - 3)>();
             __syncthreads();
             if (dma_wave) {
                 const int nst = st + kPfStages - 1;
