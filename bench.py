@@ -53,6 +53,11 @@ def parse():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-layers", type=int, default=48,
                     help="layers of one session-frame the oracle sample covers")
+    ap.add_argument("--cpu-workers", type=int, default=0,
+                    help="oracle baseline processes (0 = the host cores this process may "
+                         "use, at most 16)")
+    ap.add_argument("--cpu-frames", type=int, default=2,
+                    help="consecutive session-frames each oracle process times")
     ap.add_argument("--n-split", type=int, default=0)
     ap.add_argument("--kv-dtype", choices=["bf16", "fp8"], default=None,
                     help="KV cache element type (default: the workload's); fp8 keeps E4M3 "
@@ -685,44 +690,92 @@ def run_recycle(args):
             f.write(json.dumps(out) + "\n")
 
 
-def cpu_baseline(w, n_layers_sample):
-    """The float64 oracle (as it stands) on one session-frame at steady state,
-    restricted to ``n_layers_sample`` layers and scaled to the full depth."""
-    import numpy as np
+def _oracle_frames(job):
+    """One host worker: the float64 oracle (as it stands) fast-forwards one
+    session to steady state (append + prune, no attention), then times
+    ``frames`` consecutive session-frames over ``n_layers_sample`` layers."""
+    wname, n_layers_sample, frames, uid = job
     from threadpoolctl import threadpool_limits
     from oracle import windowed_attention as wa
     from workload import session_rng, draw_qkv
 
+    w = pick(wname)
     C, tau = w.chunk[1], w.n_decode[1]
     Hq, Hkv, D = w.n_q_heads, w.n_kv_heads, w.head_dim
     with threadpool_limits(limits=1):
         o = wa.OracleSession(Hq, Hkv, D, w.n_sink, w.window, theta=w.rope_theta,
                              n_layers=n_layers_sample)
-        rng = session_rng(w.workload_id, 0)
+        rng = session_rng(w.workload_id, uid)
         q, k, v = draw_qkv(rng, n_layers_sample, C, Hq, Hkv, D, w.act_scale)
-        for p in range(-(-steady_len(w) // C)):     # fast-forward: append + prune
+        for p in range(-(-steady_len(w) // C)):
             o.begin(C)
             for l in range(n_layers_sample):
                 o.layer_step(l, q[l], k[l], v[l], attend=False)
             o.commit()
         t0 = time.perf_counter()
-        o.begin(C)
-        for l in range(n_layers_sample):
-            o.layer_step(l, q[l], k[l], v[l])
-        o.commit()
-        for j in range(tau):
-            o.begin(1)
+        for f in range(frames):
+            o.begin(C)
             for l in range(n_layers_sample):
-                o.layer_step(l, q[l, :1], k[l, :1], v[l, :1])
+                o.layer_step(l, q[l], k[l], v[l])
             o.commit()
+            for j in range(tau):
+                o.begin(1)
+                for l in range(n_layers_sample):
+                    o.layer_step(l, q[l, :1], k[l, :1], v[l, :1])
+                o.commit()
         dt = time.perf_counter() - t0
-    per_sf = dt * w.n_layers / n_layers_sample
-    return dict(value=1.0 / per_sf, unit="session-frames/s", cores=1, kind="oracle",
-                sample=(f"1 session x 1 frame ({C}-token chunk + {tau} decodes) x "
-                        f"{n_layers_sample} of {w.n_layers} layers at steady state "
-                        f"(S + W = {w.n_sink + w.window} visible keys), float64 numpy, "
-                        f"1 thread; {dt:.1f}s measured, scaled by {w.n_layers}/{n_layers_sample}"),
-                seconds=dt)
+    return frames, dt
+
+
+def host_cpu_model():
+    try:
+        for line in open("/proc/cpuinfo"):
+            if line.startswith("model name"):
+                return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
+
+
+def cpu_workers_default():
+    try:
+        n = len(os.sched_getaffinity(0))
+    except AttributeError:
+        n = os.cpu_count() or 1
+    return max(1, min(16, n))
+
+
+def start_cpu_pool(n_workers):
+    """Worker processes for the oracle baseline, started from a fork server
+    before this process touches the GPU (the workers never use it)."""
+    import multiprocessing as mp
+    ctx = mp.get_context("forkserver")
+    return ctx.Pool(n_workers)
+
+
+def cpu_baseline(wkey, w, n_layers_sample, pool, n_workers, frames):
+    """The float64 oracle timed on the host cores: ``n_workers`` processes of
+    one thread each, each timing ``frames`` consecutive steady-state
+    session-frames of its own session, restricted to ``n_layers_sample`` layers
+    and scaled to the full depth."""
+    jobs = [(wkey, n_layers_sample, frames, 1 + i) for i in range(n_workers)]
+    t0 = time.perf_counter()
+    res = pool.map(_oracle_frames, jobs) if pool is not None else [_oracle_frames(jobs[0])]
+    wall = time.perf_counter() - t0
+    scale = n_layers_sample / w.n_layers
+    rates = [f * scale / dt for f, dt in res]        # session-frames/s per worker
+    total = sum(rates)
+    dts = [dt for _, dt in res]
+    C, tau = w.chunk[1], w.n_decode[1]
+    return dict(value=total, unit="session-frames/s", cores=len(res), kind="oracle",
+                per_core=total / len(res),
+                sample=(f"{len(res)} processes x 1 thread, each {frames} consecutive "
+                        f"session-frames ({C}-token chunk + {tau} decodes) x {n_layers_sample} "
+                        f"of {w.n_layers} layers of its own session at steady state "
+                        f"(S + W = {w.n_sink + w.window} visible keys), float64 numpy on "
+                        f"{host_cpu_model()}; timed regions {min(dts):.1f}-{max(dts):.1f}s, "
+                        f"scaled by {w.n_layers}/{n_layers_sample}"),
+                seconds=max(dts), wall_seconds=wall)
 
 
 def main():
@@ -745,12 +798,20 @@ def main():
     if args.call:
         call_report(args, w, run_call(args, w))
         return
+    pool = None
+    if not args.no_cpu_baseline:
+        n_workers = args.cpu_workers or cpu_workers_default()
+        pool = start_cpu_pool(n_workers) if n_workers > 1 else None
     res = run_gpu(args, w)
     cpu = None
     if not args.no_cpu_baseline:
-        log("[bench] timing the float64 oracle on the host")
-        cpu = cpu_baseline(w, args.cpu_layers)
-        log(f"[bench] oracle {cpu['value']:.4f} session-frames/s ({cpu['seconds']:.1f}s)")
+        log(f"[bench] timing the float64 oracle on the host ({n_workers} processes)")
+        cpu = cpu_baseline(args.workload, w, args.cpu_layers, pool, n_workers, args.cpu_frames)
+        if pool is not None:
+            pool.close()
+            pool.join()
+        log(f"[bench] oracle {cpu['value']:.4f} session-frames/s "
+            f"({cpu['seconds']:.1f}s per worker, {cpu['cores']} workers)")
     out = {
         "metric": "session-frames/sec and decode-attention HBM GB/s (% of peak) at 128 sessions",
         "value": round(res["sfps"], 2),
@@ -791,6 +852,7 @@ def main():
         "cpu_baseline": None if cpu is None else {k: cpu[k] for k in
                                                   ("value", "unit", "cores", "kind", "sample")},
         "extra": {
+            "cpu_baseline_per_core": None if cpu is None else cpu["per_core"],
             "decode_plus_merge_GBps": round(res["dec_merge_gbps"], 1),
             "merge_ms_avg": round(res["merge_ms_avg"], 4),
             "append_ms_avg": round(res["append_ms_avg"], 4),
