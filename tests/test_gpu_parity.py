@@ -190,3 +190,33 @@ def test_bf16_long_chunks_split_into_row_passes():
     for cl in ([300, 137], [1, 300], [299, 5]):
         h.frame(cl, [2, 1])
     say(f"max err {h.max_err:.2e}")
+
+
+@pytest.mark.parametrize("S,W,cmax,frames", [
+    (4, 300, 40, 14),    # windows wrap; stages every row sees whole run the unmasked loop
+    (20, 300, 33, 12),   # sinks span a whole block and part of the next
+    (0, 200, 25, 12),    # no sinks
+    (16, 1, 9, 6),       # sinks exactly one block, unit window
+    (4, None, 30, 8),    # unbounded: every key stays visible
+])
+def test_bf16_mfma_prefill_edges(S, W, cmax, frames):
+    """The MFMA chunk prefill (bf16, D = 128, G = 8) across the key-union
+    shapes its stage loops split on: masked first and last stages around a run
+    of unmasked ones, sink blocks whole or partial, no sinks, a unit window and
+    the unbounded pool; first chunks of one token give one-stage passes."""
+    say(f"bf16 mfma prefill S={S} W={W} cmax={cmax}")
+    n, hkv, g = 3, 2, 8
+    if W is None:
+        pool = make_pool(n_layers=1, hq=hkv * g, hkv=hkv, d=128, S=S, W=None, cmax=cmax,
+                         max_sessions=n, n_blocks=n * 40, dtype="bf16", max_len=600)
+        h = Harness(pool, n_sessions=n, n_layers=1, hq=hkv * g, hkv=hkv, d=128, S=S, W=None,
+                    dtype="bf16")
+    else:
+        R = -(-(W + cmax - 1) // 16) * 16
+        pool, h = _tiny(dtype="bf16", d=128, hq=hkv * g, hkv=hkv, S=S, W=W, cmax=cmax, n=n,
+                        L=1, blocks=n * (2 + -(-S // 16) + R // 16))
+    rnd = random.Random(S * 1000 + cmax)
+    h.frame([1, cmax, 2], [0, 1, 2])
+    for f in range(frames - 1):
+        h.frame([rnd.randint(1, cmax) for _ in range(n)], [rnd.randint(0, 3) for _ in range(n)])
+    say(f"max err {h.max_err:.2e}")
