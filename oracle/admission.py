@@ -16,7 +16,7 @@ pins check: with bounded KV the latency is a monotone signal of the load and
 the loop settles near N*; when the signal stays flat while resident state
 grows (unbounded KV), the same loop admits every arrival.
 
-Readings (listed in the design doc), since the paper gives the rule but not its
+Readings, since the paper gives the rule but not its
 constants or edge cases:
 
 * "nears the target": the tick's latency is at or above ``target_ms``;

@@ -7,8 +7,7 @@ What it follows (Metronome, arXiv 2607.02640): per-token KV reduction --
 techniques that shrink what each resident token stores -- is orthogonal to the
 window, which bounds which tokens stay resident, and the two compose (§4.1,
 closing remark; §6, "Attention, long context, and KV reduction").  The paper
-fixes no format, so everything below is a reading (each is listed in
-DESIGN.md):
+fixes no format, so everything below is a reading:
 
 * Format: the OCP 8-bit floating-point E4M3 encoding -- sign, 4 exponent bits
   with bias 7, 3 mantissa bits; exponent field 0 holds subnormals

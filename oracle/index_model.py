@@ -19,7 +19,7 @@ What it follows (Metronome, arXiv 2607.02640):
 * §3.1 Eq. 1: under the unbounded policy the pool fills linearly in time; the
   tests compare the exhaustion frame of this model with the equation.
 
-Reading (listed in the design doc): during a chunk of C tokens the query at the
+Reading: during a chunk of C tokens the query at the
 first new position still needs W - 1 older window tokens while the chunk's C
 tokens are being written, so the ring holds R = roundup(W + C_max - 1, block)
 slots.  Positions S .. block-1 of the last sink block are never written (the

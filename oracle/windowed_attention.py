@@ -15,7 +15,7 @@ What it computes (Metronome, arXiv 2607.02640):
 * App. A: visiting the sink keys first (or in any other order) is exact,
   because the softmax is order-invariant; each key counts once.
 
-Readings where the paper is silent or ambiguous (each is listed in the design doc):
+Readings where the paper is silent or ambiguous:
 
 * Window endpoint.  The printed interval [t-W, t] holds W+1 positions.  The
   default reading admits exactly W window keys including t, i.e. (t-W, t], so
