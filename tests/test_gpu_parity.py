@@ -220,3 +220,18 @@ def test_bf16_mfma_prefill_edges(S, W, cmax, frames):
     for f in range(frames - 1):
         h.frame([rnd.randint(1, cmax) for _ in range(n)], [rnd.randint(0, 3) for _ in range(n)])
     say(f"max err {h.max_err:.2e}")
+
+
+def test_calls_on_a_side_stream():
+    """Every launch and plan upload goes on the stream the caller passes: the
+    harness's inputs, the library's work and the outputs all live on a side
+    stream (torch's current stream inside the context)."""
+    say("side stream")
+    pool, h = _tiny(dtype="bf16", d=128, hq=16, hkv=2, S=4, W=60, cmax=12, n=3, L=2, blocks=3 * 7)
+    s = torch.cuda.Stream()
+    rnd = random.Random(11)
+    with torch.cuda.stream(s):
+        for f in range(8):
+            h.frame([rnd.randint(1, 12) for _ in range(3)], [rnd.randint(0, 3) for _ in range(3)],
+                    use_frame_step=(f % 2 == 0))
+    say(f"max err {h.max_err:.2e}")
