@@ -69,6 +69,9 @@ def parse():
     ap.add_argument("--frames", type=int, default=0, help="--call: frames (0 = the workload's)")
     ap.add_argument("--pool-blocks", type=int, default=0,
                     help="--call: pool capacity in blocks (0 = exact windowed reservation)")
+    ap.add_argument("--stagger", type=int, default=1,
+                    help="--call: session start phases staggered over the frame period in "
+                         "this many groups; each group's frames run in its own sub-tick")
     ap.add_argument("--admission", choices=["windowed", "unbounded"], default=None,
                     help="open-system admission ramp: sessions arrive at a fixed rate, an "
                          "AIMD controller on the measured tick latency admits or rejects "
@@ -368,9 +371,16 @@ def run_call(args, w):
     kc_flat = device_bank((rows, Hkv, D), tdt, dev, s0 + 2, w.act_scale)
     vc_flat = device_bank((rows, Hkv, D), tdt, dev, s0 + 3, w.act_scale)
     oc_flat = torch.empty_like(qc_flat)
-    qd = device_bank((Tmax, Lyr, N, Hq, D), tdt, dev, s0 + 4, w.act_scale)
-    kd = device_bank((Tmax, Lyr, N, Hkv, D), tdt, dev, s0 + 5, w.act_scale)
-    vd = device_bank((Tmax, Lyr, N, Hkv, D), tdt, dev, s0 + 6, w.act_scale)
+    # staggered start phases: K groups of sessions, group k served in sub-tick
+    # k of every frame period (its first frame starts k / K of a period late)
+    K = max(1, args.stagger)
+    if N % K:
+        raise SystemExit(f"--stagger {K} must divide the session count {N}")
+    ng = N // K
+    groups = [list(range(k * ng, (k + 1) * ng)) for k in range(K)]
+    qd = device_bank((Tmax, Lyr, ng, Hq, D), tdt, dev, s0 + 4, w.act_scale)
+    kd = device_bank((Tmax, Lyr, ng, Hkv, D), tdt, dev, s0 + 5, w.act_scale)
+    vd = device_bank((Tmax, Lyr, ng, Hkv, D), tdt, dev, s0 + 6, w.act_scale)
     od = torch.empty_like(qd)
 
     def chunk_view(t, tc):
@@ -398,26 +408,32 @@ def run_call(args, w):
         churn = max(1, round(0.02 * N))
         torch.cuda.synchronize()
         log(f"[call] fast-forwarded to mixed lengths (mean {have.mean():.0f} tokens)")
-    evs = [torch.cuda.Event(enable_timing=True) for _ in range(2 * frames)]
+    evs = [torch.cuda.Event(enable_timing=True) for _ in range(2 * frames * K)]
     occ, fail_frame, fail_code = [], None, None
+    n_sub = 0
     stats0 = pool.stats()
     for f in range(frames):
-        if ragged:
-            cl = rng.integers(w.chunk[0], w.chunk[1] + 1, N).tolist()
-            nd = rng.integers(w.n_decode[0], w.n_decode[1] + 1, N).tolist()
-        else:
-            cl, nd = [Cmax] * N, [Tmax] * N
-        tc = sum(cl)
-        evs[2 * f].record()
-        try:
-            pool.frame_step(sids, cl, nd, chunk_view(qc_flat, tc), chunk_view(kc_flat, tc),
-                            chunk_view(vc_flat, tc), chunk_view(oc_flat, tc), qd, kd, vd, od)
-        except mtn.MtnError as e:
-            fail_frame, fail_code = f + 1, e.code
-            log(f"[call] frame {f + 1}: {e}")
-            evs[2 * f + 1].record()
+        for k, grp in enumerate(groups):
+            if ragged:
+                cl = rng.integers(w.chunk[0], w.chunk[1] + 1, ng).tolist()
+                nd = rng.integers(w.n_decode[0], w.n_decode[1] + 1, ng).tolist()
+            else:
+                cl, nd = [Cmax] * ng, [Tmax] * ng
+            tc = sum(cl)
+            evs[2 * n_sub].record()
+            try:
+                pool.frame_step([sids[i] for i in grp], cl, nd, chunk_view(qc_flat, tc),
+                                chunk_view(kc_flat, tc), chunk_view(vc_flat, tc),
+                                chunk_view(oc_flat, tc), qd, kd, vd, od)
+            except mtn.MtnError as e:
+                fail_frame, fail_code = f + 1, e.code
+                log(f"[call] frame {f + 1}: {e}")
+                evs[2 * n_sub + 1].record()
+                break
+            evs[2 * n_sub + 1].record()
+            n_sub += 1
+        if fail_frame is not None:
             break
-        evs[2 * f + 1].record()
         st = pool.stats()
         occ.append(st["assigned"] / st["capacity"])
         if churn:
@@ -429,39 +445,46 @@ def run_call(args, w):
             log(f"[call] frame {f + 1}/{frames}")
     torch.cuda.synchronize()
     done = len(occ)
-    ticks = [evs[2 * f].elapsed_time(evs[2 * f + 1]) for f in range(done)]
+    ticks = [evs[2 * j].elapsed_time(evs[2 * j + 1]) for j in range(done * K)]
     pool.close()
     return dict(ticks=ticks, occupancy=occ, fail_frame=fail_frame, fail_code=fail_code,
-                n_blocks=n_blocks, frames=frames, reserved0=stats0["reserved"])
+                n_blocks=n_blocks, frames=frames, reserved0=stats0["reserved"], stagger=K)
 
 
 def call_report(args, w, r):
+    """Tick statistics of a simulated call.  With K staggered groups a tick is
+    one group's sub-tick and its deadline is its slot, B / K."""
     import numpy as np
+    K = r.get("stagger", 1)
     t = np.array(r["ticks"])
-    buckets = [round(float(np.median(t[i:i + 10])), 3) for i in range(0, len(t), 10)]
+    per10 = 10 * K                                   # ticks in 10 frame periods
+    buckets = [round(float(np.median(t[i:i + per10])), 3) for i in range(0, len(t), per10)]
     fill = None
     if w.window is not None and w.chunk[0] == w.chunk[1]:
         per = w.chunk[1] + w.n_decode[1]
         fill = -(-(w.n_sink + w.window) // per)     # frames until every query sees S + W keys
+    slot_ms = w.frame_period_s * 1e3 / K
     out = {
         "metric": "per-frame tick latency over a simulated call",
-        "workload": w.name, "sessions": w.n_sessions, "frames_run": len(t),
+        "workload": w.name, "sessions": w.n_sessions, "frames_run": len(t) // K,
         "frames_planned": r["frames"], "frame_budget_ms": w.frame_period_s * 1e3,
+        "stagger_groups": K, "sessions_per_tick": w.n_sessions // K, "tick_budget_ms": slot_ms,
         "tick_ms_p50_per_10_frames": buckets,
         "tick_ms_p50": round(float(np.median(t)), 3) if len(t) else None,
         "tick_ms_p99": round(float(np.percentile(t, 99)), 3) if len(t) else None,
         "tick_ms_max": round(float(t.max()), 3) if len(t) else None,
-        "deadline_misses": int((t > w.frame_period_s * 1e3).sum()),
+        "deadline_misses": int((t > slot_ms).sum()),
         "pool_blocks": r["n_blocks"],
         "occupancy_first_last": [round(r["occupancy"][0], 4), round(r["occupancy"][-1], 4)]
         if r["occupancy"] else None,
         "occupancy_per_10_frames": [round(float(x), 4) for x in r["occupancy"][9::10]],
         "pool_exhausted_in_frame": r["fail_frame"],
     }
-    if fill is not None and len(t) > fill + 10:
-        steady = t[fill:]
+    if fill is not None and len(t) > (fill + 10) * K:
+        steady = t[fill * K:]
         mean = float(steady.mean())
-        post = [float(np.median(steady[i:i + 10])) for i in range(0, len(steady) - 9, 10)]
+        post = [float(np.median(steady[i:i + per10]))
+                for i in range(0, len(steady) - per10 + 1, per10)]
         out["window_full_from_frame"] = fill + 1
         out["steady_mean_ms"] = round(mean, 3)
         out["steady_bucket_p50_max_dev_frac"] = round(max(abs(p / mean - 1) for p in post), 4)
