@@ -282,6 +282,14 @@ mtn_status mtn_plan_info(const mtn_pool *pool, int64_t *pos, int32_t *block, int
  * each open session's retained set.  Attention results must not change.       */
 mtn_status mtn_debug_poison_dead(mtn_pool *pool, void *stream);
 
+/* Tuning: query rows per chunk-prefill pass (rows are token x G + group head;
+ * each pass of each kv head is one workgroup that reads the keys its rows can
+ * see).  0 (the default) chooses per plan: 256, or 128 when the plan's 256-row
+ * passes would occupy at most half the GPU's compute units; 128 or 256 fix it.
+ * Takes effect at the next mtn_plan_begin.  Results are the same either way
+ * up to fp32 summation order.  Other values: MTN_ERR_INVALID_ARG.            */
+mtn_status mtn_pool_set_prefill_pass_rows(mtn_pool *pool, int32_t rows);
+
 /* Per-kernel device timing.  When enabled, the library records HIP events
  * around each launch it makes and accumulates per-kernel-class totals;
  * mtn_pool_kernel_times synchronises those events and returns, for classes

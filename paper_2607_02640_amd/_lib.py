@@ -42,7 +42,7 @@ EXPORTS = [
     "mtn_frame_append_kv", "mtn_attend_chunk_prefill", "mtn_attend_decode",
     "mtn_attend_decode_append",
     "mtn_frame_step", "mtn_pool_stats", "mtn_session_info", "mtn_session_block_table",
-    "mtn_plan_info", "mtn_debug_poison_dead", "mtn_pool_set_timing",
+    "mtn_plan_info", "mtn_debug_poison_dead", "mtn_pool_set_timing", "mtn_pool_set_prefill_pass_rows",
     "mtn_pool_kernel_times", "mtn_hbm_copy", "mtn_status_string", "mtn_pool_last_error",
     "mtn_admission_create", "mtn_admission_destroy", "mtn_admission_offer",
     "mtn_admission_release", "mtn_admission_observe", "mtn_admission_get",
@@ -131,6 +131,7 @@ def load() -> C.CDLL:
         "mtn_plan_info": (i32, [vp, P64, P32, P32, i32, P64, P64, P32]),
         "mtn_debug_poison_dead": (i32, [vp, vp]),
         "mtn_pool_set_timing": (i32, [vp, i32]),
+        "mtn_pool_set_prefill_pass_rows": (i32, [vp, i32]),
         "mtn_pool_kernel_times": (i32, [vp, P64, C.POINTER(C.c_double)]),
         "mtn_hbm_copy": (i32, [vp, vp, C.c_size_t, vp]),
         "mtn_admission_create": (i32, [C.POINTER(AdmissionConfig), C.POINTER(vp)]),
@@ -325,6 +326,10 @@ class Pool:
 
     def poison_dead(self, stream=None) -> None:
         self._check(self.lib.mtn_debug_poison_dead(self.h, _stream(stream)), "debug_poison_dead")
+
+    def set_prefill_pass_rows(self, rows: int) -> None:
+        """Query rows per chunk-prefill pass: 0 = per plan, or 128 / 256."""
+        self._check(self.lib.mtn_pool_set_prefill_pass_rows(self.h, rows), "set_prefill_pass_rows")
 
     def set_timing(self, on: bool) -> None:
         self._check(self.lib.mtn_pool_set_timing(self.h, 1 if on else 0), "set_timing")

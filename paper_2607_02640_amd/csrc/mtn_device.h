@@ -214,12 +214,20 @@ __device__ __forceinline__ void dma16(const void *gptr, uint32_t lds) {
 // The same copy from a uniform 64-bit base held in SGPRs plus a 32-bit lane
 // offset (the global "saddr" form): a stream whose base changes per block but
 // whose lane offsets stay fixed needs no per-lane 64-bit address arithmetic.
+// The base must be wave-uniform; it is read from the first lane so that it
+// lives in SGPRs even where the compiler cannot prove it uniform.  The
+// builtin returns int: each half goes through uint32_t, or a low word with
+// bit 31 set would sign-extend into the high word.
 __device__ __forceinline__ void dma16_s(uint32_t voff, const void *sbase, uint32_t lds) {
+    const uint64_t b = (uint64_t)(uintptr_t)sbase;
+    const uint32_t lo = (uint32_t)__builtin_amdgcn_readfirstlane((uint32_t)b);
+    const uint32_t hi = (uint32_t)__builtin_amdgcn_readfirstlane((uint32_t)(b >> 32));
+    const uint64_t sb = (uint64_t)lo | ((uint64_t)hi << 32);
     asm volatile(
         "s_mov_b32 m0, %2\n\t"
         "global_load_lds_dwordx4 %0, %1 " MTN_DMA_POLICY
         :
-        : "v"(voff), "s"(sbase), "s"(__builtin_amdgcn_readfirstlane(lds))
+        : "v"(voff), "s"(sb), "s"(__builtin_amdgcn_readfirstlane(lds))
         : "memory", "m0");
 }
 template <int N>

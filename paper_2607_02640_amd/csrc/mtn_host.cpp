@@ -114,6 +114,9 @@ struct mtn_pool {
     PlanView view{};
     int32_t *d_seq_first = nullptr, *d_seq_ntok = nullptr, *d_pf_items = nullptr;
     int32_t resident_units = 0;    // decode work units resident on the whole GPU
+    int32_t n_cu = 0;              // compute units of the pool's device
+    int32_t pf_rows_cfg = 0;       // chunk-prefill rows per pass: 0 = chosen per plan
+    int32_t pf_rows = 0;           // ... of the open plan
 
     // timing
     bool timing = false;
@@ -327,7 +330,17 @@ mtn_status plan_begin(mtn_pool *P, int32_t n_seq, const int32_t *sids, const int
     P->all_single = (P->max_ntok == 1);
     P->pf_items.clear();
     {
-        const int64_t rpp = prefill_rows_per_pass();
+        // Rows per prefill pass.  Few sequences leave most CUs idle with full
+        // passes (one workgroup per sequence and kv head); then 128-row passes
+        // give each sequence more workgroups (each reading the keys its rows
+        // see), and a pass whose waves hold one tile skips the empty second.
+        int64_t rpp = P->pf_rows_cfg ? P->pf_rows_cfg : prefill_rows_per_pass();
+        if (!P->pf_rows_cfg && P->n_cu > 0) {
+            int64_t wgs = 0;
+            for (int32_t i = 0; i < n_seq; ++i) wgs += ceil_div((int64_t)n_tok[i] * P->G, rpp);
+            if (2 * wgs * P->cfg.n_kv_heads <= P->n_cu && prefill_pass_rows_valid(128)) rpp = 128;
+        }
+        P->pf_rows = (int32_t)rpp;
         for (int32_t i = 0; i < n_seq; ++i)
             for (int64_t p = 0; p * rpp < (int64_t)n_tok[i] * P->G; ++p) {
                 P->pf_items.push_back(i);
@@ -532,7 +545,7 @@ mtn_status prefill_impl(mtn_pool *P, int32_t layer, const void *q, void *out, fl
     if (st) return st;
     if (prefill_mfma_supported(P->cfg.kv_dtype, P->cfg.head_dim, P->G)) {
         HIP_TRY(P, launch_prefill_mfma(P->cfg.kv_dtype, a, P->d_seq_first, P->d_seq_ntok, P->d_pf_items,
-                                       (int32_t)(P->pf_items.size() / 2), P->d_zero, s));
+                                       (int32_t)(P->pf_items.size() / 2), P->pf_rows, P->d_zero, s));
     } else {
         HIP_TRY(P, launch_attn_valu(P->cfg.kv_dtype, a, s));
     }
@@ -631,9 +644,10 @@ mtn_status mtn_pool_create(const mtn_pool_config *cfg, void *kv_dev, size_t kv_b
                                 (hipStream_t)stream)) != hipSuccess)
             return bail(e, "table upload");
         // per plan: 5 T token fields, 2 n_seq sequence fields, 2 U table updates
-        // (U <= T), and 2 per prefill pass (<= T G / 256 + n_seq passes, G <= 8)
+        // (U <= T), and 2 per prefill pass (<= T G / 128 + n_seq passes)
         size_t meta = sizeof(int32_t) * ((size_t)P->max_tok * 7 + 2 * (size_t)cfg->max_sessions +
-                                         2 * ((size_t)P->max_tok / 32 + (size_t)cfg->max_sessions) +
+                                         2 * ((size_t)P->max_tok * P->G / 128 +
+                                              (size_t)cfg->max_sessions) +
                                          64);
         if ((e = hipMalloc(&P->d_meta, meta)) != hipSuccess) return bail(e, "meta");
         for (int i = 0; i < kStages; ++i) {
@@ -666,6 +680,7 @@ mtn_status mtn_pool_create(const mtn_pool_config *cfg, void *kv_dev, size_t kv_b
         if ((e = hipDeviceGetAttribute(&n_cu, hipDeviceAttributeMultiprocessorCount, dev)) !=
             hipSuccess)
             return bail(e, "cu count");
+        P->n_cu = n_cu;
         P->resident_units =
             n_cu * (cfg->kv_dtype == MTN_FP8_E4M3 ? attn_fp8_resident_per_cu(P->G)
                     : use_mfma_bf16(P)            ? attn_mfma_bf16_resident_per_cu(P->G)
@@ -971,6 +986,14 @@ mtn_status mtn_debug_poison_dead(mtn_pool *P, void *stream) {
         HIP_TRY(P, launch_poison(P->cfg.kv_dtype, geom(P), P->cfg.n_layers, P->cfg.n_blocks, d_live, s));
     HIP_TRY(P, hipStreamSynchronize(s));
     HIP_TRY(P, hipFree(d_live));
+    return MTN_OK;
+}
+
+mtn_status mtn_pool_set_prefill_pass_rows(mtn_pool *P, int32_t rows) {
+    if (!P) return MTN_ERR_INVALID_ARG;
+    if (rows != 0 && !prefill_pass_rows_valid(rows))
+        return fail(P, MTN_ERR_INVALID_ARG, "prefill pass rows must be 0, 128 or 256");
+    P->pf_rows_cfg = rows;
     return MTN_OK;
 }
 

@@ -704,6 +704,7 @@ struct PfArgs {
     const int32_t *seq_ntok;
     const int32_t *items;      // (sequence, row pass) pairs: one workgroup row each
     const uint8_t *zero_page;  // 16 KiB of zeros: the DMA source of absent blocks
+    int32_t pass_rows;         // query rows per pass: 128 or kPfRowsPerPass
 };
 
 // LDS layout of one stage: K tiles of blocks 0, 1 (the 16-byte chunks of a
@@ -814,10 +815,11 @@ __global__ __launch_bounds__(64 * kPfWaves) void k_prefill_mfma(PfArgs pa) {
     const int sid = __builtin_amdgcn_readfirstlane(a.p.tok_sid[tok0]);
     const int pos0 = __builtin_amdgcn_readfirstlane(a.p.tok_pos[tok0]);
     const int n_rows = ntok * G;
-    const int pass_row0 = pass * kPfRowsPerPass;
+    const int pass_row0 = pass * pa.pass_rows;
+    const int pass_end = min(n_rows, pass_row0 + pa.pass_rows);  // rows [pass_row0, pass_end)
     // query positions spanned by this pass's rows
     const int tq_min = pos0 + pass_row0 / G;
-    const int tq_max = pos0 + (min(n_rows, pass_row0 + kPfRowsPerPass) - 1) / G;
+    const int tq_max = pos0 + (pass_end - 1) / G;
     const int32_t *trow = g.table + (int64_t)sid * g.row_len;
     const uint8_t *layer_base = g.kv + (int64_t)a.layer * g.layer_stride + (int64_t)kvh * g.head_stride;
     const uint32_t ring0 = lds_addr(&ring[0][0]);
@@ -966,9 +968,9 @@ __global__ __launch_bounds__(64 * kPfWaves) void k_prefill_mfma(PfArgs pa) {
 #pragma unroll
         for (int i = 0; i < kPfTpw; ++i) {
             const int tile0 = pass_row0 + (wv + kPfWaves * i) * 16;
-            live[i] = tile0 < n_rows;
+            live[i] = tile0 < pass_end;
             const int r = tile0 + ln16;
-            const bool rv_ = r < n_rows;
+            const bool rv_ = r < pass_end;
             const int j = rv_ ? r / G : 0;
             const int gh = rv_ ? r % G : 0;
             tq_i[i] = pos0 + j;
@@ -1039,11 +1041,13 @@ __global__ __launch_bounds__(64 * kPfWaves) void k_prefill_mfma(PfArgs pa) {
         // lane l holds row ln16 and stage keys 8 lg + r (sa) and 8 lg + 4 + r
         // (sb), r < 4: slots lkey0 + r and lkey0 + 4 + r of block lblk.
         // Scores of slots the row's query cannot see become -inf.
-        auto mask_scores = [&](int st, f32x4_t (&sa)[kPfTpw], f32x4_t (&sb)[kPfTpw]) {
+        auto mask_scores = [&](auto nt_c, int st, f32x4_t (&sa)[kPfTpw], f32x4_t (&sb)[kPfTpw])
+                               __attribute__((always_inline)) {
+            constexpr int NT = decltype(nt_c)::value;
             const PfBlock mb = vblock(2 * st + lblk);
             const int bp0 = mb.p0, blo = mb.lo, bhi = mb.hi;
 #pragma unroll
-            for (int i = 0; i < kPfTpw; ++i) {
+            for (int i = 0; i < NT; ++i) {
                 // visible slots of the block for query position tq: one range
                 const int tq = tq_i[i];
                 const int wl = g.window < 0 ? -(1 << 30) : tq - g.window + 1;
@@ -1060,9 +1064,11 @@ __global__ __launch_bounds__(64 * kPfWaves) void k_prefill_mfma(PfArgs pa) {
         // S^T of a stage for every tile of this wave (K fragments read once,
         // shared by the tiles; tiles past the last row compute on zero
         // queries and are dropped)
-        auto qk = [&](const uint8_t *sm, f32x4_t (&sa)[kPfTpw], f32x4_t (&sb)[kPfTpw]) {
+        auto qk = [&](auto nt_c, const uint8_t *sm, f32x4_t (&sa)[kPfTpw], f32x4_t (&sb)[kPfTpw])
+                      __attribute__((always_inline)) {
+            constexpr int NT = decltype(nt_c)::value;
 #pragma unroll
-            for (int i = 0; i < kPfTpw; ++i) {
+            for (int i = 0; i < NT; ++i) {
                 sa[i] = f32x4_t{0.f, 0.f, 0.f, 0.f};
                 sb[i] = f32x4_t{0.f, 0.f, 0.f, 0.f};
             }
@@ -1071,7 +1077,7 @@ __global__ __launch_bounds__(64 * kPfWaves) void k_prefill_mfma(PfArgs pa) {
                 const uint4 k0 = *(const uint4 *)(sm + koff[s]);
                 const uint4 k1 = *(const uint4 *)(sm + koff[s] + 1024);
 #pragma unroll
-                for (int i = 0; i < kPfTpw; ++i) {
+                for (int i = 0; i < NT; ++i) {
                     sa[i] = mfma16x16x32(k0, qf[i][s], sa[i]);
                     sb[i] = mfma16x16x32(k1, qf[i][s], sb[i]);
                 }
@@ -1091,9 +1097,9 @@ __global__ __launch_bounds__(64 * kPfWaves) void k_prefill_mfma(PfArgs pa) {
             f8_stage_to_bf16(&ring[0][0], stage_buf(0), tid);
             __syncthreads();
         }
-        qk(stage_buf(0), sa, sb);
         // one stage; MASKED: the stage may hold keys some row cannot see
-        auto step = [&](int st, auto masked_c) {
+        auto step = [&](auto nt_c, int st, auto masked_c) __attribute__((always_inline)) {
+            constexpr int NT = decltype(nt_c)::value;
             constexpr bool MASKED = decltype(masked_c)::value;
             const uint8_t *sm = stage_buf(st);
             // V^T chunks of stage st (visible since the previous barrier):
@@ -1102,7 +1108,7 @@ __global__ __launch_bounds__(64 * kPfWaves) void k_prefill_mfma(PfArgs pa) {
 #pragma unroll
             for (int dt = 0; dt < 8; ++dt) vf[dt] = *(const uint4 *)(sm + voff + dt * 16 * 32);
             if constexpr (MASKED) {
-                mask_scores(st, sa, sb);
+                mask_scores(nt_c, st, sa, sb);
                 uint32_t vm[4];
                 v_slot_mask(st, vm);
 #pragma unroll
@@ -1128,14 +1134,14 @@ __global__ __launch_bounds__(64 * kPfWaves) void k_prefill_mfma(PfArgs pa) {
             float m8[kPfTpw];
             bool bump = false;
 #pragma unroll
-            for (int i = 0; i < kPfTpw; ++i) {
+            for (int i = 0; i < NT; ++i) {
                 m8[i] = vmax3(vmax3(sa[i][0], sa[i][1], sa[i][2]), vmax3(sa[i][3], sb[i][0], sb[i][1]),
                               vmax2(sb[i][2], sb[i][3]));
                 bump = bump || m8[i] > m_ref[i] + kLazy;
             }
             if (__builtin_amdgcn_ballot_w64(bump)) {
 #pragma unroll
-                for (int i = 0; i < kPfTpw; ++i) {
+                for (int i = 0; i < NT; ++i) {
                     const float mx = rows_max(m8[i]);
                     const float mnew = mx > m_ref[i] + kLazy ? mx : m_ref[i];
                     const float alpha = mnew == m_ref[i] ? 1.f : __builtin_amdgcn_exp2f(m_ref[i] - mnew);
@@ -1159,12 +1165,12 @@ __global__ __launch_bounds__(64 * kPfWaves) void k_prefill_mfma(PfArgs pa) {
             }
             f32x4_t na[kPfTpw], nb[kPfTpw];
             float p[kPfTpw][8];
-            constexpr int kEpg = 2 * kPfTpw;  // probabilities per group
+            constexpr int kEpg = 2 * NT;  // probabilities per group
             const f32x4_t zero4 = f32x4_t{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
             for (int s = 0; s < 4; ++s) {
 #pragma unroll
-                for (int i = 0; i < kPfTpw; ++i) {
+                for (int i = 0; i < NT; ++i) {
                     na[i] = mfma16x16x32(kf[s][0], qf[i][s], s ? na[i] : zero4);
                     nb[i] = mfma16x16x32(kf[s][1], qf[i][s], s ? nb[i] : zero4);
                 }
@@ -1176,7 +1182,7 @@ __global__ __launch_bounds__(64 * kPfWaves) void k_prefill_mfma(PfArgs pa) {
 #ifndef MTN_PF_NO_SCHED
                 if (s == 0) __builtin_amdgcn_sched_group_barrier(0x100, 8, 0);  // all K reads first
 #pragma unroll
-                for (int k = 0; k < 2 * kPfTpw; ++k) {
+                for (int k = 0; k < 2 * NT; ++k) {
                     __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
                     __builtin_amdgcn_sched_group_barrier(0x002, 2, 0);
                 }
@@ -1185,20 +1191,20 @@ __global__ __launch_bounds__(64 * kPfWaves) void k_prefill_mfma(PfArgs pa) {
             }
             uint4 pb[kPfTpw];
 #pragma unroll
-            for (int i = 0; i < kPfTpw; ++i)
+            for (int i = 0; i < NT; ++i)
                 pb[i] = make_uint4(pack_bf16x2(p[i][0], p[i][1]), pack_bf16x2(p[i][2], p[i][3]),
                                    pack_bf16x2(p[i][4], p[i][5]), pack_bf16x2(p[i][6], p[i][7]));
             // row sums of the (bf16) probabilities: all-ones A operand
             const uint4 ones = make_uint4(0x3F803F80u, 0x3F803F80u, 0x3F803F80u, 0x3F803F80u);
 #pragma unroll
-            for (int i = 0; i < kPfTpw; ++i) l_i[i] = mfma16x16x32(ones, pb[i], l_i[i]);
+            for (int i = 0; i < NT; ++i) l_i[i] = mfma16x16x32(ones, pb[i], l_i[i]);
 #pragma unroll
             for (int dt = 0; dt < 8; ++dt) {
 #pragma unroll
-                for (int i = 0; i < kPfTpw; ++i) acc[i][dt] = mfma16x16x32(vf[dt], pb[i], acc[i][dt]);
+                for (int i = 0; i < NT; ++i) acc[i][dt] = mfma16x16x32(vf[dt], pb[i], acc[i][dt]);
             }
 #pragma unroll
-            for (int i = 0; i < kPfTpw; ++i) {
+            for (int i = 0; i < NT; ++i) {
                 sa[i] = na[i];
                 sb[i] = nb[i];
             }
@@ -1209,10 +1215,20 @@ __global__ __launch_bounds__(64 * kPfWaves) void k_prefill_mfma(PfArgs pa) {
         // each keeps its scores and accumulators in fixed registers.
         const int st_a = min(full_r_lo, n_stages);
         const int st_b = max(st_a, min(full_r_hi, n_stages));
-        int st = 0;
-        for (; st < st_a; ++st) step(st, std::true_type{});
-        for (; st < st_b; ++st) step(st, std::false_type{});
-        for (; st < n_stages; ++st) step(st, std::true_type{});
+        // NT: this wave's live tiles.  A wave whose second tile lies past the
+        // pass's rows skips its MFMAs and exponentials; every wave still runs
+        // the same barriers and DMA turns.
+        auto run = [&](auto nt_c) __attribute__((always_inline)) {
+            qk(nt_c, stage_buf(0), sa, sb);
+            int st = 0;
+            for (; st < st_a; ++st) step(nt_c, st, std::true_type{});
+            for (; st < st_b; ++st) step(nt_c, st, std::false_type{});
+            for (; st < n_stages; ++st) step(nt_c, st, std::true_type{});
+        };
+        if (kPfTpw == 1 || !live[kPfTpw - 1])
+            run(std::integral_constant<int, 1>{});
+        else
+            run(std::integral_constant<int, kPfTpw>{});
         // no DMA may land in LDS after the workgroup has ended
         if (dma_wave) vm_wait<0>();
 
@@ -1222,7 +1238,7 @@ __global__ __launch_bounds__(64 * kPfWaves) void k_prefill_mfma(PfArgs pa) {
             if (!live[i]) continue;
             const float lt = l_i[i][0];
             const int r = pass_row0 + (wv + kPfWaves * i) * 16 + ln16;
-            if (r >= n_rows) continue;
+            if (r >= pass_end) continue;
             const int j = r / G, gh = r % G;
             const int t = tok0 + j;
             const int64_t row = a.p.tok_row[t];
@@ -1354,6 +1370,9 @@ hipError_t launch_merge(int dtype, const AttnArgs &a, hipStream_t s) {
 }
 
 int prefill_rows_per_pass() { return kPfRowsPerPass; }
+// a pass covers a whole number of wave tiles of every wave: 128 rows (one
+// tile per wave) or the full kPfRowsPerPass
+bool prefill_pass_rows_valid(int rows) { return rows == kPfRowsPerPass || rows == kPfWaves * 16; }
 
 template <bool F8>
 void launch_prefill_g(int G, dim3 grid, dim3 block, hipStream_t s, const PfArgs &pa) {
@@ -1367,11 +1386,12 @@ void launch_prefill_g(int G, dim3 grid, dim3 block, hipStream_t s, const PfArgs 
 
 hipError_t launch_prefill_mfma(int dtype, const AttnArgs &a, const int32_t *seq_first,
                                const int32_t *seq_ntok, const int32_t *items, int32_t n_items,
-                               const uint8_t *zero_page, hipStream_t s) {
+                               int32_t pass_rows, const uint8_t *zero_page, hipStream_t s) {
     const int G = a.g.hq / a.g.hkv;
-    if (!prefill_mfma_supported(dtype, a.g.d, G) || n_items <= 0 || !zero_page || !items)
+    if (!prefill_mfma_supported(dtype, a.g.d, G) || n_items <= 0 || !zero_page || !items ||
+        !prefill_pass_rows_valid(pass_rows))
         return hipErrorInvalidValue;
-    PfArgs pa{a, seq_first, seq_ntok, items, zero_page};
+    PfArgs pa{a, seq_first, seq_ntok, items, zero_page, pass_rows};
     dim3 grid((unsigned)(n_items * a.g.hkv)), block(64 * kPfWaves);
     if (dtype == 2)
         launch_prefill_g<true>(G, grid, block, s, pa);

@@ -170,3 +170,16 @@ def test_windowed_admission_counts_pinned_blocks():
     assert e.value.code == mtn.MTN_ERR_POOL_EXHAUSTED
     pool.session_close(0)
     assert pool.session_open() == 0
+
+
+def test_prefill_pass_rows_setting():
+    """The tuning hook takes 0 (per plan), 128 or 256 and refuses the rest
+    without changing the pool."""
+    pool = mtn.Pool(n_layers=1, n_q_heads=8, n_kv_heads=2, head_dim=128, n_sink=4, window=64,
+                    max_chunk=8, max_sessions=2, n_blocks=12, dtype="bf16", host_only=True)
+    for rows in (0, 128, 256, 0):
+        pool.set_prefill_pass_rows(rows)
+    for rows in (-1, 1, 64, 192, 512):
+        with pytest.raises(mtn.MtnError) as e:
+            pool.set_prefill_pass_rows(rows)
+        assert e.value.code == mtn.MTN_ERR_INVALID_ARG

@@ -235,3 +235,23 @@ def test_calls_on_a_side_stream():
             h.frame([rnd.randint(1, 12) for _ in range(3)], [rnd.randint(0, 3) for _ in range(3)],
                     use_frame_step=(f % 2 == 0))
     say(f"max err {h.max_err:.2e}")
+
+
+@pytest.mark.parametrize("dtype", ["bf16", "fp8"])
+@pytest.mark.parametrize("rows", [128, 256])
+def test_prefill_pass_rows(dtype, rows):
+    """Chunk prefill with 128- and with 256-row passes (G = 8: chunks of up
+    to 40 tokens are up to 320 rows, so both sizes give one or more passes,
+    some with waves whose second tile lies past the pass) against the
+    oracle."""
+    say(f"prefill pass rows {rows} {dtype}")
+    S, W, C, n, hkv = 4, 120, 40, 3, 2
+    R = -(-(W + C - 1) // 16) * 16
+    pool = make_pool(n_layers=1, hq=8 * hkv, hkv=hkv, d=128, S=S, W=W, cmax=C, max_sessions=n,
+                     n_blocks=n * (1 + R // 16), dtype=dtype)
+    pool.set_prefill_pass_rows(rows)
+    h = Harness(pool, n_sessions=n, n_layers=1, hq=8 * hkv, hkv=hkv, d=128, S=S, W=W, dtype=dtype)
+    rnd = random.Random(rows)
+    for f in range(8):
+        h.frame([rnd.randint(1, C) for _ in range(n)], [rnd.randint(0, 2) for _ in range(n)])
+    say(f"max err {h.max_err:.2e}")
