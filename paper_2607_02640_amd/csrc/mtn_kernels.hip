@@ -665,7 +665,8 @@ __global__ void k_copy(const u32x4_t *__restrict__ src, u32x4_t *__restrict__ ds
 }
 
 // ---------------------------------------------------------------------------
-// MFMA chunk prefill (bf16, D = 128): one workgroup per (sequence, kv head)
+// MFMA chunk prefill (bf16 or fp8 pool, D = 128): one workgroup per
+// (sequence, row pass, kv head)
 // ---------------------------------------------------------------------------
 // Rows of the chunk are (token j, group head g) -> r = j * G + g, in tiles of
 // 16.  Keys stream in stages of 32 (two 16-token blocks) through LDS.
