@@ -208,11 +208,14 @@ def test_fp8_chunk_longer_than_window_poisoned():
         pool.poison_dead()
 
 
-def test_fp8_long_chunks_split_into_row_passes():
-    """300-token chunks at G = 8: ten 256-row passes over fp8 stages; sinks
-    span two blocks and the window is shorter than the chunk."""
-    say("fp8 long chunks")
+@pytest.mark.parametrize("rows", [256, 128])
+def test_fp8_long_chunks_split_into_row_passes(rows):
+    """300-token chunks at G = 8: ten 256-row (or nineteen 128-row) passes
+    over fp8 stages; sinks span two blocks and the window is shorter than
+    the chunk."""
+    say(f"fp8 long chunks, {rows}-row passes")
     pool, h, _ = _pool(hq=16, hkv=2, S=20, W=130, cmax=300, n=2, L=1)
+    pool.set_prefill_pass_rows(rows)
     for cl in ([300, 137], [1, 300], [299, 5]):
         h.frame(cl, [2, 1])
     say(f"max err {h.max_err:.2e}")

@@ -177,16 +177,19 @@ def test_fused_and_separate_calls_store_identical_pools():
         assert torch.equal(pa.kv, pb.kv), f"pool bytes differ after frame {f}"
 
 
-def test_bf16_long_chunks_split_into_row_passes():
+@pytest.mark.parametrize("rows", [256, 128])
+def test_bf16_long_chunks_split_into_row_passes(rows):
     """A re-prefill-sized chunk: 300 tokens x G = 8 is 2400 query rows, ten
-    256-row passes, each its own workgroup over the keys its rows can see;
-    the window (130) is shorter than the chunk and the sinks (20) span two
-    blocks, so passes differ in their sink, window and causal edges."""
-    say("bf16 long chunks")
+    256-row (or nineteen 128-row) passes, each its own workgroup over the
+    keys its rows can see; the window (130) is shorter than the chunk and the
+    sinks (20) span two blocks, so passes differ in their sink, window and
+    causal edges."""
+    say(f"bf16 long chunks, {rows}-row passes")
     S, W, C = 20, 130, 300
     R = -(-(W + C - 1) // 16) * 16
     pool, h = _tiny(dtype="bf16", d=128, hq=16, hkv=2, S=S, W=W, cmax=C, n=2, L=1,
                     blocks=2 * (2 + R // 16))
+    pool.set_prefill_pass_rows(rows)
     for cl in ([300, 137], [1, 300], [299, 5]):
         h.frame(cl, [2, 1])
     say(f"max err {h.max_err:.2e}")
