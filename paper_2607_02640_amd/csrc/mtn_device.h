@@ -143,6 +143,26 @@ __device__ __forceinline__ VisRange vis_range(const PoolGeom &g, int t) {
     return r;
 }
 
+// Launch indices of the decode kernels, decoded in 32 bits: 64-bit divisions
+// expand into long scalar sequences, which every wave of a CU would run back
+// to back on the shared scalar unit before its first copy.
+// unit = (t * hkv + kvh) * n_split + split
+struct UnitIdx {
+    int t, kvh, split;
+};
+__device__ __forceinline__ UnitIdx decode_unit(uint32_t unit, uint32_t n_split, uint32_t hkv) {
+    const uint32_t th = unit / n_split;
+    const uint32_t t = th / hkv;
+    return UnitIdx{(int)t, (int)(th - t * hkv), (int)(unit - th * n_split)};
+}
+// first virtual block of key segment seg (of nseg) over nv blocks:
+// floor(seg * nv / nseg), in 32 bits whenever the product fits
+__device__ __forceinline__ int seg_begin(uint32_t seg, uint32_t nseg, int nv) {
+    const uint64_t prod = (uint64_t)seg * (uint32_t)nv;
+    if (prod <= 0xFFFFFFFFull) return (int)((uint32_t)prod / nseg);
+    return (int)(prod / nseg);
+}
+
 // logical block and valid slot range [lo, hi) of virtual block v
 __device__ __forceinline__ void vblock(const PoolGeom &g, const VisRange &r, int v, int *lb,
                                        int *lo, int *hi) {

@@ -158,11 +158,9 @@ __global__ __launch_bounds__(64 * WPU * NG) void k_attn_valu(AttnArgs a) {
     const int wv = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
     const int grp = wv / WPU;                       // wave group (key segment)
     const int wq = wv - grp * WPU;                  // wave inside the group
-    const int64_t unit = blockIdx.x;
     const PoolGeom &g = a.g;
-    const int split = __builtin_amdgcn_readfirstlane((int)(unit % a.n_split));
-    const int kvh = __builtin_amdgcn_readfirstlane((int)((unit / a.n_split) % g.hkv));
-    const int t = __builtin_amdgcn_readfirstlane((int)(unit / ((int64_t)a.n_split * g.hkv)));
+    const UnitIdx ui = decode_unit(blockIdx.x, (uint32_t)a.n_split, (uint32_t)g.hkv);
+    const int split = ui.split, kvh = ui.kvh, t = ui.t;
     const int sid = __builtin_amdgcn_readfirstlane(a.p.tok_sid[t]);
     const int pos = __builtin_amdgcn_readfirstlane(a.p.tok_pos[t]);
     const int64_t row = __builtin_amdgcn_readfirstlane(a.p.tok_row[t]);
@@ -180,17 +178,21 @@ __global__ __launch_bounds__(64 * WPU * NG) void k_attn_valu(AttnArgs a) {
     // blocks [v0, v1); sinks sit in virtual block 0, so only segment 0 reads them
     const VisRange vr = vis_range(g, pos);
     const int nv = vr.n_sb + vr.n_rb;
-    const int64_t nseg = (int64_t)a.n_split * NG;
-    const int64_t seg = (int64_t)split * NG + grp;
-    const int v0 = __builtin_amdgcn_readfirstlane((int)(seg * nv / nseg));
-    const int v1 = __builtin_amdgcn_readfirstlane((int)((seg + 1) * nv / nseg));
+    const uint32_t nseg = (uint32_t)a.n_split * NG;
+    const uint32_t seg = (uint32_t)split * NG + grp;
+    const int v0 = __builtin_amdgcn_readfirstlane(seg_begin(seg, nseg, nv));
+    const int v1 = __builtin_amdgcn_readfirstlane(seg_begin(seg + 1, nseg, nv));
     const int nblk = v1 - v0;
     // the barrier is workgroup-wide: every group runs the longest group's steps
     int nstep = 0;
+    {
+        int b = seg_begin((uint32_t)split * NG, nseg, nv);
 #pragma unroll
-    for (int q2 = 0; q2 < NG; ++q2) {
-        const int64_t s2 = (int64_t)split * NG + q2;
-        nstep = max(nstep, (int)((s2 + 1) * nv / nseg - s2 * nv / nseg));
+        for (int q2 = 0; q2 < NG; ++q2) {
+            const int e = seg_begin((uint32_t)split * NG + q2 + 1, nseg, nv);
+            nstep = max(nstep, e - b);
+            b = e;
+        }
     }
     nstep = __builtin_amdgcn_readfirstlane(nstep);
     const uint8_t *head_base = g.kv + (int64_t)a.layer * g.layer_stride + (int64_t)kvh * g.head_stride;

@@ -167,11 +167,10 @@ __global__ __launch_bounds__(64 * NG) void k_attn_mfma(AttnArgs a) {
     const int lane = threadIdx.x & 63;
     const int n = lane & 15, g4 = lane >> 4;
     const int wv = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
-    const int64_t unit = blockIdx.x;
     const PoolGeom &g = a.g;
-    const int split = __builtin_amdgcn_readfirstlane((int)(unit % a.n_split));
-    const int kvh = __builtin_amdgcn_readfirstlane((int)((unit / a.n_split) % g.hkv));
-    const int t = __builtin_amdgcn_readfirstlane((int)(unit / ((int64_t)a.n_split * g.hkv)));
+    const uint32_t ns = (uint32_t)a.n_split;
+    const UnitIdx ui = decode_unit(blockIdx.x, ns, (uint32_t)g.hkv);
+    const int split = ui.split, kvh = ui.kvh, t = ui.t;
     const int sid = __builtin_amdgcn_readfirstlane(a.p.tok_sid[t]);
     const int pos = __builtin_amdgcn_readfirstlane(a.p.tok_pos[t]);
     const int64_t row = __builtin_amdgcn_readfirstlane(a.p.tok_row[t]);
@@ -183,10 +182,9 @@ __global__ __launch_bounds__(64 * NG) void k_attn_mfma(AttnArgs a) {
 
     const VisRange vr = vis_range(g, pos);
     const int nv = vr.n_sb + vr.n_rb;
-    const int64_t nseg = (int64_t)a.n_split * NG;
-    const int64_t seg = (int64_t)split * NG + wv;
-    const int v0 = __builtin_amdgcn_readfirstlane((int)(seg * nv / nseg));
-    const int v1 = __builtin_amdgcn_readfirstlane((int)((seg + 1) * nv / nseg));
+    const uint32_t nseg = ns * NG, seg = (uint32_t)split * NG + wv;
+    const int v0 = __builtin_amdgcn_readfirstlane(seg_begin(seg, nseg, nv));
+    const int v1 = __builtin_amdgcn_readfirstlane(seg_begin(seg + 1, nseg, nv));
     const int nblk = v1 - v0;
     const uint8_t *head_base = g.kv + (int64_t)a.layer * g.layer_stride + (int64_t)kvh * g.head_stride;
     const int32_t *trow = g.table + (int64_t)sid * g.row_len;
@@ -441,86 +439,82 @@ __global__ __launch_bounds__(64 * NG) void k_attn_mfma(AttnArgs a) {
         }
     };
 
+    const int hq0 = kvh * G;
     if constexpr (NG > 1) {
-        // waves 1.. hand (m, l, acc) to wave 0 through their own drained rings
-        if (wv > 0) {
-            float *scr = (float *)&ring[wv][0][0] + n * D + d0;  // [16][D]
+        // every wave hands (m, l, acc) over through its own drained ring; then
+        // all threads of the workgroup merge them by log-sum-exp, one pair of
+        // output dims per thread and step (a wave covers one head's row)
+        float *scr = (float *)&ring[wv][0][0] + n * D + d0;  // [16][D]
 #pragma unroll
-            for (int i = 0; i < 4; ++i) {
-                *(float4 *)(scr + 8 * i) = make_float4(acc[0][i], acc[1][i], acc[2][i], acc[3][i]);
-                *(float4 *)(scr + 8 * i + 4) = make_float4(acc[4][i], acc[5][i], acc[6][i], acc[7][i]);
-            }
-            if (g4 == 0) {
-                sM[wv][n] = m_ref;
-                sL[wv][n] = L;
-            }
+        for (int i = 0; i < 4; ++i) {
+            *(float4 *)(scr + 8 * i) = make_float4(acc[0][i], acc[1][i], acc[2][i], acc[3][i]);
+            *(float4 *)(scr + 8 * i + 4) = make_float4(acc[4][i], acc[5][i], acc[6][i], acc[7][i]);
+        }
+        if (g4 == 0) {
+            sM[wv][n] = m_ref;
+            sL[wv][n] = L;
         }
         __syncthreads();
-        if (wv > 0) {
-            if (own_new) store_new();
-            return;
-        }
-        float M = m_ref;
+        if (own_new) store_new();
+        for (int e = threadIdx.x; e < G * (D / 2); e += 64 * NG) {
+            const int h = e / (D / 2), d = 2 * (e % (D / 2));
+            float M = sM[0][h];
 #pragma unroll
-        for (int q = 1; q < NG; ++q) M = fmaxf(M, sM[q][n]);
-        const float Mn = M == -INFINITY ? 0.f : M;
-        const float w0 = __builtin_amdgcn_exp2f(m_ref - Mn);
-        L *= w0;
+            for (int q = 1; q < NG; ++q) M = fmaxf(M, sM[q][h]);
+            const float Mn = M == -INFINITY ? 0.f : M;
+            float l = 0.f, o0 = 0.f, o1 = 0.f;
 #pragma unroll
-        for (int j = 0; j < 8; ++j) acc[j] *= w0;
-#pragma unroll
-        for (int q = 1; q < NG; ++q) {
-            const float wq = __builtin_amdgcn_exp2f(sM[q][n] - Mn);
-            L = fmaf(sL[q][n], wq, L);
-            const float *scr = (const float *)&ring[q][0][0] + n * D + d0;
-#pragma unroll
-            for (int i = 0; i < 4; ++i) {
-                const float4 lo4 = *(const float4 *)(scr + 8 * i);
-                const float4 hi4 = *(const float4 *)(scr + 8 * i + 4);
-                acc[0][i] = fmaf(wq, lo4.x, acc[0][i]);
-                acc[1][i] = fmaf(wq, lo4.y, acc[1][i]);
-                acc[2][i] = fmaf(wq, lo4.z, acc[2][i]);
-                acc[3][i] = fmaf(wq, lo4.w, acc[3][i]);
-                acc[4][i] = fmaf(wq, hi4.x, acc[4][i]);
-                acc[5][i] = fmaf(wq, hi4.y, acc[5][i]);
-                acc[6][i] = fmaf(wq, hi4.z, acc[6][i]);
-                acc[7][i] = fmaf(wq, hi4.w, acc[7][i]);
+            for (int q = 0; q < NG; ++q) {
+                const float wq = __builtin_amdgcn_exp2f(sM[q][h] - Mn);
+                const float2 x = *(const float2 *)((const float *)&ring[q][0][0] + h * D + d);
+                l = fmaf(sL[q][h], wq, l);
+                o0 = fmaf(wq, x.x, o0);
+                o1 = fmaf(wq, x.y, o1);
+            }
+            if (a.n_split == 1) {
+                const float inv = 1.f / l;
+                *(uint32_t *)((bf16_t *)a.out + (row * g.hq + hq0 + h) * D + d) = pack_bf16x2(o0 * inv, o1 * inv);
+                if (a.lse && d == 0)
+                    a.lse[row * g.hq + hq0 + h] = (M + __builtin_amdgcn_logf(l)) * 0.6931471805599453f;
+            } else {
+                const int64_t base = ((int64_t)t * g.hq + hq0 + h) * ns + split;
+                *(float2 *)(a.part + base * D + d) = make_float2(o0, o1);
+                if (d == 0) {
+                    float *pml = a.part + (int64_t)a.p.n_tok * g.hq * ns * D;
+                    pml[base * 2] = M;
+                    pml[base * 2 + 1] = l;
+                }
             }
         }
-        m_ref = M;
-    }
-
-    const int hq0 = kvh * G;
-    if (n < G) {
-        if (a.n_split == 1) {
-            const float inv = 1.f / L;
-            bf16_t *ob = (bf16_t *)a.out + (row * g.hq + hq0 + n) * D + d0;
+    } else {
+        if (n < G) {
+            if (a.n_split == 1) {
+                const float inv = 1.f / L;
+                bf16_t *ob = (bf16_t *)a.out + (row * g.hq + hq0 + n) * D + d0;
 #pragma unroll
-            for (int i = 0; i < 4; ++i)
-                *(uint4 *)(ob + 8 * i) =
-                    make_uint4(pack_bf16x2(acc[0][i] * inv, acc[1][i] * inv),
-                               pack_bf16x2(acc[2][i] * inv, acc[3][i] * inv),
-                               pack_bf16x2(acc[4][i] * inv, acc[5][i] * inv),
-                               pack_bf16x2(acc[6][i] * inv, acc[7][i] * inv));
-            if (a.lse && g4 == 0)
-                a.lse[row * g.hq + hq0 + n] = (m_ref + __builtin_amdgcn_logf(L)) * 0.6931471805599453f;
-        } else {
-            const int64_t ns = a.n_split;
-            const int64_t base = ((int64_t)t * g.hq + hq0 + n) * ns + split;
-            float *pacc = a.part + base * D + d0;
+                for (int i = 0; i < 4; ++i)
+                    *(uint4 *)(ob + 8 * i) =
+                        make_uint4(pack_bf16x2(acc[0][i] * inv, acc[1][i] * inv),
+                                   pack_bf16x2(acc[2][i] * inv, acc[3][i] * inv),
+                                   pack_bf16x2(acc[4][i] * inv, acc[5][i] * inv),
+                                   pack_bf16x2(acc[6][i] * inv, acc[7][i] * inv));
+                if (a.lse && g4 == 0)
+                    a.lse[row * g.hq + hq0 + n] = (m_ref + __builtin_amdgcn_logf(L)) * 0.6931471805599453f;
+            } else {
+                const int64_t base = ((int64_t)t * g.hq + hq0 + n) * ns + split;
+                float *pacc = a.part + base * D + d0;
 #pragma unroll
-            for (int i = 0; i < 4; ++i) {
-                *(float4 *)(pacc + 8 * i) = make_float4(acc[0][i], acc[1][i], acc[2][i], acc[3][i]);
-                *(float4 *)(pacc + 8 * i + 4) = make_float4(acc[4][i], acc[5][i], acc[6][i], acc[7][i]);
-            }
-            if (g4 == 0) {
-                float *pml = a.part + (int64_t)a.p.n_tok * g.hq * ns * D;
-                pml[base * 2] = m_ref;
-                pml[base * 2 + 1] = L;
+                for (int i = 0; i < 4; ++i) {
+                    *(float4 *)(pacc + 8 * i) = make_float4(acc[0][i], acc[1][i], acc[2][i], acc[3][i]);
+                    *(float4 *)(pacc + 8 * i + 4) = make_float4(acc[4][i], acc[5][i], acc[6][i], acc[7][i]);
+                }
+                if (g4 == 0) {
+                    float *pml = a.part + (int64_t)a.p.n_tok * g.hq * ns * D;
+                    pml[base * 2] = m_ref;
+                    pml[base * 2 + 1] = L;
+                }
             }
         }
-    }
-    if constexpr (NG == 1) {
         if (own_new) store_new();  // one wave: it owns the newest key
     }
 }

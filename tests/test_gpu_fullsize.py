@@ -13,7 +13,7 @@ import torch
 
 from oracle import windowed_attention as wa
 from tests._gpu_util import make_pool, say
-from workload import QWEN3_OMNI as W, device_bank
+from workload import MINICPM_O, MOSHI, QWEN3_OMNI as W, device_bank
 
 pytestmark = pytest.mark.gpu
 
@@ -79,3 +79,116 @@ def test_qwen3_omni_shape_sampled_parity(dtype, n_split):
         worst = max(worst, err)
     assert worst <= 2e-2, worst
     pool.close()
+
+
+def _ragged_fullsize(wl, dtype, lengths, chunk_len, n_dec, samples, seed):
+    """Fast-forward every session of workload `wl` to its own length by
+    append-only plans (only the sessions still short of their length take
+    part, at most max_chunk tokens each), run one ragged frame through
+    mtn_frame_step, and recompute the sampled (session, layer) pairs with the
+    float64 oracle from the same rows.  Returns the worst max-abs error."""
+    N, Lyr, Hq, Hkv, D = wl.n_sessions, wl.n_layers, wl.n_q_heads, wl.n_kv_heads, wl.head_dim
+    cmax = wl.max_chunk
+    R = -(-(wl.window + cmax - 1) // 16) * 16
+    n_blocks = N * (-(-wl.n_sink // 16) + R // 16)
+    say(f"{wl.name}: pool of {n_blocks} blocks, {dtype}")
+    pool = make_pool(n_layers=Lyr, hq=Hq, hkv=Hkv, d=D, S=wl.n_sink, W=wl.window, cmax=cmax,
+                     max_sessions=N, n_blocks=n_blocks, dtype=dtype, theta=wl.rope_theta)
+    sids = [pool.session_open() for _ in range(N)]
+    dev = torch.device("cuda")
+    bf = torch.bfloat16
+    sc = wl.act_scale
+    ff_k = device_bank((Lyr, N * cmax, Hkv, D), bf, dev, seed + 1, sc)
+    ff_v = device_bank((Lyr, N * cmax, Hkv, D), bf, dev, seed + 2, sc)
+    have = [0] * N
+    plans = []  # per plan: {session: (row offset, n_tok)}
+    while True:
+        idx = [i for i in range(N) if have[i] < lengths[i]]
+        if not idx:
+            break
+        nt = [min(cmax, lengths[i] - have[i]) for i in idx]
+        pool.plan_begin([sids[i] for i in idx], nt)
+        for l in range(Lyr):
+            pool.frame_append_kv(l, ff_k[l], ff_v[l])
+        pool.plan_commit()
+        rows, off = {}, 0
+        for i, n in zip(idx, nt):
+            rows[i] = (off, n)
+            off += n
+            have[i] += n
+        plans.append(rows)
+    say(f"fast-forward done: {len(plans)} plans")
+    T = sum(chunk_len)
+    tau = max(n_dec)
+    qc = device_bank((Lyr, T, Hq, D), bf, dev, seed + 3, sc)
+    kc = device_bank((Lyr, T, Hkv, D), bf, dev, seed + 4, sc)
+    vc = device_bank((Lyr, T, Hkv, D), bf, dev, seed + 5, sc)
+    qd = device_bank((tau, Lyr, N, Hq, D), bf, dev, seed + 6, sc)
+    kd = device_bank((tau, Lyr, N, Hkv, D), bf, dev, seed + 7, sc)
+    vd = device_bank((tau, Lyr, N, Hkv, D), bf, dev, seed + 8, sc)
+    oc = torch.empty_like(qc)
+    od = torch.zeros_like(qd)
+    pool.frame_step(sids, chunk_len, n_dec, qc, kc, vc, oc, qd, kd, vd, od)
+    torch.cuda.synchronize()
+    assert torch.isfinite(oc.float()).all() and torch.isfinite(od.float()).all()
+    say("frame done; oracle samples")
+    c_off = np.concatenate([[0], np.cumsum(chunk_len)])
+    worst = 0.0
+    for (i, l) in samples:
+        o = wa.OracleSession(Hq, Hkv, D, wl.n_sink, wl.window, theta=wl.rope_theta, n_layers=1,
+                             kv_quant="fp8_e4m3" if dtype == "fp8" else None)
+        for rows in plans:
+            if i not in rows:
+                continue
+            off, n = rows[i]
+            o.begin(n)
+            o.layer_step(0, np.zeros((n, Hq, D)), _f64(ff_k[l, off:off + n]),
+                         _f64(ff_v[l, off:off + n]), attend=False)
+            o.commit()
+        a, b = int(c_off[i]), int(c_off[i + 1])
+        o.begin(b - a)
+        ref, _ = o.layer_step(0, _f64(qc[l, a:b]), _f64(kc[l, a:b]), _f64(vc[l, a:b]))
+        o.commit()
+        err = float(np.max(np.abs(_f64(oc[l, a:b]) - ref)))
+        for j in range(n_dec[i]):
+            o.begin(1)
+            rd, _ = o.layer_step(0, _f64(qd[j, l, i:i + 1]), _f64(kd[j, l, i:i + 1]),
+                                 _f64(vd[j, l, i:i + 1]))
+            o.commit()
+            err = max(err, float(np.max(np.abs(_f64(od[j, l, i:i + 1]) - rd))))
+        say(f"session {i} (length {lengths[i]}) layer {l}: max abs err {err:.3e}")
+        worst = max(worst, err)
+    pool.close()
+    return worst
+
+
+@pytest.mark.parametrize("dtype", ["bf16", "fp8"])
+def test_minicpm_shape_ragged_sampled_parity(dtype):
+    """MiniCPM-o-shaped backbone at full size: 256 sessions, 36 layers, GQA
+    32/8, S = 4, W = 2048, chunks U{10..40}, decodes U{8..24}; 30 % of the
+    sessions still filling their window, 70 % wrapped once or twice."""
+    wl = MINICPM_O
+    rng = np.random.default_rng(2026)
+    N = wl.n_sessions
+    full = wl.n_sink + wl.window
+    lengths = [int(rng.integers(1, full - 60)) if i % 10 < 3 else int(rng.integers(full, 2 * full))
+               for i in range(N)]
+    chunk_len = [int(x) for x in rng.integers(wl.chunk[0], wl.chunk[1] + 1, N)]
+    n_dec = [int(x) for x in rng.integers(wl.n_decode[0], wl.n_decode[1] + 1, N)]
+    samples = [(0, 0), (5, 17), (200, 35), (N - 1, 9)]
+    worst = _ragged_fullsize(wl, dtype, lengths, chunk_len, n_dec, samples, seed=510)
+    assert worst <= 2e-2, worst
+
+
+@pytest.mark.parametrize("dtype", ["bf16", "fp8"])
+def test_moshi_shape_sampled_parity(dtype):
+    """Moshi-shaped temporal transformer at full size: 64 sessions, 32 layers,
+    MHA 32/32, S = 4, W = 2048, one appended token and one decode per frame;
+    a quarter of the sessions still filling their window, the rest wrapped."""
+    wl = MOSHI
+    N = wl.n_sessions
+    full = wl.n_sink + wl.window
+    lengths = [300 + 7 * i if i % 4 == 0 else full + 3 + 11 * i for i in range(N)]
+    samples = [(0, 0), (1, 15), (62, 31)]
+    worst = _ragged_fullsize(wl, dtype, lengths, [1] * N, [1] * N, samples, seed=520)
+    assert worst <= 2e-2, worst
