@@ -1266,6 +1266,7 @@ hipError_t launch_valu_t(const AttnArgs &a, hipStream_t s) {
     using DS = DecodeShape<G>;
     int64_t units = (int64_t)a.p.n_tok * a.g.hkv * a.n_split;
     if (units == 0) return hipSuccess;
+    if (units > INT32_MAX) return hipErrorInvalidValue;  // one grid dimension, 32-bit unit index
     hipLaunchKernelGGL((k_attn_valu<T, D, G, DS::WPU, DS::NG, DS::NBUF>), dim3((unsigned)units),
                        dim3(64 * DS::WPU * DS::NG), 0, s, a);
     return hipGetLastError();

@@ -553,6 +553,7 @@ hipError_t launch_mfma_g(const AttnArgs &a, hipStream_t s) {
     using S = MfmaShape<F8, G>;
     const int64_t units = (int64_t)a.p.n_tok * a.g.hkv * a.n_split;
     if (units == 0) return hipSuccess;
+    if (units > INT32_MAX) return hipErrorInvalidValue;  // one grid dimension, 32-bit unit index
     hipLaunchKernelGGL((k_attn_mfma<F8, G, S::NG, S::NBUF>), dim3((unsigned)units), dim3(64 * S::NG),
                        0, s, a);
     return hipGetLastError();
