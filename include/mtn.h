@@ -65,6 +65,8 @@ typedef int32_t mtn_status;
 #define MTN_ERR_BAD_STATE       (-8)  /* call out of order (plan open/missing,
                                          layer not appended, ...)              */
 #define MTN_ERR_UNSUPPORTED     (-9)  /* shape/dtype with no compiled kernel   */
+#define MTN_ERR_HOST_MEMORY     (-10) /* a host allocation failed (no C++
+                                         exception ever leaves the library)    */
 
 enum { MTN_F32 = 0, MTN_BF16 = 1, MTN_FP8_E4M3 = 2 };
 

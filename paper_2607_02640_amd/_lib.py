@@ -25,6 +25,7 @@ MTN_ERR_SESSION_FULL = -6
 MTN_ERR_DEVICE = -7
 MTN_ERR_BAD_STATE = -8
 MTN_ERR_UNSUPPORTED = -9
+MTN_ERR_HOST_MEMORY = -10
 
 MTN_F32 = 0
 MTN_BF16 = 1

@@ -15,6 +15,7 @@
 #include <cmath>
 #include <cstdio>
 #include <cstring>
+#include <new>
 #include <string>
 #include <vector>
 
@@ -130,14 +131,36 @@ struct mtn_pool {
 
 namespace {
 
-mtn_status fail(mtn_pool *p, mtn_status s, const char *msg) {
-    if (p) p->last_error = msg;
+mtn_status fail(mtn_pool *p, mtn_status s, const char *msg) noexcept {
+    if (p) {
+        try {
+            p->last_error = msg;
+        } catch (...) {
+            // the status still says what failed
+        }
+    }
     return s;
 }
 
-mtn_status hip_fail(mtn_pool *p, hipError_t e, const char *where) {
+// No C++ exception crosses the C ABI: a host allocation that fails inside an
+// entry point returns MTN_ERR_HOST_MEMORY.  The planner reserves its
+// per-plan vectors at pool creation, so plan_begin allocates only during
+// validation, before it changes any state.
+template <class F>
+mtn_status guarded(mtn_pool *p, F &&f) noexcept {
+    try {
+        return f();
+    } catch (...) {
+        return fail(p, MTN_ERR_HOST_MEMORY, "host allocation failed");
+    }
+}
+
+mtn_status hip_fail(mtn_pool *p, hipError_t e, const char *where) noexcept {
     if (p) {
-        p->last_error = std::string(where) + ": " + hipGetErrorString(e);
+        try {
+            p->last_error = std::string(where) + ": " + hipGetErrorString(e);
+        } catch (...) {
+        }
     }
     return MTN_ERR_DEVICE;
 }
@@ -182,6 +205,14 @@ mtn_status validate(const mtn_pool_config *c) {
     if (!(c->rope_theta > 1.0)) return MTN_ERR_INVALID_ARG;
     if (c->softmax_scale < 0.f || !std::isfinite(c->softmax_scale)) return MTN_ERR_INVALID_ARG;
     if ((int64_t)c->max_sessions * c->max_chunk > (int64_t)1 << 24) return MTN_ERR_INVALID_ARG;
+    {
+        // block-table entries are addressed with 32-bit indices (plan updates)
+        const int64_t ring = c->window == MTN_WINDOW_UNBOUNDED
+                                 ? ceil_div(c->max_len, kBlock)
+                                 : ceil_div((int64_t)c->window + c->max_chunk - 1, kBlock) +
+                                       ceil_div(c->n_sink, kBlock);
+        if ((int64_t)c->max_sessions * ring >= ((int64_t)1 << 31)) return MTN_ERR_INVALID_ARG;
+    }
     if (c->flags & ~MTN_POOL_HOST_ONLY) return MTN_ERR_INVALID_ARG;
     return MTN_OK;
 }
@@ -552,6 +583,8 @@ mtn_status prefill_impl(mtn_pool *P, int32_t layer, const void *q, void *out, fl
     return timing_end(P, 1, e0, s);
 }
 
+mtn_status pool_init(mtn_pool *P, const mtn_pool_config *cfg, void *kv_dev, void *stream);
+
 }  // namespace
 
 extern "C" {
@@ -568,6 +601,7 @@ const char *mtn_status_string(mtn_status s) {
         case MTN_ERR_DEVICE: return "device error";
         case MTN_ERR_BAD_STATE: return "call out of order";
         case MTN_ERR_UNSUPPORTED: return "unsupported shape or dtype";
+        case MTN_ERR_HOST_MEMORY: return "host allocation failed";
         default: return "unknown status";
     }
 }
@@ -599,7 +633,29 @@ mtn_status mtn_pool_create(const mtn_pool_config *cfg, void *kv_dev, size_t kv_b
                                           : !attn_valu_supported(cfg->kv_dtype, cfg->head_dim, g))
             return MTN_ERR_UNSUPPORTED;
     }
-    mtn_pool *P = new mtn_pool();
+    mtn_pool *P = new (std::nothrow) mtn_pool();
+    if (!P) return MTN_ERR_HOST_MEMORY;
+    try {
+        st = pool_init(P, cfg, kv_dev, stream);
+    } catch (...) {
+        st = MTN_ERR_HOST_MEMORY;
+    }
+    if (st) {
+        mtn_pool_destroy(P);
+        return st;
+    }
+    *out = P;
+    return MTN_OK;
+}
+
+}  // extern "C"
+
+namespace {
+
+// Everything of pool creation past validation; on failure the caller
+// destroys the partly built pool.
+mtn_status pool_init(mtn_pool *P, const mtn_pool_config *cfg, void *kv_dev, void *stream) {
+    const bool host_only = cfg->flags & MTN_POOL_HOST_ONLY;
     P->cfg = *cfg;
     P->host_only = host_only;
     P->unbounded = cfg->window == MTN_WINDOW_UNBOUNDED;
@@ -630,9 +686,19 @@ mtn_status mtn_pool_create(const mtn_pool_config *cfg, void *kv_dev, size_t kv_b
     P->n_assigned.assign((size_t)cfg->max_sessions, 0);
     P->alloc.reset(cfg->n_blocks);
     P->max_tok = cfg->max_sessions * cfg->max_chunk;
+    // the planner's per-plan vectors at their largest, so that planning
+    // allocates nothing once validation has passed
+    P->seq_sid.reserve((size_t)cfg->max_sessions);
+    P->seq_ntok.reserve((size_t)cfg->max_sessions);
+    P->seq_first.reserve((size_t)cfg->max_sessions);
+    P->seq_pos0.reserve((size_t)cfg->max_sessions);
+    for (auto *v : {&P->tok_sid, &P->tok_pos, &P->tok_row, &P->tok_block, &P->tok_off, &P->upd_idx,
+                    &P->upd_val})
+        v->reserve((size_t)P->max_tok);
+    P->pf_items.reserve(2 * ((size_t)P->max_tok * P->G / 128 + (size_t)cfg->max_sessions + 1));
+    P->layer_done.reserve((size_t)cfg->n_layers);
     if (!host_only) {
         auto bail = [&](hipError_t e, const char *w) {
-            mtn_pool_destroy(P);
             (void)e;
             (void)w;
             return MTN_ERR_DEVICE;
@@ -688,9 +754,12 @@ mtn_status mtn_pool_create(const mtn_pool_config *cfg, void *kv_dev, size_t kv_b
         if ((e = hipStreamSynchronize((hipStream_t)stream)) != hipSuccess)
             return bail(e, "sync");
     }
-    *out = P;
     return MTN_OK;
 }
+
+}  // namespace
+
+extern "C" {
 
 void mtn_pool_destroy(mtn_pool *P) {
     if (!P) return;
@@ -717,188 +786,206 @@ void mtn_pool_destroy(mtn_pool *P) {
 }
 
 mtn_status mtn_session_open(mtn_pool *P, int32_t *sid_out) {
-    if (!P || !sid_out) return MTN_ERR_INVALID_ARG;
-    int32_t sid = -1;
-    for (int32_t i = 0; i < P->cfg.max_sessions; ++i)
-        if (!P->is_open[i]) {
-            sid = i;
-            break;
+    return guarded(P, [&]() -> mtn_status {
+        if (!P || !sid_out) return MTN_ERR_INVALID_ARG;
+        int32_t sid = -1;
+        for (int32_t i = 0; i < P->cfg.max_sessions; ++i)
+            if (!P->is_open[i]) {
+                sid = i;
+                break;
+            }
+        if (sid < 0) return fail(P, MTN_ERR_NO_SESSION_SLOT, "no free session slot");
+        if (!P->unbounded) {
+            if (P->reserved + P->row_len > P->cfg.n_blocks)
+                return fail(P, MTN_ERR_POOL_EXHAUSTED, "reservation exceeds pool capacity");
+            P->reserved += P->row_len;
         }
-    if (sid < 0) return fail(P, MTN_ERR_NO_SESSION_SLOT, "no free session slot");
-    if (!P->unbounded) {
-        if (P->reserved + P->row_len > P->cfg.n_blocks)
-            return fail(P, MTN_ERR_POOL_EXHAUSTED, "reservation exceeds pool capacity");
-        P->reserved += P->row_len;
-    }
-    P->is_open[sid] = 1;
-    P->len[sid] = 0;
-    P->n_assigned[sid] = 0;
-    P->n_open++;
-    *sid_out = sid;
-    return MTN_OK;
+        P->is_open[sid] = 1;
+        P->len[sid] = 0;
+        P->n_assigned[sid] = 0;
+        P->n_open++;
+        *sid_out = sid;
+        return MTN_OK;
+    });
 }
 
 mtn_status mtn_session_close(mtn_pool *P, int32_t sid) {
-    if (!P) return MTN_ERR_INVALID_ARG;
-    if (P->plan_open) return fail(P, MTN_ERR_BAD_STATE, "plan open");
-    if (sid < 0 || sid >= P->cfg.max_sessions || !P->is_open[sid])
-        return fail(P, MTN_ERR_BAD_SESSION, "session not open");
-    int32_t *row = &P->table[(size_t)sid * P->row_len];
-    for (int32_t j = 0; j < P->row_len; ++j) {
-        if (row[j] >= 0) {
-            P->alloc.give(row[j]);
-            P->assigned--;
-            row[j] = -1;
+    return guarded(P, [&]() -> mtn_status {
+        if (!P) return MTN_ERR_INVALID_ARG;
+        if (P->plan_open) return fail(P, MTN_ERR_BAD_STATE, "plan open");
+        if (sid < 0 || sid >= P->cfg.max_sessions || !P->is_open[sid])
+            return fail(P, MTN_ERR_BAD_SESSION, "session not open");
+        int32_t *row = &P->table[(size_t)sid * P->row_len];
+        for (int32_t j = 0; j < P->row_len; ++j) {
+            if (row[j] >= 0) {
+                P->alloc.give(row[j]);
+                P->assigned--;
+                row[j] = -1;
+            }
         }
-    }
-    if (!P->unbounded) P->reserved -= P->row_len;
-    else P->reserved = P->assigned;
-    P->is_open[sid] = 0;
-    P->len[sid] = 0;
-    P->n_assigned[sid] = 0;
-    P->n_open--;
-    // The device copy of the row is left as is: kernels still in flight may
-    // read it, and a reopened session only ever reads logical blocks that its
-    // own plans assigned (and uploaded, in stream order) again.
-    return MTN_OK;
+        if (!P->unbounded) P->reserved -= P->row_len;
+        else P->reserved = P->assigned;
+        P->is_open[sid] = 0;
+        P->len[sid] = 0;
+        P->n_assigned[sid] = 0;
+        P->n_open--;
+        // The device copy of the row is left as is: kernels still in flight may
+        // read it, and a reopened session only ever reads logical blocks that its
+        // own plans assigned (and uploaded, in stream order) again.
+        return MTN_OK;
+    });
 }
 
 mtn_status mtn_plan_begin(mtn_pool *P, int32_t n_seq, const int32_t *sids, const int32_t *n_tok,
                           void *stream) {
-    if (!P) return MTN_ERR_INVALID_ARG;
-    return plan_begin(P, n_seq, sids, n_tok, nullptr, stream);
+    return guarded(P, [&]() -> mtn_status {
+        if (!P) return MTN_ERR_INVALID_ARG;
+        return plan_begin(P, n_seq, sids, n_tok, nullptr, stream);
+    });
 }
 
 mtn_status mtn_plan_commit(mtn_pool *P) {
-    if (!P) return MTN_ERR_INVALID_ARG;
-    return plan_commit(P);
+    return guarded(P, [&]() -> mtn_status {
+        if (!P) return MTN_ERR_INVALID_ARG;
+        return plan_commit(P);
+    });
 }
 
 mtn_status mtn_frame_append_kv(mtn_pool *P, int32_t layer, const void *k, const void *v,
                                void *stream) {
-    mtn_status st = check_call(P, layer, stream);
-    if (st) return st;
-    if (!k || !v) return fail(P, MTN_ERR_INVALID_ARG, "null k or v");
-    return append_impl(P, layer, k, v, stream);
+    return guarded(P, [&]() -> mtn_status {
+        mtn_status st = check_call(P, layer, stream);
+        if (st) return st;
+        if (!k || !v) return fail(P, MTN_ERR_INVALID_ARG, "null k or v");
+        return append_impl(P, layer, k, v, stream);
+    });
 }
 
 mtn_status mtn_attend_chunk_prefill(mtn_pool *P, int32_t layer, const void *q, void *out,
                                     float *lse, void *stream) {
-    mtn_status st = check_call(P, layer, stream);
-    if (st) return st;
-    if (!q || !out) return fail(P, MTN_ERR_INVALID_ARG, "null q or out");
-    if (!P->layer_done[layer]) return fail(P, MTN_ERR_BAD_STATE, "layer not appended");
-    return prefill_impl(P, layer, q, out, lse, stream);
+    return guarded(P, [&]() -> mtn_status {
+        mtn_status st = check_call(P, layer, stream);
+        if (st) return st;
+        if (!q || !out) return fail(P, MTN_ERR_INVALID_ARG, "null q or out");
+        if (!P->layer_done[layer]) return fail(P, MTN_ERR_BAD_STATE, "layer not appended");
+        return prefill_impl(P, layer, q, out, lse, stream);
+    });
 }
 
 mtn_status mtn_attend_decode(mtn_pool *P, int32_t layer, const void *q, void *out, float *lse,
                              int32_t n_split, void *stream) {
-    mtn_status st = check_call(P, layer, stream);
-    if (st) return st;
-    if (!q || !out) return fail(P, MTN_ERR_INVALID_ARG, "null q or out");
-    if (!P->all_single) return fail(P, MTN_ERR_BAD_STATE, "decode needs n_tok == 1 everywhere");
-    if (n_split < 0 || n_split > kMaxSplit) return fail(P, MTN_ERR_INVALID_ARG, "bad n_split");
-    if (!P->layer_done[layer]) return fail(P, MTN_ERR_BAD_STATE, "layer not appended");
-    return decode_impl(P, layer, q, out, lse, n_split, stream);
+    return guarded(P, [&]() -> mtn_status {
+        mtn_status st = check_call(P, layer, stream);
+        if (st) return st;
+        if (!q || !out) return fail(P, MTN_ERR_INVALID_ARG, "null q or out");
+        if (!P->all_single) return fail(P, MTN_ERR_BAD_STATE, "decode needs n_tok == 1 everywhere");
+        if (n_split < 0 || n_split > kMaxSplit) return fail(P, MTN_ERR_INVALID_ARG, "bad n_split");
+        if (!P->layer_done[layer]) return fail(P, MTN_ERR_BAD_STATE, "layer not appended");
+        return decode_impl(P, layer, q, out, lse, n_split, stream);
+    });
 }
 
 mtn_status mtn_attend_decode_append(mtn_pool *P, int32_t layer, const void *k, const void *v,
                                     const void *q, void *out, float *lse, int32_t n_split,
                                     void *stream) {
-    mtn_status st = check_call(P, layer, stream);
-    if (st) return st;
-    if (!k || !v || !q || !out) return fail(P, MTN_ERR_INVALID_ARG, "null k, v, q or out");
-    if (!P->all_single) return fail(P, MTN_ERR_BAD_STATE, "decode needs n_tok == 1 everywhere");
-    if (n_split < 0 || n_split > kMaxSplit) return fail(P, MTN_ERR_INVALID_ARG, "bad n_split");
-    if (P->layer_done[layer]) return fail(P, MTN_ERR_BAD_STATE, "layer already appended");
-    return decode_impl(P, layer, q, out, lse, n_split, stream, k, v);
+    return guarded(P, [&]() -> mtn_status {
+        mtn_status st = check_call(P, layer, stream);
+        if (st) return st;
+        if (!k || !v || !q || !out) return fail(P, MTN_ERR_INVALID_ARG, "null k, v, q or out");
+        if (!P->all_single) return fail(P, MTN_ERR_BAD_STATE, "decode needs n_tok == 1 everywhere");
+        if (n_split < 0 || n_split > kMaxSplit) return fail(P, MTN_ERR_INVALID_ARG, "bad n_split");
+        if (P->layer_done[layer]) return fail(P, MTN_ERR_BAD_STATE, "layer already appended");
+        return decode_impl(P, layer, q, out, lse, n_split, stream, k, v);
+    });
 }
 
 mtn_status mtn_frame_step(mtn_pool *P, const mtn_frame_batch *b, void *stream) {
-    if (!P || !b) return MTN_ERR_INVALID_ARG;
-    if (P->host_only) return fail(P, MTN_ERR_BAD_STATE, "host-only pool has no device path");
-    if (P->plan_open) return fail(P, MTN_ERR_BAD_STATE, "a plan is already open");
-    const int32_t n = b->n_seq;
-    if (n < 1 || n > P->cfg.max_sessions || !b->sids || !b->chunk_len || !b->n_decode)
-        return fail(P, MTN_ERR_INVALID_ARG, "bad batch");
-    if (!b->q_chunk || !b->k_chunk || !b->v_chunk || !b->out_chunk)
-        return fail(P, MTN_ERR_INVALID_ARG, "null chunk buffer");
-    if (b->n_split < 0 || b->n_split > kMaxSplit) return fail(P, MTN_ERR_INVALID_ARG, "bad n_split");
-    int32_t max_dec = 0;
-    int64_t Tc = 0;
-    std::vector<uint8_t> seen((size_t)P->cfg.max_sessions, 0);
-    for (int32_t i = 0; i < n; ++i) {
-        int32_t sid = b->sids[i];
-        if (sid < 0 || sid >= P->cfg.max_sessions || !P->is_open[sid])
-            return fail(P, MTN_ERR_BAD_SESSION, "session not open");
-        if (seen[sid]) return fail(P, MTN_ERR_INVALID_ARG, "duplicate session in batch");
-        seen[sid] = 1;
-        if (b->chunk_len[i] < 1) return fail(P, MTN_ERR_INVALID_ARG, "chunk_len < 1");
-        if (b->chunk_len[i] > P->cfg.max_chunk)
-            return fail(P, MTN_ERR_CHUNK_TOO_LARGE, "chunk_len > max_chunk");
-        if (b->n_decode[i] < 0) return fail(P, MTN_ERR_INVALID_ARG, "n_decode < 0");
-        if (P->unbounded && P->len[sid] + b->chunk_len[i] + b->n_decode[i] > P->cfg.max_len)
-            return fail(P, MTN_ERR_SESSION_FULL, "frame would pass max_len");
-        max_dec = std::max(max_dec, b->n_decode[i]);
-        Tc += b->chunk_len[i];
-    }
-    if (max_dec > 0 && (!b->q_dec || !b->k_dec || !b->v_dec || !b->out_dec))
-        return fail(P, MTN_ERR_INVALID_ARG, "null decode buffer");
-    {   // whole-frame capacity check before any launch
-        std::vector<uint8_t> lbseen((size_t)P->row_len, 0);
-        int64_t need = 0;
-        for (int32_t i = 0; i < n; ++i)
-            need += new_blocks_needed(P, b->sids[i], P->len[b->sids[i]],
-                                      (int64_t)b->chunk_len[i] + b->n_decode[i], lbseen);
-        if (need > P->alloc.n_free()) return fail(P, MTN_ERR_POOL_EXHAUSTED, "pool exhausted");
-    }
-    const int32_t L = P->cfg.n_layers, Hq = P->cfg.n_q_heads, Hkv = P->cfg.n_kv_heads;
-    const size_t e = P->elt, D = (size_t)P->cfg.head_dim;
-    auto off = [&](const void *base, size_t elems) {
-        return (const void *)((const uint8_t *)base + elems * e);
-    };
-    mtn_status st = plan_begin(P, n, b->sids, b->chunk_len, nullptr, stream);
-    if (st) return st;
-    for (int32_t l = 0; l < L; ++l) {
-        size_t rq = (size_t)l * Tc * Hq * D, rk = (size_t)l * Tc * Hkv * D;
-        float *lse = b->lse_chunk ? b->lse_chunk + (size_t)l * Tc * Hq : nullptr;
-        if (P->all_single) {  // one-token chunks: decode with the append fused in
-            st = decode_impl(P, l, off(b->q_chunk, rq), (void *)off(b->out_chunk, rq), lse,
-                             b->n_split, stream, off(b->k_chunk, rk), off(b->v_chunk, rk));
-        } else {
-            st = append_impl(P, l, off(b->k_chunk, rk), off(b->v_chunk, rk), stream);
-            if (st) return st;
-            st = prefill_impl(P, l, off(b->q_chunk, rq), (void *)off(b->out_chunk, rq), lse,
-                              stream);
+    return guarded(P, [&]() -> mtn_status {
+        if (!P || !b) return MTN_ERR_INVALID_ARG;
+        if (P->host_only) return fail(P, MTN_ERR_BAD_STATE, "host-only pool has no device path");
+        if (P->plan_open) return fail(P, MTN_ERR_BAD_STATE, "a plan is already open");
+        const int32_t n = b->n_seq;
+        if (n < 1 || n > P->cfg.max_sessions || !b->sids || !b->chunk_len || !b->n_decode)
+            return fail(P, MTN_ERR_INVALID_ARG, "bad batch");
+        if (!b->q_chunk || !b->k_chunk || !b->v_chunk || !b->out_chunk)
+            return fail(P, MTN_ERR_INVALID_ARG, "null chunk buffer");
+        if (b->n_split < 0 || b->n_split > kMaxSplit) return fail(P, MTN_ERR_INVALID_ARG, "bad n_split");
+        int32_t max_dec = 0;
+        int64_t Tc = 0;
+        std::vector<uint8_t> seen((size_t)P->cfg.max_sessions, 0);
+        for (int32_t i = 0; i < n; ++i) {
+            int32_t sid = b->sids[i];
+            if (sid < 0 || sid >= P->cfg.max_sessions || !P->is_open[sid])
+                return fail(P, MTN_ERR_BAD_SESSION, "session not open");
+            if (seen[sid]) return fail(P, MTN_ERR_INVALID_ARG, "duplicate session in batch");
+            seen[sid] = 1;
+            if (b->chunk_len[i] < 1) return fail(P, MTN_ERR_INVALID_ARG, "chunk_len < 1");
+            if (b->chunk_len[i] > P->cfg.max_chunk)
+                return fail(P, MTN_ERR_CHUNK_TOO_LARGE, "chunk_len > max_chunk");
+            if (b->n_decode[i] < 0) return fail(P, MTN_ERR_INVALID_ARG, "n_decode < 0");
+            if (P->unbounded && P->len[sid] + b->chunk_len[i] + b->n_decode[i] > P->cfg.max_len)
+                return fail(P, MTN_ERR_SESSION_FULL, "frame would pass max_len");
+            max_dec = std::max(max_dec, b->n_decode[i]);
+            Tc += b->chunk_len[i];
         }
-        if (st) return st;
-    }
-    st = plan_commit(P);
-    if (st) return st;
-    std::vector<int32_t> sids, ones, rows;
-    for (int32_t j = 0; j < max_dec; ++j) {
-        sids.clear();
-        rows.clear();
-        for (int32_t i = 0; i < n; ++i)
-            if (b->n_decode[i] > j) {
-                sids.push_back(b->sids[i]);
-                rows.push_back(i);
-            }
-        ones.assign(sids.size(), 1);
-        st = plan_begin(P, (int32_t)sids.size(), sids.data(), ones.data(), rows.data(), stream);
+        if (max_dec > 0 && (!b->q_dec || !b->k_dec || !b->v_dec || !b->out_dec))
+            return fail(P, MTN_ERR_INVALID_ARG, "null decode buffer");
+        {   // whole-frame capacity check before any launch
+            std::vector<uint8_t> lbseen((size_t)P->row_len, 0);
+            int64_t need = 0;
+            for (int32_t i = 0; i < n; ++i)
+                need += new_blocks_needed(P, b->sids[i], P->len[b->sids[i]],
+                                          (int64_t)b->chunk_len[i] + b->n_decode[i], lbseen);
+            if (need > P->alloc.n_free()) return fail(P, MTN_ERR_POOL_EXHAUSTED, "pool exhausted");
+        }
+        const int32_t L = P->cfg.n_layers, Hq = P->cfg.n_q_heads, Hkv = P->cfg.n_kv_heads;
+        const size_t e = P->elt, D = (size_t)P->cfg.head_dim;
+        auto off = [&](const void *base, size_t elems) {
+            return (const void *)((const uint8_t *)base + elems * e);
+        };
+        mtn_status st = plan_begin(P, n, b->sids, b->chunk_len, nullptr, stream);
         if (st) return st;
         for (int32_t l = 0; l < L; ++l) {
-            size_t base = ((size_t)j * L + l) * n;
-            float *lse = b->lse_dec ? b->lse_dec + base * Hq : nullptr;
-            st = decode_impl(P, l, off(b->q_dec, base * Hq * D),
-                             (void *)off(b->out_dec, base * Hq * D), lse, b->n_split, stream,
-                             off(b->k_dec, base * Hkv * D), off(b->v_dec, base * Hkv * D));
+            size_t rq = (size_t)l * Tc * Hq * D, rk = (size_t)l * Tc * Hkv * D;
+            float *lse = b->lse_chunk ? b->lse_chunk + (size_t)l * Tc * Hq : nullptr;
+            if (P->all_single) {  // one-token chunks: decode with the append fused in
+                st = decode_impl(P, l, off(b->q_chunk, rq), (void *)off(b->out_chunk, rq), lse,
+                                 b->n_split, stream, off(b->k_chunk, rk), off(b->v_chunk, rk));
+            } else {
+                st = append_impl(P, l, off(b->k_chunk, rk), off(b->v_chunk, rk), stream);
+                if (st) return st;
+                st = prefill_impl(P, l, off(b->q_chunk, rq), (void *)off(b->out_chunk, rq), lse,
+                                  stream);
+            }
             if (st) return st;
         }
         st = plan_commit(P);
         if (st) return st;
-    }
-    return MTN_OK;
+        std::vector<int32_t> sids, ones, rows;
+        for (int32_t j = 0; j < max_dec; ++j) {
+            sids.clear();
+            rows.clear();
+            for (int32_t i = 0; i < n; ++i)
+                if (b->n_decode[i] > j) {
+                    sids.push_back(b->sids[i]);
+                    rows.push_back(i);
+                }
+            ones.assign(sids.size(), 1);
+            st = plan_begin(P, (int32_t)sids.size(), sids.data(), ones.data(), rows.data(), stream);
+            if (st) return st;
+            for (int32_t l = 0; l < L; ++l) {
+                size_t base = ((size_t)j * L + l) * n;
+                float *lse = b->lse_dec ? b->lse_dec + base * Hq : nullptr;
+                st = decode_impl(P, l, off(b->q_dec, base * Hq * D),
+                                 (void *)off(b->out_dec, base * Hq * D), lse, b->n_split, stream,
+                                 off(b->k_dec, base * Hkv * D), off(b->v_dec, base * Hkv * D));
+                if (st) return st;
+            }
+            st = plan_commit(P);
+            if (st) return st;
+        }
+        return MTN_OK;
+    });
 }
 
 mtn_status mtn_pool_stats(const mtn_pool *P, mtn_pool_stats_t *out) {
@@ -957,71 +1044,79 @@ mtn_status mtn_plan_info(const mtn_pool *P, int64_t *pos, int32_t *block, int32_
 }
 
 mtn_status mtn_debug_poison_dead(mtn_pool *P, void *stream) {
-    if (!P) return MTN_ERR_INVALID_ARG;
-    if (P->host_only) return fail(P, MTN_ERR_BAD_STATE, "host-only pool has no device path");
-    if (P->plan_open) return fail(P, MTN_ERR_BAD_STATE, "plan open");
-    // live[b] bit o set <=> slot o of block b holds a retained position
-    std::vector<uint16_t> live((size_t)P->cfg.n_blocks, 0);
-    for (int32_t sid = 0; sid < P->cfg.max_sessions; ++sid) {
-        if (!P->is_open[sid]) continue;
-        const int32_t *row = &P->table[(size_t)sid * P->row_len];
-        int64_t L = P->len[sid];
-        int64_t lo = P->unbounded ? 0 : std::max<int64_t>(P->S, L - P->W);
-        auto mark = [&](int64_t p) {
-            int32_t lb, off;
-            logical_slot(P, p, &lb, &off);
-            if (row[lb] >= 0) live[(size_t)row[lb]] |= (uint16_t)(1u << off);
-        };
-        for (int64_t p = 0; p < std::min<int64_t>(P->S, L); ++p) mark(p);
-        for (int64_t p = lo; p < L; ++p) mark(p);
-    }
-    hipStream_t s = (hipStream_t)stream;
-    uint16_t *d_live = nullptr;
-    HIP_TRY(P, hipMalloc(&d_live, sizeof(uint16_t) * live.size()));
-    HIP_TRY(P, hipMemcpy(d_live, live.data(), sizeof(uint16_t) * live.size(),
-                         hipMemcpyHostToDevice));
-    if (P->cfg.kv_dtype == MTN_FP8_E4M3)
-        HIP_TRY(P, launch_poison_fp8(geom(P), P->cfg.n_layers, P->cfg.n_blocks, d_live, s));
-    else
-        HIP_TRY(P, launch_poison(P->cfg.kv_dtype, geom(P), P->cfg.n_layers, P->cfg.n_blocks, d_live, s));
-    HIP_TRY(P, hipStreamSynchronize(s));
-    HIP_TRY(P, hipFree(d_live));
-    return MTN_OK;
+    return guarded(P, [&]() -> mtn_status {
+        if (!P) return MTN_ERR_INVALID_ARG;
+        if (P->host_only) return fail(P, MTN_ERR_BAD_STATE, "host-only pool has no device path");
+        if (P->plan_open) return fail(P, MTN_ERR_BAD_STATE, "plan open");
+        // live[b] bit o set <=> slot o of block b holds a retained position
+        std::vector<uint16_t> live((size_t)P->cfg.n_blocks, 0);
+        for (int32_t sid = 0; sid < P->cfg.max_sessions; ++sid) {
+            if (!P->is_open[sid]) continue;
+            const int32_t *row = &P->table[(size_t)sid * P->row_len];
+            int64_t L = P->len[sid];
+            int64_t lo = P->unbounded ? 0 : std::max<int64_t>(P->S, L - P->W);
+            auto mark = [&](int64_t p) {
+                int32_t lb, off;
+                logical_slot(P, p, &lb, &off);
+                if (row[lb] >= 0) live[(size_t)row[lb]] |= (uint16_t)(1u << off);
+            };
+            for (int64_t p = 0; p < std::min<int64_t>(P->S, L); ++p) mark(p);
+            for (int64_t p = lo; p < L; ++p) mark(p);
+        }
+        hipStream_t s = (hipStream_t)stream;
+        uint16_t *d_live = nullptr;
+        HIP_TRY(P, hipMalloc(&d_live, sizeof(uint16_t) * live.size()));
+        HIP_TRY(P, hipMemcpy(d_live, live.data(), sizeof(uint16_t) * live.size(),
+                             hipMemcpyHostToDevice));
+        if (P->cfg.kv_dtype == MTN_FP8_E4M3)
+            HIP_TRY(P, launch_poison_fp8(geom(P), P->cfg.n_layers, P->cfg.n_blocks, d_live, s));
+        else
+            HIP_TRY(P, launch_poison(P->cfg.kv_dtype, geom(P), P->cfg.n_layers, P->cfg.n_blocks, d_live, s));
+        HIP_TRY(P, hipStreamSynchronize(s));
+        HIP_TRY(P, hipFree(d_live));
+        return MTN_OK;
+    });
 }
 
 mtn_status mtn_pool_set_prefill_pass_rows(mtn_pool *P, int32_t rows) {
-    if (!P) return MTN_ERR_INVALID_ARG;
-    if (rows != 0 && !prefill_pass_rows_valid(rows))
-        return fail(P, MTN_ERR_INVALID_ARG, "prefill pass rows must be 0, 128 or 256");
-    P->pf_rows_cfg = rows;
-    return MTN_OK;
+    return guarded(P, [&]() -> mtn_status {
+        if (!P) return MTN_ERR_INVALID_ARG;
+        if (rows != 0 && !prefill_pass_rows_valid(rows))
+            return fail(P, MTN_ERR_INVALID_ARG, "prefill pass rows must be 0, 128 or 256");
+        P->pf_rows_cfg = rows;
+        return MTN_OK;
+    });
 }
 
 mtn_status mtn_pool_set_timing(mtn_pool *P, int32_t enable) {
-    if (!P) return MTN_ERR_INVALID_ARG;
-    P->timing = enable != 0;
-    return MTN_OK;
+    return guarded(P, [&]() -> mtn_status {
+        if (!P) return MTN_ERR_INVALID_ARG;
+        P->timing = enable != 0;
+        return MTN_OK;
+    });
 }
 
 mtn_status mtn_pool_kernel_times(mtn_pool *P, int64_t *launches, double *ms) {
-    if (!P || !launches || !ms) return MTN_ERR_INVALID_ARG;
-    for (int c = 0; c < 4; ++c) {
-        for (auto &pr : P->ev_open[c]) {
-            HIP_TRY(P, hipEventSynchronize(pr.b));
-            float t = 0.f;
-            HIP_TRY(P, hipEventElapsedTime(&t, pr.a, pr.b));
-            P->t_ms[c] += t;
-            P->t_launch[c]++;
-            P->ev_spare.push_back(pr.a);
-            P->ev_spare.push_back(pr.b);
+    return guarded(P, [&]() -> mtn_status {
+        if (!P || !launches || !ms) return MTN_ERR_INVALID_ARG;
+        for (int c = 0; c < 4; ++c) {
+            for (auto &pr : P->ev_open[c]) {
+                HIP_TRY(P, hipEventSynchronize(pr.b));
+                float t = 0.f;
+                HIP_TRY(P, hipEventElapsedTime(&t, pr.a, pr.b));
+                P->t_ms[c] += t;
+                P->t_launch[c]++;
+                P->ev_spare.push_back(pr.a);
+                P->ev_spare.push_back(pr.b);
+            }
+            P->ev_open[c].clear();
+            launches[c] = P->t_launch[c];
+            ms[c] = P->t_ms[c];
+            P->t_launch[c] = 0;
+            P->t_ms[c] = 0.0;
         }
-        P->ev_open[c].clear();
-        launches[c] = P->t_launch[c];
-        ms[c] = P->t_ms[c];
-        P->t_launch[c] = 0;
-        P->t_ms[c] = 0.0;
-    }
-    return MTN_OK;
+        return MTN_OK;
+    });
 }
 
 mtn_status mtn_hbm_copy(const void *src, void *dst, size_t bytes, void *stream) {

@@ -183,3 +183,49 @@ def test_prefill_pass_rows_setting():
         with pytest.raises(mtn.MtnError) as e:
             pool.set_prefill_pass_rows(rows)
         assert e.value.code == mtn.MTN_ERR_INVALID_ARG
+
+
+def test_table_index_width_and_status_strings():
+    """Block-table entries are addressed with 32-bit indices: a configuration
+    whose table would pass 2^31 entries is refused at validation; every status
+    code has its own text."""
+    lib = mtn.load()
+    with pytest.raises(mtn.MtnError) as e:
+        mtn.Pool(n_layers=1, n_q_heads=4, n_kv_heads=2, head_dim=64, n_sink=4, window=(1 << 21),
+                 max_chunk=1, max_sessions=(1 << 14), n_blocks=10, dtype="f32", host_only=True)
+    assert e.value.code == mtn.MTN_ERR_INVALID_ARG
+    lib.mtn_status_string.restype = __import__("ctypes").c_char_p
+    texts = {lib.mtn_status_string(c) for c in range(-10, 1)}
+    assert len(texts) == 11 and b"unknown status" not in texts
+    assert lib.mtn_status_string(mtn.MTN_ERR_HOST_MEMORY) == b"host allocation failed"
+
+
+_OOM_CHILD = r"""
+import resource, sys
+sys.path.insert(0, sys.argv[1])
+import paper_2607_02640_amd as mtn
+mtn.load()
+with open("/proc/self/statm") as f:
+    vm = int(f.read().split()[0]) * resource.getpagesize()
+lim = vm + (512 << 20)
+resource.setrlimit(resource.RLIMIT_AS, (lim, lim))
+try:
+    # a 6 GiB host block table: far past the 512 MiB of headroom
+    mtn.Pool(n_layers=1, n_q_heads=4, n_kv_heads=2, head_dim=64, n_sink=0, window=2032,
+             max_chunk=1, max_sessions=(1 << 24), n_blocks=10, dtype="f32", host_only=True)
+    print("created")
+except mtn.MtnError as e:
+    print("code", e.code)
+"""
+
+
+def test_host_allocation_failure_returns_a_status():
+    """No C++ exception leaves the library: pool creation under an address
+    space limit too small for its host block table returns
+    MTN_ERR_HOST_MEMORY (the process survives)."""
+    import subprocess
+    import sys
+    r = subprocess.run([sys.executable, "-c", _OOM_CHILD, ROOT], capture_output=True, text=True,
+                       timeout=120)
+    assert r.returncode == 0, r.stderr[-2000:]
+    assert r.stdout.strip() == f"code {mtn.MTN_ERR_HOST_MEMORY}", r.stdout + r.stderr[-2000:]
