@@ -943,6 +943,11 @@ mtn_status mtn_frame_step(mtn_pool *P, const mtn_frame_batch *b, void *stream) {
         auto off = [&](const void *base, size_t elems) {
             return (const void *)((const uint8_t *)base + elems * e);
         };
+        // the decode rounds' batches, allocated before anything changes
+        std::vector<int32_t> sids, ones, rows;
+        sids.reserve((size_t)n);
+        ones.reserve((size_t)n);
+        rows.reserve((size_t)n);
         mtn_status st = plan_begin(P, n, b->sids, b->chunk_len, nullptr, stream);
         if (st) return st;
         for (int32_t l = 0; l < L; ++l) {
@@ -961,7 +966,6 @@ mtn_status mtn_frame_step(mtn_pool *P, const mtn_frame_batch *b, void *stream) {
         }
         st = plan_commit(P);
         if (st) return st;
-        std::vector<int32_t> sids, ones, rows;
         for (int32_t j = 0; j < max_dec; ++j) {
             sids.clear();
             rows.clear();
