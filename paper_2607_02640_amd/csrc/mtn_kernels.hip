@@ -1181,13 +1181,16 @@ __global__ __launch_bounds__(64 * kPfWaves) void k_prefill_mfma(PfArgs pa) {
                 for (int u = 0; u < kEpg; ++u) {
                     const int f = s * kEpg + u, i = f >> 3, e = f & 7;
                     p[i][e] = __builtin_amdgcn_exp2f((e < 4 ? sa[i][e] : sb[i][e - 4]) - m_ref[i]);
+                    // keep it in this group: without the pin the compiler sinks every
+                    // exponential below the last group, after the QK MFMAs
+                    asm volatile("" : "+v"(p[i][e]));
                 }
 #ifndef MTN_PF_NO_SCHED
                 if (s == 0) __builtin_amdgcn_sched_group_barrier(0x100, 8, 0);  // all K reads first
 #pragma unroll
                 for (int k = 0; k < 2 * NT; ++k) {
                     __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
-                    __builtin_amdgcn_sched_group_barrier(0x002, 2, 0);
+                    __builtin_amdgcn_sched_group_barrier(0x402, 2, 0);  // VALU or TRANS
                 }
                 __builtin_amdgcn_sched_barrier(0);
 #endif
