@@ -1133,6 +1133,19 @@ __global__ __launch_bounds__(64 * kPfWaves) void k_prefill_mfma(PfArgs pa) {
                 f8_stage_to_bf16(&ring[(st + 1) % kPfStages][0], stage_buf(st + 1), tid);
                 __syncthreads();
             }
+            // K fragments of stage st + 1.  bf16: read before the max test, whose
+            // instructions then cover their LDS latency (2.7-7.5 % per layer);
+            // fp8 measured no gain, its reads stay with the QK MFMAs
+            const uint8_t *nsm = stage_buf(st + 1);
+            uint4 kf[4][2];
+            auto load_kf = [&]() __attribute__((always_inline)) {
+#pragma unroll
+                for (int s = 0; s < 4; ++s) {
+                    kf[s][0] = *(const uint4 *)(nsm + koff[s]);
+                    kf[s][1] = *(const uint4 *)(nsm + koff[s] + 1024);
+                }
+            };
+            if constexpr (!F8) load_kf();
             // lazy reference max: lane-local test, row max only on a bump
             float m8[kPfTpw];
             bool bump = false;
@@ -1159,13 +1172,7 @@ __global__ __launch_bounds__(64 * kPfWaves) void k_prefill_mfma(PfArgs pa) {
             // stage's probabilities: in each of four groups, one MFMA then
             // two VALU instructions, so the exponentials run while the matrix
             // core works
-            const uint8_t *nsm = stage_buf(st + 1);
-            uint4 kf[4][2];
-#pragma unroll
-            for (int s = 0; s < 4; ++s) {
-                kf[s][0] = *(const uint4 *)(nsm + koff[s]);
-                kf[s][1] = *(const uint4 *)(nsm + koff[s] + 1024);
-            }
+            if constexpr (F8) load_kf();
             f32x4_t na[kPfTpw], nb[kPfTpw];
             float p[kPfTpw][8];
             constexpr int kEpg = 2 * NT;  // probabilities per group
