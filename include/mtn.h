@@ -11,8 +11,8 @@
  *   - Retention and masking: §4.1 and App. A ("Window half", "Sink half").  A
  *     query at absolute position t sees keys k <= t with k < S or k in the W
  *     positions ending at t.
- *   - Positions are absolute and never rebased (§4.1: the request keeps
- *     growing logically while only the bound is retained).
+ *   - Positions are absolute and never rebased (§4.1): eviction drops old
+ *     keys from memory but never renumbers the ones that stay.
  *   - Frame structure: §2, "The task model" (prefill the chunk, then decode up
  *     to tau tokens), batched over all due sessions (continuous batching).
  *   - Pool: App. A pins ceil(S / block) blocks per session and counts them in
@@ -27,7 +27,11 @@
  *   - `stream` is a hipStream_t passed as void* (NULL = the null stream).  All
  *     device work is asynchronous on it; device faults surface at the next
  *     synchronisation.  All calls that belong to one plan must use the same
- *     stream; a pool is driven from one host thread at a time.
+ *     stream (else MTN_ERR_INVALID_ARG).  A plan may use another stream than
+ *     the previous plan: mtn_plan_begin then makes the new stream wait for
+ *     everything issued on the previous plan's stream, because plans reuse
+ *     the library's device metadata and workspace.  A pool is driven from one
+ *     host thread at a time.
  *   - Layouts are row-major with the last index fastest.
  *   - Element types: MTN_F32 is IEEE binary32, MTN_BF16 is bfloat16.  The KV
  *     cache and q/k/v/out share one element type (kv_dtype == io_dtype),
@@ -77,8 +81,9 @@ enum { MTN_F32 = 0, MTN_BF16 = 1, MTN_FP8_E4M3 = 2 };
 /* flags */
 #define MTN_POOL_HOST_ONLY 1u /* no device work at all: planning, block tables
                                  and counters only (kv_dev may be NULL); every
-                                 append/attend call returns MTN_ERR_BAD_STATE
-                                 and plans commit without per-layer appends    */
+                                 append/attend call returns MTN_ERR_BAD_STATE,
+                                 plans commit without per-layer appends, and
+                                 mtn_frame_step plans without launching        */
 
 typedef struct mtn_pool mtn_pool; /* opaque; owned by the library */
 
@@ -123,10 +128,15 @@ typedef struct {
  */
 mtn_status mtn_pool_required_bytes(const mtn_pool_config *cfg, size_t *kv_bytes);
 
-/* Validates cfg, allocates the library's host state and its device metadata
- * and workspace (hipMalloc on the current device), and takes kv_dev (device,
- * caller-owned, >= required bytes, 256-byte aligned) as the pool.  The pool
- * contents are not initialised.  *out receives the handle.                    */
+/* One shared, paged KV pool for every session (§4.1: the windowed cache sits
+ * in the engine's paged pool; App. A: pinned sink blocks count against its
+ * capacity).  Validates cfg, allocates the library's host state and its
+ * device metadata and workspace (hipMalloc on the current device; the decode
+ * split partials take max_sessions * Hq * 64 * (D + 2) floats), and takes
+ * kv_dev (device, caller-owned, >= required bytes, 256-byte aligned) as the
+ * pool.  The pool contents are not initialised.  *out receives the handle.
+ * Errors: MTN_ERR_INVALID_ARG / MTN_ERR_UNSUPPORTED for cfg, MTN_ERR_DEVICE
+ * for a failed HIP allocation, MTN_ERR_HOST_MEMORY; nothing is kept.        */
 mtn_status mtn_pool_create(const mtn_pool_config *cfg, void *kv_dev, size_t kv_bytes,
                            void *stream, mtn_pool **out);
 
@@ -173,19 +183,36 @@ mtn_status mtn_plan_begin(mtn_pool *pool, int32_t n_seq, const int32_t *sids /*h
  * (their slots become reusable); nothing is moved.                            */
 mtn_status mtn_plan_commit(mtn_pool *pool);
 
+/* Abandon the open plan instead of committing it, e.g. after a per-layer call
+ * failed (failing cleanly instead of stalling every session, §3; or crashing
+ * them, App. B).  Every block the plan assigned returns to the pool: block
+ * tables, the free list (and so every later lowest-free assignment) and the
+ * counters are exactly as before mtn_plan_begin; lengths are unchanged.
+ * Device work already issued for the plan is not cancelled; it wrote only
+ * slots of positions at or past each session's length, which no later query
+ * can see before a later plan has written them again.  MTN_ERR_BAD_STATE
+ * when no plan is open.  mtn_frame_step calls it on any error inside a plan. */
+mtn_status mtn_plan_abort(mtn_pool *pool);
+
 /*
- * Fused RoPE + append + evict for one layer of the open plan.
+ * Fused RoPE + append + evict for one layer of the open plan (§4.1: keys keep
+ * the absolute position they were appended at; App. A: positions behind the
+ * window are not retained, sink blocks stay).
  * k, v: device, [T][Hkv][D] in kv_dtype, T = total planned tokens, packed in
  * plan order.  Each key row is rotated (rotate-half RoPE at its absolute
  * position, angle computed in fp64) and written with its value into the
  * token's slot of layer `layer`, overwriting whatever position left the window
- * there (eviction is slot reuse).
+ * there (eviction is slot reuse).  Errors: MTN_ERR_BAD_STATE (no open plan,
+ * host-only pool), MTN_ERR_INVALID_ARG (layer, null pointer, stream other
+ * than the plan's), MTN_ERR_DEVICE (launch).
  */
 mtn_status mtn_frame_append_kv(mtn_pool *pool, int32_t layer, const void *k, const void *v,
                                void *stream);
 
 /*
- * Chunk-prefill attention for one layer of the open plan (after its append).
+ * Chunk-prefill attention for one layer of the open plan (after its append):
+ * the frame's chunk attends causally inside itself and to the retained cache
+ * (§2, the task model; §4.1 and App. A for the per-query mask).
  * q, out: device, [T][Hq][D], packed like k/v.  Each planned query row at
  * position t is rotated at t and attends to sinks [0, min(S, t+1)) and window
  * [max(S, t-W+1), t] of its own session (all earlier chunk tokens included).
@@ -201,7 +228,8 @@ mtn_status mtn_attend_chunk_prefill(mtn_pool *pool, int32_t layer, const void *q
  * NULL.  The G query heads sharing a KV head read its sinks ∪ window once;
  * n_split > 1 splits the keys into segments merged by log-sum-exp, sinks in
  * segment 0 only (App. A segmented decode).  n_split = 0 picks a split from
- * the batch size; 1 <= n_split <= 64 forces it.
+ * the batch size; 1 <= n_split <= 64 forces it (the workspace holds 64
+ * segments of every query; mtn_pool_last_split reports the split used).
  */
 mtn_status mtn_attend_decode(mtn_pool *pool, int32_t layer, const void *q, void *out,
                              float *lse, int32_t n_split, void *stream);
@@ -226,6 +254,12 @@ mtn_status mtn_attend_decode_append(mtn_pool *pool, int32_t layer, const void *k
  * decode round j (only sessions with n_decode[i] > j) plan one token, for each
  * layer append + decode attend (one launch, as mtn_attend_decode_append),
  * commit.  Chunks of one token everywhere use the decode kernel the same way.
+ * Every host check (sessions, sizes, and block capacity for the whole frame)
+ * runs before the first plan.  An error inside a plan (a failed launch)
+ * abandons that plan as mtn_plan_abort does; plans of the frame that already
+ * committed stay committed (each session's length tells how far it got), and
+ * output rows of unfinished plans are undefined.  On a host-only pool the
+ * frame is planned and committed without device work (buffers may be NULL).
  */
 typedef struct {
     int32_t        n_seq;
@@ -291,6 +325,24 @@ mtn_status mtn_debug_poison_dead(mtn_pool *pool, void *stream);
  * Takes effect at the next mtn_plan_begin.  Results are the same either way
  * up to fp32 summation order.  Other values: MTN_ERR_INVALID_ARG.            */
 mtn_status mtn_pool_set_prefill_pass_rows(mtn_pool *pool, int32_t rows);
+
+/* Test / tuning: the decode kernel.  0 (default) chooses by shape; 1 forces
+ * the vector kernel (fp32 and bf16 pools); 2 forces the matrix-core kernel
+ * (bf16 pools with head_dim 128; FP8 pools always use it).  Takes effect at
+ * the next launch; results agree up to fp32 summation order.
+ * MTN_ERR_UNSUPPORTED where the kernel does not exist for the pool,
+ * MTN_ERR_BAD_STATE while a plan is open.                                    */
+mtn_status mtn_pool_set_decode_kernel(mtn_pool *pool, int32_t kind);
+
+/* Key segments (split) of the most recent decode launch of this pool.        */
+mtn_status mtn_pool_last_split(const mtn_pool *pool, int32_t *n_split);
+
+/* Test hook: the launch point with index launch_index (0 = the next one)
+ * among this pool's later append / prefill / decode launch points fails with
+ * MTN_ERR_DEVICE before launching; -1 disarms.  Host-only pools pass through
+ * the same points inside mtn_frame_step, so error paths can be exercised on a
+ * host without a GPU.                                                        */
+mtn_status mtn_debug_inject_failure(mtn_pool *pool, int64_t launch_index);
 
 /* Per-kernel device timing.  When enabled, the library records HIP events
  * around each launch it makes and accumulates per-kernel-class totals;

@@ -103,6 +103,7 @@ class IndexModel:
         self.plan: Optional[List[Tuple[int, int]]] = None
         self.plan_tokens: List[PlannedToken] = []
         self.plan_evicted: List[Tuple[int, int]] = []
+        self.plan_fresh: List[Tuple[int, int]] = []   # (sid, logical block) the plan assigned
 
     # -- slot map ----------------------------------------------------------
     def logical_slot(self, pos: int) -> Tuple[int, int]:
@@ -168,6 +169,7 @@ class IndexModel:
         if need > len(self.free):
             raise IndexError_(ERR_POOL_EXHAUSTED, "pool exhausted")
         toks: List[PlannedToken] = []
+        fresh: List[Tuple[int, int]] = []
         for sid, n in zip(sids, n_tok):
             L = self.sessions[sid].length
             row = self.sessions[sid].row
@@ -175,7 +177,9 @@ class IndexModel:
                 lb, off = self.logical_slot(p)
                 if row[lb] < 0:
                     row[lb] = heapq.heappop(self.free)
+                    fresh.append((sid, lb))
                 toks.append(PlannedToken(sid, p, row[lb], off))
+        self.plan_fresh = fresh
         self.plan = list(zip(sids, n_tok))
         self.plan_tokens = toks
         ev = []
@@ -194,6 +198,20 @@ class IndexModel:
         for sid, n in self.plan:
             self.sessions[sid].length += n
         self.plan = None
+        self.plan_fresh = []
+
+    def plan_abort(self) -> None:
+        """Abandon the open plan: the blocks it assigned go back to the free
+        set, so the pool (and every later lowest-free choice) is as if the
+        plan had never begun; lengths do not move."""
+        if self.plan is None:
+            raise IndexError_(ERR_BAD_STATE, "no plan")
+        for sid, lb in reversed(self.plan_fresh):
+            row = self.sessions[sid].row
+            heapq.heappush(self.free, row[lb])
+            row[lb] = -1
+        self.plan = None
+        self.plan_fresh = []
 
     # -- observability -----------------------------------------------------
     def assigned(self) -> int:

@@ -8,8 +8,8 @@ What it computes (Metronome, arXiv 2607.02640):
   tokens pinned plus its most recent W tokens; the attention mask of a query at
   absolute position t admits keys in [0, S) together with the window that ends
   at t, always under causality (k <= t).
-* §4.1: the resident request keeps growing logically; positions are absolute
-  and are never rebased after eviction.
+* §4.1: positions are absolute; eviction removes old keys from memory but
+  never renumbers the ones that remain.
 * §2, "The task model": each frame appends (prefills) a chunk of new tokens and
   then decodes up to tau tokens, one at a time.
 * App. A: visiting the sink keys first (or in any other order) is exact,

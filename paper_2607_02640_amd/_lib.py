@@ -40,11 +40,13 @@ MTN_POOL_HOST_ONLY = 1
 EXPORTS = [
     "mtn_pool_required_bytes", "mtn_pool_create", "mtn_pool_destroy",
     "mtn_session_open", "mtn_session_close", "mtn_plan_begin", "mtn_plan_commit",
+    "mtn_plan_abort",
     "mtn_frame_append_kv", "mtn_attend_chunk_prefill", "mtn_attend_decode",
     "mtn_attend_decode_append",
     "mtn_frame_step", "mtn_pool_stats", "mtn_session_info", "mtn_session_block_table",
     "mtn_plan_info", "mtn_debug_poison_dead", "mtn_pool_set_timing", "mtn_pool_set_prefill_pass_rows",
     "mtn_pool_kernel_times", "mtn_hbm_copy", "mtn_status_string", "mtn_pool_last_error",
+    "mtn_pool_set_decode_kernel", "mtn_pool_last_split", "mtn_debug_inject_failure",
     "mtn_admission_create", "mtn_admission_destroy", "mtn_admission_offer",
     "mtn_admission_release", "mtn_admission_observe", "mtn_admission_get",
 ]
@@ -121,6 +123,10 @@ def load() -> C.CDLL:
         "mtn_session_close": (i32, [vp, i32]),
         "mtn_plan_begin": (i32, [vp, i32, P32, P32, vp]),
         "mtn_plan_commit": (i32, [vp]),
+        "mtn_plan_abort": (i32, [vp]),
+        "mtn_pool_set_decode_kernel": (i32, [vp, i32]),
+        "mtn_pool_last_split": (i32, [vp, P32]),
+        "mtn_debug_inject_failure": (i32, [vp, i64]),
         "mtn_frame_append_kv": (i32, [vp, i32, vp, vp, vp]),
         "mtn_attend_chunk_prefill": (i32, [vp, i32, vp, vp, vp, vp]),
         "mtn_attend_decode": (i32, [vp, i32, vp, vp, vp, i32, vp]),
@@ -263,6 +269,21 @@ class Pool:
     def plan_commit(self) -> None:
         self._check(self.lib.mtn_plan_commit(self.h), "plan_commit")
 
+    def plan_abort(self) -> None:
+        self._check(self.lib.mtn_plan_abort(self.h), "plan_abort")
+
+    def set_decode_kernel(self, kind: int) -> None:
+        """0 = by shape, 1 = vector kernel, 2 = matrix-core kernel."""
+        self._check(self.lib.mtn_pool_set_decode_kernel(self.h, kind), "set_decode_kernel")
+
+    def last_split(self) -> int:
+        n = C.c_int32()
+        self._check(self.lib.mtn_pool_last_split(self.h, C.byref(n)), "last_split")
+        return n.value
+
+    def inject_failure(self, launch_index: int) -> None:
+        self._check(self.lib.mtn_debug_inject_failure(self.h, launch_index), "inject_failure")
+
     def frame_append_kv(self, layer, k, v, stream=None) -> None:
         self._check(self.lib.mtn_frame_append_kv(self.h, layer, _ptr(k), _ptr(v), _stream(stream)),
                     "frame_append_kv")
@@ -293,7 +314,9 @@ class Pool:
         b.q_dec, b.k_dec, b.v_dec = _ptr(q_dec), _ptr(k_dec), _ptr(v_dec)
         b.out_dec, b.lse_dec = _ptr(out_dec), _ptr(lse_dec)
         b.n_split = n_split
-        self._check(self.lib.mtn_frame_step(self.h, C.byref(b), _stream(stream)), "frame_step")
+        self._check(self.lib.mtn_frame_step(self.h, C.byref(b),
+                                            None if self.host_only else _stream(stream)),
+                    "frame_step")
 
     def stats(self) -> dict:
         s = PoolStats()

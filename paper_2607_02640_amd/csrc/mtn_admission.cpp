@@ -27,7 +27,7 @@ mtn_status mtn_admission_create(const mtn_admission_config *cfg, mtn_admission *
         cfg->max_cap < cfg->initial_cap || cfg->hold_ticks < 0)
         return MTN_ERR_INVALID_ARG;
     mtn_admission *a = new (std::nothrow) mtn_admission;
-    if (!a) return MTN_ERR_INVALID_ARG;
+    if (!a) return MTN_ERR_HOST_MEMORY;
     a->cfg = *cfg;
     a->cap = cfg->initial_cap;
     *out = a;

@@ -69,27 +69,33 @@ __device__ __forceinline__ float shfl_xor_f(float x, int m) {
 }
 
 // Exchange between rows (16-lane groups) with the gfx950 permlane swaps.
-// With b a copy of a, `v_permlane16_swap a, b` leaves rows (0, 0, 2, 2) of the
-// input in a and rows (1, 1, 3, 3) in b; `v_permlane32_swap a, b` leaves rows
-// (0, 1, 0, 1) and (2, 3, 2, 3): combining a and b reduces across the pair.
-// Pure VALU, no LDS round trip.  The copy, the swap and explicit wait states
-// on both sides are one asm statement: with the copy issued as separate
-// inline asm three instructions before the swap, rows 1 and 3 of a sum came
-// out wrong (the swap took a stale copy), and the compiler cannot space
-// instructions it does not see.
+// Given (a, a), v_permlane16_swap returns rows (0, 0, 2, 2) of a in its first
+// result and rows (1, 1, 3, 3) in its second; v_permlane32_swap returns rows
+// (0, 1, 0, 1) and (2, 3, 2, 3): combining the two reduces across the pair.
+// Pure VALU, no LDS round trip.  Only the compiler builtins are used, never
+// inline assembly: the swap reads both of its operands and writes both, and
+// a VALU write of either operand needs wait states before the swap.  The
+// compiler's hazard recognizer inserts those (and the MFMA-result wait states
+// when an operand comes from a matrix instruction) only for instructions it
+// sees; an inline-asm copy feeding the swap was invisible to it, and rows 1
+// and 3 -- the rows a swap takes from its second operand -- then read a stale
+// copy.
 template <bool HALF>
-__device__ __forceinline__ void row_swap(unsigned &a, unsigned &b) {
-    if constexpr (HALF)
-        asm volatile("v_mov_b32 %1, %0\n\ts_nop 7\n\tv_permlane32_swap_b32 %0, %1\n\ts_nop 7"
-                     : "+v"(a), "=&v"(b));
-    else
-        asm volatile("v_mov_b32 %1, %0\n\ts_nop 7\n\tv_permlane16_swap_b32 %0, %1\n\ts_nop 7"
-                     : "+v"(a), "=&v"(b));
+__device__ __forceinline__ void row_swap(unsigned x, unsigned &a, unsigned &b) {
+    if constexpr (HALF) {
+        const auto r = __builtin_amdgcn_permlane32_swap(x, x, false, false);
+        a = r[0];
+        b = r[1];
+    } else {
+        const auto r = __builtin_amdgcn_permlane16_swap(x, x, false, false);
+        a = r[0];
+        b = r[1];
+    }
 }
 template <bool SUM, bool HALF>
 __device__ __forceinline__ float rows_pair(float x) {
-    unsigned a = __builtin_bit_cast(unsigned, x), b;
-    row_swap<HALF>(a, b);
+    unsigned a, b;
+    row_swap<HALF>(__builtin_bit_cast(unsigned, x), a, b);
     const float fa = __builtin_bit_cast(float, a), fb = __builtin_bit_cast(float, b);
     return SUM ? fa + fb : fmaxf(fa, fb);
 }
@@ -217,6 +223,9 @@ struct BlockIter {
 // of the wave writes LDS bytes [lds + 16 i, lds + 16 i + 16).  Issued from
 // inline assembly so that the compiler does not guard later LDS reads with a
 // full vmcnt(0); completion is awaited explicitly with vm_wait<N>().
+// The M0 write and the load are one asm statement, with the wait state the
+// hardware needs between an SALU write of M0 and an LDS DMA that reads it
+// (the compiler inserts the same s_nop for its own LDS-DMA builtin).
 // The K/V stream is read exactly once per launch: non-temporal ("nt") loads
 // keep it from displacing reused lines in the caches (measured +2 % on the
 // 128-session decode).
@@ -226,6 +235,7 @@ struct BlockIter {
 __device__ __forceinline__ void dma16(const void *gptr, uint32_t lds) {
     asm volatile(
         "s_mov_b32 m0, %1\n\t"
+        "s_nop 0\n\t"
         "global_load_lds_dwordx4 %0, off " MTN_DMA_POLICY
         :
         : "v"(gptr), "s"(__builtin_amdgcn_readfirstlane(lds))
@@ -245,6 +255,7 @@ __device__ __forceinline__ void dma16_s(uint32_t voff, const void *sbase, uint32
     const uint64_t sb = (uint64_t)lo | ((uint64_t)hi << 32);
     asm volatile(
         "s_mov_b32 m0, %2\n\t"
+        "s_nop 0\n\t"
         "global_load_lds_dwordx4 %0, %1 " MTN_DMA_POLICY
         :
         : "v"(voff), "s"(sb), "s"(__builtin_amdgcn_readfirstlane(lds))
@@ -289,25 +300,17 @@ __device__ __forceinline__ f32x4_t mfma16x16x32(const uint4 &a, const uint4 &b, 
     return __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8_t, a),
                                                     __builtin_bit_cast(bf16x8_t, b), c, 0, 0, 0);
 }
-// Plain v_max3_f32 / v_max_f32.  Scores are finite or -inf (masked), never
-// NaN, so the NaN-quieting the compiler adds around fmaxf is not needed.
+// Maxima written as ordinary code, so that the compiler sees every read of
+// a matrix-instruction result and spaces it as the hardware requires (inline
+// assembly reading an MFMA accumulator is issued with no wait states).  Three
+// operands map to one v_max3_f32.
 __device__ __forceinline__ float vmax3(float a, float b, float c) {
-    float r;
-    asm("v_max3_f32 %0, %1, %2, %3" : "=v"(r) : "v"(a), "v"(b), "v"(c));
-    return r;
+    return fmaxf(fmaxf(a, b), c);
 }
-__device__ __forceinline__ float vmax2(float a, float b) {
-    float r;
-    asm("v_max_f32 %0, %1, %2" : "=v"(r) : "v"(a), "v"(b));
-    return r;
-}
+__device__ __forceinline__ float vmax2(float a, float b) { return fmaxf(a, b); }
 // max over the four 16-lane rows (lanes with equal lane % 16)
 __device__ __forceinline__ float rows_max(float x) {
-    unsigned a = __builtin_bit_cast(unsigned, x), b;
-    row_swap<false>(a, b);
-    unsigned c = __builtin_bit_cast(unsigned, vmax2(__builtin_bit_cast(float, a), __builtin_bit_cast(float, b)));
-    row_swap<true>(c, b);
-    return vmax2(__builtin_bit_cast(float, c), __builtin_bit_cast(float, b));
+    return rows_pair<false, true>(rows_pair<false, false>(x));
 }
 
 }  // namespace

@@ -118,6 +118,18 @@ struct mtn_pool {
     int32_t n_cu = 0;              // compute units of the pool's device
     int32_t pf_rows_cfg = 0;       // chunk-prefill rows per pass: 0 = chosen per plan
     int32_t pf_rows = 0;           // ... of the open plan
+    int32_t decode_kernel = 0;     // 0 automatic, 1 vector, 2 matrix (test / tuning hook)
+    int32_t last_split = 0;        // key segments of the most recent decode launch
+
+    // stream order between plans: the per-plan device buffers (metadata, RoPE
+    // table, split partials) are reused by the next plan, so a plan on another
+    // stream first waits for everything issued on the previous plan's stream
+    hipEvent_t order_ev = nullptr;
+    bool have_last_stream = false;
+    void *last_stream = nullptr;
+
+    // failure injection (test hook): the launch point with this index fails
+    int64_t fail_at = -1;
 
     // timing
     bool timing = false;
@@ -278,6 +290,51 @@ mtn_status timing_end(mtn_pool *P, int cls, hipEvent_t a, hipStream_t s) {
     return MTN_OK;
 }
 
+// Return the blocks of the open plan's assignments (table index, physical
+// block) to the pool, newest first.  The bitmap allocator then holds exactly
+// its pre-plan free set, so later assignments are those of a pool that never
+// saw the plan.  The device copy of the table keeps the stale entries, as
+// after a session close: no kernel reads a logical block before a plan that
+// assigns it again has uploaded the new entry.
+void undo_assignments(mtn_pool *P) noexcept {
+    for (size_t i = P->upd_idx.size(); i-- > 0;) {
+        const int32_t idx = P->upd_idx[i];
+        const int32_t sid = idx / P->row_len;
+        P->table[(size_t)idx] = -1;
+        P->alloc.give(P->upd_val[i]);
+        P->n_assigned[sid]--;
+        P->assigned--;
+    }
+    P->upd_idx.clear();
+    P->upd_val.clear();
+    if (P->unbounded) P->reserved = P->assigned;
+}
+
+// Abandon the open plan (nothing is committed).  Device work already issued
+// for it wrote only slots of positions at or past each session's length;
+// within one plan (at most max_chunk tokens per session) such a slot held
+// no position that a later query can see, and the next plan over those
+// positions writes them again before any query reads them.
+void plan_abort_impl(mtn_pool *P) noexcept {
+    undo_assignments(P);
+    P->plan_open = false;
+    P->n_seq = 0;
+    P->T = 0;
+}
+
+// A point where device work is launched; the injected failure (test hook)
+// fires here.  Host-only pools pass through the same points without launching.
+mtn_status launch_gate(mtn_pool *P) {
+    if (P->fail_at >= 0) {
+        if (P->fail_at == 0) {
+            P->fail_at = -1;
+            return fail(P, MTN_ERR_DEVICE, "injected failure");
+        }
+        P->fail_at--;
+    }
+    return MTN_OK;
+}
+
 // Internal plan begin.  rows == nullptr packs io rows in plan order.
 mtn_status plan_begin(mtn_pool *P, int32_t n_seq, const int32_t *sids, const int32_t *n_tok,
                       const int32_t *rows, void *stream) {
@@ -315,6 +372,12 @@ mtn_status plan_begin(mtn_pool *P, int32_t n_seq, const int32_t *sids, const int
         int si = P->stage_i;
         if (P->stage_used[si]) HIP_TRY(P, hipEventSynchronize(P->stage_ev[si]));
         stage = P->h_stage[si];
+        if (P->have_last_stream && stream != P->last_stream) {
+            HIP_TRY(P, hipEventRecord(P->order_ev, (hipStream_t)P->last_stream));
+            HIP_TRY(P, hipStreamWaitEvent((hipStream_t)stream, P->order_ev, 0));
+        }
+        P->have_last_stream = true;
+        P->last_stream = stream;
     }
     // ---- assignment (lowest free first, plan order)
     P->n_seq = n_seq;
@@ -403,8 +466,15 @@ mtn_status plan_begin(mtn_pool *P, int32_t n_seq, const int32_t *sids, const int
     put(P->pf_items.data(), (int32_t)P->pf_items.size());
     hipStream_t s = (hipStream_t)stream;
     int32_t *d = P->d_meta;
-    HIP_TRY(P, hipMemcpyAsync(d, h, o * sizeof(int32_t), hipMemcpyHostToDevice, s));
-    HIP_TRY(P, hipEventRecord(P->stage_ev[P->stage_i], s));
+    // a failed upload abandons the plan: the pool is as before the call
+    auto upload_fail = [&](hipError_t e, const char *where) {
+        plan_abort_impl(P);
+        return hip_fail(P, e, where);
+    };
+    hipError_t he = hipMemcpyAsync(d, h, o * sizeof(int32_t), hipMemcpyHostToDevice, s);
+    if (he != hipSuccess) return upload_fail(he, "plan upload");
+    he = hipEventRecord(P->stage_ev[P->stage_i], s);
+    if (he != hipSuccess) return upload_fail(he, "plan upload event");
     P->stage_used[P->stage_i] = true;
     P->stage_i = (P->stage_i + 1) % kStages;
     P->view.tok_sid = d;
@@ -418,8 +488,9 @@ mtn_status plan_begin(mtn_pool *P, int32_t n_seq, const int32_t *sids, const int
     P->view.n_tok = (int32_t)T;
     const int32_t *d_upd_idx = d + 5 * T + 2 * n_seq;
     P->d_pf_items = d + 5 * T + 2 * n_seq + 2 * U;
-    HIP_TRY(P, launch_plan_apply(d_upd_idx, d_upd_idx + U, U, P->d_table, P->view.tok_pos,
-                                 (int32_t)T, P->d_inv_freq, P->cfg.head_dim / 2, P->d_rope, s));
+    he = launch_plan_apply(d_upd_idx, d_upd_idx + U, U, P->d_table, P->view.tok_pos, (int32_t)T,
+                           P->d_inv_freq, P->cfg.head_dim / 2, P->d_rope, s);
+    if (he != hipSuccess) return upload_fail(he, "launch_plan_apply");
     return MTN_OK;
 }
 
@@ -462,9 +533,15 @@ mtn_status check_call(mtn_pool *P, int32_t layer, void *stream) {
 }
 
 mtn_status append_impl(mtn_pool *P, int32_t layer, const void *k, const void *v, void *stream) {
+    mtn_status st = launch_gate(P);
+    if (st) return st;
+    if (P->host_only) {  // frame_step on a host-only pool: planning only
+        P->layer_done[layer] = 1;
+        return MTN_OK;
+    }
     hipStream_t s = (hipStream_t)stream;
     hipEvent_t e0;
-    mtn_status st = timing_begin(P, s, &e0);
+    st = timing_begin(P, s, &e0);
     if (st) return st;
     if (P->cfg.kv_dtype == MTN_FP8_E4M3)
         HIP_TRY(P, launch_append_fp8(geom(P), P->view, layer, k, v, s));
@@ -500,13 +577,22 @@ AttnArgs attn_args(mtn_pool *P, int32_t layer, const void *q, void *out, float *
 // for the vector kernel; at the 64-session G = 1 and 256-session G = 4 shapes
 // the vector kernel's one-wave workgroups win (6.86 and 6.68 TB/s against
 // 6.61 and 6.53).
+// mtn_pool_set_decode_kernel can force either kernel where it exists.
 bool use_mfma_bf16(const mtn_pool *P) {
-#ifdef MTN_BF16_DECODE_VALU
-    return false;
-#else
-    return P->cfg.kv_dtype == MTN_BF16 && P->G == 8 &&
-           attn_mfma_bf16_supported(P->cfg.head_dim, P->G);
-#endif
+    if (P->cfg.kv_dtype != MTN_BF16 || !attn_mfma_bf16_supported(P->cfg.head_dim, P->G))
+        return false;
+    if (P->decode_kernel == 1) return false;
+    if (P->decode_kernel == 2) return true;
+    return P->G == 8;
+}
+
+// decode work units resident on the whole GPU for the pool's decode kernel
+int32_t count_resident_units(const mtn_pool *P) {
+    const mtn_pool_config &c = P->cfg;
+    const int per_cu = c.kv_dtype == MTN_FP8_E4M3 ? attn_fp8_resident_per_cu(P->G)
+                       : use_mfma_bf16(P)         ? attn_mfma_bf16_resident_per_cu(P->G)
+                                                  : attn_valu_resident_per_cu(c.kv_dtype, c.head_dim, P->G);
+    return P->n_cu * per_cu;
 }
 
 // Decode split heuristic.  A unit (query, kv head, segment) streams its keys
@@ -528,24 +614,34 @@ int32_t auto_split(const mtn_pool *P, int32_t n_items) {
 
 // k_new / v_new non-null: the decode also appends the planned tokens of this
 // layer (each is the newest key of its own query), in the same launch.
+// The split partials workspace holds kMaxSplit segments of every query a
+// plan can carry (max_sessions), so every split 1 <= n_split <= kMaxSplit runs
+// as asked.
 mtn_status decode_impl(mtn_pool *P, int32_t layer, const void *q, void *out, float *lse,
                        int32_t n_split, void *stream, const void *k_new = nullptr,
-                       const void *v_new = nullptr) {
+                       const void *v_new = nullptr, float *part = nullptr,
+                       size_t part_floats = 0) {
+    mtn_status st = launch_gate(P);
+    if (st) return st;
+    if (P->host_only) {  // frame_step on a host-only pool: planning only
+        if (k_new) P->layer_done[layer] = 1;
+        return MTN_OK;
+    }
     hipStream_t s = (hipStream_t)stream;
     if (n_split == 0) n_split = auto_split(P, P->T);
-    int64_t need = (int64_t)P->T * P->cfg.n_q_heads * n_split * (P->cfg.head_dim + 2);
-    if (n_split > 1 && (size_t)need > P->part_floats) {
-        // fall back to the largest split the workspace holds
-        n_split = (int32_t)std::max<int64_t>(
-            1, (int64_t)P->part_floats /
-                   ((int64_t)P->T * P->cfg.n_q_heads * (P->cfg.head_dim + 2)));
-        n_split = std::min(n_split, kMaxSplit);
+    if (!part) {
+        part = P->d_part;
+        part_floats = P->part_floats;
     }
+    if (n_split > 1 &&
+        (size_t)P->T * P->cfg.n_q_heads * n_split * (P->cfg.head_dim + 2) > part_floats)
+        return fail(P, MTN_ERR_INVALID_ARG, "split partials exceed the workspace");
     AttnArgs a = attn_args(P, layer, q, out, lse, n_split);
+    a.part = part;
     a.k_new = k_new;
     a.v_new = v_new;
     hipEvent_t e0;
-    mtn_status st = timing_begin(P, s, &e0);
+    st = timing_begin(P, s, &e0);
     if (st) return st;
     if (P->cfg.kv_dtype == MTN_FP8_E4M3)
         HIP_TRY(P, launch_attn_fp8(a, s));
@@ -555,6 +651,7 @@ mtn_status decode_impl(mtn_pool *P, int32_t layer, const void *q, void *out, flo
         HIP_TRY(P, launch_attn_valu(P->cfg.kv_dtype, a, s));
     st = timing_end(P, 2, e0, s);
     if (st) return st;
+    P->last_split = n_split;
     if (k_new) P->layer_done[layer] = 1;
     if (n_split > 1) {
         st = timing_begin(P, s, &e0);
@@ -570,9 +667,12 @@ mtn_status prefill_impl(mtn_pool *P, int32_t layer, const void *q, void *out, fl
                         void *stream) {
     hipStream_t s = (hipStream_t)stream;
     if (P->all_single) return decode_impl(P, layer, q, out, lse, 0, stream);
+    mtn_status st = launch_gate(P);
+    if (st) return st;
+    if (P->host_only) return MTN_OK;
     AttnArgs a = attn_args(P, layer, q, out, lse, 1);
     hipEvent_t e0;
-    mtn_status st = timing_begin(P, s, &e0);
+    st = timing_begin(P, s, &e0);
     if (st) return st;
     if (prefill_mfma_supported(P->cfg.kv_dtype, P->cfg.head_dim, P->G)) {
         HIP_TRY(P, launch_prefill_mfma(P->cfg.kv_dtype, a, P->d_seq_first, P->d_seq_ntok, P->d_pf_items,
@@ -581,6 +681,63 @@ mtn_status prefill_impl(mtn_pool *P, int32_t layer, const void *q, void *out, fl
         HIP_TRY(P, launch_attn_valu(P->cfg.kv_dtype, a, s));
     }
     return timing_end(P, 1, e0, s);
+}
+
+// The plans of one frame (after mtn_frame_step's validation): the chunk plan
+// with every layer's append + chunk prefill (or the fused one-token decode),
+// then one plan per decode round.  Returns at the first error, with the
+// failing plan still open.
+mtn_status frame_plans(mtn_pool *P, const mtn_frame_batch *b, void *stream, int64_t Tc,
+                       int32_t max_dec, std::vector<int32_t> &sids, std::vector<int32_t> &ones,
+                       std::vector<int32_t> &rows) {
+    const int32_t n = b->n_seq, L = P->cfg.n_layers;
+    const int32_t Hq = P->cfg.n_q_heads, Hkv = P->cfg.n_kv_heads;
+    const size_t e = P->elt, D = (size_t)P->cfg.head_dim;
+    // host-only pools take null buffers: no offset is formed from them
+    auto off = [&](const void *base, size_t elems) -> const void * {
+        return base ? (const void *)((const uint8_t *)base + elems * e) : nullptr;
+    };
+    mtn_status st = plan_begin(P, n, b->sids, b->chunk_len, nullptr, stream);
+    if (st) return st;
+    for (int32_t l = 0; l < L; ++l) {
+        const size_t rq = (size_t)l * Tc * Hq * D, rk = (size_t)l * Tc * Hkv * D;
+        float *lse = b->lse_chunk ? b->lse_chunk + (size_t)l * Tc * Hq : nullptr;
+        if (P->all_single) {  // one-token chunks: decode with the append fused in
+            st = decode_impl(P, l, off(b->q_chunk, rq), (void *)off(b->out_chunk, rq), lse,
+                             b->n_split, stream, off(b->k_chunk, rk), off(b->v_chunk, rk));
+        } else {
+            st = append_impl(P, l, off(b->k_chunk, rk), off(b->v_chunk, rk), stream);
+            if (st) return st;
+            st = prefill_impl(P, l, off(b->q_chunk, rq), (void *)off(b->out_chunk, rq), lse,
+                              stream);
+        }
+        if (st) return st;
+    }
+    st = plan_commit(P);
+    if (st) return st;
+    for (int32_t j = 0; j < max_dec; ++j) {
+        sids.clear();
+        rows.clear();
+        for (int32_t i = 0; i < n; ++i)
+            if (b->n_decode[i] > j) {
+                sids.push_back(b->sids[i]);
+                rows.push_back(i);
+            }
+        ones.assign(sids.size(), 1);
+        st = plan_begin(P, (int32_t)sids.size(), sids.data(), ones.data(), rows.data(), stream);
+        if (st) return st;
+        for (int32_t l = 0; l < L; ++l) {
+            const size_t base = ((size_t)j * L + l) * n;
+            float *lse = b->lse_dec ? b->lse_dec + base * Hq : nullptr;
+            st = decode_impl(P, l, off(b->q_dec, base * Hq * D),
+                             (void *)off(b->out_dec, base * Hq * D), lse, b->n_split, stream,
+                             off(b->k_dec, base * Hkv * D), off(b->v_dec, base * Hkv * D));
+            if (st) return st;
+        }
+        st = plan_commit(P);
+        if (st) return st;
+    }
+    return MTN_OK;
 }
 
 mtn_status pool_init(mtn_pool *P, const mtn_pool_config *cfg, void *kv_dev, void *stream);
@@ -738,7 +895,7 @@ mtn_status pool_init(mtn_pool *P, const mtn_pool_config *cfg, void *kv_dev, void
         if ((e = hipMalloc(&P->d_zero, kZeroPage)) != hipSuccess) return bail(e, "zero page");
         if ((e = hipMemsetAsync(P->d_zero, 0, kZeroPage, (hipStream_t)stream)) != hipSuccess)
             return bail(e, "zero page clear");
-        P->part_floats = (size_t)cfg->max_sessions * cfg->n_q_heads * 32 * (cfg->head_dim + 2);
+        P->part_floats = (size_t)cfg->max_sessions * cfg->n_q_heads * kMaxSplit * (cfg->head_dim + 2);
         if ((e = hipMalloc(&P->d_part, sizeof(float) * P->part_floats)) != hipSuccess)
             return bail(e, "partials");
         int dev = 0, n_cu = 0;
@@ -747,10 +904,9 @@ mtn_status pool_init(mtn_pool *P, const mtn_pool_config *cfg, void *kv_dev, void
             hipSuccess)
             return bail(e, "cu count");
         P->n_cu = n_cu;
-        P->resident_units =
-            n_cu * (cfg->kv_dtype == MTN_FP8_E4M3 ? attn_fp8_resident_per_cu(P->G)
-                    : use_mfma_bf16(P)            ? attn_mfma_bf16_resident_per_cu(P->G)
-                                                  : attn_valu_resident_per_cu(cfg->kv_dtype, cfg->head_dim, P->G));
+        P->resident_units = count_resident_units(P);
+        if ((e = hipEventCreateWithFlags(&P->order_ev, hipEventDisableTiming)) != hipSuccess)
+            return bail(e, "event");
         if ((e = hipStreamSynchronize((hipStream_t)stream)) != hipSuccess)
             return bail(e, "sync");
     }
@@ -781,6 +937,7 @@ void mtn_pool_destroy(mtn_pool *P) {
                 (void)hipEventDestroy(pr.b);
             }
         for (auto e : P->ev_spare) (void)hipEventDestroy(e);
+        if (P->order_ev) (void)hipEventDestroy(P->order_ev);
     }
     delete P;
 }
@@ -851,6 +1008,15 @@ mtn_status mtn_plan_commit(mtn_pool *P) {
     });
 }
 
+mtn_status mtn_plan_abort(mtn_pool *P) {
+    return guarded(P, [&]() -> mtn_status {
+        if (!P) return MTN_ERR_INVALID_ARG;
+        if (!P->plan_open) return fail(P, MTN_ERR_BAD_STATE, "no open plan");
+        plan_abort_impl(P);
+        return MTN_OK;
+    });
+}
+
 mtn_status mtn_frame_append_kv(mtn_pool *P, int32_t layer, const void *k, const void *v,
                                void *stream) {
     return guarded(P, [&]() -> mtn_status {
@@ -902,12 +1068,11 @@ mtn_status mtn_attend_decode_append(mtn_pool *P, int32_t layer, const void *k, c
 mtn_status mtn_frame_step(mtn_pool *P, const mtn_frame_batch *b, void *stream) {
     return guarded(P, [&]() -> mtn_status {
         if (!P || !b) return MTN_ERR_INVALID_ARG;
-        if (P->host_only) return fail(P, MTN_ERR_BAD_STATE, "host-only pool has no device path");
         if (P->plan_open) return fail(P, MTN_ERR_BAD_STATE, "a plan is already open");
         const int32_t n = b->n_seq;
         if (n < 1 || n > P->cfg.max_sessions || !b->sids || !b->chunk_len || !b->n_decode)
             return fail(P, MTN_ERR_INVALID_ARG, "bad batch");
-        if (!b->q_chunk || !b->k_chunk || !b->v_chunk || !b->out_chunk)
+        if (!P->host_only && (!b->q_chunk || !b->k_chunk || !b->v_chunk || !b->out_chunk))
             return fail(P, MTN_ERR_INVALID_ARG, "null chunk buffer");
         if (b->n_split < 0 || b->n_split > kMaxSplit) return fail(P, MTN_ERR_INVALID_ARG, "bad n_split");
         int32_t max_dec = 0;
@@ -928,7 +1093,7 @@ mtn_status mtn_frame_step(mtn_pool *P, const mtn_frame_batch *b, void *stream) {
             max_dec = std::max(max_dec, b->n_decode[i]);
             Tc += b->chunk_len[i];
         }
-        if (max_dec > 0 && (!b->q_dec || !b->k_dec || !b->v_dec || !b->out_dec))
+        if (!P->host_only && max_dec > 0 && (!b->q_dec || !b->k_dec || !b->v_dec || !b->out_dec))
             return fail(P, MTN_ERR_INVALID_ARG, "null decode buffer");
         {   // whole-frame capacity check before any launch
             std::vector<uint8_t> lbseen((size_t)P->row_len, 0);
@@ -938,57 +1103,16 @@ mtn_status mtn_frame_step(mtn_pool *P, const mtn_frame_batch *b, void *stream) {
                                           (int64_t)b->chunk_len[i] + b->n_decode[i], lbseen);
             if (need > P->alloc.n_free()) return fail(P, MTN_ERR_POOL_EXHAUSTED, "pool exhausted");
         }
-        const int32_t L = P->cfg.n_layers, Hq = P->cfg.n_q_heads, Hkv = P->cfg.n_kv_heads;
-        const size_t e = P->elt, D = (size_t)P->cfg.head_dim;
-        auto off = [&](const void *base, size_t elems) {
-            return (const void *)((const uint8_t *)base + elems * e);
-        };
         // the decode rounds' batches, allocated before anything changes
         std::vector<int32_t> sids, ones, rows;
         sids.reserve((size_t)n);
         ones.reserve((size_t)n);
         rows.reserve((size_t)n);
-        mtn_status st = plan_begin(P, n, b->sids, b->chunk_len, nullptr, stream);
-        if (st) return st;
-        for (int32_t l = 0; l < L; ++l) {
-            size_t rq = (size_t)l * Tc * Hq * D, rk = (size_t)l * Tc * Hkv * D;
-            float *lse = b->lse_chunk ? b->lse_chunk + (size_t)l * Tc * Hq : nullptr;
-            if (P->all_single) {  // one-token chunks: decode with the append fused in
-                st = decode_impl(P, l, off(b->q_chunk, rq), (void *)off(b->out_chunk, rq), lse,
-                                 b->n_split, stream, off(b->k_chunk, rk), off(b->v_chunk, rk));
-            } else {
-                st = append_impl(P, l, off(b->k_chunk, rk), off(b->v_chunk, rk), stream);
-                if (st) return st;
-                st = prefill_impl(P, l, off(b->q_chunk, rq), (void *)off(b->out_chunk, rq), lse,
-                                  stream);
-            }
-            if (st) return st;
-        }
-        st = plan_commit(P);
-        if (st) return st;
-        for (int32_t j = 0; j < max_dec; ++j) {
-            sids.clear();
-            rows.clear();
-            for (int32_t i = 0; i < n; ++i)
-                if (b->n_decode[i] > j) {
-                    sids.push_back(b->sids[i]);
-                    rows.push_back(i);
-                }
-            ones.assign(sids.size(), 1);
-            st = plan_begin(P, (int32_t)sids.size(), sids.data(), ones.data(), rows.data(), stream);
-            if (st) return st;
-            for (int32_t l = 0; l < L; ++l) {
-                size_t base = ((size_t)j * L + l) * n;
-                float *lse = b->lse_dec ? b->lse_dec + base * Hq : nullptr;
-                st = decode_impl(P, l, off(b->q_dec, base * Hq * D),
-                                 (void *)off(b->out_dec, base * Hq * D), lse, b->n_split, stream,
-                                 off(b->k_dec, base * Hkv * D), off(b->v_dec, base * Hkv * D));
-                if (st) return st;
-            }
-            st = plan_commit(P);
-            if (st) return st;
-        }
-        return MTN_OK;
+        // From here on an error abandons the open plan (mtn_plan_abort); plans
+        // of this frame that already committed stay committed.
+        mtn_status st = frame_plans(P, b, stream, Tc, max_dec, sids, ones, rows);
+        if (st && P->plan_open) plan_abort_impl(P);
+        return st;
     });
 }
 
@@ -1090,6 +1214,36 @@ mtn_status mtn_pool_set_prefill_pass_rows(mtn_pool *P, int32_t rows) {
         P->pf_rows_cfg = rows;
         return MTN_OK;
     });
+}
+
+mtn_status mtn_pool_set_decode_kernel(mtn_pool *P, int32_t kind) {
+    return guarded(P, [&]() -> mtn_status {
+        if (!P) return MTN_ERR_INVALID_ARG;
+        if (kind < 0 || kind > 2) return fail(P, MTN_ERR_INVALID_ARG, "kind must be 0, 1 or 2");
+        if (P->plan_open) return fail(P, MTN_ERR_BAD_STATE, "plan open");
+        const mtn_pool_config &c = P->cfg;
+        if (kind == 1 && c.kv_dtype == MTN_FP8_E4M3)
+            return fail(P, MTN_ERR_UNSUPPORTED, "the FP8 cache has no vector decode kernel");
+        if (kind == 2 && c.kv_dtype == MTN_F32)
+            return fail(P, MTN_ERR_UNSUPPORTED, "fp32 pools have no matrix decode kernel");
+        if (kind == 2 && !attn_mfma_bf16_supported(c.head_dim, P->G))
+            return fail(P, MTN_ERR_UNSUPPORTED, "no matrix decode kernel for this shape");
+        P->decode_kernel = kind;
+        if (!P->host_only) P->resident_units = count_resident_units(P);
+        return MTN_OK;
+    });
+}
+
+mtn_status mtn_pool_last_split(const mtn_pool *P, int32_t *n_split) {
+    if (!P || !n_split) return MTN_ERR_INVALID_ARG;
+    *n_split = P->last_split;
+    return MTN_OK;
+}
+
+mtn_status mtn_debug_inject_failure(mtn_pool *P, int64_t launch_index) {
+    if (!P || launch_index < -1) return MTN_ERR_INVALID_ARG;
+    P->fail_at = launch_index;
+    return MTN_OK;
 }
 
 mtn_status mtn_pool_set_timing(mtn_pool *P, int32_t enable) {

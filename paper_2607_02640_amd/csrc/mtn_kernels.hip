@@ -1151,8 +1151,10 @@ __global__ __launch_bounds__(64 * kPfWaves) void k_prefill_mfma(PfArgs pa) {
             bool bump = false;
 #pragma unroll
             for (int i = 0; i < NT; ++i) {
+                // three-operand maxima only (a two-operand one costs the
+                // compiler two NaN-quieting instructions); sa[i][0] twice
                 m8[i] = vmax3(vmax3(sa[i][0], sa[i][1], sa[i][2]), vmax3(sa[i][3], sb[i][0], sb[i][1]),
-                              vmax2(sb[i][2], sb[i][3]));
+                              vmax3(sb[i][2], sb[i][3], sa[i][0]));
                 bump = bump || m8[i] > m_ref[i] + kLazy;
             }
             if (__builtin_amdgcn_ballot_w64(bump)) {

@@ -359,7 +359,7 @@ __global__ __launch_bounds__(64 * NG) void k_attn_mfma(AttnArgs a) {
                 sc[r] = (key >= lo && key < hi) ? sc[r] : -INFINITY;
             }
         }
-        const float mx = rows_max(vmax2(vmax2(sc[0], sc[1]), vmax2(sc[2], sc[3])));
+        const float mx = rows_max(vmax3(vmax3(sc[0], sc[1], sc[2]), sc[3], sc[0]));
         const bool bump = mx > m_ref + 8.f;
         if (__builtin_amdgcn_ballot_w64(bump)) {
             const float mnew = bump ? mx : m_ref;

@@ -100,8 +100,12 @@ def test_host_planner_matches_index_model(policy, seed):
                 if rnd.random() < 0.1:   # closing during a plan is refused
                     c, _ = _code(pool.session_close, sids[0])
                     assert c == mtn.MTN_ERR_BAD_STATE
-                pool.plan_commit()
-                model.plan_commit()
+                if rnd.random() < 0.15:  # abandon the plan instead
+                    pool.plan_abort()
+                    model.plan_abort()
+                else:
+                    pool.plan_commit()
+                    model.plan_commit()
         _compare(pool, model)
 
 
@@ -229,3 +233,113 @@ def test_host_allocation_failure_returns_a_status():
                        timeout=120)
     assert r.returncode == 0, r.stderr[-2000:]
     assert r.stdout.strip() == f"code {mtn.MTN_ERR_HOST_MEMORY}", r.stdout + r.stderr[-2000:]
+
+
+def _snapshot(pool, sids):
+    return pool.stats(), {s: (pool.block_table(s), pool.session_info(s)) for s in sids}
+
+
+@pytest.mark.parametrize("policy", ["windowed", "unbounded"])
+def test_plan_abort_restores_the_pool(policy):
+    """Failures inside a plan (a layer out of range, a null buffer: host-only
+    pools refuse device calls too) leave the plan open; mtn_plan_abort then
+    returns the pool to its state before mtn_plan_begin, bit for bit, and the
+    next plan assigns exactly what it would have assigned without the abandoned
+    one (failing cleanly instead of stalling, §3; App. B)."""
+    W = None if policy == "unbounded" else 40
+    nb = 60 if W is None else 30
+    pool, model = _pair(nb, 4, W, 9, 3, max_len=200 if W is None else None)
+    ref, ref_model = _pair(nb, 4, W, 9, 3, max_len=200 if W is None else None)
+    sids = [pool.session_open() for _ in range(3)]
+    for p_ in (model, ref, ref_model):
+        [p_.session_open() if hasattr(p_, "session_open") else p_.open() for _ in range(3)]
+    rnd = random.Random(7)
+    lib = pool.lib
+    for step in range(20 if W is None else 40):
+        n_tok = [rnd.randint(1, 9) for _ in sids]
+        before = _snapshot(pool, sids)
+        pool.plan_begin(sids, n_tok)
+        model.plan_begin(sids, n_tok)
+        # per-layer calls that fail inside the plan
+        assert lib.mtn_frame_append_kv(pool.h, 99, None, None, None) != mtn.MTN_OK
+        assert lib.mtn_attend_chunk_prefill(pool.h, 0, None, None, None, None) != mtn.MTN_OK
+        assert lib.mtn_plan_begin(pool.h, 1, mtn._lib._arr32(sids[:1]),
+                                  mtn._lib._arr32([1]), None) == mtn.MTN_ERR_BAD_STATE
+        if step % 3 == 0:
+            pool.plan_abort()
+            model.plan_abort()
+            assert _snapshot(pool, sids) == before
+            # the pool plans on as if the abandoned plan had never begun
+            pool.plan_begin(sids, n_tok)
+            model.plan_begin(sids, n_tok)
+        ref.plan_begin(sids, n_tok)
+        ref_model.plan_begin(sids, n_tok)
+        assert pool.plan_info(len(sids)) == ref.plan_info(len(sids))
+        for p_ in (pool, model, ref, ref_model):
+            p_.plan_commit()
+        _compare(pool, model)
+        _compare(ref, ref_model)
+        assert _snapshot(pool, sids) == _snapshot(ref, sids)
+    with pytest.raises(mtn.MtnError) as e:
+        pool.plan_abort()
+    assert e.value.code == mtn.MTN_ERR_BAD_STATE
+
+
+def _model_frame(model, sids, chunk, n_dec, n_layers, fail_at=None):
+    """The frame as mtn_frame_step runs it -- the chunk plan, then one plan per
+    decode round -- on the index model; with fail_at, the plan holding that
+    launch point (chunk plans: one point per layer for one-token chunks, else
+    two; decode rounds: one per layer) is abandoned and the frame stops."""
+    per_chunk = n_layers * (1 if max(chunk) == 1 else 2)
+    plans = [(list(sids), list(chunk), per_chunk)]
+    for j in range(max(n_dec)):
+        act = [s for s, d in zip(sids, n_dec) if d > j]
+        plans.append((act, [1] * len(act), n_layers))
+    k = fail_at
+    for ps, nt, launches in plans:
+        model.plan_begin(ps, nt)
+        if k is not None and k < launches:
+            model.plan_abort()
+            return False
+        if k is not None:
+            k -= launches
+        model.plan_commit()
+    return True
+
+
+@pytest.mark.parametrize("policy", ["windowed", "unbounded"])
+def test_frame_step_plans_and_rolls_back_like_the_model(policy):
+    """mtn_frame_step on a host-only pool plans every frame exactly as the index
+    model's chunk plan + decode rounds; a launch failure injected anywhere in
+    the frame abandons the plan it falls in, keeps the rounds already committed
+    and leaves nothing open."""
+    W = None if policy == "unbounded" else 48
+    cmax, n_layers = 10, 3
+    pool = mtn.Pool(n_layers=n_layers, n_q_heads=4, n_kv_heads=2, head_dim=64, n_sink=4,
+                    window=W, max_chunk=cmax, max_sessions=4, n_blocks=80, dtype="f32",
+                    max_len=400 if W is None else 0, host_only=True)
+    model = im.IndexModel(80, 16, 4, W, cmax, 4, max_len=400 if W is None else None)
+    sids = [pool.session_open() for _ in range(4)]
+    for _ in range(4):
+        model.open()
+    rnd = random.Random(3)
+    for frame in range(30):
+        batch = rnd.sample(sids, rnd.randint(1, 4))
+        chunk = [rnd.choice([1, rnd.randint(1, cmax)]) for _ in batch]
+        n_dec = [rnd.randint(0, 4) for _ in batch]
+        per_chunk = n_layers * (1 if max(chunk) == 1 else 2)
+        total = per_chunk + n_layers * max(n_dec)
+        fail_at = rnd.randrange(total) if rnd.random() < 0.4 else None
+        if fail_at is not None:
+            pool.inject_failure(fail_at)
+        try:
+            pool.frame_step(batch, chunk, n_dec, None, None, None, None)
+            ok = True
+        except mtn.MtnError as e:
+            assert e.code == mtn.MTN_ERR_DEVICE and fail_at is not None
+            ok = False
+        assert ok == _model_frame(model, batch, chunk, n_dec, n_layers, fail_at)
+        # nothing is left open: a plan can begin and be abandoned
+        pool.plan_begin(batch[:1], [1])
+        pool.plan_abort()
+        _compare(pool, model)

@@ -124,12 +124,13 @@ def test_fp8_per_layer_calls(fused):
     say(f"max err {h.max_err:.2e}")
 
 
-@pytest.mark.parametrize("n_split", [1, 2, 3, 7, 64])
+@pytest.mark.parametrize("n_split", [1, 2, 3, 7, 33, 64])
 def test_fp8_decode_split_counts(n_split):
     say(f"fp8 split {n_split}")
     pool, h, _ = _pool(hq=8, hkv=2, S=4, W=150, cmax=1, n=3)
     for f in range(12):
         h.frame([1, 1, 1], [12, 5, 9], n_split=n_split)
+        assert pool.last_split() == n_split
 
 
 def test_fp8_fused_and_separate_store_identical_pools():
@@ -172,10 +173,11 @@ def test_fp8_quantization_error_against_exact_attention():
     pool, h, _ = _pool(hq=8, hkv=2, S=4, W=64, cmax=1, n=2)
     exact = [wa.OracleSession(8, 2, 128, 4, 64) for _ in range(2)]
     worst = 0.0
+    gen = torch.Generator().manual_seed(20261)
     for f in range(20):
-        q = torch.randn(1, 2, 8, 128).to(torch.bfloat16)
-        k = torch.randn(1, 2, 2, 128).to(torch.bfloat16)
-        v = (torch.randn(1, 2, 2, 128) * 0.3).to(torch.bfloat16)
+        q = torch.randn(1, 2, 8, 128, generator=gen).to(torch.bfloat16)
+        k = torch.randn(1, 2, 2, 128, generator=gen).to(torch.bfloat16)
+        v = (torch.randn(1, 2, 2, 128, generator=gen) * 0.3).to(torch.bfloat16)
         out = torch.empty_like(q).cuda()
         pool.frame_step(h.sids, [1, 1], [0, 0], q.cuda(), k.cuda(), v.cuda(), out)
         torch.cuda.synchronize()

@@ -192,3 +192,72 @@ def test_moshi_shape_sampled_parity(dtype):
     samples = [(0, 0), (1, 15), (62, 31)]
     worst = _ragged_fullsize(wl, dtype, lengths, [1] * N, [1] * N, samples, seed=520)
     assert worst <= 2e-2, worst
+
+
+@pytest.mark.parametrize("rows", [256, 128])
+def test_recycle_reprefill_sampled_parity(rows):
+    """The application-level recycling arm's re-prefill at the Qwen3-Omni
+    shape (§4.1's alternative, measured in §5): a fresh session takes the
+    sinks plus the last W tokens of an old one, S + W = 4100 tokens, as one
+    chunk on an unbounded pool with max_chunk 4100 -- 32 800 query rows per KV
+    head in 129 passes of 256 rows (257 of 128), each over the keys its own
+    rows see.  A second session takes a 37-token chunk in the same plan, then
+    both decode one token.  Sampled chunk tokens (all 32 heads) and every
+    other output against the float64 oracle."""
+    Hq, Hkv, D, C, C2 = W.n_q_heads, W.n_kv_heads, W.head_dim, W.n_sink + W.window, 37
+    say(f"recycle re-prefill: chunk {C}, {rows}-row passes")
+    n_blocks = 2 * (-(-(C + 8) // 16))
+    pool = make_pool(n_layers=1, hq=Hq, hkv=Hkv, d=D, S=0, W=None, cmax=C, max_sessions=2,
+                     n_blocks=n_blocks, dtype="bf16", theta=W.rope_theta, max_len=C + 8)
+    pool.set_prefill_pass_rows(rows)
+    sids = [pool.session_open(), pool.session_open()]
+    dev, bf = torch.device("cuda"), torch.bfloat16
+    q = device_bank((C + C2, Hq, D), bf, dev, 91)
+    k = device_bank((C + C2, Hkv, D), bf, dev, 92)
+    v = device_bank((C + C2, Hkv, D), bf, dev, 93)
+    out = torch.empty_like(q)
+    pool.plan_begin(sids, [C, C2])
+    pool.frame_append_kv(0, k, v)
+    pool.attend_chunk_prefill(0, q, out)
+    pool.plan_commit()
+    qd = device_bank((2, Hq, D), bf, dev, 94)
+    kd = device_bank((2, Hkv, D), bf, dev, 95)
+    vd = device_bank((2, Hkv, D), bf, dev, 96)
+    od = torch.empty_like(qd)
+    pool.plan_begin(sids, [1, 1])
+    pool.frame_append_kv(0, kd, vd)
+    pool.attend_decode(0, qd, od)
+    pool.plan_commit()
+    torch.cuda.synchronize()
+    assert torch.isfinite(out.float()).all() and torch.isfinite(od.float()).all()
+    qh, kh, vh, oh = _f64(q), _f64(k), _f64(v), _f64(out)
+    worst = 0.0
+    # session 0: the long chunk's state, then sampled queries attended one by
+    # one over the positions they see (unbounded: every earlier position)
+    o = wa.OracleSession(Hq, Hkv, D, 0, None, theta=W.rope_theta, n_layers=1)
+    o.begin(C)
+    o.layer_step(0, np.zeros((C, Hq, D)), kh[:C], vh[:C], attend=False)
+    o.commit()
+    st = o.state[0]
+    g = Hq // Hkv
+    for t in [0, 1, 15, 16, 31, 32, 33, 255, 256, 511, 1024, 2047, 2048, 3000, 4090, C - 1]:
+        vis = wa.visible_positions(t, 0, None)
+        kmat = np.stack([st[p][0] for p in vis])
+        vmat = np.stack([st[p][1] for p in vis])
+        qr = wa.rope_rotate(qh[t], t, W.rope_theta)
+        for h in range(Hq):
+            ref, _, _ = wa.attend_row(qr[h], kmat[:, h // g], vmat[:, h // g], o.scale)
+            worst = max(worst, float(np.max(np.abs(oh[t, h] - ref))))
+    o.begin(1)
+    rd, _ = o.layer_step(0, _f64(qd[0:1]), _f64(kd[0:1]), _f64(vd[0:1]))
+    o.commit()
+    worst = max(worst, float(np.max(np.abs(_f64(od[0:1]) - rd))))
+    # session 1: every output of its chunk and its decode
+    o2 = wa.OracleSession(Hq, Hkv, D, 0, None, theta=W.rope_theta, n_layers=1)
+    ref2, _ = o2.step(qh[C:], kh[C:], vh[C:])
+    worst = max(worst, float(np.max(np.abs(oh[C:] - ref2))))
+    rd2, _ = o2.step(_f64(qd[1:2]), _f64(kd[1:2]), _f64(vd[1:2]))
+    worst = max(worst, float(np.max(np.abs(_f64(od[1:2]) - rd2))))
+    say(f"max abs err {worst:.3e}")
+    assert worst <= 2e-2, worst
+    pool.close()

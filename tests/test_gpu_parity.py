@@ -7,7 +7,7 @@ import numpy as np
 import pytest
 import torch
 
-from tests._gpu_util import Harness, make_pool, say
+from tests._gpu_util import Harness, f64, make_pool, say
 
 pytestmark = pytest.mark.gpu
 
@@ -76,12 +76,16 @@ def test_other_head_dims(dtype, d):
         h.frame([rnd.randint(1, 9) for _ in range(3)], [rnd.randint(0, 4) for _ in range(3)])
 
 
-@pytest.mark.parametrize("n_split", [1, 2, 3, 7, 64])
+@pytest.mark.parametrize("n_split", [1, 2, 3, 7, 33, 64])
 def test_decode_split_counts(n_split):
+    """Forced splits run as asked (the library reports the split of its last
+    decode launch): with 64 segments over a 94-key window most segments are
+    empty, and the merge must ignore them."""
     say(f"split {n_split}")
     pool, h = _tiny(S=4, W=90, cmax=8, n=3)
     for f in range(14):
         h.frame([8] * 3, [3] * 3, n_split=n_split)
+        assert pool.last_split() == n_split
 
 
 def test_no_sinks_and_unit_window():
@@ -258,3 +262,114 @@ def test_prefill_pass_rows(dtype, rows):
     for f in range(8):
         h.frame([rnd.randint(1, C) for _ in range(n)], [rnd.randint(0, 2) for _ in range(n)])
     say(f"max err {h.max_err:.2e}")
+
+
+@pytest.mark.parametrize("d,g", [(64, 1), (64, 8), (128, 1), (128, 8)])
+def test_fp32_gqa_group_extremes(d, g):
+    """fp32 pools at one query head per KV head and at the largest group the
+    boundary accepts (the vector kernel's one-wave and two-wave-group shapes)."""
+    say(f"f32 d{d} G={g}")
+    hkv = 2
+    pool, h = _tiny(dtype="f32", d=d, hq=hkv * g, hkv=hkv, S=4, W=45, cmax=7, n=3, L=2)
+    rnd = random.Random(d + g)
+    for f in range(12):
+        h.frame([rnd.randint(1, 7) for _ in range(3)], [rnd.randint(0, 4) for _ in range(3)])
+    say(f"max err {h.max_err:.2e}")
+
+
+@pytest.mark.parametrize("g", [1, 4, 8])
+def test_bf16_d64_gqa_groups(g):
+    """bf16 at head_dim 64 (vector kernels for the chunk and the decode)."""
+    say(f"bf16 d64 G={g}")
+    hkv = 2
+    pool, h = _tiny(dtype="bf16", d=64, hq=hkv * g, hkv=hkv, S=4, W=45, cmax=7, n=3, L=2)
+    rnd = random.Random(64 + g)
+    for f in range(12):
+        h.frame([rnd.randint(1, 7) for _ in range(3)], [rnd.randint(0, 4) for _ in range(3)])
+    say(f"max err {h.max_err:.2e}")
+
+
+@pytest.mark.parametrize("kind,g", [(1, 8), (2, 1), (2, 2), (2, 4)])
+def test_bf16_decode_kernel_forced(kind, g):
+    """Each bf16 decode kernel on the shapes the automatic choice gives the
+    other: the vector kernel at G = 8, the matrix-core kernel at G = 1, 2, 4
+    (D = 128), with splits and the fused append."""
+    say(f"bf16 decode kernel {kind} G={g}")
+    hkv = 2
+    pool, h = _tiny(dtype="bf16", d=128, hq=hkv * g, hkv=hkv, S=4, W=70, cmax=9, n=3, L=2,
+                    blocks=3 * 6)
+    pool.set_decode_kernel(kind)
+    rnd = random.Random(10 * kind + g)
+    for f in range(12):
+        h.frame([rnd.randint(1, 9) for _ in range(3)], [rnd.randint(0, 4) for _ in range(3)],
+                n_split=(0, 2, 5)[f % 3])
+    say(f"max err {h.max_err:.2e}")
+
+
+def test_plans_alternating_between_streams():
+    """Consecutive plans on two streams with no host synchronisation in
+    between: the library orders each plan's uploads after the previous plan's
+    kernels (they share the metadata, RoPE table and split partials), so
+    every frame still matches the oracle."""
+    say("plans alternating between two streams")
+    n, L, hq, hkv, d = 3, 2, 16, 2, 128
+    pool, h = _tiny(dtype="bf16", d=d, hq=hq, hkv=hkv, S=4, W=60, cmax=12, n=n, L=L, blocks=3 * 7)
+    streams = [torch.cuda.Stream(), torch.cuda.Stream()]
+    rnd = random.Random(17)
+    frames = []
+    for f in range(10):
+        cl = [rnd.randint(1, 12) for _ in range(n)]
+        nd = [rnd.randint(0, 3) for _ in range(n)]
+        draws = [h._draw(i, cl[i]) for i in range(n)]
+        dec = [[h._draw(i, 1) if nd[i] > j else None for i in range(n)] for j in range(max(nd))]
+        frames.append((cl, nd, draws, dec))
+    # inputs on the device before any plan runs
+    dev = []
+    for cl, nd, draws, dec in frames:
+        qc, kc, vc = (torch.cat([dr[j] for dr in draws], dim=1).contiguous().cuda()
+                      for j in range(3))
+        md = max(nd)
+        if md:
+            def dstack(c, hh):
+                out = torch.zeros((md, L, n, hh, d), dtype=torch.bfloat16)
+                for j in range(md):
+                    for i in range(n):
+                        if dec[j][i] is not None:
+                            out[j, :, i] = dec[j][i][c][:, 0]
+                return out.cuda()
+            qd, kd, vd = dstack(0, hq), dstack(1, hkv), dstack(2, hkv)
+        else:
+            qd = kd = vd = None
+        dev.append((qc, kc, vc, torch.empty_like(qc), qd, kd, vd,
+                    torch.zeros_like(qd) if md else None))
+    torch.cuda.synchronize()
+    for f, (cl, nd, _, _) in enumerate(frames):
+        qc, kc, vc, oc, qd, kd, vd, od = dev[f]
+        with torch.cuda.stream(streams[f % 2]):
+            if f % 3 == 2:   # per-layer calls on this stream
+                pool.plan_begin(h.sids, cl)
+                for l in range(L):
+                    pool.frame_append_kv(l, kc[l], vc[l])
+                    if max(cl) == 1:
+                        pool.attend_decode(l, qc[l], oc[l])
+                    else:
+                        pool.attend_chunk_prefill(l, qc[l], oc[l])
+                pool.plan_commit()
+                nd[:] = [0] * n   # decodes of this frame are not issued
+            else:
+                pool.frame_step(h.sids, cl, nd, qc, kc, vc, oc, qd, kd, vd, od, n_split=2)
+    torch.cuda.synchronize()
+    for f, (cl, nd, draws, dec) in enumerate(frames):
+        qc, kc, vc, oc, qd, kd, vd, od = dev[f]
+        off = 0
+        for i in range(n):
+            ref, _ = h._oracle_step(i, *draws[i])
+            got = oc[:, off:off + cl[i]].cpu()
+            assert float(np.max(np.abs(f64(got) - ref))) <= 2e-2, f"frame {f} chunk s{i}"
+            off += cl[i]
+        for j in range(max(nd) if nd else 0):
+            for i in range(n):
+                if nd[i] > j:
+                    ref, _ = h._oracle_step(i, *dec[j][i])
+                    got = od[j, :, i:i + 1].cpu()
+                    assert float(np.max(np.abs(f64(got) - ref))) <= 2e-2, f"frame {f} dec{j} s{i}"
