@@ -235,6 +235,22 @@ mtn_status mtn_attend_decode(mtn_pool *pool, int32_t layer, const void *q, void 
                              float *lse, int32_t n_split, void *stream);
 
 /*
+ * mtn_attend_decode for callers that cannot allocate device memory (code
+ * under HIP graph capture, allocation-free serving loops, harnesses that
+ * forbid hipMalloc): same arguments, layouts and results, but the split
+ * partials live in a static device array of the library (4 Mi floats = 16
+ * MiB, one per GPU, held until the process ends) instead of the pool's
+ * workspace, and the call allocates nothing and records no timing events.
+ * A forced split needs n_seq * Hq * n_split * (D + 2) <= 4 Mi floats, else
+ * MTN_ERR_INVALID_ARG; n_split = 0 picks the automatic split, reduced to what
+ * the array holds.  Every call on one GPU shares the array: calls that
+ * overlap on one GPU (two streams, two pools) race and must be ordered by
+ * the caller.
+ */
+mtn_status mtn_attend_decode_noalloc(mtn_pool *pool, int32_t layer, const void *q, void *out,
+                                     float *lse, int32_t n_split, void *stream);
+
+/*
  * mtn_frame_append_kv followed by mtn_attend_decode for one layer of an open
  * plan whose every sequence has n_tok == 1, in one launch: each planned token
  * is the newest key of its own query, so the workgroup that attends to the

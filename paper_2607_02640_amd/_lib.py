@@ -42,7 +42,7 @@ EXPORTS = [
     "mtn_session_open", "mtn_session_close", "mtn_plan_begin", "mtn_plan_commit",
     "mtn_plan_abort",
     "mtn_frame_append_kv", "mtn_attend_chunk_prefill", "mtn_attend_decode",
-    "mtn_attend_decode_append",
+    "mtn_attend_decode_append", "mtn_attend_decode_noalloc",
     "mtn_frame_step", "mtn_pool_stats", "mtn_session_info", "mtn_session_block_table",
     "mtn_plan_info", "mtn_debug_poison_dead", "mtn_pool_set_timing", "mtn_pool_set_prefill_pass_rows",
     "mtn_pool_kernel_times", "mtn_hbm_copy", "mtn_status_string", "mtn_pool_last_error",
@@ -131,6 +131,7 @@ def load() -> C.CDLL:
         "mtn_attend_chunk_prefill": (i32, [vp, i32, vp, vp, vp, vp]),
         "mtn_attend_decode": (i32, [vp, i32, vp, vp, vp, i32, vp]),
         "mtn_attend_decode_append": (i32, [vp, i32, vp, vp, vp, vp, vp, i32, vp]),
+        "mtn_attend_decode_noalloc": (i32, [vp, i32, vp, vp, vp, i32, vp]),
         "mtn_frame_step": (i32, [vp, C.POINTER(FrameBatch), vp]),
         "mtn_pool_stats": (i32, [vp, C.POINTER(PoolStats)]),
         "mtn_session_info": (i32, [vp, i32, P64, P32]),
@@ -295,6 +296,11 @@ class Pool:
     def attend_decode(self, layer, q, out, lse=None, n_split=0, stream=None) -> None:
         self._check(self.lib.mtn_attend_decode(self.h, layer, _ptr(q), _ptr(out), _ptr(lse),
                                                n_split, _stream(stream)), "attend_decode")
+
+    def attend_decode_noalloc(self, layer, q, out, lse=None, n_split=0, stream=None) -> None:
+        self._check(self.lib.mtn_attend_decode_noalloc(self.h, layer, _ptr(q), _ptr(out),
+                                                       _ptr(lse), n_split, _stream(stream)),
+                    "attend_decode_noalloc")
 
     def attend_decode_append(self, layer, k, v, q, out, lse=None, n_split=0,
                              stream=None) -> None:

@@ -106,6 +106,8 @@ struct mtn_pool {
     float2 *d_rope = nullptr;      // [max_tok][D/2]
     double *d_inv_freq = nullptr;  // [D/2]
     float *d_part = nullptr;       // decode split partials
+    float *d_scratch = nullptr;    // the static partials workspace (not owned)
+    size_t scratch_floats = 0;
     uint8_t *d_zero = nullptr;     // kZeroPage bytes of zeros (DMA source of absent blocks)
     size_t part_floats = 0;
     int32_t *h_stage[kStages] = {};
@@ -617,6 +619,8 @@ int32_t auto_split(const mtn_pool *P, int32_t n_items) {
 // The split partials workspace holds kMaxSplit segments of every query a
 // plan can carry (max_sessions), so every split 1 <= n_split <= kMaxSplit runs
 // as asked.
+// part / part_floats: another partials workspace (the static one); such a
+// call records no timing events.
 mtn_status decode_impl(mtn_pool *P, int32_t layer, const void *q, void *out, float *lse,
                        int32_t n_split, void *stream, const void *k_new = nullptr,
                        const void *v_new = nullptr, float *part = nullptr,
@@ -629,6 +633,7 @@ mtn_status decode_impl(mtn_pool *P, int32_t layer, const void *q, void *out, flo
     }
     hipStream_t s = (hipStream_t)stream;
     if (n_split == 0) n_split = auto_split(P, P->T);
+    const bool events = part == nullptr;
     if (!part) {
         part = P->d_part;
         part_floats = P->part_floats;
@@ -640,25 +645,33 @@ mtn_status decode_impl(mtn_pool *P, int32_t layer, const void *q, void *out, flo
     a.part = part;
     a.k_new = k_new;
     a.v_new = v_new;
-    hipEvent_t e0;
-    st = timing_begin(P, s, &e0);
-    if (st) return st;
+    hipEvent_t e0 = nullptr;
+    if (events) {
+        st = timing_begin(P, s, &e0);
+        if (st) return st;
+    }
     if (P->cfg.kv_dtype == MTN_FP8_E4M3)
         HIP_TRY(P, launch_attn_fp8(a, s));
     else if (use_mfma_bf16(P))
         HIP_TRY(P, launch_attn_mfma_bf16(a, s));
     else
         HIP_TRY(P, launch_attn_valu(P->cfg.kv_dtype, a, s));
-    st = timing_end(P, 2, e0, s);
-    if (st) return st;
+    if (events) {
+        st = timing_end(P, 2, e0, s);
+        if (st) return st;
+    }
     P->last_split = n_split;
     if (k_new) P->layer_done[layer] = 1;
     if (n_split > 1) {
-        st = timing_begin(P, s, &e0);
-        if (st) return st;
+        if (events) {
+            st = timing_begin(P, s, &e0);
+            if (st) return st;
+        }
         HIP_TRY(P, launch_merge(P->cfg.io_dtype, a, s));  // writes io rows
-        st = timing_end(P, 3, e0, s);
-        if (st) return st;
+        if (events) {
+            st = timing_end(P, 3, e0, s);
+            if (st) return st;
+        }
     }
     return MTN_OK;
 }
@@ -898,6 +911,8 @@ mtn_status pool_init(mtn_pool *P, const mtn_pool_config *cfg, void *kv_dev, void
         P->part_floats = (size_t)cfg->max_sessions * cfg->n_q_heads * kMaxSplit * (cfg->head_dim + 2);
         if ((e = hipMalloc(&P->d_part, sizeof(float) * P->part_floats)) != hipSuccess)
             return bail(e, "partials");
+        if ((e = scratch_buffer(&P->d_scratch, &P->scratch_floats)) != hipSuccess)
+            return bail(e, "static scratch address");
         int dev = 0, n_cu = 0;
         if ((e = hipGetDevice(&dev)) != hipSuccess) return bail(e, "device");
         if ((e = hipDeviceGetAttribute(&n_cu, hipDeviceAttributeMultiprocessorCount, dev)) !=
@@ -1062,6 +1077,29 @@ mtn_status mtn_attend_decode_append(mtn_pool *P, int32_t layer, const void *k, c
         if (n_split < 0 || n_split > kMaxSplit) return fail(P, MTN_ERR_INVALID_ARG, "bad n_split");
         if (P->layer_done[layer]) return fail(P, MTN_ERR_BAD_STATE, "layer already appended");
         return decode_impl(P, layer, q, out, lse, n_split, stream, k, v);
+    });
+}
+
+mtn_status mtn_attend_decode_noalloc(mtn_pool *P, int32_t layer, const void *q, void *out,
+                                     float *lse, int32_t n_split, void *stream) {
+    return guarded(P, [&]() -> mtn_status {
+        mtn_status st = check_call(P, layer, stream);
+        if (st) return st;
+        if (!q || !out) return fail(P, MTN_ERR_INVALID_ARG, "null q or out");
+        if (!P->all_single) return fail(P, MTN_ERR_BAD_STATE, "decode needs n_tok == 1 everywhere");
+        if (n_split < 0 || n_split > kMaxSplit) return fail(P, MTN_ERR_INVALID_ARG, "bad n_split");
+        if (!P->layer_done[layer]) return fail(P, MTN_ERR_BAD_STATE, "layer not appended");
+        const size_t per_split = (size_t)P->T * P->cfg.n_q_heads * (P->cfg.head_dim + 2);
+        if (n_split == 0) {
+            // the automatic split, reduced to what the static workspace holds
+            n_split = auto_split(P, P->T);
+            while (n_split > 1 && per_split * n_split > P->scratch_floats) --n_split;
+        } else if (n_split > 1 && per_split * n_split > P->scratch_floats) {
+            return fail(P, MTN_ERR_INVALID_ARG,
+                        "split partials exceed the static workspace (4 Mi floats)");
+        }
+        return decode_impl(P, layer, q, out, lse, n_split, stream, nullptr, nullptr, P->d_scratch,
+                           P->scratch_floats);
     });
 }
 

@@ -82,6 +82,11 @@ hipError_t launch_poison(int dtype, const PoolGeom &g, int32_t n_layers, int64_t
 
 hipError_t launch_copy(const void *src, void *dst, size_t bytes, hipStream_t s);
 
+// The library's static device workspace for split partials (a file-scope
+// array, no allocation): its address on the current device and its size in
+// floats.
+hipError_t scratch_buffer(float **ptr, size_t *floats);
+
 // FP8 (E4M3) KV cache, D = 128, bf16 io: bytes per (layer, block, kv head)
 // region (0 for an unsupported head dim), the fused RoPE + quantize + append,
 // the MFMA decode (k_new / v_new in AttnArgs select the fused append) and the

@@ -14,6 +14,7 @@
 #include <stdint.h>
 
 #include <algorithm>
+#include <mutex>
 #include <type_traits>
 
 namespace mtn {
@@ -585,6 +586,13 @@ __global__ __launch_bounds__(64 * WPU * NG) void k_attn_valu(AttnArgs a) {
         if (own_new && wq == 0) store_new();  // one group: it owns the newest key
     }
 }
+
+// Split partials of mtn_attend_decode_noalloc: a file-scope device array, so
+// that callers that cannot allocate (graph capture, allocation-free serving
+// loops) still have a workspace.  Each GPU holds its own copy for the life of
+// the process; every call on one GPU shares it.
+constexpr size_t kScratchFloats = (size_t)4 << 20;  // 16 MiB
+static __device__ __align__(256) float scratch[kScratchFloats];
 
 // merge split partials: one wave per (token, q head)
 template <typename T, int D>
@@ -1383,6 +1391,28 @@ hipError_t launch_merge(int dtype, const AttnArgs &a, hipStream_t s) {
             hipLaunchKernelGGL((k_merge<float, 64>), dim3((unsigned)n), dim3(64), 0, s, a);
     }
     return hipGetLastError();
+}
+
+// Device address of `scratch` on the current device, resolved once per device
+// (the array's host-side name is not a device address).
+hipError_t scratch_buffer(float **ptr, size_t *floats) {
+    constexpr int kMaxDevices = 64;
+    static std::mutex mu;
+    static float *addr[kMaxDevices] = {};
+    int dev = 0;
+    hipError_t e = hipGetDevice(&dev);
+    if (e != hipSuccess) return e;
+    if (dev < 0 || dev >= kMaxDevices) return hipErrorInvalidDevice;
+    std::lock_guard<std::mutex> lock(mu);
+    if (!addr[dev]) {
+        void *p = nullptr;
+        e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+        if (e != hipSuccess) return e;
+        addr[dev] = (float *)p;
+    }
+    *ptr = addr[dev];
+    *floats = kScratchFloats;
+    return hipSuccess;
 }
 
 int prefill_rows_per_pass() { return kPfRowsPerPass; }
