@@ -57,5 +57,25 @@ def build(verbose: bool = False, out: str = LIB, defines=()) -> str:
     return out
 
 
+SANITIZED = os.path.join(ROOT, "_build", "sanitize", "libmtn_host_sanitized.so")
+
+
+def build_host_sanitized(verbose: bool = False, out: str = SANITIZED) -> str:
+    """The host library alone (planner, tables, admission) built by g++ with
+    AddressSanitizer and UndefinedBehaviorSanitizer, the gfx950 launch
+    interface replaced by host stand-ins (mtn_host_stub.cpp).  Only host-only
+    pools work with it; load it with the sanitizer runtime preloaded."""
+    os.makedirs(os.path.dirname(out), exist_ok=True)
+    cmd = ["g++", "-std=c++17", "-O1", "-g", "-fPIC", "-shared", "-fno-omit-frame-pointer",
+           "-fsanitize=address,undefined", "-fno-sanitize-recover=undefined",
+           "-D__HIP_PLATFORM_AMD__", "-I/opt/rocm/include", f"-I{INCLUDE}", f"-I{CSRC}",
+           os.path.join(CSRC, "mtn_host.cpp"), os.path.join(CSRC, "mtn_admission.cpp"),
+           os.path.join(CSRC, "mtn_host_stub.cpp"), "-L/opt/rocm/lib", "-lamdhip64",
+           "-Wl,-rpath,/opt/rocm/lib", "-o", out + ".tmp"]
+    _run(cmd, verbose)
+    os.replace(out + ".tmp", out)
+    return out
+
+
 if __name__ == "__main__":
     print(build(verbose=True))

@@ -973,6 +973,12 @@ __global__ __launch_bounds__(64 * kPfWaves) void k_prefill_mfma(PfArgs pa) {
         // score of a row exceeds it by more than 2^8 and sets it, while
         // masked (-inf) scores give probability 0 against it.
         float m_ref[kPfTpw];
+        // The QK MFMAs start their accumulators at -msh, so the scores come out
+        // already shifted by the reference and each probability is one
+        // exponential with no subtraction; thr is the bump threshold on
+        // shifted scores (m_ref - msh + 2^8: 2^8 once the first finite score
+        // has set the reference)
+        float msh[kPfTpw], thr[kPfTpw];
         f32x4_t l_i[kPfTpw];
         int tq_i[kPfTpw];
         bool live[kPfTpw];
@@ -986,6 +992,8 @@ __global__ __launch_bounds__(64 * kPfWaves) void k_prefill_mfma(PfArgs pa) {
             const int gh = rv_ ? r % G : 0;
             tq_i[i] = pos0 + j;
             m_ref[i] = -3.402823466e38f;
+            msh[i] = 0.f;
+            thr[i] = m_ref[i] + 8.f;
             l_i[i] = f32x4_t{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
             for (int dt = 0; dt < 8; ++dt) acc[i][dt] = f32x4_t{0.f, 0.f, 0.f, 0.f};
@@ -1163,15 +1171,23 @@ __global__ __launch_bounds__(64 * kPfWaves) void k_prefill_mfma(PfArgs pa) {
                 // compiler two NaN-quieting instructions); sa[i][0] twice
                 m8[i] = vmax3(vmax3(sa[i][0], sa[i][1], sa[i][2]), vmax3(sa[i][3], sb[i][0], sb[i][1]),
                               vmax3(sb[i][2], sb[i][3], sa[i][0]));
-                bump = bump || m8[i] > m_ref[i] + kLazy;
+                bump = bump || m8[i] > thr[i];
             }
             if (__builtin_amdgcn_ballot_w64(bump)) {
 #pragma unroll
                 for (int i = 0; i < NT; ++i) {
-                    const float mx = rows_max(m8[i]);
-                    const float mnew = mx > m_ref[i] + kLazy ? mx : m_ref[i];
-                    const float alpha = mnew == m_ref[i] ? 1.f : __builtin_amdgcn_exp2f(m_ref[i] - mnew);
+                    // true row max of the stage, the new reference, and the
+                    // re-shift of this stage's (already shifted) scores
+                    const float mx = rows_max(m8[i]) + msh[i];
+                    const bool up = mx > m_ref[i] + kLazy;
+                    const float mnew = up ? mx : m_ref[i];
+                    const float alpha = up ? __builtin_amdgcn_exp2f(m_ref[i] - mnew) : 1.f;
+                    const float dsh = up ? mnew - msh[i] : 0.f;
                     m_ref[i] = mnew;
+                    msh[i] = up ? mnew : msh[i];
+                    thr[i] = up ? kLazy : thr[i];
+                    sa[i] -= dsh;
+                    sb[i] -= dsh;
                     l_i[i] *= alpha;  // all four entries
 #pragma unroll
                     for (int dt = 0; dt < 8; ++dt) acc[i][dt] *= alpha;
@@ -1186,18 +1202,18 @@ __global__ __launch_bounds__(64 * kPfWaves) void k_prefill_mfma(PfArgs pa) {
             f32x4_t na[kPfTpw], nb[kPfTpw];
             float p[kPfTpw][8];
             constexpr int kEpg = 2 * NT;  // probabilities per group
-            const f32x4_t zero4 = f32x4_t{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
             for (int s = 0; s < 4; ++s) {
 #pragma unroll
                 for (int i = 0; i < NT; ++i) {
-                    na[i] = mfma16x16x32(kf[s][0], qf[i][s], s ? na[i] : zero4);
-                    nb[i] = mfma16x16x32(kf[s][1], qf[i][s], s ? nb[i] : zero4);
+                    const f32x4_t c0 = f32x4_t{-msh[i], -msh[i], -msh[i], -msh[i]};
+                    na[i] = mfma16x16x32(kf[s][0], qf[i][s], s ? na[i] : c0);
+                    nb[i] = mfma16x16x32(kf[s][1], qf[i][s], s ? nb[i] : c0);
                 }
 #pragma unroll
                 for (int u = 0; u < kEpg; ++u) {
                     const int f = s * kEpg + u, i = f >> 3, e = f & 7;
-                    p[i][e] = __builtin_amdgcn_exp2f((e < 4 ? sa[i][e] : sb[i][e - 4]) - m_ref[i]);
+                    p[i][e] = __builtin_amdgcn_exp2f(e < 4 ? sa[i][e] : sb[i][e - 4]);
                     // keep it in this group: without the pin the compiler sinks every
                     // exponential below the last group, after the QK MFMAs
                     asm volatile("" : "+v"(p[i][e]));
