@@ -97,6 +97,7 @@ struct mtn_pool {
     std::vector<int32_t> tok_sid, tok_pos, tok_row, tok_block, tok_off;
     std::vector<int32_t> upd_idx, upd_val;
     std::vector<int32_t> pf_items;  // prefill (sequence, row pass) pairs
+    std::vector<int32_t> run_tok0, run_len;  // append runs: consecutive slots of one block
     std::vector<uint8_t> layer_done;
 
     // device
@@ -116,6 +117,7 @@ struct mtn_pool {
     int stage_i = 0;
     PlanView view{};
     int32_t *d_seq_first = nullptr, *d_seq_ntok = nullptr, *d_pf_items = nullptr;
+    int32_t *d_run_tok0 = nullptr, *d_run_len = nullptr;
     int32_t resident_units = 0;    // decode work units resident on the whole GPU
     int32_t n_cu = 0;              // compute units of the pool's device
     int32_t pf_rows_cfg = 0;       // chunk-prefill rows per pass: 0 = chosen per plan
@@ -424,6 +426,22 @@ mtn_status plan_begin(mtn_pool *P, int32_t n_seq, const int32_t *sids, const int
     }
     if (P->unbounded) P->reserved = P->assigned;
     P->all_single = (P->max_ntok == 1);
+    // append runs: maximal stretches of one sequence's tokens in consecutive
+    // slots of one block (the append kernel writes each with one wave per kv
+    // head, K rows and V^T row segments contiguous)
+    P->run_tok0.clear();
+    P->run_len.clear();
+    for (int32_t i = 0, tt = 0; i < n_seq; ++i)
+        for (int32_t j = 0; j < n_tok[i]; ++j, ++tt) {
+            const bool cont = j > 0 && P->tok_block[tt] == P->tok_block[tt - 1] &&
+                              P->tok_off[tt] == P->tok_off[tt - 1] + 1;
+            if (cont) {
+                P->run_len.back()++;
+            } else {
+                P->run_tok0.push_back(tt);
+                P->run_len.push_back(1);
+            }
+        }
     P->pf_items.clear();
     {
         // Rows per prefill pass.  Few sequences leave most CUs idle with full
@@ -466,6 +484,9 @@ mtn_status plan_begin(mtn_pool *P, int32_t n_seq, const int32_t *sids, const int
     put(P->upd_idx.data(), U);
     put(P->upd_val.data(), U);
     put(P->pf_items.data(), (int32_t)P->pf_items.size());
+    const int32_t NR = (int32_t)P->run_tok0.size();
+    put(P->run_tok0.data(), NR);
+    put(P->run_len.data(), NR);
     hipStream_t s = (hipStream_t)stream;
     int32_t *d = P->d_meta;
     // a failed upload abandons the plan: the pool is as before the call
@@ -490,6 +511,8 @@ mtn_status plan_begin(mtn_pool *P, int32_t n_seq, const int32_t *sids, const int
     P->view.n_tok = (int32_t)T;
     const int32_t *d_upd_idx = d + 5 * T + 2 * n_seq;
     P->d_pf_items = d + 5 * T + 2 * n_seq + 2 * U;
+    P->d_run_tok0 = P->d_pf_items + P->pf_items.size();
+    P->d_run_len = P->d_run_tok0 + NR;
     he = launch_plan_apply(d_upd_idx, d_upd_idx + U, U, P->d_table, P->view.tok_pos, (int32_t)T,
                            P->d_inv_freq, P->cfg.head_dim / 2, P->d_rope, s);
     if (he != hipSuccess) return upload_fail(he, "launch_plan_apply");
@@ -548,7 +571,8 @@ mtn_status append_impl(mtn_pool *P, int32_t layer, const void *k, const void *v,
     if (P->cfg.kv_dtype == MTN_FP8_E4M3)
         HIP_TRY(P, launch_append_fp8(geom(P), P->view, layer, k, v, s));
     else
-        HIP_TRY(P, launch_append(P->cfg.kv_dtype, geom(P), P->view, layer, k, v, s));
+        HIP_TRY(P, launch_append(P->cfg.kv_dtype, geom(P), P->view, layer, k, v, P->d_run_tok0,
+                                 P->d_run_len, (int32_t)P->run_tok0.size(), s));
     st = timing_end(P, 0, e0, s);
     if (st) return st;
     P->layer_done[layer] = 1;
@@ -863,7 +887,7 @@ mtn_status pool_init(mtn_pool *P, const mtn_pool_config *cfg, void *kv_dev, void
     P->seq_first.reserve((size_t)cfg->max_sessions);
     P->seq_pos0.reserve((size_t)cfg->max_sessions);
     for (auto *v : {&P->tok_sid, &P->tok_pos, &P->tok_row, &P->tok_block, &P->tok_off, &P->upd_idx,
-                    &P->upd_val})
+                    &P->upd_val, &P->run_tok0, &P->run_len})
         v->reserve((size_t)P->max_tok);
     P->pf_items.reserve(2 * ((size_t)P->max_tok * P->G / 128 + (size_t)cfg->max_sessions + 1));
     P->layer_done.reserve((size_t)cfg->n_layers);
@@ -880,8 +904,9 @@ mtn_status pool_init(mtn_pool *P, const mtn_pool_config *cfg, void *kv_dev, void
                                 (hipStream_t)stream)) != hipSuccess)
             return bail(e, "table upload");
         // per plan: 5 T token fields, 2 n_seq sequence fields, 2 U table updates
-        // (U <= T), and 2 per prefill pass (<= T G / 128 + n_seq passes)
-        size_t meta = sizeof(int32_t) * ((size_t)P->max_tok * 7 + 2 * (size_t)cfg->max_sessions +
+        // (U <= T), 2 per prefill pass (<= T G / 128 + n_seq passes) and 2 per
+        // append run (<= T)
+        size_t meta = sizeof(int32_t) * ((size_t)P->max_tok * 9 + 2 * (size_t)cfg->max_sessions +
                                          2 * ((size_t)P->max_tok * P->G / 128 +
                                               (size_t)cfg->max_sessions) +
                                          64);

@@ -13,7 +13,7 @@ hipError_t launch_plan_apply(const int32_t *, const int32_t *, int32_t, int32_t 
     return hipErrorNotSupported;
 }
 hipError_t launch_append(int, const PoolGeom &, const PlanView &, int32_t, const void *,
-                         const void *, hipStream_t) {
+                         const void *, const int32_t *, const int32_t *, int32_t, hipStream_t) {
     return hipErrorNotSupported;
 }
 hipError_t launch_attn_valu(int, const AttnArgs &, hipStream_t) { return hipErrorNotSupported; }

@@ -57,8 +57,11 @@ hipError_t launch_plan_apply(const int32_t *upd_idx, const int32_t *upd_val, int
                              const double *inv_freq, int32_t half_d, float2 *rope,
                              hipStream_t s);
 
+// Append (fp32 / bf16 pools) over runs: run r covers planned tokens
+// run_tok0[r] .. + run_len[r] - 1, consecutive slots of one block.
 hipError_t launch_append(int dtype, const PoolGeom &g, const PlanView &p, int32_t layer,
-                         const void *k, const void *v, hipStream_t s);
+                         const void *k, const void *v, const int32_t *run_tok0,
+                         const int32_t *run_len, int32_t n_runs, hipStream_t s);
 
 // Vector (VALU) attention over items = planned tokens: decode, and the fp32
 // chunk prefill.  Returns hipErrorInvalidValue for shapes with no instance.

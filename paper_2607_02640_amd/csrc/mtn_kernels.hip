@@ -41,35 +41,57 @@ __global__ void k_plan_apply(const int32_t *__restrict__ upd_idx,
 }
 
 // ---------------------------------------------------------------------------
-// fused RoPE + append + evict: one thread per (token, kv head, rotation pair)
+// fused RoPE + append + evict: one workgroup per (run, kv head), a run being
+// one sequence's tokens in consecutive slots of one block
 // ---------------------------------------------------------------------------
+// Wave w takes the run's tokens w, w + 4, ...; per token, lane i rotates the
+// pair (i, i + D/2) and stores both elements into the token's K row
+// (consecutive lanes, consecutive bytes) and puts the values into an LDS tile
+// [D][16].  After the barrier the V^T tile [D][16] of the block takes, per
+// store instruction, 256 consecutive elements of the run's slots
+// [off0, off0 + len) in memory order: whole row segments instead of one
+// 2-byte element per 32 bytes.
+constexpr int kAppendWaves = 4;
 template <typename T>
-__global__ void k_append(PoolGeom g, PlanView p, int32_t layer, const T *__restrict__ k,
-                         const T *__restrict__ v) {
-    const int half = g.d / 2;
-    int64_t idx = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-    int64_t total = (int64_t)p.n_tok * g.hkv * half;
-    if (idx >= total) return;
-    int i = (int)(idx % half);
-    int64_t th = idx / half;
-    int h = (int)(th % g.hkv);
-    int t = (int)(th / g.hkv);
-    int64_t row = p.tok_row[t];
-    const T *kr = k + (row * g.hkv + h) * g.d;
-    const T *vr = v + (row * g.hkv + h) * g.d;
-    float2 cs = p.rope[(int64_t)t * half + i];
-    float x0 = to_f32(kr[i]), x1 = to_f32(kr[i + half]);
-    float y0 = fmaf(x0, cs.x, -x1 * cs.y);
-    float y1 = fmaf(x1, cs.x, x0 * cs.y);
+__global__ __launch_bounds__(64 * kAppendWaves) void k_append(PoolGeom g, PlanView p, int32_t layer,
+                                                            const T *__restrict__ k,
+                                                            const T *__restrict__ v,
+                                                            const int32_t *__restrict__ run_tok0,
+                                                            const int32_t *__restrict__ run_len) {
+    __shared__ T tr[128 * kBlock];  // the run's values, [d][slot]
+    const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+    const int h = (int)(blockIdx.x % g.hkv);
+    const int r = (int)(blockIdx.x / g.hkv);
+    const int t0 = run_tok0[r], len = run_len[r];
+    const int D = g.d, half = D / 2;
     uint8_t *tile = (uint8_t *)g.kv + (int64_t)layer * g.layer_stride +
-                    (int64_t)p.tok_block[t] * g.block_stride + (int64_t)h * g.head_stride;
+                    (int64_t)p.tok_block[t0] * g.block_stride + (int64_t)h * g.head_stride;
     T *K = (T *)tile;
     T *VT = (T *)(tile + g.tile_bytes);
-    int off = p.tok_off[t];
-    K[off * g.d + i] = from_f32<T>(y0);
-    K[off * g.d + i + half] = from_f32<T>(y1);
-    VT[i * kBlock + off] = vr[i];
-    VT[(i + half) * kBlock + off] = vr[i + half];
+    const int off0 = p.tok_off[t0];
+#pragma unroll
+    for (int jj = 0; jj < kBlock / kAppendWaves; ++jj) {
+        const int j = w + kAppendWaves * jj;
+        if (j >= len) break;
+        const int t = t0 + j;
+        const int64_t row = p.tok_row[t];
+        const T *kr = k + (row * g.hkv + h) * D;
+        const T *vr = v + (row * g.hkv + h) * D;
+        T *kd = K + (off0 + j) * D;
+        for (int i = lane; i < half; i += 64) {
+            const float2 cs = p.rope[(int64_t)t * half + i];
+            const float x0 = to_f32(kr[i]), x1 = to_f32(kr[i + half]);
+            kd[i] = from_f32<T>(fmaf(x0, cs.x, -x1 * cs.y));
+            kd[i + half] = from_f32<T>(fmaf(x1, cs.x, x0 * cs.y));
+            tr[i * kBlock + j] = vr[i];
+            tr[(i + half) * kBlock + j] = vr[i + half];
+        }
+    }
+    __syncthreads();
+    for (int e = threadIdx.x; e < D * len; e += 64 * kAppendWaves) {
+        const int d = e / len, j = e - d * len;
+        VT[d * kBlock + off0 + j] = tr[d * kBlock + j];
+    }
 }
 
 // ---------------------------------------------------------------------------
@@ -1370,16 +1392,19 @@ hipError_t launch_plan_apply(const int32_t *upd_idx, const int32_t *upd_val, int
 }
 
 hipError_t launch_append(int dtype, const PoolGeom &g, const PlanView &p, int32_t layer,
-                         const void *k, const void *v, hipStream_t s) {
-    int64_t total = (int64_t)p.n_tok * g.hkv * (g.d / 2);
-    if (total == 0) return hipSuccess;
-    unsigned grid = (unsigned)((total + 255) / 256);
+                         const void *k, const void *v, const int32_t *run_tok0,
+                         const int32_t *run_len, int32_t n_runs, hipStream_t s) {
+    if (g.d > 128) return hipErrorInvalidValue;  // the per-wave LDS tile holds D <= 128
+    const int64_t groups = (int64_t)n_runs * g.hkv;
+    if (groups == 0) return hipSuccess;
+    if (groups > INT32_MAX) return hipErrorInvalidValue;
+    const unsigned grid = (unsigned)groups;
     if (dtype == 1)
-        hipLaunchKernelGGL(k_append<bf16_t>, dim3(grid), dim3(256), 0, s, g, p, layer,
-                           (const bf16_t *)k, (const bf16_t *)v);
+        hipLaunchKernelGGL(k_append<bf16_t>, dim3(grid), dim3(64 * kAppendWaves), 0, s, g, p, layer,
+                           (const bf16_t *)k, (const bf16_t *)v, run_tok0, run_len);
     else
-        hipLaunchKernelGGL(k_append<float>, dim3(grid), dim3(256), 0, s, g, p, layer,
-                           (const float *)k, (const float *)v);
+        hipLaunchKernelGGL(k_append<float>, dim3(grid), dim3(64 * kAppendWaves), 0, s, g, p, layer,
+                           (const float *)k, (const float *)v, run_tok0, run_len);
     return hipGetLastError();
 }
 
