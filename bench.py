@@ -35,9 +35,17 @@ BF16_MFMA_PEAK_TFLOPS = 2500.0
 COPY_PROBE_BYTES = 4 << 30
 # sources of the decode kernel of the 128-session bf16 workload (the counters
 # go stale when these change)
-KERNEL_SRC = [os.path.join(ROOT, "paper_2607_02640_amd", "csrc", f)
-              for f in ("mtn_mfma.hip", "mtn_device.h")]
+_CSRC = os.path.join(ROOT, "paper_2607_02640_amd", "csrc")
+# the device sources each counted kernel is compiled from: a summary counts
+# only while they are unchanged
+KERNEL_SRC = {
+    "decode": [os.path.join(_CSRC, f) for f in ("mtn_mfma.hip", "mtn_device.h", "mtn_kernels.h")],
+    "prefill": [os.path.join(_CSRC, f) for f in ("mtn_kernels.hip", "mtn_device.h",
+                                                  "mtn_kernels.h")],
+}
 TRAFFIC_SUMMARY = os.path.join(ROOT, "profiles", "decode_traffic_qwen3omni_128s.json")
+PREFILL_TRAFFIC_SUMMARY = os.path.join(ROOT, "profiles", "prefill_traffic_qwen3omni_128s.json")
+READ_PROBE_BYTES = 8 << 30
 
 
 def log(*a):
@@ -67,6 +75,9 @@ def parse():
                     help="run a whole simulated call from empty sessions and report the "
                          "per-frame tick latency and pool occupancy series")
     ap.add_argument("--frames", type=int, default=0, help="--call: frames (0 = the workload's)")
+    ap.add_argument("--kernel-times", action="store_true",
+                    help="--call: HIP events around every launch, for the decode's achieved "
+                         "GB/s over the call (the events add about 3 %% to each tick)")
     ap.add_argument("--pool-blocks", type=int, default=0,
                     help="--call: pool capacity in blocks (0 = exact windowed reservation)")
     ap.add_argument("--stagger", type=int, default=1,
@@ -92,21 +103,36 @@ def parse():
     return ap.parse_args()
 
 
-def kernel_src_hash() -> str:
+def kernel_src_hash(kernel: str = "decode") -> str:
     import hashlib
     h = hashlib.sha256()
-    for fn in KERNEL_SRC:
+    for fn in KERNEL_SRC[kernel]:
         with open(fn, "rb") as f:
             h.update(f.read())
     return h.hexdigest()[:16]
 
 
+def algorithmic_bytes(w, kvd="bf16"):
+    """Per-launch algorithmic bytes of the steady-state decode and chunk
+    prefill of workload w (every query sees S + W keys)."""
+    esz = 4 if kvd == "f32" else 2
+    N, Hq, Hkv, D = w.n_sessions, w.n_q_heads, w.n_kv_heads, w.head_dim
+    C = w.chunk[1]
+    vis = w.n_sink + w.window
+    beta = Hkv * (2 * D + 2) if kvd == "fp8" else 2 * Hkv * D * esz
+    dec = N * (vis * beta + Hq * D * 2 * esz + 2 * Hkv * D * esz + beta)
+    pre = N * ((vis + C - 1) * beta + C * Hq * D * 2 * esz)
+    return dec, pre
+
+
 def traffic_summary(fetch_dir, write_dir):
-    """Per-dispatch HBM bytes of the decode kernel from FETCH_SIZE / WRITE_SIZE
-    (KiB per dispatch), each scaled by what the same counter reads for the
-    bench's own copy kernel (COPY_PROBE_BYTES read and written per dispatch)."""
+    """Per-dispatch HBM bytes of the decode and of the chunk prefill from
+    FETCH_SIZE / WRITE_SIZE (KiB per dispatch), each scaled by what the same
+    counter reads for the bench's own copy kernel (COPY_PROBE_BYTES read and
+    written per dispatch), against the kernels' algorithmic bytes."""
     import csv
     import glob
+    import workload as W
 
     def avg(d, counter, needle):
         vals = []
@@ -121,31 +147,39 @@ def traffic_summary(fetch_dir, write_dir):
     kib = COPY_PROBE_BYTES / 1024
     f_copy, _ = avg(fetch_dir, "FETCH_SIZE", "k_copy")
     w_copy, _ = avg(write_dir, "WRITE_SIZE", "k_copy")
-    f_dec, nf = avg(fetch_dir, "FETCH_SIZE", "k_attn_mfma")
-    w_dec, nw = avg(write_dir, "WRITE_SIZE", "k_attn_mfma")
     fs, ws = kib / f_copy, kib / w_copy
-    out = {
-        "kernel": "k_attn_mfma<bf16> (decode attention), 128-session Qwen3-Omni-shaped workload",
-        "kernel_src_sha256_16": kernel_src_hash(),
-        "commands": [
-            "rocprofv3 --pmc FETCH_SIZE --output-format csv -d " + fetch_dir +
-            " -o f -- python3 bench.py --steps 1 --warmup 0 --no-cpu-baseline",
-            "rocprofv3 --pmc WRITE_SIZE --output-format csv -d " + write_dir +
-            " -o w -- python3 bench.py --steps 1 --warmup 0 --no-cpu-baseline",
-            "python3 bench.py --traffic-summary " + fetch_dir + " " + write_dir,
-        ],
-        "copy_kernel_KiB_per_dispatch": {"FETCH_SIZE": f_copy, "WRITE_SIZE": w_copy,
-                                         "actual_read_KiB": kib, "actual_write_KiB": kib},
-        "scale": {"fetch": fs, "write": ws},
-        "decode_KiB_per_dispatch_raw": {"FETCH_SIZE": f_dec, "WRITE_SIZE": w_dec,
-                                        "dispatches": [nf, nw]},
-        "decode_bytes_per_launch": {"read": f_dec * fs * 1024, "write": w_dec * ws * 1024,
-                                    "total": (f_dec * fs + w_dec * ws) * 1024},
-    }
-    with open(TRAFFIC_SUMMARY, "w") as f:
-        json.dump(out, f, indent=1)
-        f.write("\n")
-    print(json.dumps(out, indent=1))
+    alg_dec, alg_pre = algorithmic_bytes(W.QWEN3_OMNI)
+    commands = [
+        "rocprofv3 --pmc FETCH_SIZE --output-format csv -d " + fetch_dir +
+        " -o f -- python3 bench.py --steps 1 --warmup 0 --no-cpu-baseline",
+        "rocprofv3 --pmc WRITE_SIZE --output-format csv -d " + write_dir +
+        " -o w -- python3 bench.py --steps 1 --warmup 0 --no-cpu-baseline",
+        "python3 bench.py --traffic-summary " + fetch_dir + " " + write_dir,
+    ]
+    for kernel, needle, label, alg, path in (
+            ("decode", "k_attn_mfma", "k_attn_mfma<bf16> (decode attention)", alg_dec,
+             TRAFFIC_SUMMARY),
+            ("prefill", "k_prefill_mfma", "k_prefill_mfma<8, bf16> (chunk prefill)", alg_pre,
+             PREFILL_TRAFFIC_SUMMARY)):
+        f_k, nf = avg(fetch_dir, "FETCH_SIZE", needle)
+        w_k, nw = avg(write_dir, "WRITE_SIZE", needle)
+        rd, wr = f_k * fs * 1024, w_k * ws * 1024
+        out = {
+            "kernel": label + ", 128-session Qwen3-Omni-shaped workload",
+            "kernel_src_sha256_16": kernel_src_hash(kernel),
+            "commands": commands,
+            "copy_kernel_KiB_per_dispatch": {"FETCH_SIZE": f_copy, "WRITE_SIZE": w_copy,
+                                             "actual_read_KiB": kib, "actual_write_KiB": kib},
+            "scale": {"fetch": fs, "write": ws},
+            "KiB_per_dispatch_raw": {"FETCH_SIZE": f_k, "WRITE_SIZE": w_k, "dispatches": [nf, nw]},
+            "bytes_per_launch": {"read": rd, "write": wr, "total": rd + wr},
+            "algorithmic_bytes_per_launch": alg,
+            "measured_over_algorithmic": (rd + wr) / alg,
+        }
+        with open(path, "w") as f:
+            json.dump(out, f, indent=1)
+            f.write("\n")
+        print(json.dumps(out, indent=1))
 
 
 def measured_traffic(workload_name: str):
@@ -160,9 +194,24 @@ def measured_traffic(workload_name: str):
             t = json.load(f)
     except OSError:
         return None
-    if t.get("kernel_src_sha256_16") != kernel_src_hash():
+    if t.get("kernel_src_sha256_16") != kernel_src_hash("decode"):
         return None
-    return t["decode_bytes_per_launch"]["total"]
+    return t["bytes_per_launch"]["total"]
+
+
+def measured_prefill_traffic(workload_name: str):
+    """The same for the chunk prefill: (bytes per launch, measured /
+    algorithmic), or None."""
+    if workload_name != "qwen3-omni":
+        return None
+    try:
+        with open(PREFILL_TRAFFIC_SUMMARY) as f:
+            t = json.load(f)
+    except OSError:
+        return None
+    if t.get("kernel_src_sha256_16") != kernel_src_hash("prefill"):
+        return None
+    return t["bytes_per_launch"]["total"], t["measured_over_algorithmic"]
 
 
 def pick(name):
@@ -256,6 +305,20 @@ def run_gpu(args, w):
     torch.cuda.synchronize()
     copy_gbps = 5 * 2 * probe_bytes / (e0.elapsed_time(e1) * 1e-3) / 1e9
     del src, dst
+    # read probe: achievable read bandwidth (non-temporal 16-byte loads, the
+    # ceiling of a read-bound kernel beside the nominal peak)
+    rsrc = torch.empty(READ_PROBE_BYTES, dtype=torch.uint8, device=dev)
+    rsrc.fill_(7)
+    rout = torch.zeros(4, dtype=torch.int32, device=dev)
+    mtn.hbm_read(rsrc, READ_PROBE_BYTES, 0x9E3779B9, rout)
+    torch.cuda.synchronize()
+    e0.record()
+    for _ in range(5):
+        mtn.hbm_read(rsrc, READ_PROBE_BYTES, 0x9E3779B9, rout)
+    e1.record()
+    torch.cuda.synchronize()
+    read_gbps = 5 * READ_PROBE_BYTES / (e0.elapsed_time(e1) * 1e-3) / 1e9
+    del rsrc, rout
 
     # Timed region 1: K frames with only frame-boundary events -> value.
     # Timed region 2: the same K frames again (steady state, so the same
@@ -321,7 +384,8 @@ def run_gpu(args, w):
         dec_bytes=dec_bytes, dec_launches=n_dec, dec_flops=dec_flops,
         merge_ms_avg=ms_mrg / max(n_mrg, 1), append_ms_avg=ms_app / max(n_app, 1),
         pre_gbps=pre_gbps, pre_tflops=pre_tflops, avg_pre_ms=avg_pre, pre_bytes=pre_bytes,
-        copy_gbps=copy_gbps, n_blocks=n_blocks, pool_gb=nbytes / 1e9, kv_dtype=kvd)
+        copy_gbps=copy_gbps, read_gbps=read_gbps, n_blocks=n_blocks, pool_gb=nbytes / 1e9,
+        kv_dtype=kvd)
     pool.close()
     return res
 
@@ -408,6 +472,53 @@ def run_call(args, w):
         churn = max(1, round(0.02 * N))
         torch.cuda.synchronize()
         log(f"[call] fast-forwarded to mixed lengths (mean {have.mean():.0f} tokens)")
+    else:
+        have = np.zeros(N, dtype=np.int64)
+    # algorithmic bytes of the decode and the chunk prefill launches, from the
+    # sessions' lengths (a one-token chunk runs on the decode kernel)
+    esz = 4 if w.dtype == "f32" else 2
+    beta = 2 * Hkv * D * esz
+    io_tok = Hq * D * 2 * esz + 2 * Hkv * D * esz
+    SW = None if w.window is None else w.n_sink + w.window
+    acct = dict(dec_bytes=0.0, pre_bytes=0.0, dec_ms=0.0, pre_ms=0.0, app_ms=0.0, mrg_ms=0.0,
+                dec_n=0, pre_n=0, served=0)
+
+    def vis(t):
+        return t + 1 if SW is None else min(t + 1, SW)
+
+    def account(grp, cl, nd):
+        dec = pre = 0.0
+        for i, c, d in zip(grp, cl, nd):
+            L = int(have[i])
+            if max(cl) == 1:
+                dec += vis(L) * beta + io_tok + beta
+            else:
+                # keys the chunk's queries see: sinks, then the window run
+                # [max(S, L - W + 1), L + c - 1]
+                if SW is None:
+                    union = L + c
+                else:
+                    union = min(w.n_sink, L + c) + max(0, L + c - max(w.n_sink, L - w.window + 1))
+                pre += union * beta + c * Hq * D * 2 * esz
+            for j in range(d):
+                dec += vis(L + c + j) * beta + io_tok + beta
+            have[i] = L + c + d
+        acct["dec_bytes"] += dec * Lyr
+        acct["pre_bytes"] += pre * Lyr
+        acct["served"] += len(grp)
+
+    def collect():
+        if not args.kernel_times:
+            return
+        kt = pool.kernel_times()
+        acct["dec_n"] += kt["decode"][0]
+        acct["dec_ms"] += kt["decode"][1]
+        acct["pre_n"] += kt["prefill"][0]
+        acct["pre_ms"] += kt["prefill"][1]
+        acct["app_ms"] += kt["append"][1]
+        acct["mrg_ms"] += kt["merge"][1]
+    if args.kernel_times:
+        pool.set_timing(True)
     evs = [torch.cuda.Event(enable_timing=True) for _ in range(2 * frames * K)]
     occ, fail_frame, fail_code = [], None, None
     n_sub = 0
@@ -432,6 +543,7 @@ def run_call(args, w):
                 break
             evs[2 * n_sub + 1].record()
             n_sub += 1
+            account(grp, cl, nd)
         if fail_frame is not None:
             break
         st = pool.stats()
@@ -440,15 +552,20 @@ def run_call(args, w):
             for i in rng.choice(N, churn, replace=False):
                 pool.session_close(sids[i])
                 sids[i] = pool.session_open()
+                have[i] = 0
+        if (f + 1) % 10 == 0:
+            collect()
         if (f + 1) % 50 == 0:
             torch.cuda.synchronize()
             log(f"[call] frame {f + 1}/{frames}")
     torch.cuda.synchronize()
+    collect()
     done = len(occ)
     ticks = [evs[2 * j].elapsed_time(evs[2 * j + 1]) for j in range(done * K)]
     pool.close()
     return dict(ticks=ticks, occupancy=occ, fail_frame=fail_frame, fail_code=fail_code,
-                n_blocks=n_blocks, frames=frames, reserved0=stats0["reserved"], stagger=K)
+                n_blocks=n_blocks, frames=frames, reserved0=stats0["reserved"], stagger=K,
+                acct=acct if args.kernel_times else None, served=acct["served"])
 
 
 def call_report(args, w, r):
@@ -479,7 +596,23 @@ def call_report(args, w, r):
         if r["occupancy"] else None,
         "occupancy_per_10_frames": [round(float(x), 4) for x in r["occupancy"][9::10]],
         "pool_exhausted_in_frame": r["fail_frame"],
+        "session_frames_per_s": round(r["served"] / (float(t.sum()) * 1e-3), 2) if len(t) else None,
     }
+    a = r.get("acct")
+    if a:
+        out["kernel_times"] = {
+            "note": "HIP events around every launch (ticks above include their cost)",
+            "decode_launches": a["dec_n"], "decode_ms_total": round(a["dec_ms"], 2),
+            "decode_algorithmic_GB": round(a["dec_bytes"] / 1e9, 3),
+            "decode_GBps": round(a["dec_bytes"] / (a["dec_ms"] * 1e-3) / 1e9, 1)
+            if a["dec_ms"] else None,
+            "decode_frac_of_8TBps": round(a["dec_bytes"] / (a["dec_ms"] * 1e-3) / 8e12, 4)
+            if a["dec_ms"] else None,
+            "prefill_launches": a["pre_n"], "prefill_ms_total": round(a["pre_ms"], 2),
+            "prefill_GBps": round(a["pre_bytes"] / (a["pre_ms"] * 1e-3) / 1e9, 1)
+            if a["pre_ms"] else None,
+            "append_ms_total": round(a["app_ms"], 2), "merge_ms_total": round(a["mrg_ms"], 2),
+        }
     if fill is not None and len(t) > (fill + 10) * K:
         steady = t[fill * K:]
         mean = float(steady.mean())
@@ -904,6 +1037,12 @@ def main():
             "tick_ms": [round(t, 3) for t in res["ticks"]],
             "frame_budget_ms": w.frame_period_s * 1e3,
             "copy_probe_GBps": round(res["copy_gbps"], 1),
+            "read_probe_GBps": round(res["read_gbps"], 1),
+            "decode_frac_of_read_probe": round(res["dec_gbps"] / res["read_gbps"], 4),
+            "prefill_traffic": (lambda t: None if t is None or res["kv_dtype"] != w.dtype else
+                                {"bytes_per_launch": round(t[0]),
+                                 "measured_over_algorithmic": round(t[1], 4)})(
+                measured_prefill_traffic(args.workload)),
             "pool_GB": round(res["pool_gb"], 2),
         },
     }

@@ -45,7 +45,7 @@ EXPORTS = [
     "mtn_attend_decode_append", "mtn_attend_decode_noalloc",
     "mtn_frame_step", "mtn_pool_stats", "mtn_session_info", "mtn_session_block_table",
     "mtn_plan_info", "mtn_debug_poison_dead", "mtn_pool_set_timing", "mtn_pool_set_prefill_pass_rows",
-    "mtn_pool_kernel_times", "mtn_hbm_copy", "mtn_status_string", "mtn_pool_last_error",
+    "mtn_pool_kernel_times", "mtn_hbm_copy", "mtn_hbm_read", "mtn_status_string", "mtn_pool_last_error",
     "mtn_pool_set_decode_kernel", "mtn_pool_last_split", "mtn_debug_inject_failure",
     "mtn_admission_create", "mtn_admission_destroy", "mtn_admission_offer",
     "mtn_admission_release", "mtn_admission_observe", "mtn_admission_get",
@@ -142,6 +142,7 @@ def load() -> C.CDLL:
         "mtn_pool_set_prefill_pass_rows": (i32, [vp, i32]),
         "mtn_pool_kernel_times": (i32, [vp, P64, C.POINTER(C.c_double)]),
         "mtn_hbm_copy": (i32, [vp, vp, C.c_size_t, vp]),
+        "mtn_hbm_read": (i32, [vp, C.c_size_t, C.c_uint32, vp, vp]),
         "mtn_admission_create": (i32, [C.POINTER(AdmissionConfig), C.POINTER(vp)]),
         "mtn_admission_destroy": (None, [vp]),
         "mtn_admission_offer": (i32, [vp, P32]),
@@ -377,6 +378,14 @@ def hbm_copy(src, dst, nbytes: int, stream=None) -> None:
     st = lib.mtn_hbm_copy(_ptr(src), _ptr(dst), C.c_size_t(nbytes), _stream(stream))
     if st != MTN_OK:
         raise MtnError(st, "hbm_copy")
+
+
+def hbm_read(src, nbytes: int, sentinel: int, out, stream=None) -> None:
+    lib = load()
+    st = lib.mtn_hbm_read(_ptr(src), C.c_size_t(nbytes), C.c_uint32(sentinel), _ptr(out),
+                          _stream(stream))
+    if st != MTN_OK:
+        raise MtnError(st, "hbm_read")
 
 
 class Admission:

@@ -28,6 +28,9 @@ hipError_t launch_poison(int, const PoolGeom &, int32_t, int64_t, const uint16_t
     return hipErrorNotSupported;
 }
 hipError_t launch_copy(const void *, void *, size_t, hipStream_t) { return hipErrorNotSupported; }
+hipError_t launch_read(const void *, size_t, uint32_t, uint32_t *, hipStream_t) {
+    return hipErrorNotSupported;
+}
 hipError_t scratch_buffer(float **, size_t *) { return hipErrorNotSupported; }
 int fp8_head_stride(int d) { return d == 128 ? 4224 : 0; }
 static bool group_ok(int g) { return g == 1 || g == 2 || g == 4 || g == 8; }

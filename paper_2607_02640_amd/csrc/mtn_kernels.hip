@@ -696,6 +696,27 @@ __global__ void k_copy(const u32x4_t *__restrict__ src, u32x4_t *__restrict__ ds
     for (; i < n; i += stride) dst[i] = src[i];
 }
 
+// plain streaming read (the achievable read bandwidth): four 16-byte
+// non-temporal loads in flight per thread, folded by XOR; a thread stores
+// its fold only when it equals `sentinel`, which the caller picks so that it
+// practically never does (the loads cannot be dropped, nothing is written)
+__global__ void k_read(const u32x4_t *__restrict__ src, int64_t n, uint32_t sentinel,
+                       uint32_t *__restrict__ out) {
+    const int64_t stride = (int64_t)gridDim.x * blockDim.x;
+    int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    u32x4_t acc = {0u, 0u, 0u, 0u};
+    for (; i + 3 * stride < n; i += 4 * stride) {
+        const u32x4_t a = __builtin_nontemporal_load(src + i);
+        const u32x4_t b = __builtin_nontemporal_load(src + i + stride);
+        const u32x4_t c = __builtin_nontemporal_load(src + i + 2 * stride);
+        const u32x4_t d = __builtin_nontemporal_load(src + i + 3 * stride);
+        acc ^= a ^ b ^ c ^ d;
+    }
+    for (; i < n; i += stride) acc ^= src[i];
+    const uint32_t x = acc.x ^ acc.y ^ acc.z ^ acc.w;
+    if (x == sentinel) out[0] = x;
+}
+
 // ---------------------------------------------------------------------------
 // MFMA chunk prefill (bf16 or fp8 pool, D = 128): one workgroup per
 // (sequence, row pass, kv head)
@@ -1503,6 +1524,16 @@ hipError_t launch_copy(const void *src, void *dst, size_t bytes, hipStream_t s) 
     int64_t grid = std::min<int64_t>((n + 255) / 256, 256 * 16);
     hipLaunchKernelGGL(k_copy, dim3((unsigned)grid), dim3(256), 0, s, (const u32x4_t *)src,
                        (u32x4_t *)dst, n);
+    return hipGetLastError();
+}
+
+hipError_t launch_read(const void *src, size_t bytes, uint32_t sentinel, uint32_t *out,
+                       hipStream_t s) {
+    const int64_t n = (int64_t)(bytes / 16);
+    if (n == 0) return hipSuccess;
+    const int64_t grid = std::min<int64_t>((n + 255) / 256, 256 * 16);
+    hipLaunchKernelGGL(k_read, dim3((unsigned)grid), dim3(256), 0, s, (const u32x4_t *)src, n,
+                       sentinel, out);
     return hipGetLastError();
 }
 
