@@ -373,12 +373,12 @@ mtn_status mtn_pool_kernel_times(mtn_pool *pool, int64_t *launches, double *ms);
  * profiler's byte counters.                                                   */
 mtn_status mtn_hbm_copy(const void *src, void *dst, size_t bytes, void *stream);
 
-/* Plain device read of `bytes` (a multiple of 16, src 16-byte aligned) with
- * non-temporal loads, nothing written unless a thread's XOR fold of its data
- * equals `sentinel` (then *out, device, receives it): the achievable read
- * bandwidth, the ceiling beside the nominal HBM peak for read-bound kernels. */
-mtn_status mtn_hbm_read(const void *src, size_t bytes, uint32_t sentinel, uint32_t *out,
-                        void *stream);
+/* Device read of `bytes` (a multiple of 8192, src 16-byte aligned) through the
+ * same non-temporal LDS DMA the decode streams its blocks with: 8 KiB chunks
+ * interleaved over the waves, two in flight per wave, nothing computed or
+ * written.  The achievable read bandwidth of that mechanism, the ceiling
+ * beside the nominal HBM peak for the decode.                               */
+mtn_status mtn_hbm_read(const void *src, size_t bytes, void *stream);
 
 /* ---- deadline-aware admission (host only) ------------------------------ */
 

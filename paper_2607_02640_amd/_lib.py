@@ -142,7 +142,7 @@ def load() -> C.CDLL:
         "mtn_pool_set_prefill_pass_rows": (i32, [vp, i32]),
         "mtn_pool_kernel_times": (i32, [vp, P64, C.POINTER(C.c_double)]),
         "mtn_hbm_copy": (i32, [vp, vp, C.c_size_t, vp]),
-        "mtn_hbm_read": (i32, [vp, C.c_size_t, C.c_uint32, vp, vp]),
+        "mtn_hbm_read": (i32, [vp, C.c_size_t, vp]),
         "mtn_admission_create": (i32, [C.POINTER(AdmissionConfig), C.POINTER(vp)]),
         "mtn_admission_destroy": (None, [vp]),
         "mtn_admission_offer": (i32, [vp, P32]),
@@ -380,10 +380,9 @@ def hbm_copy(src, dst, nbytes: int, stream=None) -> None:
         raise MtnError(st, "hbm_copy")
 
 
-def hbm_read(src, nbytes: int, sentinel: int, out, stream=None) -> None:
+def hbm_read(src, nbytes: int, stream=None) -> None:
     lib = load()
-    st = lib.mtn_hbm_read(_ptr(src), C.c_size_t(nbytes), C.c_uint32(sentinel), _ptr(out),
-                          _stream(stream))
+    st = lib.mtn_hbm_read(_ptr(src), C.c_size_t(nbytes), _stream(stream))
     if st != MTN_OK:
         raise MtnError(st, "hbm_read")
 

@@ -1340,10 +1340,9 @@ mtn_status mtn_pool_kernel_times(mtn_pool *P, int64_t *launches, double *ms) {
     });
 }
 
-mtn_status mtn_hbm_read(const void *src, size_t bytes, uint32_t sentinel, uint32_t *out,
-                        void *stream) {
-    if (!src || !out || (bytes % 16) || ((uintptr_t)src % 16)) return MTN_ERR_INVALID_ARG;
-    hipError_t e = launch_read(src, bytes, sentinel, out, (hipStream_t)stream);
+mtn_status mtn_hbm_read(const void *src, size_t bytes, void *stream) {
+    if (!src || (bytes % 8192) || ((uintptr_t)src % 16)) return MTN_ERR_INVALID_ARG;
+    hipError_t e = launch_read(src, bytes, nullptr, (hipStream_t)stream);
     return e == hipSuccess ? MTN_OK : MTN_ERR_DEVICE;
 }
 

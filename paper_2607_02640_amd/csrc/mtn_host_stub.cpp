@@ -28,7 +28,7 @@ hipError_t launch_poison(int, const PoolGeom &, int32_t, int64_t, const uint16_t
     return hipErrorNotSupported;
 }
 hipError_t launch_copy(const void *, void *, size_t, hipStream_t) { return hipErrorNotSupported; }
-hipError_t launch_read(const void *, size_t, uint32_t, uint32_t *, hipStream_t) {
+hipError_t launch_read(const void *, size_t, uint32_t *, hipStream_t) {
     return hipErrorNotSupported;
 }
 hipError_t scratch_buffer(float **, size_t *) { return hipErrorNotSupported; }

@@ -84,10 +84,9 @@ hipError_t launch_poison(int dtype, const PoolGeom &g, int32_t n_layers, int64_t
                          const uint16_t *live_mask, hipStream_t s);
 
 hipError_t launch_copy(const void *src, void *dst, size_t bytes, hipStream_t s);
-// streaming read of `bytes` (a multiple of 16); *out is written only if the
-// XOR fold of a thread's data equals `sentinel`
-hipError_t launch_read(const void *src, size_t bytes, uint32_t sentinel, uint32_t *out,
-                       hipStream_t s);
+// streaming read of the whole 8 KiB chunks of `bytes` into LDS (nothing
+// computed or written)
+hipError_t launch_read(const void *src, size_t bytes, uint32_t *out, hipStream_t s);
 
 // The library's static device workspace for split partials (a file-scope
 // array, no allocation): its address on the current device and its size in

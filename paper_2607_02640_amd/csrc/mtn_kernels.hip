@@ -696,25 +696,30 @@ __global__ void k_copy(const u32x4_t *__restrict__ src, u32x4_t *__restrict__ ds
     for (; i < n; i += stride) dst[i] = src[i];
 }
 
-// plain streaming read (the achievable read bandwidth): four 16-byte
-// non-temporal loads in flight per thread, folded by XOR; a thread stores
-// its fold only when it equals `sentinel`, which the caller picks so that it
-// practically never does (the loads cannot be dropped, nothing is written)
-__global__ void k_read(const u32x4_t *__restrict__ src, int64_t n, uint32_t sentinel,
-                       uint32_t *__restrict__ out) {
-    const int64_t stride = (int64_t)gridDim.x * blockDim.x;
-    int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-    u32x4_t acc = {0u, 0u, 0u, 0u};
-    for (; i + 3 * stride < n; i += 4 * stride) {
-        const u32x4_t a = __builtin_nontemporal_load(src + i);
-        const u32x4_t b = __builtin_nontemporal_load(src + i + stride);
-        const u32x4_t c = __builtin_nontemporal_load(src + i + 2 * stride);
-        const u32x4_t d = __builtin_nontemporal_load(src + i + 3 * stride);
-        acc ^= a ^ b ^ c ^ d;
+// streaming read (the achievable read bandwidth of the decode's copy
+// mechanism): every wave streams 8 KiB chunks into its own two-slot LDS ring
+// with the same non-temporal LDS DMA as the decode, at most two chunks in
+// flight, chunks interleaved over the waves; nothing is computed or written
+// (`out` is kept for the interface)
+constexpr int kReadWaves = 4;
+__global__ __launch_bounds__(64 * kReadWaves) void k_read(const uint8_t *__restrict__ src,
+                                                        int64_t n_chunks, uint32_t *out) {
+    __shared__ __attribute__((aligned(16))) uint8_t ring[kReadWaves][2][8192];
+    const int lane = threadIdx.x & 63;
+    const int w = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+    const int64_t gw = (int64_t)blockIdx.x * kReadWaves + w;
+    const int64_t tw = (int64_t)gridDim.x * kReadWaves;
+    const uint32_t slot0 = lds_addr(&ring[w][0][0]);
+    int i = 0;
+    for (int64_t c = gw; c < n_chunks; c += tw, ++i) {
+        vm_wait<8>();  // the chunk issued two turns ago (this slot's) has landed
+        const uint8_t *g = src + c * 8192 + lane * 16;
+        const uint32_t dst = slot0 + (uint32_t)((i & 1) * 8192);
+#pragma unroll
+        for (int j = 0; j < 8; ++j) dma16(g + j * 1024, dst + j * 1024);
     }
-    for (; i < n; i += stride) acc ^= src[i];
-    const uint32_t x = acc.x ^ acc.y ^ acc.z ^ acc.w;
-    if (x == sentinel) out[0] = x;
+    vm_wait<0>();  // no copy may land after the workgroup ends
+    (void)out;
 }
 
 // ---------------------------------------------------------------------------
@@ -1016,11 +1021,15 @@ __global__ __launch_bounds__(64 * kPfWaves) void k_prefill_mfma(PfArgs pa) {
         // score of a row exceeds it by more than 2^8 and sets it, while
         // masked (-inf) scores give probability 0 against it.
         float m_ref[kPfTpw];
-        // The QK MFMAs start their accumulators at -msh, so the scores come out
-        // already shifted by the reference and each probability is one
-        // exponential with no subtraction; thr is the bump threshold on
-        // shifted scores (m_ref - msh + 2^8: 2^8 once the first finite score
-        // has set the reference)
+        // bf16 pool: the QK MFMAs start their accumulators at -msh, so the
+        // scores come out already shifted by the reference and each
+        // probability is one exponential with no subtraction; thr is the bump
+        // threshold on shifted scores (m_ref - msh + 2^8: 2^8 once the first
+        // finite score has set the reference).  The fp8 kernel keeps unshifted
+        // scores (msh stays 0, thr = m_ref + 2^8): its conversion stage leaves
+        // no registers for the four shift values per tile (measured 0.386 ->
+        // 0.495 ms per layer with them, from spills inside the stage loops).
+        constexpr bool kShift = !F8;
         float msh[kPfTpw], thr[kPfTpw];
         f32x4_t l_i[kPfTpw];
         int tq_i[kPfTpw];
@@ -1225,12 +1234,16 @@ __global__ __launch_bounds__(64 * kPfWaves) void k_prefill_mfma(PfArgs pa) {
                     const bool up = mx > m_ref[i] + kLazy;
                     const float mnew = up ? mx : m_ref[i];
                     const float alpha = up ? __builtin_amdgcn_exp2f(m_ref[i] - mnew) : 1.f;
-                    const float dsh = up ? mnew - msh[i] : 0.f;
                     m_ref[i] = mnew;
-                    msh[i] = up ? mnew : msh[i];
-                    thr[i] = up ? kLazy : thr[i];
-                    sa[i] -= dsh;
-                    sb[i] -= dsh;
+                    if constexpr (kShift) {
+                        const float dsh = up ? mnew - msh[i] : 0.f;
+                        msh[i] = up ? mnew : msh[i];
+                        thr[i] = up ? kLazy : thr[i];
+                        sa[i] -= dsh;
+                        sb[i] -= dsh;
+                    } else {
+                        thr[i] = mnew + kLazy;
+                    }
                     l_i[i] *= alpha;  // all four entries
 #pragma unroll
                     for (int dt = 0; dt < 8; ++dt) acc[i][dt] *= alpha;
@@ -1249,14 +1262,16 @@ __global__ __launch_bounds__(64 * kPfWaves) void k_prefill_mfma(PfArgs pa) {
             for (int s = 0; s < 4; ++s) {
 #pragma unroll
                 for (int i = 0; i < NT; ++i) {
-                    const f32x4_t c0 = f32x4_t{-msh[i], -msh[i], -msh[i], -msh[i]};
+                    const f32x4_t c0 = kShift ? f32x4_t{-msh[i], -msh[i], -msh[i], -msh[i]}
+                                              : f32x4_t{0.f, 0.f, 0.f, 0.f};
                     na[i] = mfma16x16x32(kf[s][0], qf[i][s], s ? na[i] : c0);
                     nb[i] = mfma16x16x32(kf[s][1], qf[i][s], s ? nb[i] : c0);
                 }
 #pragma unroll
                 for (int u = 0; u < kEpg; ++u) {
                     const int f = s * kEpg + u, i = f >> 3, e = f & 7;
-                    p[i][e] = __builtin_amdgcn_exp2f(e < 4 ? sa[i][e] : sb[i][e - 4]);
+                    const float sc = e < 4 ? sa[i][e] : sb[i][e - 4];
+                    p[i][e] = __builtin_amdgcn_exp2f(kShift ? sc : sc - m_ref[i]);
                     // keep it in this group: without the pin the compiler sinks every
                     // exponential below the last group, after the QK MFMAs
                     asm volatile("" : "+v"(p[i][e]));
@@ -1527,13 +1542,15 @@ hipError_t launch_copy(const void *src, void *dst, size_t bytes, hipStream_t s) 
     return hipGetLastError();
 }
 
-hipError_t launch_read(const void *src, size_t bytes, uint32_t sentinel, uint32_t *out,
-                       hipStream_t s) {
-    const int64_t n = (int64_t)(bytes / 16);
+hipError_t launch_read(const void *src, size_t bytes, uint32_t *out, hipStream_t s) {
+    const int64_t n = (int64_t)(bytes / 8192);  // whole 8 KiB chunks
     if (n == 0) return hipSuccess;
-    const int64_t grid = std::min<int64_t>((n + 255) / 256, 256 * 16);
-    hipLaunchKernelGGL(k_read, dim3((unsigned)grid), dim3(256), 0, s, (const u32x4_t *)src, n,
-                       sentinel, out);
+    int dev = 0, n_cu = 256;
+    if (hipGetDevice(&dev) == hipSuccess)
+        (void)hipDeviceGetAttribute(&n_cu, hipDeviceAttributeMultiprocessorCount, dev);
+    const int64_t grid = std::min<int64_t>((n + kReadWaves - 1) / kReadWaves, 2 * (int64_t)n_cu);
+    hipLaunchKernelGGL(k_read, dim3((unsigned)grid), dim3(64 * kReadWaves), 0, s,
+                       (const uint8_t *)src, n, out);
     return hipGetLastError();
 }
 
