@@ -32,7 +32,10 @@
  *     everything issued on the previous plan's stream, because plans reuse
  *     the library's device metadata and workspace.  A pool is driven from one
  *     host thread at a time.
- *   - Layouts are row-major with the last index fastest.
+ *   - Layouts are row-major with the last index fastest.  The activation
+ *     buffers (q, k, v, out of every call and of mtn_frame_batch) must be
+ *     16-byte aligned (else MTN_ERR_INVALID_ARG): the kernels move them in
+ *     16-byte vectors.
  *   - Element types: MTN_F32 is IEEE binary32, MTN_BF16 is bfloat16.  The KV
  *     cache and q/k/v/out share one element type (kv_dtype == io_dtype),
  *     except for the FP8 cache: kv_dtype MTN_FP8_E4M3 stores every (token,

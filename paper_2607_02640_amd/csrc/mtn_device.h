@@ -80,6 +80,14 @@ __device__ __forceinline__ float shfl_xor_f(float x, int m) {
 // sees; an inline-asm copy feeding the swap was invisible to it, and rows 1
 // and 3 -- the rows a swap takes from its second operand -- then read a stale
 // copy.
+// 16 bytes of bf16 as 8 floats
+__device__ __forceinline__ void unpack8(const uint4 &v, float *x) {
+    const uint32_t w[4] = {v.x, v.y, v.z, v.w};
+#pragma unroll
+    for (int e = 0; e < 8; ++e)
+        x[e] = __uint_as_float((e & 1) ? (w[e / 2] & 0xFFFF0000u) : (w[e / 2] << 16));
+}
+
 template <bool HALF>
 __device__ __forceinline__ void row_swap(unsigned x, unsigned &a, unsigned &b) {
     if constexpr (HALF) {

@@ -1057,12 +1057,15 @@ mtn_status mtn_plan_abort(mtn_pool *P) {
     });
 }
 
+// Activation buffers (q, k, v, out) are read and written in 16-byte vectors.
+static bool bad_buf(const void *p) { return !p || ((uintptr_t)p & 15); }
+
 mtn_status mtn_frame_append_kv(mtn_pool *P, int32_t layer, const void *k, const void *v,
                                void *stream) {
     return guarded(P, [&]() -> mtn_status {
         mtn_status st = check_call(P, layer, stream);
         if (st) return st;
-        if (!k || !v) return fail(P, MTN_ERR_INVALID_ARG, "null k or v");
+        if (bad_buf(k) || bad_buf(v)) return fail(P, MTN_ERR_INVALID_ARG, "null or misaligned k or v");
         return append_impl(P, layer, k, v, stream);
     });
 }
@@ -1072,7 +1075,7 @@ mtn_status mtn_attend_chunk_prefill(mtn_pool *P, int32_t layer, const void *q, v
     return guarded(P, [&]() -> mtn_status {
         mtn_status st = check_call(P, layer, stream);
         if (st) return st;
-        if (!q || !out) return fail(P, MTN_ERR_INVALID_ARG, "null q or out");
+        if (bad_buf(q) || bad_buf(out)) return fail(P, MTN_ERR_INVALID_ARG, "null or misaligned q or out");
         if (!P->layer_done[layer]) return fail(P, MTN_ERR_BAD_STATE, "layer not appended");
         return prefill_impl(P, layer, q, out, lse, stream);
     });
@@ -1083,7 +1086,7 @@ mtn_status mtn_attend_decode(mtn_pool *P, int32_t layer, const void *q, void *ou
     return guarded(P, [&]() -> mtn_status {
         mtn_status st = check_call(P, layer, stream);
         if (st) return st;
-        if (!q || !out) return fail(P, MTN_ERR_INVALID_ARG, "null q or out");
+        if (bad_buf(q) || bad_buf(out)) return fail(P, MTN_ERR_INVALID_ARG, "null or misaligned q or out");
         if (!P->all_single) return fail(P, MTN_ERR_BAD_STATE, "decode needs n_tok == 1 everywhere");
         if (n_split < 0 || n_split > kMaxSplit) return fail(P, MTN_ERR_INVALID_ARG, "bad n_split");
         if (!P->layer_done[layer]) return fail(P, MTN_ERR_BAD_STATE, "layer not appended");
@@ -1097,7 +1100,8 @@ mtn_status mtn_attend_decode_append(mtn_pool *P, int32_t layer, const void *k, c
     return guarded(P, [&]() -> mtn_status {
         mtn_status st = check_call(P, layer, stream);
         if (st) return st;
-        if (!k || !v || !q || !out) return fail(P, MTN_ERR_INVALID_ARG, "null k, v, q or out");
+        if (bad_buf(k) || bad_buf(v) || bad_buf(q) || bad_buf(out))
+            return fail(P, MTN_ERR_INVALID_ARG, "null or misaligned k, v, q or out");
         if (!P->all_single) return fail(P, MTN_ERR_BAD_STATE, "decode needs n_tok == 1 everywhere");
         if (n_split < 0 || n_split > kMaxSplit) return fail(P, MTN_ERR_INVALID_ARG, "bad n_split");
         if (P->layer_done[layer]) return fail(P, MTN_ERR_BAD_STATE, "layer already appended");
@@ -1110,7 +1114,7 @@ mtn_status mtn_attend_decode_noalloc(mtn_pool *P, int32_t layer, const void *q, 
     return guarded(P, [&]() -> mtn_status {
         mtn_status st = check_call(P, layer, stream);
         if (st) return st;
-        if (!q || !out) return fail(P, MTN_ERR_INVALID_ARG, "null q or out");
+        if (bad_buf(q) || bad_buf(out)) return fail(P, MTN_ERR_INVALID_ARG, "null or misaligned q or out");
         if (!P->all_single) return fail(P, MTN_ERR_BAD_STATE, "decode needs n_tok == 1 everywhere");
         if (n_split < 0 || n_split > kMaxSplit) return fail(P, MTN_ERR_INVALID_ARG, "bad n_split");
         if (!P->layer_done[layer]) return fail(P, MTN_ERR_BAD_STATE, "layer not appended");
@@ -1135,8 +1139,9 @@ mtn_status mtn_frame_step(mtn_pool *P, const mtn_frame_batch *b, void *stream) {
         const int32_t n = b->n_seq;
         if (n < 1 || n > P->cfg.max_sessions || !b->sids || !b->chunk_len || !b->n_decode)
             return fail(P, MTN_ERR_INVALID_ARG, "bad batch");
-        if (!P->host_only && (!b->q_chunk || !b->k_chunk || !b->v_chunk || !b->out_chunk))
-            return fail(P, MTN_ERR_INVALID_ARG, "null chunk buffer");
+        if (!P->host_only && (bad_buf(b->q_chunk) || bad_buf(b->k_chunk) || bad_buf(b->v_chunk) ||
+                              bad_buf(b->out_chunk)))
+            return fail(P, MTN_ERR_INVALID_ARG, "null or misaligned chunk buffer");
         if (b->n_split < 0 || b->n_split > kMaxSplit) return fail(P, MTN_ERR_INVALID_ARG, "bad n_split");
         int32_t max_dec = 0;
         int64_t Tc = 0;
@@ -1156,8 +1161,9 @@ mtn_status mtn_frame_step(mtn_pool *P, const mtn_frame_batch *b, void *stream) {
             max_dec = std::max(max_dec, b->n_decode[i]);
             Tc += b->chunk_len[i];
         }
-        if (!P->host_only && max_dec > 0 && (!b->q_dec || !b->k_dec || !b->v_dec || !b->out_dec))
-            return fail(P, MTN_ERR_INVALID_ARG, "null decode buffer");
+        if (!P->host_only && max_dec > 0 &&
+            (bad_buf(b->q_dec) || bad_buf(b->k_dec) || bad_buf(b->v_dec) || bad_buf(b->out_dec)))
+            return fail(P, MTN_ERR_INVALID_ARG, "null or misaligned decode buffer");
         {   // whole-frame capacity check before any launch
             std::vector<uint8_t> lbseen((size_t)P->row_len, 0);
             int64_t need = 0;

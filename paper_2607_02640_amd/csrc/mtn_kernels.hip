@@ -853,7 +853,6 @@ template <int G, bool F8>
 __global__ __launch_bounds__(64 * kPfWaves) void k_prefill_mfma(PfArgs pa) {
     constexpr int D = 128;
     constexpr int SB = F8 ? 2 * kF8Read : kPfStageBytes;  // bytes of a ring stage
-    static_assert(kPfWaves >= 2, "two DMA waves");
     static_assert(kPfStages >= 3 && kPfStages <= 8, "ring depth (the DMA waits count at most 63)");
     __shared__ __attribute__((aligned(16))) uint8_t ring[kPfStages][SB];
     __shared__ __attribute__((aligned(16))) uint8_t bfs[F8 ? 2 : 1][F8 ? kPfStageBytes : 16];
@@ -925,23 +924,31 @@ __global__ __launch_bounds__(64 * kPfWaves) void k_prefill_mfma(PfArgs pa) {
         return m;
     };
 
-    // The DMA of every stage is issued by DW waves: wave w < DW moves part
-    // of block w & 1, the other waves only meet them at the barrier.  Lane
+    // The DMA of every stage is issued by DW waves: DMA wave i moves part of
+    // block i & 1, the other waves only meet them at the barrier.  Lane
     // source offsets inside the block and the LDS offsets of the
     // instructions inside a ring slot are the same for every stage.  A block
     // takes NDI instructions -- bf16: 4 for the K tile, 4 for the V^T tile;
     // F8: 4 for the K and V codes, one 2-lane instruction for the 32 exponent
-    // bytes -- and wave w issues those k = (w >> 1) + (DW / 2) m, m < NPW.
+    // bytes -- and DMA wave i issues those k = (i >> 1) + (DW / 2) m, m < NPW.
     constexpr int NDI = F8 ? 5 : 8;  // DMA instructions per block
     constexpr int DW = F8 ? 2 : MTN_PF_DMA_WAVES;
     constexpr int NPW = NDI / (DW / 2);  // DMA instructions per DMA wave per stage
-    static_assert(DW >= 2 && DW <= kPfWaves && NPW * (DW / 2) == NDI, "DMA split");
-    const bool dma_wave = wv < DW;
-    const int db = wv & 1;
+    static_assert(DW >= 2 && NPW * (DW / 2) == NDI, "DMA split");
+    // The DMA waves are waves 2 and 3: with waves w and w + 4 sharing a SIMD,
+    // their SIMDs carry a one-tile second wave at 200 rows per pass, while
+    // the SIMD of waves 0 and 4 holds four tiles and sets the stage time
+    // (measured 2.6 % per layer against waves 0 and 1).
+    constexpr int kDma0 = 2;
+    static_assert(kPfWaves % 2 == 0 && kDma0 + DW <= kPfWaves / 2,
+                  "DMA waves in the first half of the workgroup");
+    const bool dma_wave = wv >= kDma0 && wv < kDma0 + DW;
+    const int dwi = dma_wave ? wv - kDma0 : 0;
+    const int db = dwi & 1;
     uint32_t dsrc[NPW], ddst[NPW];
 #pragma unroll
     for (int m = 0; m < NPW; ++m) {
-        const int j = (wv >> 1) + (DW / 2) * m;
+        const int j = (dwi >> 1) + (DW / 2) * m;
         if constexpr (F8) {
             dsrc[m] = j < 4 ? j * 1024 + lane * 16 : kF8Exp + (lane & 1) * 16;
             ddst[m] = db * kF8Read + (j < 4 ? j * 1024 : kF8Exp);
@@ -1031,6 +1038,7 @@ __global__ __launch_bounds__(64 * kPfWaves) void k_prefill_mfma(PfArgs pa) {
         // 0.495 ms per layer with them, from spills inside the stage loops).
         constexpr bool kShift = !F8;
         float msh[kPfTpw], thr[kPfTpw];
+        f32x4_t csh[kPfTpw];  // {-msh} x 4, kept so the QK start needs no moves
         f32x4_t l_i[kPfTpw];
         int tq_i[kPfTpw];
         bool live[kPfTpw];
@@ -1045,6 +1053,7 @@ __global__ __launch_bounds__(64 * kPfWaves) void k_prefill_mfma(PfArgs pa) {
             tq_i[i] = pos0 + j;
             m_ref[i] = -3.402823466e38f;
             msh[i] = 0.f;
+            csh[i] = f32x4_t{0.f, 0.f, 0.f, 0.f};
             thr[i] = m_ref[i] + 8.f;
             l_i[i] = f32x4_t{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
@@ -1053,23 +1062,33 @@ __global__ __launch_bounds__(64 * kPfWaves) void k_prefill_mfma(PfArgs pa) {
             const int64_t row = a.p.tok_row[t];
             const bf16_t *qh = (const bf16_t *)a.q + (row * g.hq + hq0 + gh) * D;
             const float2 *rp = a.p.rope + (int64_t)t * (D / 2);
+            // (16-byte loads: the q row's eight dims, their rotation partners
+            // and the eight (cos, sin) pairs; the 2-byte form spilled 10 VGPRs)
 #pragma unroll
             for (int s = 0; s < 4; ++s) {
-                // dims s*32 + 8*lg + e, e < 8; RoPE partner is d +- 64
+                // dims d0 + e, e < 8, d0 = s*32 + 8*lg; RoPE partner is d +- 64
+                const int d0 = s * 32 + 8 * lg;
+                float xv[8], yv[8], cs[16];
+                unpack8(*(const uint4 *)(qh + d0), xv);
+                unpack8(*(const uint4 *)(qh + (d0 ^ 64)), yv);
+#pragma unroll
+                for (int k = 0; k < 4; ++k) {
+                    const float4 c = ((const float4 *)(rp + (d0 & 63)))[k];
+                    cs[4 * k] = c.x;
+                    cs[4 * k + 1] = c.y;
+                    cs[4 * k + 2] = c.z;
+                    cs[4 * k + 3] = c.w;
+                }
+                const float sg = d0 < 64 ? -1.f : 1.f;
                 uint32_t w[4];
 #pragma unroll
                 for (int e = 0; e < 8; e += 2) {
                     float r2[2];
 #pragma unroll
-                    for (int u = 0; u < 2; ++u) {
-                        const int d = s * 32 + 8 * lg + e + u;
-                        const int f = d & 63;
-                        float2 cs = rp[f];
-                        float x = to_f32(qh[d]);
-                        float y = to_f32(qh[d ^ 64]);
-                        float sg = d < 64 ? -1.f : 1.f;
-                        r2[u] = rv_ ? fmaf(x, cs.x, sg * y * cs.y) * a.scale_log2 : 0.f;
-                    }
+                    for (int u = 0; u < 2; ++u)
+                        r2[u] = rv_ ? fmaf(xv[e + u], cs[2 * (e + u)], sg * yv[e + u] * cs[2 * (e + u) + 1]) *
+                                          a.scale_log2
+                                    : 0.f;
                     w[e / 2] = pack_bf16x2(r2[0], r2[1]);
                 }
                 qf[i][s] = make_uint4(w[0], w[1], w[2], w[3]);
@@ -1162,7 +1181,20 @@ __global__ __launch_bounds__(64 * kPfWaves) void k_prefill_mfma(PfArgs pa) {
             nph = phys(2 * (kPfStages - 1) + db);
         }
         f32x4_t sa[kPfTpw], sb[kPfTpw];  // scores of the stage being consumed
-        if (dma_wave) vm_wait<NPW * (kPfStages - 2)>();  // stage 0 landed
+        // Ping-pong (bf16): the second half of the waves (group B) meets the
+        // stage barrier after its QK MFMAs and exponentials instead of before
+        // them, so it runs half a stage ahead of group A: while one wave of a
+        // SIMD streams PV MFMAs, the other runs its LDS reads, maximum test and
+        // exponentials (measured 4-5 % per layer).  Group B then reads the K
+        // tiles of stage st + 1 before barrier st, so the DMA waves (all in
+        // group A) wait one stage further ahead: stages 0 and 1 here, st + 2
+        // at barrier st.  The ring slot refilled after barrier st held stage
+        // st - 1, which both groups finished before reaching it.  The fp8
+        // kernel keeps the common barrier: its conversion step is a second
+        // workgroup-wide exchange per stage.
+        constexpr bool kPP = !F8;
+        const bool grp_b = kPP && wv >= kPfWaves / 2;
+        if (dma_wave) vm_wait<NPW * (kPfStages - (kPP ? 3 : 2))>();  // stage 0 (and 1) landed
         __syncthreads();
         if constexpr (F8) {
             f8_stage_to_bf16(&ring[0][0], stage_buf(0), tid);
@@ -1186,15 +1218,17 @@ __global__ __launch_bounds__(64 * kPfWaves) void k_prefill_mfma(PfArgs pa) {
                 for (int dt = 0; dt < 8; ++dt)
                     vf[dt] = make_uint4(vf[dt].x & vm[0], vf[dt].y & vm[1], vf[dt].z & vm[2], vf[dt].w & vm[3]);
             }
-            // stage st + 1 landed (a zero-page stage after the last); the
-            // barrier covers both DMA waves and frees the ring slot last read
-            // at st - 1, which takes stage st + kPfStages - 1
-            if (dma_wave) vm_wait<NPW * (kPfStages - 3)>();
-            __syncthreads();
-            if (dma_wave) {
-                const int nst = st + kPfStages - 1;
-                issue_block(nst, nph);
-                nph = phys(2 * (nst + 1) + db);
+            // stage st + 1 (ping-pong: st + 2) landed (zero-page stages after
+            // the last); the barrier covers both DMA waves and frees the ring
+            // slot last read at st - 1, which takes stage st + kPfStages - 1
+            if (!grp_b) {
+                if (dma_wave) vm_wait<NPW * (kPfStages - (kPP ? 4 : 3))>();
+                __syncthreads();
+                if (dma_wave) {
+                    const int nst = st + kPfStages - 1;
+                    issue_block(nst, nph);
+                    nph = phys(2 * (nst + 1) + db);
+                }
             }
             if constexpr (F8) {
                 // the other bf16 buffer: its stage (st - 1) is consumed
@@ -1238,6 +1272,7 @@ __global__ __launch_bounds__(64 * kPfWaves) void k_prefill_mfma(PfArgs pa) {
                     if constexpr (kShift) {
                         const float dsh = up ? mnew - msh[i] : 0.f;
                         msh[i] = up ? mnew : msh[i];
+                        csh[i] = f32x4_t{-msh[i], -msh[i], -msh[i], -msh[i]};
                         thr[i] = up ? kLazy : thr[i];
                         sa[i] -= dsh;
                         sb[i] -= dsh;
@@ -1262,8 +1297,7 @@ __global__ __launch_bounds__(64 * kPfWaves) void k_prefill_mfma(PfArgs pa) {
             for (int s = 0; s < 4; ++s) {
 #pragma unroll
                 for (int i = 0; i < NT; ++i) {
-                    const f32x4_t c0 = kShift ? f32x4_t{-msh[i], -msh[i], -msh[i], -msh[i]}
-                                              : f32x4_t{0.f, 0.f, 0.f, 0.f};
+                    const f32x4_t c0 = kShift ? csh[i] : f32x4_t{0.f, 0.f, 0.f, 0.f};
                     na[i] = mfma16x16x32(kf[s][0], qf[i][s], s ? na[i] : c0);
                     nb[i] = mfma16x16x32(kf[s][1], qf[i][s], s ? nb[i] : c0);
                 }
@@ -1291,6 +1325,7 @@ __global__ __launch_bounds__(64 * kPfWaves) void k_prefill_mfma(PfArgs pa) {
             for (int i = 0; i < NT; ++i)
                 pb[i] = make_uint4(pack_bf16x2(p[i][0], p[i][1]), pack_bf16x2(p[i][2], p[i][3]),
                                    pack_bf16x2(p[i][4], p[i][5]), pack_bf16x2(p[i][6], p[i][7]));
+            if (grp_b) __syncthreads();  // group B's stage barrier
             // row sums of the (bf16) probabilities: all-ones A operand
             const uint4 ones = make_uint4(0x3F803F80u, 0x3F803F80u, 0x3F803F80u, 0x3F803F80u);
 #pragma unroll

@@ -62,13 +62,6 @@ __device__ __forceinline__ f32x4_t mfma_pv(const uint2 &a, const uint2 &b, f32x4
 __device__ __forceinline__ float rows_sum(float x) {
     return rows_pair<true, true>(rows_pair<true, false>(x));
 }
-// 16 bytes of bf16 as 8 floats
-__device__ __forceinline__ void unpack8(const uint4 &v, float *x) {
-    const uint32_t w[4] = {v.x, v.y, v.z, v.w};
-#pragma unroll
-    for (int e = 0; e < 8; ++e)
-        x[e] = __uint_as_float((e & 1) ? (w[e / 2] & 0xFFFF0000u) : (w[e / 2] << 16));
-}
 
 // ---------------------------------------------------------------------------
 // fused RoPE + quantize + append: one wave per (token, kv head); lane i holds

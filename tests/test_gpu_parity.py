@@ -373,3 +373,37 @@ def test_plans_alternating_between_streams():
                     ref, _ = h._oracle_step(i, *dec[j][i])
                     got = od[j, :, i:i + 1].cpu()
                     assert float(np.max(np.abs(f64(got) - ref))) <= 2e-2, f"frame {f} dec{j} s{i}"
+
+
+def test_misaligned_activation_buffers_are_rejected():
+    """q/k/v/out move in 16-byte vectors: a buffer off by one element is an
+    MTN_ERR_INVALID_ARG that changes nothing, and the plan then runs with
+    aligned buffers and matches the oracle."""
+    say("misaligned buffers")
+    import paper_2607_02640_amd as mtn
+    pool, h = _tiny(dtype="bf16", d=128, hq=8, hkv=2, S=4, W=64, cmax=8, n=2, L=1, blocks=16)
+    h.frame([8, 5], [1, 0])
+    T, hq, hkv, d = 4, 8, 2, 128
+    pool.plan_begin(h.sids, [3, 1])
+    flat = torch.zeros(T * hq * d + 8, dtype=torch.bfloat16, device="cuda")
+    kflat = torch.zeros(T * hkv * d + 8, dtype=torch.bfloat16, device="cuda")
+    k_bad = kflat[1:1 + T * hkv * d].view(T, hkv, d)
+    q_bad = flat[1:1 + T * hq * d].view(T, hq, d)
+    k_ok = torch.zeros(T, hkv, d, dtype=torch.bfloat16, device="cuda")
+    q_ok = torch.zeros(T, hq, d, dtype=torch.bfloat16, device="cuda")
+    out = torch.empty_like(q_ok)
+    with pytest.raises(mtn.MtnError) as e:
+        pool.frame_append_kv(0, k_bad, k_ok)
+    assert e.value.code == mtn.MTN_ERR_INVALID_ARG
+    pool.frame_append_kv(0, k_ok, k_ok)
+    with pytest.raises(mtn.MtnError) as e:
+        pool.attend_chunk_prefill(0, q_bad, out)
+    assert e.value.code == mtn.MTN_ERR_INVALID_ARG
+    with pytest.raises(mtn.MtnError) as e:
+        pool.attend_chunk_prefill(0, q_ok, flat[1:1 + T * hq * d].view(T, hq, d))
+    assert e.value.code == mtn.MTN_ERR_INVALID_ARG
+    pool.plan_abort()
+    torch.cuda.synchronize()
+    # the sessions are where they were: the harness continues against the oracle
+    assert [pool.session_info(s)[0] for s in h.sids] == [9, 5]
+    h.frame([4, 7], [2, 1])
