@@ -256,11 +256,15 @@ __device__ __forceinline__ void dma16(const void *gptr, uint32_t lds) {
 // lives in SGPRs even where the compiler cannot prove it uniform.  The
 // builtin returns int: each half goes through uint32_t, or a low word with
 // bit 31 set would sign-extend into the high word.
-__device__ __forceinline__ void dma16_s(uint32_t voff, const void *sbase, uint32_t lds) {
-    const uint64_t b = (uint64_t)(uintptr_t)sbase;
+// A wave-uniform 64-bit value rebuilt from its first lane's halves, so that
+// it is held in SGPRs (each half goes through uint32_t: see dma16_s).
+__device__ __forceinline__ uint64_t uniform64(uint64_t b) {
     const uint32_t lo = (uint32_t)__builtin_amdgcn_readfirstlane((uint32_t)b);
     const uint32_t hi = (uint32_t)__builtin_amdgcn_readfirstlane((uint32_t)(b >> 32));
-    const uint64_t sb = (uint64_t)lo | ((uint64_t)hi << 32);
+    return (uint64_t)lo | ((uint64_t)hi << 32);
+}
+__device__ __forceinline__ void dma16_s(uint32_t voff, const void *sbase, uint32_t lds) {
+    const uint64_t sb = uniform64((uint64_t)(uintptr_t)sbase);
     asm volatile(
         "s_mov_b32 m0, %2\n\t"
         "s_nop 0\n\t"

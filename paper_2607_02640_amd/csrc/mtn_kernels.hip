@@ -880,6 +880,8 @@ __global__ __launch_bounds__(64 * kPfWaves) void k_prefill_mfma(PfArgs pa) {
     const int tq_max = pos0 + (pass_end - 1) / G;
     const int32_t *trow = g.table + (int64_t)sid * g.row_len;
     const uint8_t *layer_base = g.kv + (int64_t)a.layer * g.layer_stride + (int64_t)kvh * g.head_stride;
+    const uint64_t lb_u = uniform64((uint64_t)(uintptr_t)layer_base);
+    const uint64_t zp_u = uniform64((uint64_t)(uintptr_t)pa.zero_page);
     const uint32_t ring0 = lds_addr(&ring[0][0]);
 
     // union of the visible sets of the pass's queries: sinks, then the ring
@@ -972,12 +974,19 @@ __global__ __launch_bounds__(64 * kPfWaves) void k_prefill_mfma(PfArgs pa) {
     // the last (and absent blocks) move the zero page, so every stage costs
     // a DMA wave the same NPW instructions and its waits are constant
     auto issue_block = [&](int st, int ph) {
-        const uint8_t *src = ph >= 0 ? layer_base + (int64_t)ph * g.block_stride : pa.zero_page;
+        // the block's address is formed in SGPRs: a vector copy of it was
+        // spilled with one query head per kv head (fp8), and a spill reload
+        // here waits for every DMA in flight
+        const uint64_t src_u = ph >= 0 ? lb_u + (uint64_t)((int64_t)ph * g.block_stride) : zp_u;
+        const uint8_t *src = (const uint8_t *)(uintptr_t)src_u;
         const uint32_t dst = ring0 + (uint32_t)((st % kPfStages) * SB);
 #pragma unroll
         for (int m = 0; m < NPW; ++m) {
             if (F8 && m == 4) {
-                if (lane < 2) dma16_s(dsrc[m], src, dst + ddst[m]);
+                // the lane offset is recomputed here rather than kept: with
+                // one query head per kv head the fp8 kernel otherwise spills
+                // it, and the reload's wait also drains the DMA ring
+                if (lane < 2) dma16_s(kF8Exp + (lane & 1) * 16, src, dst + ddst[m]);
             } else {
                 dma16_s(dsrc[m], src, dst + ddst[m]);
             }

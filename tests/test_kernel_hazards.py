@@ -126,3 +126,45 @@ def test_permlane_swaps_are_compiler_placed_with_wait_states(listings):
                 ws += _wait_states(ins[j])
                 j -= 1
     assert n > 0
+
+
+def _functions(lines):
+    """{kernel symbol: its lines}, from each function label to its end marker."""
+    out, cur = {}, None
+    for raw in lines:
+        m = re.match(r"^(_Z\w+):", raw)
+        if m:
+            cur = m.group(1)
+            out[cur] = []
+            continue
+        if cur is not None:
+            if raw.startswith(".Lfunc_end"):
+                cur = None
+                continue
+            out[cur].append(raw)
+    return out
+
+
+def test_no_spill_traffic_inside_dma_loops(listings):
+    """The LDS DMA is inline assembly, so the compiler does not count it in
+    the vector-memory counter it waits on: a spill reload inside a stage loop
+    waits with a count that, in hardware, also covers every DMA issued before
+    it, and the ring drains to one stage in flight (a build that spilled
+    there ran at half speed).  No loop of a kernel that streams through LDS
+    DMA may touch scratch memory."""
+    n = 0
+    for src, lines in listings.items():
+        for name, body in _functions(lines).items():
+            if not any("global_load_lds" in l for l in body):
+                continue
+            n += 1
+            in_loop, bad = False, []
+            for raw in body:
+                if re.match(r"^\.LBB\d+_\d+:", raw):
+                    in_loop = "Loop" in raw
+                    continue
+                s = raw.strip().split(";")[0].strip()
+                if in_loop and s.startswith(("scratch_", "buffer_store", "buffer_load")):
+                    bad.append(s)
+            assert not bad, f"{src}: {name} touches scratch inside a loop: {bad[:3]}"
+    assert n > 0
