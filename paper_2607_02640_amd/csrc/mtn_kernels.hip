@@ -938,9 +938,9 @@ __global__ __launch_bounds__(64 * kPfWaves) void k_prefill_mfma(PfArgs pa) {
     constexpr int NPW = NDI / (DW / 2);  // DMA instructions per DMA wave per stage
     static_assert(DW >= 2 && NPW * (DW / 2) == NDI, "DMA split");
     // The DMA waves are waves 2 and 3: with waves w and w + 4 sharing a SIMD,
-    // their SIMDs carry a one-tile second wave at 200 rows per pass, while
-    // the SIMD of waves 0 and 4 holds four tiles and sets the stage time
-    // (measured 2.6 % per layer against waves 0 and 1).
+    // at 200 rows per pass their SIMDs carry a one-tile second wave, while the
+    // SIMD of waves 0 and 4 holds four tiles (measured 2.6 % per layer against
+    // waves 0 and 1).
     constexpr int kDma0 = 2;
     static_assert(kPfWaves % 2 == 0 && kDma0 + DW <= kPfWaves / 2,
                   "DMA waves in the first half of the workgroup");
