@@ -103,12 +103,40 @@ def parse():
     return ap.parse_args()
 
 
+def _code_only(text: str) -> str:
+    """C/C++ source with comments removed and whitespace runs collapsed: a
+    counter summary stays valid across comment and layout edits."""
+    import re
+    out, i, n = [], 0, len(text)
+    while i < n:
+        c = text[i]
+        if c == '"':  # string literal, copied as is
+            j = i + 1
+            while j < n and text[j] != '"':
+                j += 2 if text[j] == "\\" else 1
+            out.append(text[i:j + 1])
+            i = j + 1
+        elif text.startswith("//", i):
+            j = text.find("\n", i)
+            i = n if j < 0 else j
+        elif text.startswith("/*", i):
+            j = text.find("*/", i + 2)
+            i = n if j < 0 else j + 2
+            out.append(" ")
+        else:
+            out.append(c)
+            i += 1
+    return re.sub(r"\s+", " ", "".join(out)).strip()
+
+
 def kernel_src_hash(kernel: str = "decode") -> str:
+    """Hash of the code (comments and layout aside) of the device sources the
+    kernel compiles from."""
     import hashlib
     h = hashlib.sha256()
     for fn in KERNEL_SRC[kernel]:
-        with open(fn, "rb") as f:
-            h.update(f.read())
+        with open(fn, encoding="utf-8") as f:
+            h.update(_code_only(f.read()).encode())
     return h.hexdigest()[:16]
 
 
