@@ -343,3 +343,35 @@ def test_frame_step_plans_and_rolls_back_like_the_model(policy):
         pool.plan_begin(batch[:1], [1])
         pool.plan_abort()
         _compare(pool, model)
+
+
+def test_empty_plans_and_frames_are_refused_without_change():
+    """An empty batch (no sequence) is an invalid argument for a plan and for a
+    frame step, and leaves the pool as it was; so is a frame whose sessions all
+    have zero tokens."""
+    pool, model = _pair(20, 4, 16, 4, 3)
+    sids = [pool.session_open() for _ in range(2)]
+    for _ in sids:
+        model.open()
+    pool.plan_begin(sids, [3, 2])
+    model.plan_begin(sids, [3, 2])
+    pool.plan_commit()
+    model.plan_commit()
+    before = pool.stats()
+    c, _ = _code(pool.plan_begin, [], [])
+    assert c == mtn.MTN_ERR_INVALID_ARG
+    c, _ = _code(pool.frame_step, [], [], [], None, None, None, None)
+    assert c == mtn.MTN_ERR_INVALID_ARG
+    c, _ = _code(pool.frame_step, sids, [0, 0], [0, 0], None, None, None, None)
+    assert c == mtn.MTN_ERR_INVALID_ARG
+    assert pool.stats() == before
+    _compare(pool, model)
+    # and the pool still plans normally afterwards
+    pool.frame_step(sids, [1, 4], [2, 0], None, None, None, None)
+    model.plan_begin(sids, [1, 4])
+    model.plan_commit()
+    model.plan_begin(sids[:1], [1])
+    model.plan_commit()
+    model.plan_begin(sids[:1], [1])
+    model.plan_commit()
+    _compare(pool, model)
