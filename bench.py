@@ -345,6 +345,22 @@ def run_gpu(args, w):
     e1.record()
     torch.cuda.synchronize()
     read_gbps = 5 * READ_PROBE_BYTES / (e0.elapsed_time(e1) * 1e-3) / 1e9
+    # the same read at one decode launch's size (rounded down to 8 KiB), timed
+    # per launch like the decode: a launch that only streamed its bytes, with
+    # no fixed cost beyond one kernel's start and drain
+    vis = w.n_sink + w.window
+    beta = Hkv * (2 * D + 2) if kvd == "fp8" else 2 * Hkv * D * esz
+    dec_bytes_est = N * (vis * beta + Hq * D * 2 * esz + 2 * Hkv * D * esz + beta)
+    same_bytes = min(READ_PROBE_BYTES, dec_bytes_est // 8192 * 8192)
+    mtn.hbm_read(rsrc, same_bytes)
+    pairs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+             for _ in range(20)]
+    for a, b in pairs:
+        a.record()
+        mtn.hbm_read(rsrc, same_bytes)
+        b.record()
+    torch.cuda.synchronize()
+    read_same_ms = sum(a.elapsed_time(b) for a, b in pairs) / len(pairs)
     del rsrc
 
     # Timed region 1: K frames with only frame-boundary events -> value.
@@ -412,7 +428,7 @@ def run_gpu(args, w):
         merge_ms_avg=ms_mrg / max(n_mrg, 1), append_ms_avg=ms_app / max(n_app, 1),
         pre_gbps=pre_gbps, pre_tflops=pre_tflops, avg_pre_ms=avg_pre, pre_bytes=pre_bytes,
         copy_gbps=copy_gbps, read_gbps=read_gbps, n_blocks=n_blocks, pool_gb=nbytes / 1e9,
-        kv_dtype=kvd)
+        kv_dtype=kvd, read_same_ms=read_same_ms, read_same_bytes=same_bytes)
     pool.close()
     return res
 
@@ -1066,6 +1082,10 @@ def main():
             "copy_probe_GBps": round(res["copy_gbps"], 1),
             "read_probe_GBps": round(res["read_gbps"], 1),
             "decode_frac_of_read_probe": round(res["dec_gbps"] / res["read_gbps"], 4),
+            "read_probe_one_launch": {"bytes": res["read_same_bytes"],
+                                      "ms": round(res["read_same_ms"], 4),
+                                      "decode_ms_over_it": round(res["avg_dec_ms"] /
+                                                                 res["read_same_ms"], 4)},
             "prefill_traffic": (lambda t: None if t is None or res["kv_dtype"] != w.dtype else
                                 {"bytes_per_launch": round(t[0]),
                                  "measured_over_algorithmic": round(t[1], 4)})(
