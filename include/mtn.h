@@ -151,12 +151,8 @@ void mtn_pool_destroy(mtn_pool *pool);
  * session's whole bounded footprint, ceil(S/16) sink blocks plus R/16 ring
  * blocks with R = roundup(W + max_chunk - 1, 16), and fail with
  * MTN_ERR_POOL_EXHAUSTED when the reservations would exceed n_blocks (App. A:
- * the admission cap counts the pinned blocks).  The reservation is set aside
- * as the lowest run of that many consecutive free blocks (block j of the
- * session's row is then run + j); should no such run be free, the session's
- * blocks come lowest free id first.  Unbounded pools reserve nothing and take
- * blocks lowest free id first.  Either way a block enters the session's row
- * (and the assigned count) lazily, when a plan first writes it.              */
+ * the admission cap counts the pinned blocks).  Unbounded pools reserve
+ * nothing.  Blocks are assigned lazily, lowest free id first.                 */
 mtn_status mtn_session_open(mtn_pool *pool, int32_t *sid_out);
 
 /* Close a session: its blocks and reservation return to the pool, its id
@@ -192,9 +188,8 @@ mtn_status mtn_plan_commit(mtn_pool *pool);
 
 /* Abandon the open plan instead of committing it, e.g. after a per-layer call
  * failed (failing cleanly instead of stalling every session, §3; or crashing
- * them, App. B).  Every block the plan assigned returns where it came from
- * (the free list, or the session's run): block tables, the free list and
- * runs (and so every later assignment) and the
+ * them, App. B).  Every block the plan assigned returns to the pool: block
+ * tables, the free list (and so every later lowest-free assignment) and the
  * counters are exactly as before mtn_plan_begin; lengths are unchanged.
  * Device work already issued for the plan is not cancelled; it wrote only
  * slots of positions at or past each session's length, which no later query

@@ -25,13 +25,8 @@ tokens are being written, so the ring holds R = roundup(W + C_max - 1, block)
 slots.  Positions S .. block-1 of the last sink block are never written (the
 pinned blocks hold sink positions only).
 
-Block placement (a design choice of the library, not the paper's): a windowed
-session's whole footprint is set aside at open as one run of row_len
-consecutive blocks, the lowest run that is wholly free (first fit), and
-logical block j of its row is block run + j; when no such run is free, and
-always under the unbounded policy, blocks come lowest-free-first.  Either way a
-block enters the row (is "assigned") lazily, in plan order (sequences in the
-order given, positions increasing), the first time its logical block is
+Block assignment is lazy and lowest-free-first, in plan order (sequences in
+the order given, positions increasing), the first time a logical block is
 written.  Session ids are handed out lowest-free-first.
 """
 from __future__ import annotations
@@ -69,7 +64,6 @@ def round_up(a: int, b: int) -> int:
 class _Session:
     length: int
     row: List[int]
-    run: int = -1    # first block of the run set aside at open, or -1
 
 
 @dataclass
@@ -102,11 +96,6 @@ class IndexModel:
             self.ring = round_up(window + max_chunk - 1, block_size)
             self.max_len = None
         self.row_len = self.n_sink_blocks + self.ring // block_size
-        # free blocks: a flag per block, and a min-heap of candidates whose
-        # stale entries (blocks taken by a run since they were pushed) are
-        # skipped when popped
-        self.is_free: List[bool] = [True] * n_blocks
-        self.n_free = n_blocks
         self.free: List[int] = list(range(n_blocks))  # min-heap
         heapq.heapify(self.free)
         self.sessions: Dict[int, _Session] = {}
@@ -124,33 +113,6 @@ class IndexModel:
         sigma = (pos - self.n_sink) % self.ring
         return self.n_sink_blocks + sigma // self.bs, sigma % self.bs
 
-    # -- free blocks ---------------------------------------------------------
-    def _take_lowest(self) -> int:
-        while True:
-            b = heapq.heappop(self.free)
-            if self.is_free[b]:
-                self.is_free[b] = False
-                self.n_free -= 1
-                return b
-
-    def _give(self, b: int) -> None:
-        self.is_free[b] = True
-        self.n_free += 1
-        heapq.heappush(self.free, b)
-
-    def _first_free_run(self, nb: int) -> int:
-        start, run = 0, 0
-        for b in range(self.n_blocks):
-            if self.is_free[b]:
-                if run == 0:
-                    start = b
-                run += 1
-                if run == nb:
-                    return start
-            else:
-                run = 0
-        return -1
-
     # -- sessions ----------------------------------------------------------
     def open(self) -> int:
         sid = next((i for i in range(self.max_sessions)
@@ -161,14 +123,7 @@ class IndexModel:
             if self.reserved + self.row_len > self.n_blocks:
                 raise IndexError_(ERR_POOL_EXHAUSTED, "reservation exceeds pool")
             self.reserved += self.row_len
-            run = self._first_free_run(self.row_len)
-            if run >= 0:
-                for b in range(run, run + self.row_len):
-                    self.is_free[b] = False
-                self.n_free -= self.row_len
-        else:
-            run = -1
-        self.sessions[sid] = _Session(0, [-1] * self.row_len, run)
+        self.sessions[sid] = _Session(0, [-1] * self.row_len)
         return sid
 
     def close(self, sid: int) -> None:
@@ -177,13 +132,9 @@ class IndexModel:
         s = self.sessions.get(sid)
         if s is None:
             raise IndexError_(ERR_BAD_SESSION, "not open")
-        if s.run >= 0:
-            for b in range(s.run, s.run + self.row_len):
-                self._give(b)
-        else:
-            for b in s.row:
-                if b >= 0:
-                    self._give(b)
+        for b in s.row:
+            if b >= 0:
+                heapq.heappush(self.free, b)
         if self.window is not None:
             self.reserved -= self.row_len
         del self.sessions[sid]
@@ -208,17 +159,14 @@ class IndexModel:
             if self.max_len is not None and self.sessions[sid].length + n > self.max_len:
                 raise IndexError_(ERR_SESSION_FULL, "past max_len")
         # Count the blocks this plan needs first, so that a failure changes
-        # nothing; then assign them in plan order (from the session's run,
-        # else lowest free first).
+        # nothing; then assign them lowest-free-first in plan order.
         need = 0
         for sid, n in zip(sids, n_tok):
-            if self.sessions[sid].run >= 0:
-                continue   # its blocks were set aside at open
             L = self.sessions[sid].length
             row = self.sessions[sid].row
             fresh = {self.logical_slot(p)[0] for p in range(L, L + n)}
             need += sum(1 for lb in fresh if row[lb] < 0)
-        if need > self.n_free:
+        if need > len(self.free):
             raise IndexError_(ERR_POOL_EXHAUSTED, "pool exhausted")
         toks: List[PlannedToken] = []
         fresh: List[Tuple[int, int]] = []
@@ -228,8 +176,7 @@ class IndexModel:
             for p in range(L, L + n):
                 lb, off = self.logical_slot(p)
                 if row[lb] < 0:
-                    run = self.sessions[sid].run
-                    row[lb] = run + lb if run >= 0 else self._take_lowest()
+                    row[lb] = heapq.heappop(self.free)
                     fresh.append((sid, lb))
                 toks.append(PlannedToken(sid, p, row[lb], off))
         self.plan_fresh = fresh
@@ -254,15 +201,14 @@ class IndexModel:
         self.plan_fresh = []
 
     def plan_abort(self) -> None:
-        """Abandon the open plan: the blocks it assigned go back where they
-        came from (the free set, or the session's run), so the pool (and every
-        later choice) is as if the plan had never begun; lengths do not move."""
+        """Abandon the open plan: the blocks it assigned go back to the free
+        set, so the pool (and every later lowest-free choice) is as if the
+        plan had never begun; lengths do not move."""
         if self.plan is None:
             raise IndexError_(ERR_BAD_STATE, "no plan")
         for sid, lb in reversed(self.plan_fresh):
             row = self.sessions[sid].row
-            if self.sessions[sid].run < 0:   # a run keeps its blocks
-                self._give(row[lb])
+            heapq.heappush(self.free, row[lb])
             row[lb] = -1
         self.plan = None
         self.plan_fresh = []

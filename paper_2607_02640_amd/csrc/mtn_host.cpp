@@ -26,8 +26,7 @@ namespace {
 constexpr int kStages = 4;  // pinned staging buffers in flight
 constexpr size_t kZeroPage = 2 * kBlock * 128 * 4;  // 16 KiB
 
-// Lowest-free-first block allocator over a bitmap (bit set = free), with
-// first-fit runs of consecutive free blocks.
+// Lowest-free-first block allocator over a bitmap (bit set = free).
 class BlockAllocator {
   public:
     void reset(int64_t n) {
@@ -56,42 +55,6 @@ class BlockAllocator {
         ++free_;
     }
     bool is_free(int64_t b) const { return (words_[(size_t)(b / 64)] >> (b % 64)) & 1; }
-    // lowest b0 with blocks b0 .. b0 + nb - 1 all free, or -1
-    int64_t find_run(int64_t nb) const {
-        int64_t start = 0, len = 0;
-        for (size_t w = 0; w < words_.size(); ++w) {
-            const uint64_t x = words_[w];
-            const int64_t base = (int64_t)w * 64;
-            if (x == ~0ull && base + 64 <= n_) {  // a whole free word
-                if (len == 0) start = base;
-                len += 64;
-                if (len >= nb) return start;
-                continue;
-            }
-            if (x == 0) {  // a whole taken word
-                len = 0;
-                continue;
-            }
-            for (int b = 0; b < 64 && base + b < n_; ++b) {
-                if ((x >> b) & 1) {
-                    if (len == 0) start = base + b;
-                    if (++len >= nb) return start;
-                } else {
-                    len = 0;
-                }
-            }
-        }
-        return -1;
-    }
-    void take_range(int64_t b0, int64_t nb) {  // every block of the range is free
-        for (int64_t b = b0; b < b0 + nb; ++b) words_[(size_t)(b / 64)] &= ~(1ull << (b % 64));
-        free_ -= nb;
-    }
-    void give_range(int64_t b0, int64_t nb) {
-        for (int64_t b = b0; b < b0 + nb; ++b) words_[(size_t)(b / 64)] |= 1ull << (b % 64);
-        hint_ = std::min(hint_, (size_t)(b0 / 64));
-        free_ += nb;
-    }
 
   private:
     std::vector<uint64_t> words_;
@@ -120,9 +83,6 @@ struct mtn_pool {
     std::vector<uint8_t> is_open;
     std::vector<int64_t> len;
     std::vector<int32_t> n_assigned;
-    // windowed sessions: first block of the run of row_len consecutive blocks
-    // set aside at open (row entry j is block run0 + j), or -1 (no run free)
-    std::vector<int64_t> run0;
     BlockAllocator alloc;
     int64_t assigned = 0, reserved = 0;
     int32_t n_open = 0;
@@ -289,7 +249,6 @@ inline void logical_slot(const mtn_pool *P, int64_t p, int32_t *lb, int32_t *off
 // growing from L to L + n tokens.
 int64_t new_blocks_needed(const mtn_pool *P, int32_t sid, int64_t L, int64_t n,
                           std::vector<uint8_t> &seen) {
-    if (P->run0[sid] >= 0) return 0;  // its blocks were set aside at open
     const int32_t *row = &P->table[(size_t)sid * P->row_len];
     int64_t need = 0;
     std::vector<int32_t> touched;
@@ -346,7 +305,7 @@ void undo_assignments(mtn_pool *P) noexcept {
         const int32_t idx = P->upd_idx[i];
         const int32_t sid = idx / P->row_len;
         P->table[(size_t)idx] = -1;
-        if (P->run0[sid] < 0) P->alloc.give(P->upd_val[i]);  // a run keeps its blocks
+        P->alloc.give(P->upd_val[i]);
         P->n_assigned[sid]--;
         P->assigned--;
     }
@@ -424,7 +383,7 @@ mtn_status plan_begin(mtn_pool *P, int32_t n_seq, const int32_t *sids, const int
         P->have_last_stream = true;
         P->last_stream = stream;
     }
-    // ---- assignment (plan order: the session's run, else lowest free first)
+    // ---- assignment (lowest free first, plan order)
     P->n_seq = n_seq;
     P->T = (int32_t)T;
     P->seq_sid.assign(sids, sids + n_seq);
@@ -451,7 +410,7 @@ mtn_status plan_begin(mtn_pool *P, int32_t n_seq, const int32_t *sids, const int
             int32_t lb, off;
             logical_slot(P, pos, &lb, &off);
             if (row[lb] < 0) {
-                const int64_t b = P->run0[sid] >= 0 ? P->run0[sid] + lb : P->alloc.take();
+                int64_t b = P->alloc.take();
                 row[lb] = (int32_t)b;
                 P->n_assigned[sid]++;
                 P->assigned++;
@@ -919,7 +878,6 @@ mtn_status pool_init(mtn_pool *P, const mtn_pool_config *cfg, void *kv_dev, void
     P->is_open.assign((size_t)cfg->max_sessions, 0);
     P->len.assign((size_t)cfg->max_sessions, 0);
     P->n_assigned.assign((size_t)cfg->max_sessions, 0);
-    P->run0.assign((size_t)cfg->max_sessions, -1);
     P->alloc.reset(cfg->n_blocks);
     P->max_tok = cfg->max_sessions * cfg->max_chunk;
     // the planner's per-plan vectors at their largest, so that planning
@@ -1038,13 +996,6 @@ mtn_status mtn_session_open(mtn_pool *P, int32_t *sid_out) {
             if (P->reserved + P->row_len > P->cfg.n_blocks)
                 return fail(P, MTN_ERR_POOL_EXHAUSTED, "reservation exceeds pool capacity");
             P->reserved += P->row_len;
-            // the session's whole footprint as one run of consecutive blocks
-            // when one is free (first fit): each KV head's blocks then lie at
-            // a fixed stride in HBM, which the block streams read faster than
-            // scattered blocks; otherwise blocks come lowest free first
-            const int64_t b0 = P->alloc.find_run(P->row_len);
-            if (b0 >= 0) P->alloc.take_range(b0, P->row_len);
-            P->run0[sid] = b0;
         }
         P->is_open[sid] = 1;
         P->len[sid] = 0;
@@ -1062,16 +1013,13 @@ mtn_status mtn_session_close(mtn_pool *P, int32_t sid) {
         if (sid < 0 || sid >= P->cfg.max_sessions || !P->is_open[sid])
             return fail(P, MTN_ERR_BAD_SESSION, "session not open");
         int32_t *row = &P->table[(size_t)sid * P->row_len];
-        const bool has_run = P->run0[sid] >= 0;
         for (int32_t j = 0; j < P->row_len; ++j) {
             if (row[j] >= 0) {
-                if (!has_run) P->alloc.give(row[j]);
+                P->alloc.give(row[j]);
                 P->assigned--;
                 row[j] = -1;
             }
         }
-        if (has_run) P->alloc.give_range(P->run0[sid], P->row_len);
-        P->run0[sid] = -1;
         if (!P->unbounded) P->reserved -= P->row_len;
         else P->reserved = P->assigned;
         P->is_open[sid] = 0;

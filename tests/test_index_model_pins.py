@@ -107,48 +107,28 @@ def test_ring_never_overwrites_a_needed_key(S, W, cmax, seed):
         assert set(res) == wa.retained_positions(m.sessions[sid].length, S, W)
 
 
-def test_run_placement_and_reuse_after_churn_hand_case():
+def test_lowest_free_reuse_after_churn_hand_case():
     # S = 4 -> 1 sink block; W = 32, C_max = 1 -> R = 32 -> 2 ring blocks:
-    # 3 blocks per session, pool of 10 blocks.  Each session is given the
-    # lowest wholly free run of 3 consecutive blocks when it opens.
+    # 3 blocks per session, pool of 10 blocks.
     m = im.IndexModel(10, 16, 4, 32, 1, 3)
     assert m.row_len == 3
     a, b, c = m.open(), m.open(), m.open()
     assert (a, b, c) == (0, 1, 2)
-    # runs: a 0..2, b 3..5, c 6..8; block 9 stays free
     # a takes positions 0..20: sink block, then ring block 0 and 1
     for _ in range(21):
         m.plan_begin([a], [1]); m.plan_commit()
     assert m.block_table(a) == [0, 1, 2]
     m.plan_begin([b, c], [1, 1]); m.plan_commit()
-    assert m.block_table(b) == [3, -1, -1] and m.block_table(c) == [6, -1, -1]
-    # blocks enter the row lazily: only the written ones count as assigned
-    assert m.assigned() == 5 and m.reserved_blocks() == 9
+    assert m.block_table(b) == [3, -1, -1] and m.block_table(c) == [4, -1, -1]
     m.close(a)
     assert m.open() == 0            # lowest free session id is reused
-    # its run is again 0..2, the lowest wholly free run (9 alone is too short)
     for _ in range(5):
         m.plan_begin([c, 0], [1, 1]); m.plan_commit()
-    # plan 1: the new session's sink takes block 0 of its run; plan 4: c
-    # reaches position 4 (its first ring block) and takes 6 + 1; plan 5: the
-    # new session reaches position 4 and takes 0 + 1.
-    assert m.block_table(c) == [6, 7, -1]
-    assert m.block_table(0) == [0, 1, -1]
-
-
-def test_lowest_free_blocks_when_no_run_is_free_hand_case():
-    # Unbounded policy, max_len 48 (3 blocks per session), pool of 4: no run
-    # is set aside, blocks are taken lowest free first as they are written.
-    m = im.IndexModel(4, 16, 0, None, 16, 2, max_len=48)
-    s0, s1 = m.open(), m.open()
-    m.plan_begin([s0, s1], [16, 1]); m.plan_commit()
-    assert m.block_table(s0) == [0, -1, -1] and m.block_table(s1) == [1, -1, -1]
-    m.plan_begin([s0, s1], [1, 16]); m.plan_commit()
-    # s0 position 16 -> its second block takes 2; s1 reaches 16 -> takes 3
-    assert m.block_table(s0) == [0, 2, -1] and m.block_table(s1) == [1, 3, -1]
-    m.close(s0)
-    m.plan_begin([s1], [16]); m.plan_commit()
-    assert m.block_table(s1) == [1, 3, 0]   # the lowest freed block
+    # plan 1: the new session's sink takes freed block 0; plan 4: c reaches
+    # position 4 (its first ring block) and takes 1; plan 5: the new session
+    # reaches position 4 and takes 2.
+    assert m.block_table(c) == [4, 1, -1]
+    assert m.block_table(0) == [0, 2, -1]
 
 
 def test_errors_are_atomic():
