@@ -179,9 +179,9 @@ def traffic_summary(fetch_dir, write_dir):
     alg_dec, alg_pre = algorithmic_bytes(W.QWEN3_OMNI)
     commands = [
         "rocprofv3 --pmc FETCH_SIZE --output-format csv -d " + fetch_dir +
-        " -o f -- python3 bench.py --steps 1 --warmup 0 --no-cpu-baseline",
+        " -o p -- python3 bench.py --steps 1 --warmup 0 --no-cpu-baseline",
         "rocprofv3 --pmc WRITE_SIZE --output-format csv -d " + write_dir +
-        " -o w -- python3 bench.py --steps 1 --warmup 0 --no-cpu-baseline",
+        " -o p -- python3 bench.py --steps 1 --warmup 0 --no-cpu-baseline",
         "python3 bench.py --traffic-summary " + fetch_dir + " " + write_dir,
     ]
     for kernel, needle, label, alg, path in (

@@ -96,7 +96,7 @@ struct mtn_pool {
     std::vector<int64_t> seq_pos0;
     std::vector<int32_t> tok_sid, tok_pos, tok_row, tok_block, tok_off;
     std::vector<int32_t> upd_idx, upd_val;
-    std::vector<int32_t> pf_items;  // prefill (sequence, row pass) pairs
+    std::vector<int32_t> pf_items;  // prefill work records (kPfItem ints per row pass)
     std::vector<int32_t> run_tok0, run_len;  // append runs: consecutive slots of one block
     std::vector<uint8_t> layer_done;
 
@@ -116,7 +116,7 @@ struct mtn_pool {
     bool stage_used[kStages] = {};
     int stage_i = 0;
     PlanView view{};
-    int32_t *d_seq_first = nullptr, *d_seq_ntok = nullptr, *d_pf_items = nullptr;
+    int32_t *d_pf_items = nullptr;
     int32_t *d_run_tok0 = nullptr, *d_run_len = nullptr;
     int32_t resident_units = 0;    // decode work units resident on the whole GPU
     int32_t n_cu = 0;              // compute units of the pool's device
@@ -455,11 +455,18 @@ mtn_status plan_begin(mtn_pool *P, int32_t n_seq, const int32_t *sids, const int
             if (2 * wgs * P->cfg.n_kv_heads <= P->n_cu && prefill_pass_rows_valid(128)) rpp = 128;
         }
         P->pf_rows = (int32_t)rpp;
-        for (int32_t i = 0; i < n_seq; ++i)
+        // one record per (sequence, row pass) with everything its workgroup
+        // needs before the first copy, so that it takes one metadata load
+        for (int32_t i = 0; i < n_seq; ++i) {
+            const int32_t t0 = P->seq_first[i];
+            bool contig = true;
+            for (int32_t j = 1; j < n_tok[i]; ++j) contig = contig && P->tok_row[t0 + j] == P->tok_row[t0] + j;
             for (int64_t p = 0; p * rpp < (int64_t)n_tok[i] * P->G; ++p) {
-                P->pf_items.push_back(i);
-                P->pf_items.push_back((int32_t)p);
+                const int32_t rec[kPfItem] = {(int32_t)p,          t0, n_tok[i], sids[i],
+                                              (int32_t)P->seq_pos0[i], P->tok_row[t0], contig ? 1 : 0, 0};
+                P->pf_items.insert(P->pf_items.end(), rec, rec + kPfItem);
             }
+        }
     }
     P->layer_done.assign((size_t)P->cfg.n_layers, 0);
     P->plan_open = true;
@@ -479,10 +486,10 @@ mtn_status plan_begin(mtn_pool *P, int32_t n_seq, const int32_t *sids, const int
     put(P->tok_row.data(), T);
     put(P->tok_block.data(), T);
     put(P->tok_off.data(), T);
-    put(P->seq_first.data(), n_seq);
-    put(P->seq_ntok.data(), n_seq);
     put(P->upd_idx.data(), U);
     put(P->upd_val.data(), U);
+    const size_t o_items = (o + kPfItem - 1) / kPfItem * kPfItem;  // records 32-byte aligned
+    while (o < o_items) h[o++] = 0;
     put(P->pf_items.data(), (int32_t)P->pf_items.size());
     const int32_t NR = (int32_t)P->run_tok0.size();
     put(P->run_tok0.data(), NR);
@@ -505,12 +512,10 @@ mtn_status plan_begin(mtn_pool *P, int32_t n_seq, const int32_t *sids, const int
     P->view.tok_row = d + 2 * T;
     P->view.tok_block = d + 3 * T;
     P->view.tok_off = d + 4 * T;
-    P->d_seq_first = d + 5 * T;
-    P->d_seq_ntok = d + 5 * T + n_seq;
     P->view.rope = P->d_rope;
     P->view.n_tok = (int32_t)T;
-    const int32_t *d_upd_idx = d + 5 * T + 2 * n_seq;
-    P->d_pf_items = d + 5 * T + 2 * n_seq + 2 * U;
+    const int32_t *d_upd_idx = d + 5 * T;
+    P->d_pf_items = d + o_items;
     P->d_run_tok0 = P->d_pf_items + P->pf_items.size();
     P->d_run_len = P->d_run_tok0 + NR;
     he = launch_plan_apply(d_upd_idx, d_upd_idx + U, U, P->d_table, P->view.tok_pos, (int32_t)T,
@@ -712,8 +717,8 @@ mtn_status prefill_impl(mtn_pool *P, int32_t layer, const void *q, void *out, fl
     st = timing_begin(P, s, &e0);
     if (st) return st;
     if (prefill_mfma_supported(P->cfg.kv_dtype, P->cfg.head_dim, P->G)) {
-        HIP_TRY(P, launch_prefill_mfma(P->cfg.kv_dtype, a, P->d_seq_first, P->d_seq_ntok, P->d_pf_items,
-                                       (int32_t)(P->pf_items.size() / 2), P->pf_rows, P->d_zero, s));
+        HIP_TRY(P, launch_prefill_mfma(P->cfg.kv_dtype, a, P->d_pf_items,
+                                       (int32_t)(P->pf_items.size() / kPfItem), P->pf_rows, P->d_zero, s));
     } else {
         HIP_TRY(P, launch_attn_valu(P->cfg.kv_dtype, a, s));
     }
@@ -889,7 +894,7 @@ mtn_status pool_init(mtn_pool *P, const mtn_pool_config *cfg, void *kv_dev, void
     for (auto *v : {&P->tok_sid, &P->tok_pos, &P->tok_row, &P->tok_block, &P->tok_off, &P->upd_idx,
                     &P->upd_val, &P->run_tok0, &P->run_len})
         v->reserve((size_t)P->max_tok);
-    P->pf_items.reserve(2 * ((size_t)P->max_tok * P->G / 128 + (size_t)cfg->max_sessions + 1));
+    P->pf_items.reserve(kPfItem * ((size_t)P->max_tok * P->G / 128 + (size_t)cfg->max_sessions + 1));
     P->layer_done.reserve((size_t)cfg->n_layers);
     if (!host_only) {
         auto bail = [&](hipError_t e, const char *w) {
@@ -903,12 +908,12 @@ mtn_status pool_init(mtn_pool *P, const mtn_pool_config *cfg, void *kv_dev, void
         if ((e = hipMemcpyAsync(P->d_table, P->table.data(), tbl, hipMemcpyHostToDevice,
                                 (hipStream_t)stream)) != hipSuccess)
             return bail(e, "table upload");
-        // per plan: 5 T token fields, 2 n_seq sequence fields, 2 U table updates
-        // (U <= T), 2 per prefill pass (<= T G / 128 + n_seq passes) and 2 per
-        // append run (<= T)
-        size_t meta = sizeof(int32_t) * ((size_t)P->max_tok * 9 + 2 * (size_t)cfg->max_sessions +
-                                         2 * ((size_t)P->max_tok * P->G / 128 +
-                                              (size_t)cfg->max_sessions) +
+        // per plan: 5 T token fields, 2 U table updates (U <= T), kPfItem per
+        // prefill pass (<= T G / 128 + n_seq passes, aligned to a record) and 2
+        // per append run (<= T)
+        size_t meta = sizeof(int32_t) * ((size_t)P->max_tok * 9 +
+                                         kPfItem * ((size_t)P->max_tok * P->G / 128 +
+                                                    (size_t)cfg->max_sessions + 1) +
                                          64);
         if ((e = hipMalloc(&P->d_meta, meta)) != hipSuccess) return bail(e, "meta");
         for (int i = 0; i < kStages; ++i) {

@@ -20,8 +20,8 @@ hipError_t launch_attn_valu(int, const AttnArgs &, hipStream_t) { return hipErro
 hipError_t launch_merge(int, const AttnArgs &, hipStream_t) { return hipErrorNotSupported; }
 int prefill_rows_per_pass() { return 256; }
 bool prefill_pass_rows_valid(int rows) { return rows == 128 || rows == 256; }
-hipError_t launch_prefill_mfma(int, const AttnArgs &, const int32_t *, const int32_t *,
-                               const int32_t *, int32_t, int32_t, const uint8_t *, hipStream_t) {
+hipError_t launch_prefill_mfma(int, const AttnArgs &, const int32_t *, int32_t, int32_t,
+                               const uint8_t *, hipStream_t) {
     return hipErrorNotSupported;
 }
 hipError_t launch_poison(int, const PoolGeom &, int32_t, int64_t, const uint16_t *, hipStream_t) {

@@ -69,15 +69,18 @@ hipError_t launch_attn_valu(int dtype, const AttnArgs &a, hipStream_t s);
 hipError_t launch_merge(int dtype, const AttnArgs &a, hipStream_t s);
 
 // MFMA chunk-prefill attention (bf16 or fp8 pool, D = 128): one workgroup per (sequence,
-// row pass, kv head).  items: n_items (sequence, pass) pairs, pass p of a
-// sequence covering its query rows [p, p + 1) * pass_rows (rows are token * G
-// + group head).  pass_rows: prefill_rows_per_pass() or, to spread few
-// sequences over more workgroups, 128 (prefill_pass_rows_valid).  zero_page:
-// 16 KiB of device zeros, the DMA source of blocks a pass does not see.
+// row pass, kv head).  items: n_items records of kPfItem int32 (32-byte
+// aligned), one per row pass: {pass, first planned token t0, tokens, session
+// id, position of t0, io row of t0, 1 if the sequence's io rows are t0's row
+// + j (else 0: rows come from the plan's tok_row), 0}; pass p covers the
+// sequence's query rows [p, p + 1) * pass_rows (rows are token * G + group
+// head).  pass_rows: prefill_rows_per_pass() or, to spread few sequences over
+// more workgroups, 128 (prefill_pass_rows_valid).  zero_page: 16 KiB of
+// device zeros, the DMA source of blocks a pass does not see.
+constexpr int kPfItem = 8;
 int prefill_rows_per_pass();
 bool prefill_pass_rows_valid(int rows);
-hipError_t launch_prefill_mfma(int dtype, const AttnArgs &a, const int32_t *seq_first_tok,
-                               const int32_t *seq_ntok, const int32_t *items, int32_t n_items,
+hipError_t launch_prefill_mfma(int dtype, const AttnArgs &a, const int32_t *items, int32_t n_items,
                                int32_t pass_rows, const uint8_t *zero_page, hipStream_t s);
 
 hipError_t launch_poison(int dtype, const PoolGeom &g, int32_t n_layers, int64_t n_blocks,

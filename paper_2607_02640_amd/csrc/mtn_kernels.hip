@@ -755,13 +755,15 @@ constexpr int kPfWaves = MTN_PF_WAVES;          // waves per workgroup
 constexpr int kPfTpw = MTN_PF_TILES_PER_WAVE;   // 16-row query tiles per wave per pass
 constexpr int kPfRowsPerPass = kPfWaves * kPfTpw * 16;
 constexpr int kPfStages = MTN_PF_STAGES;        // LDS ring depth in stages of two blocks (16 KiB each)
+#ifndef MTN_PF_EARLY
+#define MTN_PF_EARLY 3
+#endif
+constexpr int kPfEarly = MTN_PF_EARLY;          // ring stages copied before the query rotation
 constexpr int kPfStageBytes = 16384;
 
 struct PfArgs {
     AttnArgs a;
-    const int32_t *seq_first;  // first planned token of each sequence
-    const int32_t *seq_ntok;
-    const int32_t *items;      // (sequence, row pass) pairs: one workgroup row each
+    const int32_t *items;      // kPfItem-int records, one per (sequence, row pass)
     const uint8_t *zero_page;  // 16 KiB of zeros: the DMA source of absent blocks
     int32_t pass_rows;         // query rows per pass: 128 or kPfRowsPerPass
 };
@@ -854,6 +856,7 @@ __global__ __launch_bounds__(64 * kPfWaves) void k_prefill_mfma(PfArgs pa) {
     constexpr int D = 128;
     constexpr int SB = F8 ? 2 * kF8Read : kPfStageBytes;  // bytes of a ring stage
     static_assert(kPfStages >= 3 && kPfStages <= 8, "ring depth (the DMA waits count at most 63)");
+    static_assert(kPfEarly >= 1 && kPfEarly <= kPfStages - 1, "early stages are ring prologue stages");
     __shared__ __attribute__((aligned(16))) uint8_t ring[kPfStages][SB];
     __shared__ __attribute__((aligned(16))) uint8_t bfs[F8 ? 2 : 1][F8 ? kPfStageBytes : 16];
     const AttnArgs &a = pa.a;
@@ -862,16 +865,19 @@ __global__ __launch_bounds__(64 * kPfWaves) void k_prefill_mfma(PfArgs pa) {
     // run in parallel, each over the keys its own rows can see
     const int item = blockIdx.x / g.hkv;
     const int kvh = blockIdx.x % g.hkv;
-    const int seq = __builtin_amdgcn_readfirstlane(pa.items[2 * item]);
-    const int pass = __builtin_amdgcn_readfirstlane(pa.items[2 * item + 1]);
+    // the pass's record: one scalar load before the union and the first copies
+    const int32_t *rec = pa.items + (int64_t)item * kPfItem;
+    const int pass = scalar_ld(rec, 0);
+    const int tok0 = scalar_ld(rec, 1);
+    const int ntok = scalar_ld(rec, 2);
+    const int sid = scalar_ld(rec, 3);
+    const int pos0 = scalar_ld(rec, 4);
+    const int row_t0 = scalar_ld(rec, 5);
+    const bool rows_contig = scalar_ld(rec, 6) != 0;
     const int tid = threadIdx.x;
     const int lane = tid & 63;
     const int wv = __builtin_amdgcn_readfirstlane(tid >> 6);
     const int ln16 = lane & 15, lg = lane >> 4;
-    const int tok0 = __builtin_amdgcn_readfirstlane(pa.seq_first[seq]);
-    const int ntok = __builtin_amdgcn_readfirstlane(pa.seq_ntok[seq]);
-    const int sid = __builtin_amdgcn_readfirstlane(a.p.tok_sid[tok0]);
-    const int pos0 = __builtin_amdgcn_readfirstlane(a.p.tok_pos[tok0]);
     const int n_rows = ntok * G;
     const int pass_row0 = pass * pa.pass_rows;
     const int pass_end = min(n_rows, pass_row0 + pa.pass_rows);  // rows [pass_row0, pass_end)
@@ -1051,15 +1057,27 @@ __global__ __launch_bounds__(64 * kPfWaves) void k_prefill_mfma(PfArgs pa) {
         f32x4_t l_i[kPfTpw];
         int tq_i[kPfTpw];
         bool live[kPfTpw];
+        // The tiles' loads go out together, ahead of any rotation: the io row
+        // of each tile's token first, then every q dim pair and (cos, sin)
+        // pair of both tiles, then the arithmetic.  (Interleaved with the
+        // rotation, the loads took one memory round trip per slice: about
+        // 10 us of every workgroup's prologue.)  Slices s and s + 2 share
+        // their (cos, sin) pairs (dims d and d + 64 hold one rotation pair).
+        int tq_j[kPfTpw], gh_i[kPfTpw];
+        bool rv_i[kPfTpw];
+        int64_t row_i[kPfTpw];
 #pragma unroll
         for (int i = 0; i < kPfTpw; ++i) {
             const int tile0 = pass_row0 + (wv + kPfWaves * i) * 16;
             live[i] = tile0 < pass_end;
             const int r = tile0 + ln16;
-            const bool rv_ = r < pass_end;
-            const int j = rv_ ? r / G : 0;
-            const int gh = rv_ ? r % G : 0;
-            tq_i[i] = pos0 + j;
+            rv_i[i] = r < pass_end;
+            tq_j[i] = rv_i[i] ? r / G : 0;
+            gh_i[i] = rv_i[i] ? r % G : 0;
+            tq_i[i] = pos0 + tq_j[i];
+            // io rows are consecutive within a chunk (every plan without an
+            // explicit row list): no load before the q loads
+            row_i[i] = rows_contig ? row_t0 + tq_j[i] : a.p.tok_row[tok0 + tq_j[i]];
             m_ref[i] = -3.402823466e38f;
             msh[i] = 0.f;
             csh[i] = f32x4_t{0.f, 0.f, 0.f, 0.f};
@@ -1067,39 +1085,71 @@ __global__ __launch_bounds__(64 * kPfWaves) void k_prefill_mfma(PfArgs pa) {
             l_i[i] = f32x4_t{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
             for (int dt = 0; dt < 8; ++dt) acc[i][dt] = f32x4_t{0.f, 0.f, 0.f, 0.f};
-            const int t = tok0 + j;
-            const int64_t row = a.p.tok_row[t];
-            const bf16_t *qh = (const bf16_t *)a.q + (row * g.hq + hq0 + gh) * D;
+        }
+        uint4 qx[kPfTpw][4], qy[kPfTpw][4];  // dims d0 .. d0 + 7 and their partners d0 ^ 64
+        float4 qc[kPfTpw][2][4];             // (cos, sin) of dims (d0 & 63) .. + 7
+#pragma unroll
+        for (int i = 0; i < kPfTpw; ++i) {
+            const int t = tok0 + tq_j[i];
+            const bf16_t *qh = (const bf16_t *)a.q + (row_i[i] * g.hq + hq0 + gh_i[i]) * D;
             const float2 *rp = a.p.rope + (int64_t)t * (D / 2);
-            // (16-byte loads: the q row's eight dims, their rotation partners
-            // and the eight (cos, sin) pairs; the 2-byte form spilled 10 VGPRs)
+#pragma unroll
+            for (int s = 0; s < 4; ++s) {
+                const int d0 = s * 32 + 8 * lg;
+                qx[i][s] = *(const uint4 *)(qh + d0);
+                qy[i][s] = *(const uint4 *)(qh + (d0 ^ 64));
+            }
+#pragma unroll
+            for (int h2 = 0; h2 < 2; ++h2)
+#pragma unroll
+                for (int k = 0; k < 4; ++k) qc[i][h2][k] = ((const float4 *)(rp + h2 * 32 + 8 * lg))[k];
+        }
+        // The DMA waves copy the first kPfEarly stages right behind the q
+        // loads: the first barriers need them, and the rotation's waits for
+        // the q loads (counted by the compiler, which does not see the copies)
+        // then cover exactly these copies.  The rest of the ring follows the
+        // rotation.
+        if (dma_wave) {
+#pragma unroll
+            for (int st = 0; st < kPfEarly; ++st) issue_block(st, phys(2 * st + db));
+        }
+        __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+        for (int i = 0; i < kPfTpw; ++i) {
 #pragma unroll
             for (int s = 0; s < 4; ++s) {
                 // dims d0 + e, e < 8, d0 = s*32 + 8*lg; RoPE partner is d +- 64
                 const int d0 = s * 32 + 8 * lg;
                 float xv[8], yv[8], cs[16];
-                unpack8(*(const uint4 *)(qh + d0), xv);
-                unpack8(*(const uint4 *)(qh + (d0 ^ 64)), yv);
+                unpack8(qx[i][s], xv);
+                unpack8(qy[i][s], yv);
 #pragma unroll
                 for (int k = 0; k < 4; ++k) {
-                    const float4 c = ((const float4 *)(rp + (d0 & 63)))[k];
+                    const float4 c = qc[i][s & 1][k];
                     cs[4 * k] = c.x;
                     cs[4 * k + 1] = c.y;
                     cs[4 * k + 2] = c.z;
                     cs[4 * k + 3] = c.w;
                 }
                 const float sg = d0 < 64 ? -1.f : 1.f;
+                // rows past the pass become zero queries; a mask rather than a
+                // select, so that the compiler keeps the loads unconditional
+                const uint32_t keep = rv_i[i] ? 0xFFFFFFFFu : 0u;
                 uint32_t w[4];
 #pragma unroll
                 for (int e = 0; e < 8; e += 2) {
                     float r2[2];
 #pragma unroll
                     for (int u = 0; u < 2; ++u)
-                        r2[u] = rv_ ? fmaf(xv[e + u], cs[2 * (e + u)], sg * yv[e + u] * cs[2 * (e + u) + 1]) *
-                                          a.scale_log2
-                                    : 0.f;
-                    w[e / 2] = pack_bf16x2(r2[0], r2[1]);
+                        r2[u] = fmaf(xv[e + u], cs[2 * (e + u)], sg * yv[e + u] * cs[2 * (e + u) + 1]) *
+                                a.scale_log2;
+                    w[e / 2] = pack_bf16x2(r2[0], r2[1]) & keep;
                 }
+                // computed here, before the DMA waves issue the ring: the
+                // compiler's waits for these loads count only its own loads, so
+                // left after the copies they would wait for most of the ring
+#pragma unroll
+                for (int e = 0; e < 4; ++e) asm volatile("" : "+v"(w[e]));
                 qf[i][s] = make_uint4(w[0], w[1], w[2], w[3]);
             }
         }
@@ -1182,11 +1232,11 @@ __global__ __launch_bounds__(64 * kPfWaves) void k_prefill_mfma(PfArgs pa) {
                 }
             }
         };
-        // ring prologue: stages 0 .. kPfStages - 2 in flight
+        // ring prologue: stages kPfEarly .. kPfStages - 2 join the first ones in flight
         int nph = -1;  // DMA waves: physical block of the next stage to issue
         if (dma_wave) {
 #pragma unroll
-            for (int st = 0; st < kPfStages - 1; ++st) issue_block(st, phys(2 * st + db));
+            for (int st = kPfEarly; st < kPfStages - 1; ++st) issue_block(st, phys(2 * st + db));
             nph = phys(2 * (kPfStages - 1) + db);
         }
         f32x4_t sa[kPfTpw], sb[kPfTpw];  // scores of the stage being consumed
@@ -1381,8 +1431,7 @@ __global__ __launch_bounds__(64 * kPfWaves) void k_prefill_mfma(PfArgs pa) {
             const int r = pass_row0 + (wv + kPfWaves * i) * 16 + ln16;
             if (r >= pass_end) continue;
             const int j = r / G, gh = r % G;
-            const int t = tok0 + j;
-            const int64_t row = a.p.tok_row[t];
+            const int64_t row = rows_contig ? row_t0 + j : a.p.tok_row[tok0 + j];
             bf16_t *ob = (bf16_t *)a.out + (row * g.hq + hq0 + gh) * D;
             const float inv = 1.f / lt;
 #pragma unroll
@@ -1551,14 +1600,14 @@ void launch_prefill_g(int G, dim3 grid, dim3 block, hipStream_t s, const PfArgs 
     }
 }
 
-hipError_t launch_prefill_mfma(int dtype, const AttnArgs &a, const int32_t *seq_first,
-                               const int32_t *seq_ntok, const int32_t *items, int32_t n_items,
+hipError_t launch_prefill_mfma(int dtype, const AttnArgs &a, const int32_t *items, int32_t n_items,
                                int32_t pass_rows, const uint8_t *zero_page, hipStream_t s) {
     const int G = a.g.hq / a.g.hkv;
     if (!prefill_mfma_supported(dtype, a.g.d, G) || n_items <= 0 || !zero_page || !items ||
         !prefill_pass_rows_valid(pass_rows))
         return hipErrorInvalidValue;
-    PfArgs pa{a, seq_first, seq_ntok, items, zero_page, pass_rows};
+    if (((uintptr_t)items & 31) != 0) return hipErrorInvalidValue;  // records are 32-byte aligned
+    PfArgs pa{a, items, zero_page, pass_rows};
     dim3 grid((unsigned)(n_items * a.g.hkv)), block(64 * kPfWaves);
     if (dtype == 2)
         launch_prefill_g<true>(G, grid, block, s, pa);
