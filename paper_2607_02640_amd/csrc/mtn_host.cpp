@@ -355,6 +355,9 @@ mtn_status plan_begin(mtn_pool *P, int32_t n_seq, const int32_t *sids, const int
         if (seen[sid]) return fail(P, MTN_ERR_INVALID_ARG, "duplicate session in plan");
         seen[sid] = 1;
         if (n_tok[i] < 1) return fail(P, MTN_ERR_INVALID_ARG, "n_tok < 1");
+        // an io row list names one row per sequence: one-token sequences only
+        // (the chunk prefill takes consecutive rows from a sequence's first)
+        if (rows && n_tok[i] != 1) return fail(P, MTN_ERR_INVALID_ARG, "row list with n_tok > 1");
         if (n_tok[i] > P->cfg.max_chunk)
             return fail(P, MTN_ERR_CHUNK_TOO_LARGE, "n_tok > max_chunk");
         if (P->unbounded && P->len[sid] + n_tok[i] > P->cfg.max_len)
@@ -456,14 +459,15 @@ mtn_status plan_begin(mtn_pool *P, int32_t n_seq, const int32_t *sids, const int
         }
         P->pf_rows = (int32_t)rpp;
         // one record per (sequence, row pass) with everything its workgroup
-        // needs before the first copy, so that it takes one metadata load
+        // needs before the first copy, so that it takes one metadata load.
+        // The prefill takes io row (row of t0) + j for token t0 + j: plans
+        // with an explicit row list (frame_step's decode rounds) carry one
+        // token per sequence and never reach it.
         for (int32_t i = 0; i < n_seq; ++i) {
             const int32_t t0 = P->seq_first[i];
-            bool contig = true;
-            for (int32_t j = 1; j < n_tok[i]; ++j) contig = contig && P->tok_row[t0 + j] == P->tok_row[t0] + j;
             for (int64_t p = 0; p * rpp < (int64_t)n_tok[i] * P->G; ++p) {
-                const int32_t rec[kPfItem] = {(int32_t)p,          t0, n_tok[i], sids[i],
-                                              (int32_t)P->seq_pos0[i], P->tok_row[t0], contig ? 1 : 0, 0};
+                const int32_t rec[kPfItem] = {(int32_t)p, t0, n_tok[i], sids[i],
+                                              (int32_t)P->seq_pos0[i], P->tok_row[t0], 0, 0};
                 P->pf_items.insert(P->pf_items.end(), rec, rec + kPfItem);
             }
         }

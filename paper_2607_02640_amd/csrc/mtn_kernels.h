@@ -71,8 +71,8 @@ hipError_t launch_merge(int dtype, const AttnArgs &a, hipStream_t s);
 // MFMA chunk-prefill attention (bf16 or fp8 pool, D = 128): one workgroup per (sequence,
 // row pass, kv head).  items: n_items records of kPfItem int32 (32-byte
 // aligned), one per row pass: {pass, first planned token t0, tokens, session
-// id, position of t0, io row of t0, 1 if the sequence's io rows are t0's row
-// + j (else 0: rows come from the plan's tok_row), 0}; pass p covers the
+// id, position of t0, io row of t0, 0, 0}; token t0 + j of the sequence uses
+// io row (row of t0) + j (multi-token plans always do); pass p covers the
 // sequence's query rows [p, p + 1) * pass_rows (rows are token * G + group
 // head).  pass_rows: prefill_rows_per_pass() or, to spread few sequences over
 // more workgroups, 128 (prefill_pass_rows_valid).  zero_page: 16 KiB of

@@ -872,8 +872,7 @@ __global__ __launch_bounds__(64 * kPfWaves) void k_prefill_mfma(PfArgs pa) {
     const int ntok = scalar_ld(rec, 2);
     const int sid = scalar_ld(rec, 3);
     const int pos0 = scalar_ld(rec, 4);
-    const int row_t0 = scalar_ld(rec, 5);
-    const bool rows_contig = scalar_ld(rec, 6) != 0;
+    const int row_t0 = scalar_ld(rec, 5);  // io rows of the sequence: row_t0 + j
     const int tid = threadIdx.x;
     const int lane = tid & 63;
     const int wv = __builtin_amdgcn_readfirstlane(tid >> 6);
@@ -1075,9 +1074,7 @@ __global__ __launch_bounds__(64 * kPfWaves) void k_prefill_mfma(PfArgs pa) {
             tq_j[i] = rv_i[i] ? r / G : 0;
             gh_i[i] = rv_i[i] ? r % G : 0;
             tq_i[i] = pos0 + tq_j[i];
-            // io rows are consecutive within a chunk (every plan without an
-            // explicit row list): no load before the q loads
-            row_i[i] = rows_contig ? row_t0 + tq_j[i] : a.p.tok_row[tok0 + tq_j[i]];
+            row_i[i] = row_t0 + tq_j[i];  // no load before the q loads
             m_ref[i] = -3.402823466e38f;
             msh[i] = 0.f;
             csh[i] = f32x4_t{0.f, 0.f, 0.f, 0.f};
@@ -1431,7 +1428,7 @@ __global__ __launch_bounds__(64 * kPfWaves) void k_prefill_mfma(PfArgs pa) {
             const int r = pass_row0 + (wv + kPfWaves * i) * 16 + ln16;
             if (r >= pass_end) continue;
             const int j = r / G, gh = r % G;
-            const int64_t row = rows_contig ? row_t0 + j : a.p.tok_row[tok0 + j];
+            const int64_t row = row_t0 + j;
             bf16_t *ob = (bf16_t *)a.out + (row * g.hq + hq0 + gh) * D;
             const float inv = 1.f / lt;
 #pragma unroll
