@@ -313,10 +313,6 @@ def run_gpu(args, w):
         pool.frame_step(sids, [C] * N, [tau] * N, bk["qc"], bk["kc"], bk["vc"], oc,
                         bk["qd"], bk["kd"], bk["vd"], od, n_split=args.n_split)
 
-    for f in range(args.warmup):
-        step(f)
-    torch.cuda.synchronize()
-    log(f"[bench] warmup {args.warmup} frames done")
 
     # copy probe: achievable HBM bandwidth (read + write bytes / time); also
     # the calibration kernel of the profiler's byte counters
@@ -362,6 +358,14 @@ def run_gpu(args, w):
     torch.cuda.synchronize()
     read_same_ms = sum(a.elapsed_time(b) for a, b in pairs) / len(pairs)
     del rsrc
+    torch.cuda.synchronize()
+
+    # warm-up frames last, right before the timed frames (the probes above
+    # stream 16 GB of other memory)
+    for f in range(args.warmup):
+        step(f)
+    torch.cuda.synchronize()
+    log(f"[bench] warmup {args.warmup} frames done")
 
     # Timed region 1: K frames with only frame-boundary events -> value.
     # Timed region 2: the same K frames again (steady state, so the same
