@@ -313,7 +313,6 @@ def run_gpu(args, w):
         pool.frame_step(sids, [C] * N, [tau] * N, bk["qc"], bk["kc"], bk["vc"], oc,
                         bk["qd"], bk["kd"], bk["vd"], od, n_split=args.n_split)
 
-
     # copy probe: achievable HBM bandwidth (read + write bytes / time); also
     # the calibration kernel of the profiler's byte counters
     probe_bytes = COPY_PROBE_BYTES

@@ -1056,12 +1056,13 @@ __global__ __launch_bounds__(64 * kPfWaves) void k_prefill_mfma(PfArgs pa) {
         f32x4_t l_i[kPfTpw];
         int tq_i[kPfTpw];
         bool live[kPfTpw];
-        // The tiles' loads go out together, ahead of any rotation: the io row
-        // of each tile's token first, then every q dim pair and (cos, sin)
-        // pair of both tiles, then the arithmetic.  (Interleaved with the
-        // rotation, the loads took one memory round trip per slice: about
-        // 10 us of every workgroup's prologue.)  Slices s and s + 2 share
-        // their (cos, sin) pairs (dims d and d + 64 hold one rotation pair).
+        // The tiles' loads go out together, ahead of any rotation: every q dim
+        // pair and (cos, sin) pair of both tiles (the io rows follow from the
+        // pass record), then the arithmetic.  (Interleaved with the rotation,
+        // with the io row loaded first, the loads took one memory round trip
+        // per slice: about 10 us of every workgroup's prologue.)  Slices s and
+        // s + 2 share their (cos, sin) pairs (dims d and d + 64 hold one
+        // rotation pair).
         int tq_j[kPfTpw], gh_i[kPfTpw];
         bool rv_i[kPfTpw];
         int64_t row_i[kPfTpw];
