@@ -19,9 +19,9 @@ def _config(seed):
     hkv = rnd.choice([1, 2])
     g = rnd.choice([1, 2, 4, 8])
     S = rnd.choice([0, 1, 4, 17])
-    W = rnd.choice([1, 7, 16, 33, 100])
-    cmax = rnd.choice([1, 5, 25, 40])
-    n = rnd.randint(1, 4)
+    W = rnd.choice([1, 7, 16, 33, 100, 300])
+    cmax = rnd.choice([1, 5, 25, 40, 64])
+    n = rnd.randint(1, 6)
     frames = rnd.randint(4, 7)
     rows = rnd.choice([0, 128, 256])
     kernel = rnd.choice([0, 0, 1, 2])
@@ -29,7 +29,7 @@ def _config(seed):
                 rows=rows, kernel=kernel, seed=seed)
 
 
-@pytest.mark.parametrize("seed", range(12))
+@pytest.mark.parametrize("seed", range(24))
 def test_random_configuration_against_oracle(seed):
     c = _config(seed)
     say(f"random config {c}")
