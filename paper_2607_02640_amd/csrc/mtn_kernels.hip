@@ -616,27 +616,54 @@ __global__ __launch_bounds__(64 * WPU * NG) void k_attn_valu(AttnArgs a) {
 constexpr size_t kScratchFloats = (size_t)4 << 20;  // 16 MiB
 static __device__ __align__(256) float scratch[kScratchFloats];
 
-// merge split partials: one wave per (token, q head)
+// merge split partials: one wave per (token, q head).  Lane s takes split s's
+// (max, sum); the splits' accumulators do not depend on them and are loaded in
+// the same round, eight splits at a time.  The maximum and the weighted sum
+// are formed across the wave, and each split's weight is broadcast from its
+// lane.  (One memory round trip for up to eight splits, where a loop over the
+// splits first for the maximum and then for the sums took two.)
 template <typename T, int D>
 __global__ __launch_bounds__(64) void k_merge(AttnArgs a) {
+    constexpr int VD = D / 64;  // output dims per lane
+    constexpr int CH = 8;       // splits whose accumulators are in flight together
     const int64_t th = blockIdx.x;  // t * Hq + hq
     const int lane = threadIdx.x;
-    const int64_t ns = a.n_split;
-    const float *pacc = a.part;
-    const float *pml = a.part + (int64_t)a.p.n_tok * a.g.hq * ns * D;
-    float M = -INFINITY;
-    for (int s = 0; s < ns; ++s) M = fmaxf(M, pml[(th * ns + s) * 2]);
-    constexpr int VD = D / 64;
+    const int ns = a.n_split;       // 2 .. 64
+    const float *pacc = a.part + th * ns * D + lane * VD;
+    const float *pml = a.part + (int64_t)a.p.n_tok * a.g.hq * ns * D + th * ns * 2;
     float acc[VD];
 #pragma unroll
     for (int r = 0; r < VD; ++r) acc[r] = 0.f;
-    float Lsum = 0.f;
-    for (int s = 0; s < ns; ++s) {
-        float ms = pml[(th * ns + s) * 2], ls = pml[(th * ns + s) * 2 + 1];
-        float w = (ms == -INFINITY) ? 0.f : __builtin_amdgcn_exp2f(ms - M);
-        Lsum += ls * w;
+    float part[CH][VD];
+    auto load = [&](int s0) {
 #pragma unroll
-        for (int r = 0; r < VD; ++r) acc[r] += w * pacc[(th * ns + s) * D + lane * VD + r];
+        for (int c = 0; c < CH; ++c)
+#pragma unroll
+            for (int r = 0; r < VD; ++r) part[c][r] = pacc[min(s0 + c, ns - 1) * D + r];  // past ns: unused
+    };
+    load(0);
+    const float2 ml0 = *(const float2 *)(pml + 2 * min(lane, ns - 1));  // lanes past ns: unused
+    __builtin_amdgcn_sched_barrier(0);  // every load above is in flight before the first wait
+    const float2 ml = lane < ns ? ml0 : make_float2(-INFINITY, 0.f);
+    float M = ml.x;
+#pragma unroll
+    for (int m = 32; m >= 1; m >>= 1) M = fmaxf(M, __shfl_xor(M, m, 64));
+    const float Mn = M == -INFINITY ? 0.f : M;
+    const float w = ml.x == -INFINITY ? 0.f : __builtin_amdgcn_exp2f(ml.x - Mn);
+    float Lsum = ml.y * w;
+#pragma unroll
+    for (int m = 32; m >= 1; m >>= 1) Lsum += __shfl_xor(Lsum, m, 64);
+    for (int s0 = 0; s0 < ns; s0 += CH) {
+        if (s0) load(s0);
+#pragma unroll
+        for (int c = 0; c < CH; ++c) {
+            // no branch: a split past ns weighs 0 (its slot repeats a finite partial)
+            const float wl = __builtin_bit_cast(
+                float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, w), min(s0 + c, 63)));
+            const float ws = s0 + c < ns ? wl : 0.f;
+#pragma unroll
+            for (int r = 0; r < VD; ++r) acc[r] = fmaf(ws, part[c][r], acc[r]);
+        }
     }
     const int t = (int)(th / a.g.hq), hq = (int)(th % a.g.hq);
     const int64_t row = a.p.tok_row[t];
