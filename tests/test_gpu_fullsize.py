@@ -13,7 +13,7 @@ import torch
 
 from oracle import windowed_attention as wa
 from tests._gpu_util import make_pool, say
-from workload import MINICPM_O, MOSHI, QWEN3_OMNI as W, device_bank
+from workload import MINICPM_O, MOSHI, POOL_STRESS_UNBOUNDED, QWEN3_OMNI as W, device_bank
 
 pytestmark = pytest.mark.gpu
 
@@ -259,5 +259,74 @@ def test_recycle_reprefill_sampled_parity(rows):
     rd2, _ = o2.step(_f64(qd[1:2]), _f64(kd[1:2]), _f64(vd[1:2]))
     worst = max(worst, float(np.max(np.abs(_f64(od[1:2]) - rd2))))
     say(f"max abs err {worst:.3e}")
+    assert worst <= 2e-2, worst
+    pool.close()
+
+
+@pytest.mark.parametrize("dtype", ["bf16", "fp8"])
+def test_pool_stress_unbounded_sampled_parity(dtype):
+    """The pool-stress workload's unbounded arm at its last frame: 128
+    sessions at the Qwen3-Omni head shapes on an unbounded pool (no window,
+    no eviction), fast-forwarded to 299 frames of 41 tokens (12 259 tokens
+    each), then frame 300 -- a 25-token chunk and 16 decodes -- through
+    mtn_frame_step: every query sees its whole history, up to 12 300 keys
+    (770 blocks per unit, three times the windowed arm).  Two layers (the
+    launch configuration of a layer does not depend on the layer count).
+    Sampled (session, layer) pairs against the float64 oracle."""
+    wl = POOL_STRESS_UNBOUNDED
+    N, Lyr, Hq, Hkv, D = wl.n_sessions, 2, wl.n_q_heads, wl.n_kv_heads, wl.head_dim
+    C, tau = wl.chunk[1], wl.n_decode[1]
+    L0 = 299 * (C + tau)
+    max_len = L0 + C + tau
+    n_blocks = N * -(-max_len // 16)
+    say(f"unbounded full-size pool: {n_blocks} blocks, {dtype}, sessions at {L0} tokens")
+    pool = make_pool(n_layers=Lyr, hq=Hq, hkv=Hkv, d=D, S=0, W=None, cmax=C, max_sessions=N,
+                     n_blocks=n_blocks, dtype=dtype, theta=wl.rope_theta, max_len=max_len)
+    sids = [pool.session_open() for _ in range(N)]
+    dev, bf = torch.device("cuda"), torch.bfloat16
+    ff_k = device_bank((Lyr, N * C, Hkv, D), bf, dev, 171)
+    ff_v = device_bank((Lyr, N * C, Hkv, D), bf, dev, 172)
+    ff = [C] * (L0 // C) + ([L0 % C] if L0 % C else [])
+    for n in ff:
+        pool.plan_begin(sids, [n] * N)
+        for l in range(Lyr):
+            pool.frame_append_kv(l, ff_k[l], ff_v[l])
+        pool.plan_commit()
+    say(f"fast-forward done: {len(ff)} plans")
+    qc = device_bank((Lyr, N * C, Hq, D), bf, dev, 173)
+    kc = device_bank((Lyr, N * C, Hkv, D), bf, dev, 174)
+    vc = device_bank((Lyr, N * C, Hkv, D), bf, dev, 175)
+    qd = device_bank((tau, Lyr, N, Hq, D), bf, dev, 176)
+    kd = device_bank((tau, Lyr, N, Hkv, D), bf, dev, 177)
+    vd = device_bank((tau, Lyr, N, Hkv, D), bf, dev, 178)
+    oc = torch.empty_like(qc)
+    od = torch.empty_like(qd)
+    pool.frame_step(sids, [C] * N, [tau] * N, qc, kc, vc, oc, qd, kd, vd, od)
+    torch.cuda.synchronize()
+    assert torch.isfinite(oc.float()).all() and torch.isfinite(od.float()).all()
+    say("frame done; oracle samples")
+    worst = 0.0
+    for (i, l) in [(0, 0), (77, 1), (127, 1)]:
+        o = wa.OracleSession(Hq, Hkv, D, 0, None, theta=wl.rope_theta, n_layers=1,
+                             kv_quant="fp8_e4m3" if dtype == "fp8" else None)
+        for n in ff:
+            # each fast-forward plan appended the session's first n rows of the bank
+            o.begin(n)
+            o.layer_step(0, np.zeros((n, Hq, D)), _f64(ff_k[l, i * n:(i + 1) * n]),
+                         _f64(ff_v[l, i * n:(i + 1) * n]), attend=False)
+            o.commit()
+        o.begin(C)
+        ref, _ = o.layer_step(0, _f64(qc[l, i * C:(i + 1) * C]), _f64(kc[l, i * C:(i + 1) * C]),
+                              _f64(vc[l, i * C:(i + 1) * C]))
+        o.commit()
+        err = float(np.max(np.abs(_f64(oc[l, i * C:(i + 1) * C]) - ref)))
+        for j in range(tau):
+            o.begin(1)
+            rd, _ = o.layer_step(0, _f64(qd[j, l, i:i + 1]), _f64(kd[j, l, i:i + 1]),
+                                 _f64(vd[j, l, i:i + 1]))
+            o.commit()
+            err = max(err, float(np.max(np.abs(_f64(od[j, l, i:i + 1]) - rd))))
+        say(f"session {i} layer {l}: max abs err {err:.3e}")
+        worst = max(worst, err)
     assert worst <= 2e-2, worst
     pool.close()
