@@ -324,6 +324,10 @@ __device__ __forceinline__ float vmax2(float a, float b) { return fmaxf(a, b); }
 __device__ __forceinline__ float rows_max(float x) {
     return rows_pair<false, true>(rows_pair<false, false>(x));
 }
+// sum over the four 16-lane rows (lanes with equal lane % 16)
+__device__ __forceinline__ float rows_sum(float x) {
+    return rows_pair<true, true>(rows_pair<true, false>(x));
+}
 
 }  // namespace
 }  // namespace mtn

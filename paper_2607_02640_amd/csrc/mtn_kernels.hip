@@ -1063,9 +1063,13 @@ __global__ __launch_bounds__(64 * kPfWaves) void k_prefill_mfma(PfArgs pa) {
         // ---- per-wave query tiles: rows r = pass_row0 + (wv + kPfWaves i) * 16 + ln16
         uint4 qf[kPfTpw][4];
         f32x4_t acc[kPfTpw][8];
-        // row reference max (log2 units) and the row sum of the probabilities,
-        // accumulated by an MFMA against all-ones (every entry = the row sum).
-        // The reference starts at the lowest finite float: the first finite
+        // row reference max (log2 units) and the row sum of the probabilities.
+        // bf16 pool: the sum of their bf16 roundings, accumulated by an MFMA
+        // against all-ones (every entry = the row sum).  fp8 pool: ls holds
+        // the lane's part of the fp32 sum (its eight keys of every
+        // stage), the four lanes of a row added in the epilogue; vector adds
+        // in place of that MFMA free registers the fp8 stage loop otherwise
+        // spills (2-3 % per layer; the bf16 kernel measured no gain).  The reference starts at the lowest finite float: the first finite
         // score of a row exceeds it by more than 2^8 and sets it, while
         // masked (-inf) scores give probability 0 against it.
         float m_ref[kPfTpw];
@@ -1080,7 +1084,9 @@ __global__ __launch_bounds__(64 * kPfWaves) void k_prefill_mfma(PfArgs pa) {
         constexpr bool kShift = !F8;
         float msh[kPfTpw], thr[kPfTpw];
         f32x4_t csh[kPfTpw];  // {-msh} x 4, kept so the QK start needs no moves
+        constexpr bool kMfmaSum = !F8;
         f32x4_t l_i[kPfTpw];
+        float ls[kPfTpw];
         int tq_i[kPfTpw];
         bool live[kPfTpw];
         // The tiles' loads go out together, ahead of any rotation: every q dim
@@ -1108,6 +1114,7 @@ __global__ __launch_bounds__(64 * kPfWaves) void k_prefill_mfma(PfArgs pa) {
             csh[i] = f32x4_t{0.f, 0.f, 0.f, 0.f};
             thr[i] = m_ref[i] + 8.f;
             l_i[i] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+            ls[i] = 0.f;
 #pragma unroll
             for (int dt = 0; dt < 8; ++dt) acc[i][dt] = f32x4_t{0.f, 0.f, 0.f, 0.f};
         }
@@ -1363,7 +1370,10 @@ __global__ __launch_bounds__(64 * kPfWaves) void k_prefill_mfma(PfArgs pa) {
                     } else {
                         thr[i] = mnew + kLazy;
                     }
-                    l_i[i] *= alpha;  // all four entries
+                    if constexpr (kMfmaSum)
+                        l_i[i] *= alpha;  // all four entries
+                    else
+                        ls[i] *= alpha;
 #pragma unroll
                     for (int dt = 0; dt < 8; ++dt) acc[i][dt] *= alpha;
                 }
@@ -1410,10 +1420,17 @@ __global__ __launch_bounds__(64 * kPfWaves) void k_prefill_mfma(PfArgs pa) {
                 pb[i] = make_uint4(pack_bf16x2(p[i][0], p[i][1]), pack_bf16x2(p[i][2], p[i][3]),
                                    pack_bf16x2(p[i][4], p[i][5]), pack_bf16x2(p[i][6], p[i][7]));
             if (grp_b) __syncthreads();  // group B's stage barrier
-            // row sums of the (bf16) probabilities: all-ones A operand
+            // row sums: of the bf16 probabilities by an all-ones A operand, or
+            // the lane's part by vector adds
             const uint4 ones = make_uint4(0x3F803F80u, 0x3F803F80u, 0x3F803F80u, 0x3F803F80u);
 #pragma unroll
-            for (int i = 0; i < NT; ++i) l_i[i] = mfma16x16x32(ones, pb[i], l_i[i]);
+            for (int i = 0; i < NT; ++i) {
+                if constexpr (kMfmaSum)
+                    l_i[i] = mfma16x16x32(ones, pb[i], l_i[i]);
+                else
+                    ls[i] += ((p[i][0] + p[i][1]) + (p[i][2] + p[i][3])) +
+                             ((p[i][4] + p[i][5]) + (p[i][6] + p[i][7]));
+            }
 #pragma unroll
             for (int dt = 0; dt < 8; ++dt) {
 #pragma unroll
@@ -1452,7 +1469,8 @@ __global__ __launch_bounds__(64 * kPfWaves) void k_prefill_mfma(PfArgs pa) {
 #pragma unroll
         for (int i = 0; i < kPfTpw; ++i) {
             if (!live[i]) continue;
-            const float lt = l_i[i][0];
+            // (every lane of the wave takes part in the row sum)
+            const float lt = kMfmaSum ? l_i[i][0] : rows_sum(ls[i]);
             const int r = pass_row0 + (wv + kPfWaves * i) * 16 + ln16;
             if (r >= pass_end) continue;
             const int j = r / G, gh = r % G;

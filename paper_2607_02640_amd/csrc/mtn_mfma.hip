@@ -58,10 +58,6 @@ __device__ __forceinline__ f32x4_t mfma_pv(const uint2 &a, const uint2 &b, f32x4
     return __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(__builtin_bit_cast(s16x4_t, a),
                                                       __builtin_bit_cast(s16x4_t, b), c, 0, 0, 0);
 }
-// sum over the four 16-lane rows (lanes with equal lane % 16)
-__device__ __forceinline__ float rows_sum(float x) {
-    return rows_pair<true, true>(rows_pair<true, false>(x));
-}
 
 // ---------------------------------------------------------------------------
 // fused RoPE + quantize + append: one wave per (token, kv head); lane i holds
