@@ -7,7 +7,8 @@ sessions, each frame a 25-token chunk prefill then 16 decode steps, 4 pinned
 sinks plus a 4096-token window in a paged pool of 16-token blocks.  Sessions
 are first brought to steady state (window full and wrapping) by append-only
 plans; every timed step is then one whole frame for all 128 sessions:
-48 x (append + chunk prefill) followed by 16 x 48 x (append + decode).
+48 x chunk prefill followed by 16 x 48 x decode, each launch appending its
+own tokens.
 
 Inputs are synthetic N(0, 1) draws (torch's seeded device generator) in a
 two-frame bank; they stand in for the paper's real-audio sessions.
@@ -140,16 +141,20 @@ def kernel_src_hash(kernel: str = "decode") -> str:
     return h.hexdigest()[:16]
 
 
-def algorithmic_bytes(w, kvd="bf16"):
+def algorithmic_bytes(w, kvd="bf16", fused_append=True):
     """Per-launch algorithmic bytes of the steady-state decode and chunk
-    prefill of workload w (every query sees S + W keys)."""
+    prefill of workload w (every query sees S + W keys).  Both launches also
+    append their tokens (read k, v; write the pool copy): the decode always,
+    the prefill when the chunk append is fused into it (every sequence in one
+    row pass)."""
     esz = 4 if kvd == "f32" else 2
     N, Hq, Hkv, D = w.n_sessions, w.n_q_heads, w.n_kv_heads, w.head_dim
     C = w.chunk[1]
     vis = w.n_sink + w.window
     beta = Hkv * (2 * D + 2) if kvd == "fp8" else 2 * Hkv * D * esz
-    dec = N * (vis * beta + Hq * D * 2 * esz + 2 * Hkv * D * esz + beta)
-    pre = N * ((vis + C - 1) * beta + C * Hq * D * 2 * esz)
+    app = 2 * Hkv * D * esz + beta                       # one token's append
+    dec = N * (vis * beta + Hq * D * 2 * esz + app)
+    pre = N * ((vis + C - 1) * beta + C * Hq * D * 2 * esz + (C * app if fused_append else 0))
     return dec, pre
 
 
@@ -398,22 +403,26 @@ def run_gpu(args, w):
     log(f"[bench] {args.steps} frames with per-launch events in {timed_ms:.1f} ms; kernels {kt}")
 
     # algorithmic bytes (steady state: every query sees S + W keys).  A decode
-    # launch also appends its token (read k, v; write the pool copy)
+    # launch also appends its token (read k, v; write the pool copy), and so
+    # does a chunk prefill with the append fused in (no append launches in the
+    # timed frames)
     # pool bytes of one token (all kv heads): K and V rows, plus the two scale
     # exponent bytes per head of the fp8 cache
-    vis = w.n_sink + w.window
-    beta = Hkv * (2 * D + 2) if kvd == "fp8" else 2 * Hkv * D * esz
-    # per decode launch: the visible keys, q in and out, the new token's k and v
-    # in (io type) and its pool copy out
-    dec_bytes = N * (vis * beta + Hq * D * 2 * esz + 2 * Hkv * D * esz + beta)
-    dec_flops = N * 4 * Hq * D * vis
-    chunk_union = vis + C - 1                                 # keys a chunk reads
-    pre_bytes = N * (chunk_union * beta + C * Hq * D * 2 * esz)
-    pre_flops = N * 4 * Hq * D * vis * C
     n_dec, ms_dec = kt["decode"]
     n_mrg, ms_mrg = kt["merge"]
     n_pre, ms_pre = kt["prefill"]
     n_app, ms_app = kt["append"]
+    vis = w.n_sink + w.window
+    beta = Hkv * (2 * D + 2) if kvd == "fp8" else 2 * Hkv * D * esz
+    app_tok = 2 * Hkv * D * esz + beta
+    # per decode launch: the visible keys, q in and out, the new token's k and v
+    # in (io type) and its pool copy out
+    dec_bytes = N * (vis * beta + Hq * D * 2 * esz + app_tok)
+    dec_flops = N * 4 * Hq * D * vis
+    chunk_union = vis + C - 1                                 # keys a chunk reads
+    pre_fused = n_app == 0
+    pre_bytes = N * (chunk_union * beta + C * Hq * D * 2 * esz + (C * app_tok if pre_fused else 0))
+    pre_flops = N * 4 * Hq * D * vis * C
     avg_dec = ms_dec / max(n_dec, 1)
     dec_gbps = dec_bytes / (avg_dec * 1e-3) / 1e9
     dec_merge_gbps = dec_bytes * n_dec / ((ms_dec + ms_mrg) * 1e-3) / 1e9
@@ -430,6 +439,7 @@ def run_gpu(args, w):
         dec_bytes=dec_bytes, dec_launches=n_dec, dec_flops=dec_flops,
         merge_ms_avg=ms_mrg / max(n_mrg, 1), append_ms_avg=ms_app / max(n_app, 1),
         pre_gbps=pre_gbps, pre_tflops=pre_tflops, avg_pre_ms=avg_pre, pre_bytes=pre_bytes,
+        pre_fused=pre_fused,
         copy_gbps=copy_gbps, read_gbps=read_gbps, n_blocks=n_blocks, pool_gb=nbytes / 1e9,
         kv_dtype=kvd, read_same_ms=read_same_ms, read_same_bytes=same_bytes)
     pool.close()
@@ -532,7 +542,8 @@ def run_call(args, w):
     def vis(t):
         return t + 1 if SW is None else min(t + 1, SW)
 
-    def account(grp, cl, nd):
+    def account(grp, cl, nd, fused):
+        """fused: the chunk prefill appended the chunk (no append launches)"""
         dec = pre = 0.0
         for i, c, d in zip(grp, cl, nd):
             L = int(have[i])
@@ -545,7 +556,8 @@ def run_call(args, w):
                     union = L + c
                 else:
                     union = min(w.n_sink, L + c) + max(0, L + c - max(w.n_sink, L - w.window + 1))
-                pre += union * beta + c * Hq * D * 2 * esz
+                pre += union * beta + c * Hq * D * 2 * esz + (c * (io_tok - Hq * D * 2 * esz + beta)
+                                                              if fused else 0)
             for j in range(d):
                 dec += vis(L + c + j) * beta + io_tok + beta
             have[i] = L + c + d
@@ -554,8 +566,10 @@ def run_call(args, w):
         acct["served"] += len(grp)
 
     def collect():
+        """Kernel times since the last call; whether a chunk append ran as its
+        own launch (else the chunk prefill took it)."""
         if not args.kernel_times:
-            return
+            return False
         kt = pool.kernel_times()
         acct["dec_n"] += kt["decode"][0]
         acct["dec_ms"] += kt["decode"][1]
@@ -563,6 +577,7 @@ def run_call(args, w):
         acct["pre_ms"] += kt["prefill"][1]
         acct["app_ms"] += kt["append"][1]
         acct["mrg_ms"] += kt["merge"][1]
+        return kt["append"][0] > 0
     if args.kernel_times:
         pool.set_timing(True)
     evs = [torch.cuda.Event(enable_timing=True) for _ in range(2 * frames * K)]
@@ -589,7 +604,11 @@ def run_call(args, w):
                 break
             evs[2 * n_sub + 1].record()
             n_sub += 1
-            account(grp, cl, nd)
+            # with --kernel-times, every sub-tick's launches are read back at
+            # once (a host wait per sub-tick), so the bytes follow the path
+            # each chunk plan took
+            separate = collect()
+            account(grp, cl, nd, args.kernel_times and not separate)
         if fail_frame is not None:
             break
         st = pool.stats()
@@ -599,8 +618,6 @@ def run_call(args, w):
                 pool.session_close(sids[i])
                 sids[i] = pool.session_open()
                 have[i] = 0
-        if (f + 1) % 10 == 0:
-            collect()
         if (f + 1) % 50 == 0:
             torch.cuda.synchronize()
             log(f"[call] frame {f + 1}/{frames}")
@@ -1073,6 +1090,7 @@ def main():
             "decode_plus_merge_GBps": round(res["dec_merge_gbps"], 1),
             "merge_ms_avg": round(res["merge_ms_avg"], 4),
             "append_ms_avg": round(res["append_ms_avg"], 4),
+            "prefill_appends_chunk": res["pre_fused"],
             "prefill_GBps": None if res["pre_gbps"] is None else round(res["pre_gbps"], 1),
             "prefill_TFLOPs": None if res["pre_tflops"] is None else round(res["pre_tflops"], 2),
             "prefill_mfma_frac_of_bf16_peak": None if res["pre_tflops"] is None

@@ -92,6 +92,7 @@ struct mtn_pool {
     void *plan_stream = nullptr;
     int32_t n_seq = 0, T = 0, max_ntok = 0;
     bool all_single = false;
+    bool pf_one_pass = false;  // every sequence takes one chunk-prefill row pass
     std::vector<int32_t> seq_sid, seq_ntok, seq_first;
     std::vector<int64_t> seq_pos0;
     std::vector<int32_t> tok_sid, tok_pos, tok_row, tok_block, tok_off;
@@ -471,6 +472,7 @@ mtn_status plan_begin(mtn_pool *P, int32_t n_seq, const int32_t *sids, const int
                 P->pf_items.insert(P->pf_items.end(), rec, rec + kPfItem);
             }
         }
+        P->pf_one_pass = P->pf_items.size() == (size_t)kPfItem * n_seq;
     }
     P->layer_done.assign((size_t)P->cfg.n_layers, 0);
     P->plan_open = true;
@@ -709,14 +711,29 @@ mtn_status decode_impl(mtn_pool *P, int32_t layer, const void *q, void *out, flo
     return MTN_OK;
 }
 
+// Whether frame_step may fuse the chunk append into the chunk prefill: the
+// matrix-core prefill with every sequence in one row pass (its workgroup is
+// then the only reader of the sequence's blocks of its kv head).
+bool prefill_fuses_append(const mtn_pool *P) {
+    return !P->all_single && P->pf_one_pass &&
+           prefill_mfma_supported(P->cfg.kv_dtype, P->cfg.head_dim, P->G);
+}
+
+// k_new / v_new non-null (only when prefill_fuses_append): the launch also
+// appends the planned tokens, and the layer counts as appended.
 mtn_status prefill_impl(mtn_pool *P, int32_t layer, const void *q, void *out, float *lse,
-                        void *stream) {
+                        void *stream, const void *k_new = nullptr, const void *v_new = nullptr) {
     hipStream_t s = (hipStream_t)stream;
     if (P->all_single) return decode_impl(P, layer, q, out, lse, 0, stream);
     mtn_status st = launch_gate(P);
     if (st) return st;
-    if (P->host_only) return MTN_OK;
+    if (P->host_only) {
+        if (k_new) P->layer_done[layer] = 1;
+        return MTN_OK;
+    }
     AttnArgs a = attn_args(P, layer, q, out, lse, 1);
+    a.k_new = k_new;
+    a.v_new = v_new;
     hipEvent_t e0;
     st = timing_begin(P, s, &e0);
     if (st) return st;
@@ -726,7 +743,10 @@ mtn_status prefill_impl(mtn_pool *P, int32_t layer, const void *q, void *out, fl
     } else {
         HIP_TRY(P, launch_attn_valu(P->cfg.kv_dtype, a, s));
     }
-    return timing_end(P, 1, e0, s);
+    st = timing_end(P, 1, e0, s);
+    if (st) return st;
+    if (k_new) P->layer_done[layer] = 1;
+    return MTN_OK;
 }
 
 // The plans of one frame (after mtn_frame_step's validation): the chunk plan
@@ -751,6 +771,9 @@ mtn_status frame_plans(mtn_pool *P, const mtn_frame_batch *b, void *stream, int6
         if (P->all_single) {  // one-token chunks: decode with the append fused in
             st = decode_impl(P, l, off(b->q_chunk, rq), (void *)off(b->out_chunk, rq), lse,
                              b->n_split, stream, off(b->k_chunk, rk), off(b->v_chunk, rk));
+        } else if (prefill_fuses_append(P)) {  // append fused into the prefill
+            st = prefill_impl(P, l, off(b->q_chunk, rq), (void *)off(b->out_chunk, rq), lse,
+                              stream, off(b->k_chunk, rk), off(b->v_chunk, rk));
         } else {
             st = append_impl(P, l, off(b->k_chunk, rk), off(b->v_chunk, rk), stream);
             if (st) return st;

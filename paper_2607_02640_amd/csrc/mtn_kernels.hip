@@ -1040,6 +1040,62 @@ __global__ __launch_bounds__(64 * kPfWaves) void k_prefill_mfma(PfArgs pa) {
     const int voff = lds_v16(lblk, ln16, lg & 1);  // + dt * 16 * 32 for d tile dt
 
     const int hq0 = kvh * G;
+    // Fused chunk append (a.k_new set: the host passes it only when every
+    // sequence of the plan takes one row pass, so no other workgroup reads
+    // this sequence's blocks of this kv head).  The waves that issue no
+    // copies write the sequence's tokens into the pool -- K rotated, V as it
+    // comes: their first batch of loads goes out just ahead of the query
+    // loads, the stores follow the query rotation.  When the chunk's first
+    // token lies in one of the stages the prologue copies (a short sequence),
+    // those copies wait behind the completed stores and a barrier.
+    // Otherwise the first copy of a block holding appended tokens is issued
+    // after the first stage barrier; the stores, issued before it by waves of
+    // this workgroup, are ordered before it at workgroup scope.  A copy of
+    // the ring block that also holds the window's oldest keys may meet the
+    // append's stores to its other slots: those slots are masked there.
+    const bool fuse = a.k_new != nullptr;
+    bool early_chunk = false;
+    if (fuse) {
+        const int cv = pos0 < sink_tokens ? pos0 / kBlock : n_sb + (pos0 - ring_p0) / kBlock;
+        early_chunk = cv / 2 < kPfStages - 1;
+    }
+    constexpr int NAW = kPfWaves - DW;          // appending waves
+    constexpr int AB = F8 ? 3 : 4;              // tokens per batch (more spill)
+    const int aw = wv < kDma0 ? wv : wv - DW;   // this wave's index among them
+    struct AppBatch {
+        float k0[AB], k1[AB], v0[AB], v1[AB];
+        float2 cs[AB];
+        int blk[AB], off[AB];
+    };
+    // tokens j0, j0 + NAW, ... (indices clamped into the sequence)
+    auto app_load = [&](int j0, AppBatch &b) __attribute__((always_inline)) {
+#pragma unroll
+        for (int u = 0; u < AB; ++u) {
+            const int j = min(j0 + u * NAW, ntok - 1);
+            const int t = tok0 + j;
+            const int64_t ri = ((int64_t)(row_t0 + j) * g.hkv + kvh) * D;
+            const bf16_t *kr = (const bf16_t *)a.k_new + ri;
+            const bf16_t *vr = (const bf16_t *)a.v_new + ri;
+            b.k0[u] = to_f32(kr[lane]);
+            b.k1[u] = to_f32(kr[lane + 64]);
+            b.v0[u] = to_f32(vr[lane]);
+            b.v1[u] = to_f32(vr[lane + 64]);
+            b.cs[u] = a.p.rope[(int64_t)t * (D / 2) + lane];
+            b.blk[u] = scalar_ld(a.p.tok_block, t);
+            b.off[u] = scalar_ld(a.p.tok_off, t);
+        }
+    };
+    auto app_store = [&](int j0, const AppBatch &b) __attribute__((always_inline)) {
+        uint8_t *lw = const_cast<uint8_t *>(layer_base);
+#pragma unroll
+        for (int u = 0; u < AB; ++u) {
+            if (j0 + u * NAW >= ntok) break;
+            const float y0 = fmaf(b.k0[u], b.cs[u].x, -b.k1[u] * b.cs[u].y);
+            const float y1 = fmaf(b.k1[u], b.cs[u].x, b.k0[u] * b.cs[u].y);
+            store_token_kv<F8>(lw + (int64_t)b.blk[u] * g.block_stride, b.off[u], y0, y1, b.v0[u],
+                               b.v1[u], lane);
+        }
+    };
     {
         // ring blocks every row of the pass sees whole: [fr_lo, fr_hi) (as
         // virtual indices)
@@ -1120,6 +1176,8 @@ __global__ __launch_bounds__(64 * kPfWaves) void k_prefill_mfma(PfArgs pa) {
         }
         uint4 qx[kPfTpw][4], qy[kPfTpw][4];  // dims d0 .. d0 + 7 and their partners d0 ^ 64
         float4 qc[kPfTpw][2][4];             // (cos, sin) of dims (d0 & 63) .. + 7
+        AppBatch ab;
+        if (fuse && !dma_wave) app_load(aw, ab);
 #pragma unroll
         for (int i = 0; i < kPfTpw; ++i) {
             const int t = tok0 + tq_j[i];
@@ -1141,7 +1199,7 @@ __global__ __launch_bounds__(64 * kPfWaves) void k_prefill_mfma(PfArgs pa) {
         // the q loads (counted by the compiler, which does not see the copies)
         // then cover exactly these copies.  The rest of the ring follows the
         // rotation.
-        if (dma_wave) {
+        if (dma_wave && !early_chunk) {
 #pragma unroll
             for (int st = 0; st < kPfEarly; ++st) issue_block(st, phys(2 * st + db));
         }
@@ -1264,6 +1322,25 @@ __global__ __launch_bounds__(64 * kPfWaves) void k_prefill_mfma(PfArgs pa) {
                 }
             }
         };
+        if (fuse) {
+            if (!dma_wave) {
+                app_store(aw, ab);
+                for (int j0 = aw + AB * NAW; j0 < ntok; j0 += AB * NAW) {
+                    app_load(j0, ab);
+                    app_store(j0, ab);
+                }
+                // copies issued right after the next barrier read them: the
+                // stores are acknowledged by the L2 first
+                if (early_chunk) vm_wait<0>();
+            }
+            if (early_chunk) {
+                __syncthreads();
+                if (dma_wave) {
+#pragma unroll
+                    for (int st = 0; st < kPfEarly; ++st) issue_block(st, phys(2 * st + db));
+                }
+            }
+        }
         // ring prologue: stages kPfEarly .. kPfStages - 2 join the first ones in flight
         int nph = -1;  // DMA waves: physical block of the next stage to issue
         if (dma_wave) {
@@ -1650,6 +1727,7 @@ hipError_t launch_prefill_mfma(int dtype, const AttnArgs &a, const int32_t *item
         !prefill_pass_rows_valid(pass_rows))
         return hipErrorInvalidValue;
     if (((uintptr_t)items & 31) != 0) return hipErrorInvalidValue;  // records are 32-byte aligned
+    if ((a.k_new == nullptr) != (a.v_new == nullptr)) return hipErrorInvalidValue;
     PfArgs pa{a, items, zero_page, pass_rows};
     dim3 grid((unsigned)(n_items * a.g.hkv)), block(64 * kPfWaves);
     if (dtype == 2)

@@ -29,19 +29,6 @@
 namespace mtn {
 namespace {
 
-// smallest e with amax <= 448 * 2^e, clamped to [-126, 127]; 0 for amax = 0
-__device__ __forceinline__ int f8_scale_exp(float amax) {
-    if (!(amax > 0.f)) return 0;
-    int e = __builtin_amdgcn_frexp_expf(amax) - 9;  // amax * 2^-e in [256, 512)
-    if (ldexpf(amax, -e) > 448.f) ++e;
-    return min(max(e, -126), 127);
-}
-// E4M3 codes of (a, b) into bytes 0, 1 (hi = false) or 2, 3 of `old`;
-// round to nearest even, |a|, |b| <= 448
-template <bool HI>
-__device__ __forceinline__ uint32_t f8_pack(float a, float b, uint32_t old) {
-    return (uint32_t)__builtin_amdgcn_cvt_pk_fp8_f32(a, b, (int)old, HI);
-}
 // two E4M3 codes (bytes 0, 1 or 2, 3 of w) -> two bf16, exact
 template <bool HI>
 __device__ __forceinline__ uint32_t f8_bf16x2(uint32_t w) {
@@ -79,27 +66,9 @@ __global__ __launch_bounds__(256) void k_append_fp8(PoolGeom g, PlanView p, int3
     const float y0 = fmaf(x0, cs.x, -x1 * cs.y);
     const float y1 = fmaf(x1, cs.x, x0 * cs.y);
     const float v0 = to_f32(vr[lane]), v1 = to_f32(vr[lane + 64]);
-    float ak = fmaxf(fabsf(y0), fabsf(y1)), av = fmaxf(fabsf(v0), fabsf(v1));
-#pragma unroll
-    for (int m = 32; m >= 1; m >>= 1) {
-        ak = fmaxf(ak, __shfl_xor(ak, m, 64));
-        av = fmaxf(av, __shfl_xor(av, m, 64));
-    }
-    const int ek = f8_scale_exp(ak), ev = f8_scale_exp(av);
-    const uint32_t kc = f8_pack<false>(ldexpf(y0, -ek), ldexpf(y1, -ek), 0u);
-    const uint32_t vc = f8_pack<false>(ldexpf(v0, -ev), ldexpf(v1, -ev), 0u);
     uint8_t *tile = (uint8_t *)g.kv + (int64_t)layer * g.layer_stride +
                     (int64_t)p.tok_block[t] * g.block_stride + (int64_t)h * g.head_stride;
-    const int off = p.tok_off[t];
-    tile[off * kF8D + lane] = (uint8_t)kc;
-    tile[off * kF8D + lane + 64] = (uint8_t)(kc >> 8);
-    uint8_t *vq = tile + kF8Tile + (off >> 2) * (4 * kF8D) + (off & 3);
-    vq[lane * 4] = (uint8_t)vc;
-    vq[(lane + 64) * 4] = (uint8_t)(vc >> 8);
-    if (lane == 0) {
-        tile[kF8Exp + off] = (uint8_t)(ek + 127);
-        tile[kF8Exp + kBlock + off] = (uint8_t)(ev + 127);
-    }
+    store_token_kv<true>(tile, p.tok_off[t], y0, y1, v0, v1, lane);
 }
 
 // ---------------------------------------------------------------------------

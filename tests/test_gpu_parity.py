@@ -181,6 +181,45 @@ def test_fused_and_separate_calls_store_identical_pools():
         assert torch.equal(pa.kv, pb.kv), f"pool bytes differ after frame {f}"
 
 
+@pytest.mark.parametrize("dtype", ["bf16", "fp8"])
+@pytest.mark.parametrize("rows", [0, 256])
+def test_prefill_with_fused_append_stores_what_the_append_stores(dtype, rows):
+    """mtn_frame_step folds the chunk append into the chunk prefill when every
+    sequence takes one row pass.  Two NaN-poisoned pools fed the same frames,
+    one through mtn_frame_step and one through the separate per-layer calls,
+    hold bit-identical bytes after every frame, and both match the oracle.
+    Chunks of up to 40 tokens at G = 8 take one or two 256-row passes (two or
+    three 128-row ones), so some plans fuse and some do not; the sequences
+    start empty (the chunk lies in the first stages a workgroup copies, so
+    the copies wait behind the append) and grow past 14 blocks (the append
+    then runs beside the first copies)."""
+    say(f"prefill fused append vs separate pool bytes, {dtype}, rows {rows}")
+    n, L = 3, 2
+    cfg = dict(dtype=dtype, d=128, hq=16, hkv=2, S=4, W=300, cmax=40, n=n, L=L,
+               blocks=n * (1 + 22) + 2)
+    pa, ha = _tiny(**cfg)
+    pb, hb = _tiny(**cfg)
+    for p in (pa, pb):
+        if rows:
+            p.set_prefill_pass_rows(rows)
+        p.kv.zero_()      # fp8 regions hold 96 padding bytes that no kernel writes
+        p.poison_dead()
+        p.set_timing(True)
+        p.kernel_times()
+    rnd = random.Random(11)
+    for f in range(12):
+        cl = [rnd.randint(1, 40) for _ in range(n)]
+        nd = [rnd.randint(0, 2) for _ in range(n)]
+        ha.frame(cl, nd, use_frame_step=True)
+        hb.frame(cl, nd, use_frame_step=False, fused=False)
+        torch.cuda.synchronize()
+        assert torch.equal(pa.kv, pb.kv), f"pool bytes differ after frame {f}"
+    ka, kb = pa.kernel_times(), pb.kernel_times()
+    say(f"appends: frame_step {ka['append'][0]}, per-layer {kb['append'][0]}; "
+        f"max err {ha.max_err:.2e} / {hb.max_err:.2e}")
+    assert ka["append"][0] < kb["append"][0], "no chunk plan took the fused prefill"
+
+
 @pytest.mark.parametrize("rows", [256, 128])
 def test_bf16_long_chunks_split_into_row_passes(rows):
     """A re-prefill-sized chunk: 300 tokens x G = 8 is 2400 query rows, ten
