@@ -1047,17 +1047,18 @@ __global__ __launch_bounds__(64 * kPfWaves) void k_prefill_mfma(PfArgs pa) {
     // comes: their first batch of loads goes out just ahead of the query
     // loads, the stores follow the query rotation.  When the chunk's first
     // token lies in one of the stages the prologue copies (a short sequence),
-    // those copies wait behind the completed stores and a barrier.
-    // Otherwise the first copy of a block holding appended tokens is issued
-    // after the first stage barrier; the stores, issued before it by waves of
-    // this workgroup, are ordered before it at workgroup scope.  A copy of
+    // those copies wait behind the completed stores and a barrier, and so do
+    // sequences whose first such copy would go out at the first two stage
+    // barriers.  Otherwise that copy is issued at a later stage barrier; the
+    // stores, issued before the first one by waves of this workgroup, are
+    // ordered before it at workgroup scope.  A copy of
     // the ring block that also holds the window's oldest keys may meet the
     // append's stores to its other slots: those slots are masked there.
     const bool fuse = a.k_new != nullptr;
     bool early_chunk = false;
     if (fuse) {
         const int cv = pos0 < sink_tokens ? pos0 / kBlock : n_sb + (pos0 - ring_p0) / kBlock;
-        early_chunk = cv / 2 < kPfStages - 1;
+        early_chunk = cv / 2 < kPfStages + 1;  // copied by the prologue or at barrier 0 or 1
     }
     constexpr int NAW = kPfWaves - DW;          // appending waves
     constexpr int AB = F8 ? 3 : 4;              // tokens per batch (more spill)
