@@ -7,8 +7,8 @@ sessions, each frame a 25-token chunk prefill then 16 decode steps, 4 pinned
 sinks plus a 4096-token window in a paged pool of 16-token blocks.  Sessions
 are first brought to steady state (window full and wrapping) by append-only
 plans; every timed step is then one whole frame for all 128 sessions:
-48 x chunk prefill followed by 16 x 48 x decode, each launch appending its
-own tokens.
+48 x (append + chunk prefill) followed by 16 x 48 x decode, each decode
+launch appending its own token.
 
 Inputs are synthetic N(0, 1) draws (torch's seeded device generator) in a
 two-frame bank; they stand in for the paper's real-audio sessions.
@@ -141,12 +141,14 @@ def kernel_src_hash(kernel: str = "decode") -> str:
     return h.hexdigest()[:16]
 
 
-def algorithmic_bytes(w, kvd="bf16", fused_append=True):
+def algorithmic_bytes(w, kvd="bf16", fused_append=None):
     """Per-launch algorithmic bytes of the steady-state decode and chunk
-    prefill of workload w (every query sees S + W keys).  Both launches also
+    prefill of workload w (every query sees S + W keys).  Both launches may
     append their tokens (read k, v; write the pool copy): the decode always,
-    the prefill when the chunk append is fused into it (every sequence in one
-    row pass)."""
+    the prefill when the chunk append is fused into it (by default for the
+    fp8 pool, whose frame step fuses it at this shape)."""
+    if fused_append is None:
+        fused_append = kvd == "fp8"
     esz = 4 if kvd == "f32" else 2
     N, Hq, Hkv, D = w.n_sessions, w.n_q_heads, w.n_kv_heads, w.head_dim
     C = w.chunk[1]

@@ -273,8 +273,8 @@ mtn_status mtn_attend_decode_append(mtn_pool *pool, int32_t layer, const void *k
  * decode round j (only sessions with n_decode[i] > j) plan one token, for each
  * layer append + decode attend (one launch, as mtn_attend_decode_append),
  * commit.  Chunks of one token everywhere use the decode kernel the same way.
- * When every sequence's chunk rows fit one prefill row pass (the bf16 and fp8
- * pools' matrix-core prefill), the chunk append also runs inside the
+ * With the fp8 pool, when every sequence's chunk rows fit one prefill row
+ * pass (and the launch is small enough), the chunk append runs inside the
  * prefill's launch; the pool holds the same bytes either way.
  * Every host check (sessions, sizes, and block capacity for the whole frame)
  * runs before the first plan.  An error inside a plan (a failed launch)

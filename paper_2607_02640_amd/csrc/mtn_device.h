@@ -340,38 +340,28 @@ __device__ __forceinline__ uint32_t f8_pack(float a, float b, uint32_t old) {
 
 // One token's K (already rotated) and V for one kv head into slot `off` of
 // its pool region (D = 128), one wave: lane i holds dims i and i + 64 (the
-// rotation pair).  bf16 pool: the K row and the slot's V^T column.  fp8
-// pool: E4M3 codes under one power-of-two scale per row (K and V apart,
-// from the row's largest magnitude), lane 0 writing the two exponent bytes.
-template <bool F8>
-__device__ __forceinline__ void store_token_kv(uint8_t *region, int off, float k0, float k1,
-                                               float v0, float v1, int lane) {
-    if constexpr (F8) {
-        float ak = fmaxf(fabsf(k0), fabsf(k1)), av = fmaxf(fabsf(v0), fabsf(v1));
+// rotation pair).  fp8 pool: E4M3 codes under one power-of-two scale per row
+// (K and V apart, from the row's largest magnitude), lane 0 writing the two
+// exponent bytes.
+__device__ __forceinline__ void store_token_fp8(uint8_t *region, int off, float k0, float k1,
+                                                float v0, float v1, int lane) {
+    float ak = fmaxf(fabsf(k0), fabsf(k1)), av = fmaxf(fabsf(v0), fabsf(v1));
 #pragma unroll
-        for (int m = 32; m >= 1; m >>= 1) {
-            ak = fmaxf(ak, __shfl_xor(ak, m, 64));
-            av = fmaxf(av, __shfl_xor(av, m, 64));
-        }
-        const int ek = f8_scale_exp(ak), ev = f8_scale_exp(av);
-        const uint32_t kc = f8_pack<false>(ldexpf(k0, -ek), ldexpf(k1, -ek), 0u);
-        const uint32_t vc = f8_pack<false>(ldexpf(v0, -ev), ldexpf(v1, -ev), 0u);
-        region[off * kF8D + lane] = (uint8_t)kc;
-        region[off * kF8D + lane + 64] = (uint8_t)(kc >> 8);
-        uint8_t *vq = region + kF8Tile + (off >> 2) * (4 * kF8D) + (off & 3);
-        vq[lane * 4] = (uint8_t)vc;
-        vq[(lane + 64) * 4] = (uint8_t)(vc >> 8);
-        if (lane == 0) {
-            region[kF8Exp + off] = (uint8_t)(ek + 127);
-            region[kF8Exp + kBlock + off] = (uint8_t)(ev + 127);
-        }
-    } else {
-        bf16_t *K = (bf16_t *)region;
-        bf16_t *VT = (bf16_t *)(region + kBlock * 128 * 2);
-        K[off * 128 + lane] = from_f32<bf16_t>(k0);
-        K[off * 128 + lane + 64] = from_f32<bf16_t>(k1);
-        VT[lane * kBlock + off] = from_f32<bf16_t>(v0);
-        VT[(lane + 64) * kBlock + off] = from_f32<bf16_t>(v1);
+    for (int m = 32; m >= 1; m >>= 1) {
+        ak = fmaxf(ak, __shfl_xor(ak, m, 64));
+        av = fmaxf(av, __shfl_xor(av, m, 64));
+    }
+    const int ek = f8_scale_exp(ak), ev = f8_scale_exp(av);
+    const uint32_t kc = f8_pack<false>(ldexpf(k0, -ek), ldexpf(k1, -ek), 0u);
+    const uint32_t vc = f8_pack<false>(ldexpf(v0, -ev), ldexpf(v1, -ev), 0u);
+    region[off * kF8D + lane] = (uint8_t)kc;
+    region[off * kF8D + lane + 64] = (uint8_t)(kc >> 8);
+    uint8_t *vq = region + kF8Tile + (off >> 2) * (4 * kF8D) + (off & 3);
+    vq[lane * 4] = (uint8_t)vc;
+    vq[(lane + 64) * 4] = (uint8_t)(vc >> 8);
+    if (lane == 0) {
+        region[kF8Exp + off] = (uint8_t)(ek + 127);
+        region[kF8Exp + kBlock + off] = (uint8_t)(ev + 127);
     }
 }
 

@@ -711,16 +711,18 @@ mtn_status decode_impl(mtn_pool *P, int32_t layer, const void *q, void *out, flo
     return MTN_OK;
 }
 
-// Whether frame_step fuses the chunk append into the chunk prefill: the
-// matrix-core prefill with every sequence in one row pass (its workgroup is
-// then the only reader of the sequence's blocks of its kv head), and at most
-// two workgroups per CU.  Each workgroup pays the append's loads before its
-// first stage: measured, that costs less than the append launch at two
-// rounds of workgroups per CU (128 sessions x 4 kv heads) and more at eight
-// (256 sessions x 8 kv heads).
+// Whether frame_step fuses the chunk append into the chunk prefill: the fp8
+// pool's matrix-core prefill with every sequence in one row pass (its
+// workgroup is then the only reader of the sequence's blocks of its kv head),
+// and at most two workgroups per CU.  Each workgroup pays the append's work
+// before its first stage: measured, that costs less than the quantizing
+// append launch at two rounds of workgroups per CU (128 sessions x 4 kv
+// heads), more at eight (256 sessions x 8 kv heads), and for the bf16 pool
+// no less than its append launch.
 bool prefill_fuses_append(const mtn_pool *P) {
     const int64_t wgs = (int64_t)(P->pf_items.size() / kPfItem) * P->cfg.n_kv_heads;
     return !P->all_single && P->pf_one_pass && P->n_cu > 0 && wgs <= 2 * (int64_t)P->n_cu &&
+           P->cfg.kv_dtype == MTN_FP8_E4M3 &&
            prefill_mfma_supported(P->cfg.kv_dtype, P->cfg.head_dim, P->G);
 }
 

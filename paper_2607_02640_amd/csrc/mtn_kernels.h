@@ -77,9 +77,9 @@ hipError_t launch_merge(int dtype, const AttnArgs &a, hipStream_t s);
 // head).  pass_rows: prefill_rows_per_pass() or, to spread few sequences over
 // more workgroups, 128 (prefill_pass_rows_valid).  zero_page: 16 KiB of
 // device zeros, the DMA source of blocks a pass does not see.  a.k_new /
-// a.v_new (both or neither; [rows][Hkv][D] bf16): the launch also appends the
-// planned tokens (RoPE on K), which the caller may ask for only when every
-// sequence takes exactly one row pass.
+// a.v_new (both or neither; fp8 pool only; [rows][Hkv][D] bf16): the launch
+// also appends the planned tokens (RoPE on K, quantized), which the caller may
+// ask for only when every sequence takes exactly one row pass.
 constexpr int kPfItem = 8;
 int prefill_rows_per_pass();
 bool prefill_pass_rows_valid(int rows);

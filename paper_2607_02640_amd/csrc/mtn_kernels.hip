@@ -1040,9 +1040,10 @@ __global__ __launch_bounds__(64 * kPfWaves) void k_prefill_mfma(PfArgs pa) {
     const int voff = lds_v16(lblk, ln16, lg & 1);  // + dt * 16 * 32 for d tile dt
 
     const int hq0 = kvh * G;
-    // Fused chunk append (a.k_new set: the host passes it only when every
-    // sequence of the plan takes one row pass, so no other workgroup reads
-    // this sequence's blocks of this kv head).  The waves that issue no
+    // Fused chunk append (fp8 pool, a.k_new set: the host passes it only when
+    // every sequence of the plan takes one row pass, so no other workgroup
+    // reads this sequence's blocks of this kv head; for the bf16 pool the
+    // separate append measured as fast, so that kernel has no such path).  The waves that issue no
     // copies write the sequence's tokens into the pool -- K rotated, V as it
     // comes: their first batch of loads goes out just ahead of the query
     // loads, the stores follow the query rotation.  When the chunk's first
@@ -1054,17 +1055,20 @@ __global__ __launch_bounds__(64 * kPfWaves) void k_prefill_mfma(PfArgs pa) {
     // ordered before it at workgroup scope.  A copy of
     // the ring block that also holds the window's oldest keys may meet the
     // append's stores to its other slots: those slots are masked there.
-    const bool fuse = a.k_new != nullptr;
+    const bool fuse = F8 && a.k_new != nullptr;
     bool early_chunk = false;
     if (fuse) {
         const int cv = pos0 < sink_tokens ? pos0 / kBlock : n_sb + (pos0 - ring_p0) / kBlock;
         early_chunk = cv / 2 < kPfStages + 1;  // copied by the prologue or at barrier 0 or 1
     }
     constexpr int NAW = kPfWaves - DW;          // appending waves
-    constexpr int AB = F8 ? 3 : 4;              // tokens per batch (more spill)
+    constexpr int AB = 4;                       // tokens per batch (more spill across the loops)
     const int aw = wv < kDma0 ? wv : wv - DW;   // this wave's index among them
+    // The loads keep the raw bf16 bits: converted on load, the compiler
+    // consumed each value right away and waited for every load in turn
+    // (four memory round trips before the query loads went out).
     struct AppBatch {
-        float k0[AB], k1[AB], v0[AB], v1[AB];
+        uint32_t k0[AB], k1[AB], v0[AB], v1[AB];  // bf16 bits, zero-extended
         float2 cs[AB];
         int blk[AB], off[AB];
     };
@@ -1075,26 +1079,33 @@ __global__ __launch_bounds__(64 * kPfWaves) void k_prefill_mfma(PfArgs pa) {
             const int j = min(j0 + u * NAW, ntok - 1);
             const int t = tok0 + j;
             const int64_t ri = ((int64_t)(row_t0 + j) * g.hkv + kvh) * D;
-            const bf16_t *kr = (const bf16_t *)a.k_new + ri;
-            const bf16_t *vr = (const bf16_t *)a.v_new + ri;
-            b.k0[u] = to_f32(kr[lane]);
-            b.k1[u] = to_f32(kr[lane + 64]);
-            b.v0[u] = to_f32(vr[lane]);
-            b.v1[u] = to_f32(vr[lane + 64]);
+            const uint16_t *kr = (const uint16_t *)a.k_new + ri;
+            const uint16_t *vr = (const uint16_t *)a.v_new + ri;
+            b.k0[u] = kr[lane];
+            b.k1[u] = kr[lane + 64];
+            b.v0[u] = vr[lane];
+            b.v1[u] = vr[lane + 64];
             b.cs[u] = a.p.rope[(int64_t)t * (D / 2) + lane];
             b.blk[u] = scalar_ld(a.p.tok_block, t);
             b.off[u] = scalar_ld(a.p.tok_off, t);
         }
     };
-    auto app_store = [&](int j0, const AppBatch &b) __attribute__((always_inline)) {
+    auto app_store = [&](int j0, AppBatch &b) __attribute__((always_inline)) {
         uint8_t *lw = const_cast<uint8_t *>(layer_base);
+        auto f = [](uint32_t bits) { return __uint_as_float(bits << 16); };
+        // every use of the loaded values stays here: without the pins the
+        // compiler moved their conversions up beside the loads
+#pragma unroll
+        for (int u = 0; u < AB; ++u)
+            asm volatile("" : "+v"(b.k0[u]), "+v"(b.k1[u]), "+v"(b.v0[u]), "+v"(b.v1[u]));
 #pragma unroll
         for (int u = 0; u < AB; ++u) {
             if (j0 + u * NAW >= ntok) break;
-            const float y0 = fmaf(b.k0[u], b.cs[u].x, -b.k1[u] * b.cs[u].y);
-            const float y1 = fmaf(b.k1[u], b.cs[u].x, b.k0[u] * b.cs[u].y);
-            store_token_kv<F8>(lw + (int64_t)b.blk[u] * g.block_stride, b.off[u], y0, y1, b.v0[u],
-                               b.v1[u], lane);
+            const float k0 = f(b.k0[u]), k1 = f(b.k1[u]);
+            const float y0 = fmaf(k0, b.cs[u].x, -k1 * b.cs[u].y);
+            const float y1 = fmaf(k1, b.cs[u].x, k0 * b.cs[u].y);
+            store_token_fp8(lw + (int64_t)b.blk[u] * g.block_stride, b.off[u], y0, y1,
+                            f(b.v0[u]), f(b.v1[u]), lane);
         }
     };
     {
@@ -1179,6 +1190,7 @@ __global__ __launch_bounds__(64 * kPfWaves) void k_prefill_mfma(PfArgs pa) {
         float4 qc[kPfTpw][2][4];             // (cos, sin) of dims (d0 & 63) .. + 7
         AppBatch ab;
         if (fuse && !dma_wave) app_load(aw, ab);
+        __builtin_amdgcn_sched_barrier(0);  // the query loads follow at once
 #pragma unroll
         for (int i = 0; i < kPfTpw; ++i) {
             const int t = tok0 + tq_j[i];
@@ -1728,7 +1740,8 @@ hipError_t launch_prefill_mfma(int dtype, const AttnArgs &a, const int32_t *item
         !prefill_pass_rows_valid(pass_rows))
         return hipErrorInvalidValue;
     if (((uintptr_t)items & 31) != 0) return hipErrorInvalidValue;  // records are 32-byte aligned
-    if ((a.k_new == nullptr) != (a.v_new == nullptr)) return hipErrorInvalidValue;
+    if ((a.k_new == nullptr) != (a.v_new == nullptr) || (a.k_new && dtype != 2))
+        return hipErrorInvalidValue;  // the fused append is the fp8 kernel's
     PfArgs pa{a, items, zero_page, pass_rows};
     dim3 grid((unsigned)(n_items * a.g.hkv)), block(64 * kPfWaves);
     if (dtype == 2)

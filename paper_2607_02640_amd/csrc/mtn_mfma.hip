@@ -68,7 +68,7 @@ __global__ __launch_bounds__(256) void k_append_fp8(PoolGeom g, PlanView p, int3
     const float v0 = to_f32(vr[lane]), v1 = to_f32(vr[lane + 64]);
     uint8_t *tile = (uint8_t *)g.kv + (int64_t)layer * g.layer_stride +
                     (int64_t)p.tok_block[t] * g.block_stride + (int64_t)h * g.head_stride;
-    store_token_kv<true>(tile, p.tok_off[t], y0, y1, v0, v1, lane);
+    store_token_fp8(tile, p.tok_off[t], y0, y1, v0, v1, lane);
 }
 
 // ---------------------------------------------------------------------------

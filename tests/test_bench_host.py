@@ -36,13 +36,13 @@ def test_committed_counter_summaries_match_the_current_sources():
 
 def test_algorithmic_bytes_of_the_headline_workload():
     """Decode: N (|vis| beta + Hq D (b_q + b_o) + 2 beta); prefill: N ((S + W + C - 1)
-    beta + C Hq D (b_q + b_o) + 2 C beta) with the chunk append fused (the k, v
-    rows in and the pool copy out), with beta = 2 Hkv D b."""
+    beta + C Hq D (b_q + b_o)), plus 2 C beta with the chunk append fused (the
+    k, v rows in and the pool copy out), with beta = 2 Hkv D b."""
     dec, pre = bench.algorithmic_bytes(W.QWEN3_OMNI)
     beta = 2 * 4 * 128 * 2
     assert dec == 128 * (4100 * beta + 32 * 128 * 4 + 2 * beta) == 1077411840
-    assert pre == 128 * ((4 + 4096 + 25 - 1) * beta + 25 * 32 * 128 * 4 + 25 * 2 * beta)
-    _, pre_sep = bench.algorithmic_bytes(W.QWEN3_OMNI, fused_append=False)
-    assert pre_sep == 128 * ((4 + 4096 + 25 - 1) * beta + 25 * 32 * 128 * 4)
+    assert pre == 128 * ((4 + 4096 + 25 - 1) * beta + 25 * 32 * 128 * 4)
+    _, pre_fused = bench.algorithmic_bytes(W.QWEN3_OMNI, fused_append=True)
+    assert pre_fused == pre + 128 * 25 * 2 * beta
     dec8, _ = bench.algorithmic_bytes(W.QWEN3_OMNI, "fp8")
     assert dec8 == 544084992

@@ -181,18 +181,20 @@ def test_fused_and_separate_calls_store_identical_pools():
         assert torch.equal(pa.kv, pb.kv), f"pool bytes differ after frame {f}"
 
 
-@pytest.mark.parametrize("dtype", ["bf16", "fp8"])
+@pytest.mark.parametrize("dtype", ["fp8", "bf16"])
 @pytest.mark.parametrize("rows", [0, 256])
 def test_prefill_with_fused_append_stores_what_the_append_stores(dtype, rows):
-    """mtn_frame_step folds the chunk append into the chunk prefill when every
-    sequence takes one row pass.  Two NaN-poisoned pools fed the same frames,
+    """mtn_frame_step folds the chunk append into the fp8 pool's chunk prefill
+    when every sequence takes one row pass (the bf16 pool keeps the append
+    launch, and the comparison then checks frame_step against the per-layer
+    calls).  Two NaN-poisoned pools fed the same frames,
     one through mtn_frame_step and one through the separate per-layer calls,
     hold bit-identical bytes after every frame, and both match the oracle.
     Chunks of up to 40 tokens at G = 8 take one or two 256-row passes (two or
     three 128-row ones), so some plans fuse and some do not; the sequences
     start empty (the chunk lies in the first stages a workgroup copies, so
-    the copies wait behind the append) and grow past 14 blocks (the append
-    then runs beside the first copies)."""
+    the copies wait behind the append) and grow past 18 blocks and through
+    the window's wrap (the append then runs beside the first copies)."""
     say(f"prefill fused append vs separate pool bytes, {dtype}, rows {rows}")
     n, L = 3, 2
     cfg = dict(dtype=dtype, d=128, hq=16, hkv=2, S=4, W=300, cmax=40, n=n, L=L,
@@ -207,9 +209,11 @@ def test_prefill_with_fused_append_stores_what_the_append_stores(dtype, rows):
         p.set_timing(True)
         p.kernel_times()
     rnd = random.Random(11)
-    for f in range(12):
+    n_chunk_plans = 0  # plans whose chunk prefill runs (not all one-token chunks)
+    for f in range(16):
         cl = [rnd.randint(1, 40) for _ in range(n)]
         nd = [rnd.randint(0, 2) for _ in range(n)]
+        n_chunk_plans += max(cl) > 1
         ha.frame(cl, nd, use_frame_step=True)
         hb.frame(cl, nd, use_frame_step=False, fused=False)
         torch.cuda.synchronize()
@@ -217,7 +221,12 @@ def test_prefill_with_fused_append_stores_what_the_append_stores(dtype, rows):
     ka, kb = pa.kernel_times(), pb.kernel_times()
     say(f"appends: frame_step {ka['append'][0]}, per-layer {kb['append'][0]}; "
         f"max err {ha.max_err:.2e} / {hb.max_err:.2e}")
-    assert ka["append"][0] < kb["append"][0], "no chunk plan took the fused prefill"
+    # frame_step launches an append only for chunk plans it does not fuse (its
+    # decode rounds always fuse theirs)
+    if dtype == "fp8":
+        assert ka["append"][0] < n_chunk_plans * L, "no chunk plan took the fused prefill"
+    else:
+        assert ka["append"][0] == n_chunk_plans * L
 
 
 @pytest.mark.parametrize("rows", [256, 128])
