@@ -1040,21 +1040,21 @@ __global__ __launch_bounds__(64 * kPfWaves) void k_prefill_mfma(PfArgs pa) {
     const int voff = lds_v16(lblk, ln16, lg & 1);  // + dt * 16 * 32 for d tile dt
 
     const int hq0 = kvh * G;
-    // Fused chunk append (fp8 pool, a.k_new set: the host passes it only when
-    // every sequence of the plan takes one row pass, so no other workgroup
-    // reads this sequence's blocks of this kv head; for the bf16 pool the
-    // separate append measured as fast, so that kernel has no such path).  The waves that issue no
-    // copies write the sequence's tokens into the pool -- K rotated, V as it
-    // comes: their first batch of loads goes out just ahead of the query
-    // loads, the stores follow the query rotation.  When the chunk's first
-    // token lies in one of the stages the prologue copies (a short sequence),
-    // those copies wait behind the completed stores and a barrier, and so do
-    // sequences whose first such copy would go out at the first two stage
-    // barriers.  Otherwise that copy is issued at a later stage barrier; the
-    // stores, issued before the first one by waves of this workgroup, are
-    // ordered before it at workgroup scope.  A copy of
-    // the ring block that also holds the window's oldest keys may meet the
-    // append's stores to its other slots: those slots are masked there.
+    // Fused chunk append (fp8 pool; a.k_new set).  The host passes it only
+    // when every sequence of the plan takes one row pass, so no other
+    // workgroup reads this sequence's blocks of this kv head.  (For the bf16
+    // pool the separate append launch measured as fast, so that kernel has no
+    // such path.)  The waves that issue no copies rotate K, quantize K and V
+    // and store the sequence's tokens: their first batch of loads goes out
+    // just ahead of the query loads, the stores follow the query rotation.
+    // When the chunk's first token lies in a stage that the prologue copies
+    // (a short sequence), or that is copied at the first two stage barriers,
+    // those copies wait behind the completed stores and a barrier.  Otherwise
+    // that copy is issued at a later stage barrier, and the stores, issued
+    // before the first one by waves of this workgroup, are ordered before it
+    // at workgroup scope.  A copy of the ring block that also holds the
+    // window's oldest keys may meet the append's stores to its other slots:
+    // those slots are masked there.
     const bool fuse = F8 && a.k_new != nullptr;
     bool early_chunk = false;
     if (fuse) {
