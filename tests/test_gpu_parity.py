@@ -181,9 +181,9 @@ def test_fused_and_separate_calls_store_identical_pools():
         assert torch.equal(pa.kv, pb.kv), f"pool bytes differ after frame {f}"
 
 
-@pytest.mark.parametrize("dtype", ["fp8", "bf16"])
+@pytest.mark.parametrize("dtype,g", [("fp8", 8), ("fp8", 4), ("fp8", 1), ("bf16", 8)])
 @pytest.mark.parametrize("rows", [0, 256])
-def test_prefill_with_fused_append_stores_what_the_append_stores(dtype, rows):
+def test_prefill_with_fused_append_stores_what_the_append_stores(dtype, g, rows):
     """mtn_frame_step folds the chunk append into the fp8 pool's chunk prefill
     when every sequence takes one row pass (the bf16 pool keeps the append
     launch, and the comparison then checks frame_step against the per-layer
@@ -191,13 +191,14 @@ def test_prefill_with_fused_append_stores_what_the_append_stores(dtype, rows):
     one through mtn_frame_step and one through the separate per-layer calls,
     hold bit-identical bytes after every frame, and both match the oracle.
     Chunks of up to 40 tokens at G = 8 take one or two 256-row passes (two or
-    three 128-row ones), so some plans fuse and some do not; the sequences
+    three 128-row ones), so some plans fuse and some do not (at G = 1 every
+    plan fuses, its waves storing up to seven tokens each in two batches); the sequences
     start empty (the chunk lies in the first stages a workgroup copies, so
     the copies wait behind the append) and grow past 18 blocks and through
     the window's wrap (the append then runs beside the first copies)."""
-    say(f"prefill fused append vs separate pool bytes, {dtype}, rows {rows}")
+    say(f"prefill fused append vs separate pool bytes, {dtype}, G={g}, rows {rows}")
     n, L = 3, 2
-    cfg = dict(dtype=dtype, d=128, hq=16, hkv=2, S=4, W=300, cmax=40, n=n, L=L,
+    cfg = dict(dtype=dtype, d=128, hq=2 * g, hkv=2, S=4, W=300, cmax=40, n=n, L=L,
                blocks=n * (1 + 22) + 2)
     pa, ha = _tiny(**cfg)
     pb, hb = _tiny(**cfg)
