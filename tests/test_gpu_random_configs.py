@@ -29,7 +29,7 @@ def _config(seed):
                 rows=rows, kernel=kernel, seed=seed)
 
 
-@pytest.mark.parametrize("seed", range(24))
+@pytest.mark.parametrize("seed", range(48))
 def test_random_configuration_against_oracle(seed):
     c = _config(seed)
     say(f"random config {c}")
