@@ -132,12 +132,15 @@ def _code_only(text: str) -> str:
 
 def kernel_src_hash(kernel: str = "decode") -> str:
     """Hash of the code (comments and layout aside) of the device sources the
-    kernel compiles from."""
+    kernel compiles from, and of the options its source is compiled with."""
     import hashlib
+    from paper_2607_02640_amd import build as pkg_build
     h = hashlib.sha256()
     for fn in KERNEL_SRC[kernel]:
         with open(fn, encoding="utf-8") as f:
             h.update(_code_only(f.read()).encode())
+    main = os.path.basename(KERNEL_SRC[kernel][0])
+    h.update(" ".join(pkg_build.compile_flags(main)).replace(ROOT, "").encode())
     return h.hexdigest()[:16]
 
 

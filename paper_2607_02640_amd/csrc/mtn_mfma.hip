@@ -523,7 +523,11 @@ int resident_mfma_g() {
     if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, k_attn_mfma<F8, G, S::NG, S::NBUF>,
                                                      64 * S::NG, 0) != hipSuccess)
         return 1;
-    return n > 0 ? n : 1;
+    // The split rule fills the resident slots; it counts at most two
+    // workgroups per CU.  More rings streaming at once made the decode slower
+    // (deeper rings, more waves per unit), and at 128 sessions the fp8
+    // launch, whose registers allow four, ran 4 % slower split to fill them.
+    return std::min(std::max(n, 1), 2);
 }
 template <bool F8>
 hipError_t launch_mfma(const AttnArgs &a, hipStream_t s) {

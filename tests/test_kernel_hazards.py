@@ -12,6 +12,7 @@ state.  The device code is compiled to assembly here (no GPU) and read."""
 import os
 import re
 import subprocess
+import sys
 from concurrent.futures import ThreadPoolExecutor
 
 import pytest
@@ -24,10 +25,12 @@ REG = re.compile(r"\bv(?:\[(\d+):(\d+)\]|(\d+)\b)")
 
 
 def _asm(src, out_dir):
+    """The gfx950 assembly of `src`, built with the library's own options."""
+    sys.path.insert(0, ROOT)
+    from paper_2607_02640_amd import build
     out = os.path.join(out_dir, src + ".s")
-    cmd = [HIPCC, "--offload-arch=gfx950", "-O3", "-std=c++17", "-Xclang", "-target-feature",
-           "-Xclang", "-packed-fp32-ops", f"-I{os.path.join(ROOT, 'include')}", f"-I{CSRC}",
-           "--cuda-device-only", "-S", os.path.join(CSRC, src), "-o", out]
+    cmd = [HIPCC, *build.compile_flags(src), "--cuda-device-only", "-S", os.path.join(CSRC, src),
+           "-o", out]
     r = subprocess.run(cmd, capture_output=True, text=True)
     assert r.returncode == 0, r.stderr[-3000:]
     return out
