@@ -623,7 +623,9 @@ bool use_mfma_bf16(const mtn_pool *P) {
     return P->G == 8;
 }
 
-// decode work units resident on the whole GPU for the pool's decode kernel
+// decode work units the split rule counts as one round on the whole GPU: the
+// kernels' own per-CU figure (the vector decode's occupancy; for the
+// matrix-core decode the workgroups holding about 64 KiB of copies in flight)
 int32_t count_resident_units(const mtn_pool *P) {
     const mtn_pool_config &c = P->cfg;
     const int per_cu = c.kv_dtype == MTN_FP8_E4M3 ? attn_fp8_resident_per_cu(P->G)

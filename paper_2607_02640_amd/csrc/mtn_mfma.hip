@@ -523,11 +523,18 @@ int resident_mfma_g() {
     if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, k_attn_mfma<F8, G, S::NG, S::NBUF>,
                                                      64 * S::NG, 0) != hipSuccess)
         return 1;
-    // The split rule fills the resident slots; it counts at most two
-    // workgroups per CU.  More rings streaming at once made the decode slower
-    // (deeper rings, more waves per unit), and at 128 sessions the fp8
-    // launch, whose registers allow four, ran 4 % slower split to fill them.
-    return std::min(std::max(n, 1), 2);
+    // The split rule fills these slots.  It counts the workgroups whose rings
+    // hold about 64 KiB of copies in flight per CU (bf16: one of 4 waves x 2
+    // blocks x 8 KiB; fp8: two of 4 x 2 x 4128 bytes), not the occupancy
+    // limit.  Measured per launch with the split merge, 128 units (32
+    // sessions, G = 8): bf16 49.7 us at split 2 against 52.1 at 4, fp8 32.4
+    // at split 4 against 37.7 at 2; 256 units: bf16 87.2 unsplit against 93.2
+    // at split 2, fp8 53.7 at split 2 against 60.8 unsplit.  (With more
+    // streams in flight the decode ran slower: deeper rings, more waves per
+    // unit, and fp8 split to fill the four workgroups its registers allow.)
+    constexpr int kRing = S::NG * S::NBUF * (F8 ? kF8Read : 2 * kBlock * kF8D * 2);
+    constexpr int kTarget = ((64 << 10) + kRing / 2) / kRing;
+    return std::min(std::max(n, 1), std::max(kTarget, 1));
 }
 template <bool F8>
 hipError_t launch_mfma(const AttnArgs &a, hipStream_t s) {
